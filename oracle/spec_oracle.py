@@ -1,0 +1,309 @@
+"""Plain fp64 CPU oracle of the SpeContext per-decode-step hot path.
+
+TEST INFRASTRUCTURE ONLY.  This module is the slow, obviously-correct
+definition that the HIP path is checked against.  Only the test suite, the
+smoke check and the CPU-baseline leg of the benchmark may import it; the
+product library never does, and nothing here is shared with the HIP sources.
+
+What it computes (SpeContext, arXiv 2512.00722):
+
+* retrieval scoring (Sec. 4.3 "Implementation Details", Eq. 1): the
+  lightweight retrieval head keeps a full key cache K_r and, for the current
+  query q_r, forms attention weights softmax(q_r K_r^T / sqrt(d_r)) per head;
+  the per-head weights are summed over heads into one importance score per
+  cached token (batch-level mapping of Sec. 4.2: one token set shared by every
+  head and, per Sec. 7.2.1, by every layer);
+* token selection (Sec. 4.3): the k tokens with the largest score;
+* sparse attention (Sec. 4.3 "Support for MHA" / "Support for GQA", Eq. 1):
+  the LLM's K/V rows at the selected indices are gathered per KV head and
+  decode attention runs over them only; the G = H_q / H_kv query heads of a
+  group share one KV head;
+* elastic loading (Sec. 5.4): with S_last the set held on the device and
+  S_now the new selection, only S_now - S_last is loaded, into the places freed
+  by S_last - S_now (equal in size because the budget is fixed).
+
+Everything is computed in float64 from the bf16-rounded inputs (bf16 embeds
+exactly in float64).  Readings of points the paper leaves open:
+
+* scale: Eq. 1 divides by sqrt(d) without naming d; the retrieval head uses
+  1/sqrt(d_r) and the LLM attention 1/sqrt(d) (head dimensions);
+* k_b = min(k, L_b): a budget above the context takes every token, so sparse
+  attention with k = L_b is dense attention;
+* ties: equal scores are ordered by lower token index; the returned index set
+  is sorted ascending (attention is permutation invariant, so order only
+  fixes the rounding order);
+* no token is forced into the set (no sink or recent window: those are prior
+  work in Sec. 2.2, not the method);
+* the slot pairing of elastic loading (which freed slot receives which new
+  token) is not stated; the oracle pairs the i-th smallest freed slot with the
+  i-th smallest new token.  Only the resulting slot->token map is compared.
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+__all__ = [
+    "retrieval_logits",
+    "head_softmax",
+    "head_sum",
+    "retrieval_scores",
+    "topk_indices",
+    "group_max_scores",
+    "sparse_gqa_attention",
+    "dense_gqa_attention",
+    "elastic_update",
+    "decode_step",
+    "accept_index_set",
+    "bf16_to_f64",
+]
+
+
+def bf16_to_f64(x_u16: np.ndarray) -> np.ndarray:
+    """Decode raw bf16 bit patterns (uint16) to float64 exactly.
+
+    bf16 is the upper half of an IEEE binary32, so shifting the 16 bits into
+    the high half of a uint32 gives the float32 with the same value.
+    """
+    u = np.asarray(x_u16, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return u.view(np.float32).astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Retrieval head (Sec. 4.3, Eq. 1)
+# ---------------------------------------------------------------------------
+
+def retrieval_logits(q_r: np.ndarray, K_r: np.ndarray, L: int,
+                     scale: float | None = None) -> np.ndarray:
+    """Per-head attention logits of the retrieval head, Eq. 1 before softmax.
+
+    q_r: [H_r, d_r] query of the current token for each retrieval head.
+    K_r: [L_cap, H_r, d_r] full retrieval key cache (token-major).
+    L:   number of cached tokens (only t < L are scored).
+    Returns logits l[h, t] = (q_r[h] . K_r[t, h]) * scale, shape [H_r, L].
+    """
+    q_r = np.asarray(q_r, dtype=np.float64)
+    K_r = np.asarray(K_r, dtype=np.float64)
+    H_r, d_r = q_r.shape
+    if scale is None:
+        scale = 1.0 / math.sqrt(d_r)
+    out = np.empty((H_r, L), dtype=np.float64)
+    for h in range(H_r):
+        # one matrix-vector product per head: K_r[:L, h, :] @ q_r[h]
+        out[h] = (K_r[:L, h, :] @ q_r[h]) * scale
+    return out
+
+
+def head_softmax(logits: np.ndarray) -> np.ndarray:
+    """Softmax over the token axis, separately for each head (Eq. 1).
+
+    In decode every cached token precedes the query, so no causal mask is
+    applied beyond the context length.  The maximum is subtracted first so
+    that exp never overflows; this does not change the result.
+    """
+    logits = np.asarray(logits, dtype=np.float64)
+    m = logits.max(axis=1, keepdims=True)
+    e = np.exp(logits - m)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def head_sum(p: np.ndarray) -> np.ndarray:
+    """Importance score of each token: the per-head weights summed over heads."""
+    return np.asarray(p, dtype=np.float64).sum(axis=0)
+
+
+def retrieval_scores(q_r, K_r, L: int, scale: float | None = None) -> np.ndarray:
+    """score[t] for t < L: softmax per retrieval head, then sum over heads."""
+    if L == 0:
+        return np.zeros((0,), dtype=np.float64)
+    return head_sum(head_softmax(retrieval_logits(q_r, K_r, L, scale)))
+
+
+def group_max_scores(p: np.ndarray, n_groups: int) -> np.ndarray:
+    """GQA group-level weights (Sec. 4.3 "Support for GQA").
+
+    The heads of each group are reduced by an element-wise maximum, per
+    token, giving one weight row per group.  p: [H, L] -> [n_groups, L], with
+    group g holding heads g*H/n_groups ... (g+1)*H/n_groups - 1.  This is the
+    head-level selection the paper prefers; the decode step below uses the
+    summed (batch-level) score instead.
+    """
+    p = np.asarray(p, dtype=np.float64)
+    H = p.shape[0]
+    assert H % n_groups == 0
+    per = H // n_groups
+    return np.stack([p[g * per:(g + 1) * per].max(axis=0) for g in range(n_groups)])
+
+
+# ---------------------------------------------------------------------------
+# Token selection
+# ---------------------------------------------------------------------------
+
+def topk_indices(score: np.ndarray, k: int) -> np.ndarray:
+    """The min(k, L) tokens with the largest score, ascending by token index.
+
+    Order by descending score, equal scores by ascending token index, keep
+    the first k_b, and return them sorted by token index.
+    """
+    score = np.asarray(score)
+    L = score.shape[0]
+    kb = max(0, min(int(k), L))
+    t = np.arange(L)
+    # np.lexsort sorts by the last key first: primary -score, secondary t.
+    order = np.lexsort((t, -score))
+    return np.sort(order[:kb]).astype(np.int64)
+
+
+# ---------------------------------------------------------------------------
+# Sparse GQA decode attention (Eq. 1 over the selected rows)
+# ---------------------------------------------------------------------------
+
+def sparse_gqa_attention(q: np.ndarray, K: np.ndarray, V: np.ndarray,
+                         idx: np.ndarray, scale: float | None = None):
+    """Decode attention of one sequence and one layer over selected tokens.
+
+    q: [H_q, d] query; K, V: [L_cap, H_kv, d] layer KV cache (token-major).
+    idx: selected token indices (any order, distinct).
+    Query head h reads KV head g = h // G with G = H_q / H_kv (the heads of
+    one group share a KV head; G = 1 is MHA, H_kv = 1 is MQA).
+    Returns (out [H_q, d], lse [H_q]) with lse = log sum_j exp(s_j) of the
+    scaled logits; with no selected token out is 0 and lse is -inf.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    H_q, d = q.shape
+    H_kv = K.shape[1]
+    assert H_q % H_kv == 0
+    G = H_q // H_kv
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    idx = np.asarray(idx, dtype=np.int64)
+    out = np.zeros((H_q, d), dtype=np.float64)
+    lse = np.full((H_q,), -np.inf, dtype=np.float64)
+    if idx.size == 0:
+        return out, lse
+    Ks = np.asarray(K[idx], dtype=np.float64)  # [k, H_kv, d]   (gather)
+    Vs = np.asarray(V[idx], dtype=np.float64)
+    for h in range(H_q):
+        g = h // G
+        s = (Ks[:, g, :] @ q[h]) * scale       # [k]
+        m = s.max()
+        w = np.exp(s - m)
+        z = w.sum()
+        out[h] = (w / z) @ Vs[:, g, :]
+        lse[h] = m + math.log(z)
+    return out, lse
+
+
+def dense_gqa_attention(q, K, V, L: int, scale: float | None = None):
+    """Dense decode attention over all L cached tokens (for the k = L pin)."""
+    return sparse_gqa_attention(q, K, V, np.arange(L), scale)
+
+
+# ---------------------------------------------------------------------------
+# Elastic loading (Sec. 5.4)
+# ---------------------------------------------------------------------------
+
+def elastic_update(slot_tok: np.ndarray, s_now: np.ndarray):
+    """One elastic-loading update of a fixed-budget slot array.
+
+    slot_tok: [n_slots] token held by each device slot (-1 = empty); its
+              valid entries form S_last.
+    s_now:    the new selection S_now (distinct tokens), |S_now| <= n_slots.
+    Slots whose token is not in S_now are freed (S_last - S_now, plus empty
+    slots); the tokens S_now - S_last are loaded into freed slots, the i-th
+    smallest freed slot receiving the i-th smallest new token.  Slots beyond
+    |S_now| that stay free are marked -1 so that the slot multiset is S_now.
+
+    Returns (new_slot_tok, loads) where loads is a list of (slot, token)
+    copies in slot order.  With a fixed budget, |S_last - S_now| equals
+    |S_now - S_last| whenever |S_last| = |S_now|.
+    """
+    slot_tok = np.asarray(slot_tok, dtype=np.int64).copy()
+    now = set(int(t) for t in np.asarray(s_now).tolist())
+    held = set(int(t) for t in slot_tok.tolist() if t >= 0)
+    d_in = sorted(now - held)                    # S_now - S_last
+    free = [i for i, t in enumerate(slot_tok.tolist()) if t < 0 or t not in now]
+    assert len(free) >= len(d_in)
+    loads = list(zip(free[:len(d_in)], d_in))
+    for slot, tok in loads:
+        slot_tok[slot] = tok
+    for slot in free[len(d_in):]:
+        slot_tok[slot] = -1
+    return slot_tok, loads
+
+
+# ---------------------------------------------------------------------------
+# One decode step (batched), and the acceptance predicate
+# ---------------------------------------------------------------------------
+
+def decode_step(q_r, K_r, seq_lens, ks, q, K_layers, V_layers,
+                scale_r: float | None = None, scale: float | None = None):
+    """Retrieve + select + sparse attention for every sequence and layer.
+
+    q_r [B, H_r, d_r]; K_r [B, L_cap, H_r, d_r]; seq_lens [B]; ks [B];
+    q [n_layers, B, H_q, d]; K_layers/V_layers [n_layers, B, L_cap, H_kv, d].
+    One selection per sequence serves every layer and every KV head.
+    Returns (idx list of arrays, scores list, out [n_layers, B, H_q, d],
+    lse [n_layers, B, H_q]).
+    """
+    B = len(seq_lens)
+    n_layers = len(q)
+    H_q, d = np.asarray(q[0][0]).shape
+    idxs, scores = [], []
+    out = np.zeros((n_layers, B, H_q, d))
+    lse = np.full((n_layers, B, H_q), -np.inf)
+    for b in range(B):
+        L = int(seq_lens[b])
+        s = retrieval_scores(q_r[b], K_r[b], L, scale_r)
+        idx = topk_indices(s, int(ks[b]))
+        idxs.append(idx)
+        scores.append(s)
+        for layer in range(n_layers):
+            o, l_ = sparse_gqa_attention(q[layer][b], K_layers[layer][b],
+                                         V_layers[layer][b], idx, scale)
+            out[layer, b] = o
+            lse[layer, b] = l_
+    return idxs, scores, out, lse
+
+
+def accept_index_set(score: np.ndarray, k: int, cand: np.ndarray,
+                     band: float = 1e-6):
+    """Is `cand` an acceptable top-k set for the oracle scores `score`?
+
+    Let s_k be the k_b-th largest oracle score.  The candidate must hold k_b
+    distinct in-range tokens, contain every token scoring above s_k + band,
+    and hold no token scoring below s_k - band.  Outside the band around the
+    k-th score the set is therefore unique; inside it any choice is allowed
+    (the oracle itself breaks exact ties by lower index).
+    Returns (ok, info) where info reports the band population and the
+    symmetric difference to the oracle's own set.
+    """
+    score = np.asarray(score, dtype=np.float64)
+    L = score.shape[0]
+    kb = max(0, min(int(k), L))
+    cand = np.asarray(cand, dtype=np.int64)
+    ref = topk_indices(score, kb)
+    info = {"k_b": kb, "band_pop": 0, "sym_diff": 0, "reason": ""}
+    if cand.shape[0] != kb:
+        info["reason"] = f"size {cand.shape[0]} != {kb}"
+        return False, info
+    if kb == 0:
+        return True, info
+    if len(np.unique(cand)) != kb or cand.min() < 0 or cand.max() >= L:
+        info["reason"] = "duplicate or out-of-range index"
+        return False, info
+    s_k = np.sort(score)[::-1][kb - 1]
+    info["band_pop"] = int(np.sum(np.abs(score - s_k) <= band))
+    info["sym_diff"] = int(len(set(cand.tolist()) ^ set(ref.tolist())))
+    inset = np.zeros(L, dtype=bool)
+    inset[cand] = True
+    must = score > s_k + band
+    if np.any(must & ~inset):
+        info["reason"] = "missed a token above the band"
+        return False, info
+    if np.any(inset & (score < s_k - band)):
+        info["reason"] = "took a token below the band"
+        return False, info
+    return True, info

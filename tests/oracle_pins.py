@@ -1,0 +1,326 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each pin takes an oracle namespace `o` (the real oracle, or a deliberately
+broken copy in the mutation tests) and raises AssertionError when `o`
+disagrees with a value fixed independently of it: a hand-derived worked
+example, a closed form, an invariant, a brute-force enumeration, or an
+independent library routine.
+"""
+
+from __future__ import annotations
+
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import torch
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _lnval(x):
+    if isinstance(x, str):
+        assert x.startswith("ln")
+        return math.log(float(x[2:]))
+    return float(x)
+
+
+# --------------------------------------------------------------- retrieval
+
+def pin_retrieval_worked_example(o):
+    g = _load("retrieval_worked_example.json")
+    H_r, d_r, L = g["H_r"], g["d_r"], g["L"]
+    K_r = np.zeros((L, H_r, d_r))
+    for t in range(L):
+        for h in range(H_r):
+            K_r[t, h, 0] = _lnval(g["K_r_dim0"][t][h])
+            K_r[t, h, 1:] = g["K_r_other"]
+    q_r = np.array(g["q_r"], dtype=np.float64)
+    p = o.head_softmax(o.retrieval_logits(q_r, K_r, L))
+    np.testing.assert_allclose(p, np.array(g["p"]), rtol=0, atol=1e-14)
+    s = o.retrieval_scores(q_r, K_r, L)
+    np.testing.assert_allclose(s, np.array(g["score"]), rtol=0, atol=1e-14)
+    for k, want in g["topk"].items():
+        got = o.topk_indices(s, int(k))
+        assert got.tolist() == want, (k, got, want)
+
+
+def pin_scores_sum_to_heads(o):
+    """Each head's softmax sums to 1, so the head-summed scores sum to H_r."""
+    rng = np.random.default_rng(11)
+    for H_r, d_r, L in [(1, 64, 1), (2, 64, 7), (8, 64, 300), (16, 128, 257)]:
+        q_r = rng.standard_normal((H_r, d_r))
+        K_r = rng.standard_normal((L + 5, H_r, d_r)) * 3.0
+        p = o.head_softmax(o.retrieval_logits(q_r, K_r, L))
+        np.testing.assert_allclose(p.sum(axis=1), np.ones(H_r), atol=1e-12)
+        s = o.retrieval_scores(q_r, K_r, L)
+        assert s.shape == (L,)
+        assert abs(s.sum() - H_r) < 1e-10 * max(1, H_r)
+
+
+def pin_constant_keys_uniform(o):
+    """Identical keys give equal logits, so every score is H_r / L."""
+    rng = np.random.default_rng(12)
+    H_r, d_r, L = 4, 64, 37
+    q_r = rng.standard_normal((H_r, d_r))
+    row = rng.standard_normal((1, H_r, d_r))
+    K_r = np.repeat(row, L, axis=0)
+    s = o.retrieval_scores(q_r, K_r, L)
+    np.testing.assert_allclose(s, np.full(L, H_r / L), rtol=1e-12)
+
+
+def pin_logits_bruteforce(o):
+    """Logits against a naive triple loop with the 1/sqrt(d_r) scale."""
+    rng = np.random.default_rng(13)
+    H_r, d_r, L = 3, 64, 5
+    q_r = rng.standard_normal((H_r, d_r))
+    K_r = rng.standard_normal((L + 2, H_r, d_r))
+    want = np.zeros((H_r, L))
+    for h in range(H_r):
+        for t in range(L):
+            acc = 0.0
+            for i in range(d_r):
+                acc += q_r[h, i] * K_r[t, h, i]
+            want[h, t] = acc / math.sqrt(d_r)
+    np.testing.assert_allclose(o.retrieval_logits(q_r, K_r, L), want, rtol=1e-12, atol=1e-12)
+    # softmax by its definition, one element at a time
+    p = o.head_softmax(want)
+    for h in range(H_r):
+        z = sum(math.exp(want[h, t]) for t in range(L))
+        for t in range(L):
+            assert abs(p[h, t] - math.exp(want[h, t]) / z) < 1e-14
+
+
+def pin_single_head_is_logit_order(o):
+    """With H_r = 1 softmax is monotone, so top-k of scores = top-k of logits."""
+    rng = np.random.default_rng(14)
+    for L, k in [(50, 7), (200, 64), (33, 33)]:
+        q_r = rng.standard_normal((1, 64))
+        K_r = rng.standard_normal((L, 1, 64))
+        s = o.retrieval_scores(q_r, K_r, L)
+        lg = (K_r[:L, 0, :] @ q_r[0])
+        want = np.sort(np.argsort(-lg, kind="stable")[:k])
+        assert o.topk_indices(s, k).tolist() == want.tolist()
+
+
+# --------------------------------------------------------------- top-k
+
+def _valid_topk_set(score, S):
+    """Pairwise definition: every chosen token beats every unchosen one,
+    where a tie is won by the lower index."""
+    inside = set(S)
+    for i in inside:
+        for j in range(len(score)):
+            if j in inside:
+                continue
+            if not (score[i] > score[j] or (score[i] == score[j] and i < j)):
+                return False
+    return True
+
+
+def pin_topk_bruteforce(o):
+    """Enumerate every subset of tiny inputs: exactly one satisfies the
+    pairwise definition, and it is the oracle's set."""
+    rng = np.random.default_rng(15)
+    for trial in range(60):
+        L = int(rng.integers(1, 9))
+        # few distinct values, so ties are frequent
+        score = rng.integers(0, 4, size=L).astype(np.float64) / 4.0
+        for k in range(0, L + 2):
+            kb = min(k, L)
+            valid = [S for S in itertools.combinations(range(L), kb)
+                     if _valid_topk_set(score, S)]
+            assert len(valid) == 1, (score, k, valid)
+            got = o.topk_indices(score, k)
+            assert got.tolist() == list(valid[0]), (score, k, got, valid)
+
+
+def pin_topk_all_equal(o):
+    for L, k in [(10, 3), (64, 64), (100, 1)]:
+        assert o.topk_indices(np.full(L, 0.25), k).tolist() == list(range(k))
+
+
+def pin_topk_permutations(o):
+    """Every permutation of a small distinct-score row selects the same
+    values; the chosen values are the k largest."""
+    vals = np.array([0.9, 0.1, 0.5, 0.7, 0.3, 0.2])
+    for perm in itertools.permutations(range(6)):
+        s = vals[list(perm)]
+        for k in (1, 3, 5):
+            got = o.topk_indices(s, k)
+            assert sorted(s[got].tolist()) == sorted(vals)[-k:]
+            assert got.tolist() == sorted(got.tolist())
+
+
+def pin_heavy_recovered(o):
+    """Tokens whose retrieval keys are pushed along q_r (a strong plant)
+    dominate the softmax and are always selected."""
+    rng = np.random.default_rng(16)
+    H_r, d_r, L, n_heavy = 4, 64, 400, 20
+    q_r = rng.standard_normal((H_r, d_r))
+    K_r = rng.standard_normal((L, H_r, d_r))
+    heavy = np.sort(rng.choice(L, n_heavy, replace=False))
+    K_r[heavy] += 2.0 * q_r  # logit shift 2|q_r|^2/sqrt(d_r), about 16
+    s = o.retrieval_scores(q_r, K_r, L)
+    got = o.topk_indices(s, n_heavy)
+    assert got.tolist() == heavy.tolist()
+
+
+# --------------------------------------------------------------- attention
+
+def pin_attention_worked_example(o):
+    g = _load("gqa_attention_worked_example.json")
+    H_q, H_kv, d, L = g["H_q"], g["H_kv"], g["d"], g["L"]
+    K = np.zeros((L, H_kv, d))
+    for t in range(L):
+        for kv in range(H_kv):
+            K[t, kv, 0] = _lnval(g["K_dim0"][t][kv])
+    V = np.array(g["V"], dtype=np.float64)
+    q = np.array(g["q"], dtype=np.float64)
+    out, lse = o.sparse_gqa_attention(q, K, V, np.array(g["idx"]))
+    np.testing.assert_allclose(out, np.array(g["out"], dtype=np.float64), atol=1e-14)
+    np.testing.assert_allclose(lse, [_lnval(x) for x in g["lse"]], atol=1e-14)
+
+
+def _sdpa_dense(q, K, V, L, scale=None):
+    """torch's scaled_dot_product_attention (fp64, CPU) as the textbook
+    dense reference, with the KV heads repeated G times (repeat_kv)."""
+    H_q, d = q.shape
+    H_kv = K.shape[1]
+    G = H_q // H_kv
+    qt = torch.as_tensor(q, dtype=torch.float64).reshape(1, H_q, 1, d)
+    kt = torch.as_tensor(K[:L], dtype=torch.float64).permute(1, 0, 2)
+    vt = torch.as_tensor(V[:L], dtype=torch.float64).permute(1, 0, 2)
+    kt = kt.repeat_interleave(G, dim=0).unsqueeze(0).contiguous()
+    vt = vt.repeat_interleave(G, dim=0).unsqueeze(0).contiguous()
+    o = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, scale=scale)
+    return o.reshape(H_q, d).numpy()
+
+
+def pin_full_budget_is_dense(o):
+    """With k = L every token is selected and sparse attention equals dense
+    attention; checked against torch's SDPA (fp64, CPU)."""
+    rng = np.random.default_rng(17)
+    for H_q, H_kv, L in [(4, 1, 9), (8, 2, 33), (8, 8, 17), (16, 2, 64)]:
+        d = 128
+        q = rng.standard_normal((H_q, d))
+        K = rng.standard_normal((L + 3, H_kv, d))
+        V = rng.standard_normal((L + 3, H_kv, d))
+        q_r = rng.standard_normal((2, 64))
+        K_r = rng.standard_normal((L + 3, 2, 64))
+        idx = o.topk_indices(o.retrieval_scores(q_r, K_r, L), L)
+        assert idx.tolist() == list(range(L))
+        out, _ = o.sparse_gqa_attention(q, K, V, idx)
+        np.testing.assert_allclose(out, _sdpa_dense(q, K, V, L), rtol=1e-10, atol=1e-12)
+
+
+def pin_attention_special_cases(o):
+    rng = np.random.default_rng(18)
+    H_q, H_kv, d, L = 8, 2, 128, 20
+    q = rng.standard_normal((H_q, d))
+    K = rng.standard_normal((L, H_kv, d))
+    V = rng.standard_normal((L, H_kv, d))
+    # k = 1: the output is the one selected V row of the head's group
+    out, lse = o.sparse_gqa_attention(q, K, V, np.array([7]))
+    for h in range(H_q):
+        np.testing.assert_array_equal(out[h], V[7, h // (H_q // H_kv)])
+        assert abs(lse[h] - (q[h] @ K[7, h // 4]) / math.sqrt(d)) < 1e-12
+    # identical keys: uniform weights, the mean of the selected V rows
+    Kc = np.repeat(K[:1], L, axis=0)
+    sel = np.array([1, 4, 5, 11, 19])
+    out, _ = o.sparse_gqa_attention(q, Kc, V, sel)
+    for h in range(H_q):
+        np.testing.assert_allclose(out[h], V[sel, h // 4].mean(axis=0), atol=1e-13)
+    # permutation invariance over the index order
+    perm = sel[[3, 0, 4, 2, 1]]
+    a, la = o.sparse_gqa_attention(q, K, V, sel)
+    b, lb = o.sparse_gqa_attention(q, K, V, perm)
+    np.testing.assert_allclose(a, b, atol=1e-13)
+    np.testing.assert_allclose(la, lb, atol=1e-13)
+    # empty selection
+    e, le = o.sparse_gqa_attention(q, K, V, np.zeros((0,), dtype=np.int64))
+    assert np.all(e == 0) and np.all(np.isneginf(le))
+
+
+def pin_group_max_bruteforce(o):
+    rng = np.random.default_rng(19)
+    p = rng.random((8, 13))
+    gm = o.group_max_scores(p, 2)
+    for g in range(2):
+        for t in range(13):
+            assert gm[g, t] == max(p[h, t] for h in range(g * 4, g * 4 + 4))
+
+
+# --------------------------------------------------------------- elastic
+
+def pin_elastic_worked_example(o):
+    g = _load("elastic_worked_example.json")
+    new, loads = o.elastic_update(np.array(g["slot_tok"]), np.array(g["s_now"]))
+    assert new.tolist() == g["new_slot_tok"]
+    assert [list(x) for x in loads] == g["loads"]
+
+
+def pin_elastic_identities(o):
+    rng = np.random.default_rng(20)
+    for trial in range(50):
+        L = int(rng.integers(10, 200))
+        k = int(rng.integers(1, L // 2 + 1))
+        last = rng.choice(L, k, replace=False)
+        now = np.sort(rng.choice(L, k, replace=False))
+        slot = rng.permutation(last)
+        new, loads = o.elastic_update(slot, now)
+        d_in = set(now.tolist()) - set(last.tolist())
+        d_out = set(last.tolist()) - set(now.tolist())
+        assert len(d_in) == len(d_out) == len(loads)            # |S_now-S_last| = |S_last-S_now|
+        assert sorted(new.tolist()) == now.tolist()              # slots hold S_now
+        kept = [i for i, t in enumerate(slot.tolist()) if t in set(now.tolist())]
+        for i in kept:                                           # survivors stay in place
+            assert new[i] == slot[i]
+        # from an empty state every token is loaded
+        empty = np.full(k, -1)
+        new2, loads2 = o.elastic_update(empty, now)
+        assert sorted(new2.tolist()) == now.tolist() and len(loads2) == k
+        # an unchanged selection loads nothing
+        new3, loads3 = o.elastic_update(new, now)
+        assert loads3 == [] and new3.tolist() == new.tolist()
+
+
+# --------------------------------------------------------------- helpers
+
+def pin_bf16_decode(o):
+    bits = np.array([0x3F80, 0xC000, 0x3F81, 0x0000, 0x8000, 0x7F80, 0x0001], dtype=np.uint16)
+    got = o.bf16_to_f64(bits)
+    assert got[0] == 1.0 and got[1] == -2.0 and got[2] == 1.0078125
+    assert got[3] == 0.0 and got[4] == 0.0 and np.signbit(got[4])
+    assert np.isposinf(got[5])
+    assert got[6] == 2.0 ** -133
+    # against torch's own bf16 -> float conversion
+    x = torch.randn(1000, generator=torch.Generator().manual_seed(3)).to(torch.bfloat16)
+    np.testing.assert_array_equal(o.bf16_to_f64(x.view(torch.int16).numpy().view(np.uint16)),
+                                  x.double().numpy())
+
+
+def pin_acceptance_checker(o):
+    score = np.array([0.5, 0.1, 0.3, 0.3 + 5e-7, 0.9, 0.05])
+    ok, _ = o.accept_index_set(score, 3, np.array([0, 3, 4]))
+    assert ok
+    ok, info = o.accept_index_set(score, 3, np.array([0, 2, 4]))   # tie-band swap
+    assert ok and info["sym_diff"] == 2
+    ok, _ = o.accept_index_set(score, 3, np.array([0, 1, 4]))      # below band
+    assert not ok
+    ok, _ = o.accept_index_set(score, 3, np.array([2, 3, 4]))      # misses 0.5
+    assert not ok
+    ok, _ = o.accept_index_set(score, 3, np.array([0, 4]))         # wrong size
+    assert not ok
+    ok, _ = o.accept_index_set(score, 3, np.array([0, 4, 4]))      # duplicate
+    assert not ok
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -1,0 +1,49 @@
+"""Plant plausible mistakes in a copy of the oracle (on the CPU) and check
+that the pins catch every one of them."""
+import importlib.util
+import inspect
+import types
+
+import pytest
+
+import oracle.spec_oracle as real
+from tests.oracle_pins import ALL_PINS
+
+MUTANTS = {
+    "dropped_retrieval_scale": ("out[h] = (K_r[:L, h, :] @ q_r[h]) * scale", "out[h] = (K_r[:L, h, :] @ q_r[h])"),
+    "softmax_not_normalised": ("return e / e.sum(axis=1, keepdims=True)", "return e"),
+    "softmax_wrong_axis": ("return e / e.sum(axis=1, keepdims=True)", "return e / e.sum(axis=0, keepdims=True)"),
+    "max_over_heads": ("return np.asarray(p, dtype=np.float64).sum(axis=0)", "return np.asarray(p, dtype=np.float64).max(axis=0)"),
+    "ties_to_higher_index": ("order = np.lexsort((t, -score))", "order = np.lexsort((-t, -score))"),
+    "smallest_k": ("order = np.lexsort((t, -score))", "order = np.lexsort((t, score))"),
+    "gqa_modulo_mapping": ("        g = h // G\n        s = ", "        g = h % H_kv\n        s = "),
+    "v_from_head0": ("out[h] = (w / z) @ Vs[:, g, :]", "out[h] = (w / z) @ Vs[:, 0, :]"),
+    "attn_scale_over_d": ("scale = 1.0 / math.sqrt(d)\n    idx", "scale = 1.0 / d\n    idx"),
+    "lse_missing_max": ("lse[h] = m + math.log(z)", "lse[h] = math.log(z)"),
+    "gather_off_by_one": ("Ks = np.asarray(K[idx], dtype=np.float64)", "Ks = np.asarray(K[idx - 1], dtype=np.float64)"),
+    "elastic_reverse_pairing": ("loads = list(zip(free[:len(d_in)], d_in))", "loads = list(zip(free[::-1][:len(d_in)], d_in))"),
+    "elastic_keeps_stale": ("free = [i for i, t in enumerate(slot_tok.tolist()) if t < 0 or t not in now]", "free = [i for i, t in enumerate(slot_tok.tolist()) if t < 0]"),
+    "group_mean_not_max": ("return np.stack([p[g * per:(g + 1) * per].max(axis=0)", "return np.stack([p[g * per:(g + 1) * per].mean(axis=0)"),
+    "accept_no_band_low": ("if np.any(inset & (score < s_k - band)):", "if False:"),
+    "bf16_wrong_shift": ("<< np.uint32(16)", "<< np.uint32(15)"),
+}
+
+
+def _mutant(old, new):
+    src = inspect.getsource(real)
+    assert src.count(old) == 1, old
+    mod = types.ModuleType("oracle_mutant")
+    exec(compile(src.replace(old, new), "oracle_mutant", "exec"), mod.__dict__)
+    return mod
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name):
+    mod = _mutant(*MUTANTS[name])
+    caught = []
+    for pin in ALL_PINS:
+        try:
+            pin(mod)
+        except Exception:  # AssertionError, or a crash the mistake causes
+            caught.append(pin.__name__)
+    assert caught, f"no pin caught mutant {name}"

@@ -1,0 +1,215 @@
+"""Seeded synthetic decode-step workloads (input generation only).
+
+This package builds the inputs that both the HIP path and the CPU oracle
+consume.  It holds none of the method's arithmetic: it draws Gaussian
+tensors, plants structure into the retrieval key cache, rounds to bf16 and
+places the tensors on a device.  The paper measures on LongBench/LongWriter
+with 8B models; these workloads stand in for their decode-step shapes
+(32 layers, 32 query / 8 KV heads, head dim 128, contexts 4K-128K, budgets
+512-4096).  No benchmark item is used.
+
+Structure recipe (all tensors drawn N(0,1) in fp32, planted, then rounded to
+bf16 with round-to-nearest-even):
+
+* heavy tokens: K_r[b, t, h, :] += heavy_gain * q_r[b, h] / |q_r[b, h]| in
+  every retrieval head, for a seeded set of positions;
+* recency bias: the last `recent` tokens get += recent_gain * q_r/|q_r|;
+* clusters: `n_clusters` runs of `cluster_len` contiguous heavy tokens.
+
+Positions and ragged lengths come from numpy's PCG64 (portable); tensor
+values come from a torch generator on the target device, seeded per tensor
+from (seed, tensor name).
+"""
+
+from __future__ import annotations
+
+import dataclasses
+import zlib
+from typing import Optional
+
+import numpy as np
+import torch
+
+__all__ = ["Workload", "WORKLOADS", "BENCH_WORKLOAD", "tensor_seed",
+           "generate", "algorithmic_bytes", "small_workload"]
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    L: int                 # context length (upper bound for ragged)
+    H_r: int
+    d_r: int
+    n_layers: int
+    H_q: int
+    H_kv: int
+    d: int
+    k: int
+    heavy_frac: float = 0.0
+    recent: int = 0        # length of the recency-biased tail
+    recent_gain: float = 1.0
+    heavy_gain: float = 2.0
+    n_clusters: int = 0
+    cluster_len: int = 0
+    ragged_min: int = 0    # >0: L_b uniform integer in [ragged_min, L]
+    k_frac_den: int = 0    # >0: k_b = min(k, L_b // k_frac_den)
+    extra_cap: int = 0     # spare capacity for appended tokens
+    steps: int = 1         # decode steps simulated (elastic workload)
+    drift: float = 0.95    # AR(1) coefficient of q_r across steps
+
+    @property
+    def L_cap(self) -> int:
+        return self.L + self.extra_cap
+
+    @property
+    def G(self) -> int:
+        return self.H_q // self.H_kv
+
+
+# The five decode-step workloads (shapes of the paper's cloud/edge settings).
+WORKLOADS = {
+    "b1_l4096_k512_1layer": Workload(
+        "b1_l4096_k512_1layer", B=1, L=4096, H_r=8, d_r=64, n_layers=1,
+        H_q=32, H_kv=8, d=128, k=512, heavy_frac=0.05),
+    "b8_l32768_k2048_32layers": Workload(
+        "b8_l32768_k2048_32layers", B=8, L=32768, H_r=8, d_r=64, n_layers=32,
+        H_q=32, H_kv=8, d=128, k=2048, heavy_frac=0.02, recent=256),
+    "b32_l16384_k1024_hr16": Workload(
+        "b32_l16384_k1024_hr16", B=32, L=16384, H_r=16, d_r=64, n_layers=32,
+        H_q=32, H_kv=8, d=128, k=1024, heavy_frac=0.01),
+    "b1_l131072_k4096_g8": Workload(
+        "b1_l131072_k4096_g8", B=1, L=131072, H_r=8, d_r=128, n_layers=32,
+        H_q=64, H_kv=8, d=128, k=4096, n_clusters=3, cluster_len=512),
+    "b64_ragged_l2k_16k_elastic": Workload(
+        "b64_ragged_l2k_16k_elastic", B=64, L=16384, H_r=8, d_r=64,
+        n_layers=32, H_q=32, H_kv=8, d=128, k=2048, heavy_frac=0.02,
+        ragged_min=2048, k_frac_den=4, extra_cap=16, steps=16),
+}
+
+# The workload the throughput metric is quoted on.
+BENCH_WORKLOAD = "b8_l32768_k2048_32layers"
+
+
+def small_workload(**kw) -> Workload:
+    """A custom (usually tiny) workload for tests."""
+    base = dict(name="custom", B=1, L=64, H_r=2, d_r=64, n_layers=1, H_q=4,
+                H_kv=1, d=128, k=8)
+    base.update(kw)
+    return Workload(**base)
+
+
+def tensor_seed(seed: int, name: str) -> int:
+    return zlib.crc32(f"{int(seed)}:{name}".encode()) & 0x7FFFFFFF
+
+
+def _gen(device, seed, name) -> torch.Generator:
+    g = torch.Generator(device=device)
+    g.manual_seed(tensor_seed(seed, name))
+    return g
+
+
+def _lengths(w: Workload, rng: np.random.Generator) -> np.ndarray:
+    if w.ragged_min > 0:
+        return rng.integers(w.ragged_min, w.L, size=w.B, endpoint=True)
+    return np.full(w.B, w.L, dtype=np.int64)
+
+
+def _budgets(w: Workload, lens: np.ndarray) -> np.ndarray:
+    if w.k_frac_den > 0:
+        return np.minimum(w.k, lens // w.k_frac_den)
+    return np.full(w.B, w.k, dtype=np.int64)
+
+
+def _heavy_positions(w: Workload, L_b: int, rng: np.random.Generator) -> np.ndarray:
+    """Planted heavy positions for one sequence (sorted, distinct)."""
+    if w.n_clusters > 0:
+        starts = []
+        span = L_b - w.cluster_len
+        while len(starts) < w.n_clusters:
+            s = int(rng.integers(0, span + 1))
+            if all(abs(s - o) >= w.cluster_len for o in starts):
+                starts.append(s)
+        pos = np.concatenate([np.arange(s, s + w.cluster_len) for s in sorted(starts)])
+        return pos
+    n_heavy = int(round(w.heavy_frac * L_b))
+    if n_heavy == 0:
+        return np.zeros((0,), dtype=np.int64)
+    hi = L_b - w.recent if w.recent > 0 else L_b
+    return np.sort(rng.choice(hi, size=n_heavy, replace=False))
+
+
+def generate(w: Workload, seed: int = 0, device="cpu", with_kv: bool = True,
+             layers: Optional[range] = None):
+    """Draw one decode step's inputs for workload `w`.
+
+    Returns a dict of tensors on `device`:
+      q_r [B, H_r, d_r] bf16, K_r [B, L_cap, H_r, d_r] bf16,
+      seq_lens [B] int32, ks [B] int32,
+      q [n_layers, B, H_q, d] bf16,
+      K, V [n_layers, B, L_cap, H_kv, d] bf16 (if with_kv),
+      heavy: list of numpy arrays of planted positions per sequence.
+    Rows at or beyond a sequence's length hold random values too; they must
+    never be read by the method.
+    """
+    device = torch.device(device)
+    rng = np.random.default_rng(seed)
+    lens = _lengths(w, rng)
+    ks = _budgets(w, lens)
+    heavy = [_heavy_positions(w, int(lens[b]), rng) for b in range(w.B)]
+
+    q_r = torch.randn((w.B, w.H_r, w.d_r), generator=_gen(device, seed, "q_r"),
+                      device=device, dtype=torch.float32).to(torch.bfloat16)
+    qf = q_r.float()
+    qhat = qf / qf.norm(dim=-1, keepdim=True)             # [B, H_r, d_r]
+
+    K_r = torch.empty((w.B, w.L_cap, w.H_r, w.d_r), dtype=torch.bfloat16, device=device)
+    for b in range(w.B):
+        row = torch.randn((w.L_cap, w.H_r, w.d_r), generator=_gen(device, seed, f"K_r.{b}"),
+                          device=device, dtype=torch.float32)
+        if len(heavy[b]):
+            pos = torch.as_tensor(heavy[b], device=device, dtype=torch.long)
+            row[pos] += w.heavy_gain * qhat[b]
+        if w.recent > 0:
+            L_b = int(lens[b])
+            row[L_b - w.recent:L_b] += w.recent_gain * qhat[b]
+        K_r[b] = row.to(torch.bfloat16)
+        del row
+
+    q = torch.randn((w.n_layers, w.B, w.H_q, w.d), generator=_gen(device, seed, "q"),
+                    device=device, dtype=torch.float32).to(torch.bfloat16)
+    out = {
+        "q_r": q_r, "K_r": K_r,
+        "seq_lens": torch.as_tensor(lens, dtype=torch.int32, device=device),
+        "ks": torch.as_tensor(ks, dtype=torch.int32, device=device),
+        "q": q, "heavy": heavy,
+    }
+    if with_kv:
+        rng_layers = layers if layers is not None else range(w.n_layers)
+        shape = (len(rng_layers), w.B, w.L_cap, w.H_kv, w.d)
+        K = torch.empty(shape, dtype=torch.bfloat16, device=device)
+        V = torch.empty(shape, dtype=torch.bfloat16, device=device)
+        for i, layer in enumerate(rng_layers):
+            K[i].normal_(generator=_gen(device, seed, f"K.{layer}"))
+            V[i].normal_(generator=_gen(device, seed, f"V.{layer}"))
+        out["K"], out["V"] = K, V
+    return out
+
+
+def algorithmic_bytes(w: Workload, seq_lens, ks, delta_rows: int = 0) -> int:
+    """Bytes the method must move for one decode step.
+
+    K_r rows of every cached token, q_r, and per layer the selected K and V
+    rows, the query and the fp32 output; plus, for elastic loading, a read
+    and a write of every changed K/V row in every layer (delta_rows = total
+    changed indices over the batch).  Scratch (logits, scores, indices,
+    partials) is implementation traffic and is not counted.
+    """
+    seq_lens = [int(x) for x in seq_lens]
+    ks = [int(x) for x in ks]
+    kb = [min(k, L) for k, L in zip(ks, seq_lens)]
+    kr = sum(seq_lens) * w.H_r * w.d_r * 2 + w.B * w.H_r * w.d_r * 2
+    per_layer = (sum(kb) * w.H_kv * w.d * 2 * 2 + w.B * w.H_q * w.d * 2
+                 + w.B * w.H_q * w.d * 4)
+    delta = 2 * delta_rows * w.H_kv * w.d * 2 * 2 * w.n_layers
+    return kr + w.n_layers * per_layer + delta
