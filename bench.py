@@ -1,0 +1,260 @@
+#!/usr/bin/env python3
+"""Decode-step throughput of the SpeContext hot path on one MI355X.
+
+One step = retrieval scoring over every cached token + exact top-k + sparse
+GQA attention over the selected K/V rows of every layer (spec_step, one call
+on torch's current stream).  Inputs are seeded synthetic tensors already
+resident in HBM when the timed region starts.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+Prints ONE JSON line (see the fields below).  Single-GPU build: --gpus N with
+N > 1 exits with a message.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode steps/s of retrieve+top-k+sparse attn; achieved HBM GB/s vs peak"
+PEAK_HBM_GBPS = 8000.0  # MI355X published HBM3E bandwidth
+ATTN_SRC = os.path.join(ROOT, "paper_2512_00722_amd", "csrc", "attn.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--attn-iters", type=int, default=20)
+    return ap.parse_args()
+
+
+def attn_bytes(w, counts):
+    """Algorithmic bytes of one attention launch: selected K and V rows of
+    every layer, the bf16 queries and the fp32 outputs."""
+    kb = sum(int(c) for c in counts)
+    return w.n_layers * (kb * w.H_kv * w.d * 2 * 2 + w.B * w.H_q * w.d * 2 + w.B * w.H_q * w.d * 4)
+
+
+def stored_traffic():
+    """Per-launch HBM bytes of the attention kernels measured with rocprofv3
+    PMC counters, valid only for the attention source they were taken on."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+        sha = hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()
+        if t.get("attn_source_sha256") != sha:
+            return None
+        return t.get("bytes_per_launch")
+    except (OSError, ValueError):
+        return None
+
+
+def cpu_baseline(w, x, res, budget_s=20.0):
+    """Time the fp64 oracle on a bounded sample of the same step on the host
+    cores: every sequence's scoring + top-k, and attention for as many
+    layers as fit the budget (selected rows copied to the host untimed);
+    the per-step time is scaled to all layers."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+
+    def f64(t):
+        return t.float().cpu().numpy().astype(np.float64)
+
+    seq = x["seq_lens"].cpu().numpy()
+    ks = x["ks"].cpu().numpy()
+    t_score = 0.0
+    idxs = []
+    for b in range(w.B):
+        qrn, krn = f64(x["q_r"][b]), f64(x["K_r"][b, :int(seq[b])])
+        t0 = time.perf_counter()
+        s = oracle.retrieval_scores(qrn, krn, int(seq[b]))
+        idx = oracle.topk_indices(s, int(ks[b]))
+        t_score += time.perf_counter() - t0
+        idxs.append(idx)
+    t_attn = 0.0
+    layers_done = 0
+    for layer in range(w.n_layers):
+        for b in range(w.B):
+            sel = torch.as_tensor(idxs[b], device=x["K"].device)
+            Ks = f64(x["K"][layer, b, sel])
+            Vs = f64(x["V"][layer, b, sel])
+            qn = f64(x["q"][layer, b])
+            t0 = time.perf_counter()
+            oracle.sparse_gqa_attention(qn, Ks, Vs, np.arange(len(idxs[b])))
+            t_attn += time.perf_counter() - t0
+        layers_done += 1
+        if t_score + t_attn > budget_s:
+            break
+    per_step = t_score + t_attn * w.n_layers / layers_done
+    return {
+        "value": 1.0 / per_step,
+        "unit": "steps/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"fp64 numpy oracle, one step of the same workload: scoring + top-k for all "
+                   f"{w.B} sequences, attention for {layers_done} of {w.n_layers} layers "
+                   f"(selected rows copied to host untimed), scaled to {w.n_layers} layers; "
+                   f"{t_score + t_attn:.1f} s of CPU work"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the decode step shards by sequence with no exchange; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2512_00722_amd as spec
+    from workloads import BENCH_WORKLOAD, WORKLOADS, algorithmic_bytes, generate
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    spec.load_library()
+    dev = torch.device("cuda:0")
+    name = args.workload or BENCH_WORKLOAD
+    w = WORKLOADS[name]
+    t_gen = time.perf_counter()
+    x = generate(w, seed=args.seed, device=dev)
+    torch.cuda.synchronize()
+    t_gen = time.perf_counter() - t_gen
+    print(f"[bench] workload {name} generated in {t_gen:.1f}s", file=sys.stderr, flush=True)
+
+    call = dict(q_r=x["q_r"], K_r=x["K_r"], seq_lens=x["seq_lens"], ks=x["ks"], q=x["q"],
+                K=x["K"], V=x["V"], k_max=w.k)
+    outputs = {}
+    res = spec.step(**call, outputs=outputs)
+    torch.cuda.synchronize()
+    ws = torch.zeros(spec.workspace_size(_dims_of(spec, w, x), spec.OP_STEP),
+                     dtype=torch.uint8, device=dev)
+
+    for _ in range(args.warmup):
+        spec.step(**call, outputs=outputs, ws=ws)
+    torch.cuda.synchronize()
+
+    # ---- timed region: exactly K steps between two device synchronisations
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    evs[0].record()
+    for i in range(args.steps):
+        spec.step(**call, outputs=outputs, ws=ws)
+        evs[i + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
+    ms_per_step = wall * 1e3 / args.steps
+    print(f"[bench] {args.steps} steps in {wall:.3f}s", file=sys.stderr, flush=True)
+
+    # ---- per-op times (same inputs, same stream), HIP events
+    counts = outputs["counts"].cpu().tolist()
+    seq = x["seq_lens"].cpu().tolist()
+    n_it = args.attn_iters
+    attn_out = torch.empty_like(outputs["out"])
+    dims_a = _dims_attn(spec, w, x, outputs)
+    ws_attn = torch.zeros(max(16, spec.workspace_size(dims_a, spec.OP_ATTN)), dtype=torch.uint8,
+                          device=dev)
+    scores = torch.empty((w.B, w.L_cap), dtype=torch.float32, device=dev)
+    t_ops = {"score": [], "topk": [], "attn": []}
+    for _ in range(n_it):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record()
+        spec.score(x["q_r"], x["K_r"], x["seq_lens"], out=scores)
+        e[1].record()
+        spec.topk(scores, x["seq_lens"], x["ks"], w.k, idx=outputs["idx"], counts=outputs["counts"])
+        e[2].record()
+        spec.sparse_decode_attn(x["q"], x["K"], x["V"], outputs["counts"], idx=outputs["idx"],
+                                out=attn_out, with_lse=False, ws=ws_attn)
+        e[3].record()
+        torch.cuda.synchronize()
+        t_ops["score"].append(e[0].elapsed_time(e[1]))
+        t_ops["topk"].append(e[1].elapsed_time(e[2]))
+        t_ops["attn"].append(e[2].elapsed_time(e[3]))
+    op_us = {k: 1e3 * statistics.mean(v) for k, v in t_ops.items()}
+
+    step_bytes = algorithmic_bytes(w, seq, x["ks"].cpu().tolist())
+    a_bytes = attn_bytes(w, counts)
+    attn_s = op_us["attn"] * 1e-6
+    achieved = a_bytes / attn_s / 1e9
+    traffic = stored_traffic()
+    value = args.steps / wall
+    line = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": name, "B": w.B, "L": w.L, "H_r": w.H_r, "d_r": w.d_r,
+                   "n_layers": w.n_layers, "H_q": w.H_q, "H_kv": w.H_kv, "d": w.d, "k": w.k},
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBPS, 4),
+            "traffic": traffic,
+            "kernel": "sparse GQA decode attention (attn_split_kernel + attn_combine_kernel)",
+            "bytes_per_launch": a_bytes,
+            "avg_launch_us": round(op_us["attn"], 2),
+        },
+        "step_hbm_gbps": round(step_bytes * value / 1e9, 1),
+        "step_frac_of_peak": round(step_bytes * value / 1e9 / PEAK_HBM_GBPS, 4),
+        "step_algorithmic_bytes": step_bytes,
+        "step_ms_median_events": round(statistics.median(step_ms), 4),
+        "op_us": {k: round(v, 2) for k, v in op_us.items()},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(w, x, res)
+    print(json.dumps(line), flush=True)
+
+
+def _dims_of(spec, w, x):
+    return spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, H_r=w.H_r, d_r=w.d_r,
+                          n_layers=w.n_layers, H_q=w.H_q, H_kv=w.H_kv, d=w.d,
+                          kr_stride_b=x["K_r"].stride(0), kv_stride_layer=x["K"].stride(0),
+                          kv_stride_b=x["K"].stride(1))
+
+
+def _dims_attn(spec, w, x, outputs):
+    return spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, n_layers=w.n_layers,
+                          H_q=w.H_q, H_kv=w.H_kv, d=w.d, kv_stride_layer=x["K"].stride(0),
+                          kv_stride_b=x["K"].stride(1))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,220 @@
+/*
+ * spec.h -- C ABI of the SpeContext decode-step hot path for MI355X (gfx950).
+ *
+ * SpeContext (arXiv 2512.00722) runs a lightweight retrieval head before the
+ * LLM: it keeps a full key cache K_r, forms attention weights for the current
+ * query after the Q/K projection, and selects the important tokens once per
+ * decode step (Sec. 4.3, "Implementation Details").  The LLM then attends
+ * only to the K/V rows at those tokens, gathered per KV head (Sec. 4.3,
+ * "Support for MHA"/"Support for GQA"); the same selection serves every layer
+ * (Sec. 7.2.1).  Elastic loading keeps the previous selection S_last and
+ * loads only S_now - S_last into the places of S_last - S_now (Sec. 5.4).
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ *  - bf16 tensors are passed as uint16_t bit patterns.  All tensor pointers
+ *    are DEVICE pointers; `spec_dims` and `spec_elastic` are host structs.
+ *  - Layouts are token-major and row-major:
+ *        q_r     [B][H_r][d_r]
+ *        K_r     [B][L_cap][H_r][d_r]        (sequence stride kr_stride_b)
+ *        q       [n_layers][B][H_q][d]
+ *        K, V    [n_layers][B][L_cap][H_kv][d] (strides kv_stride_layer,
+ *                                              kv_stride_b; the inner
+ *                                              [token][head][dim] block is
+ *                                              contiguous)
+ *        scores  [B][L_max] fp32
+ *        idx     [B][k_max] int32, out [n_layers][B][H_q][d] fp32,
+ *        lse     [n_layers][B][H_q] fp32.
+ *  - Per-sequence lengths live on the device and are clamped in the kernels,
+ *    not validated: L_b = min(seq_lens[b], L_max) (negative -> 0) and
+ *    k_b = min(ks[b], L_b, k_max) (negative -> 0).
+ *  - Ownership: the caller allocates every buffer, including the workspace
+ *    sized by spec_workspace_size().  The library never allocates, frees or
+ *    synchronises; every call only enqueues work on `stream` (a hipStream_t,
+ *    NULL = the null stream).  Outputs are valid once the stream reaches them.
+ *  - Alignment: bf16 tensors, `out` and the workspace must be 16-byte
+ *    aligned; int32/fp32 arrays (seq_lens, ks, scores, idx, counts, lse,
+ *    slot_tok, n_changed) 4-byte aligned.
+ *  - Errors: every argument check is done on the host BEFORE any HIP call,
+ *    so on error nothing is enqueued.  SPEC_ERR_INVALID: null pointer,
+ *    non-positive dimension, H_q % H_kv != 0, L_max > L_cap, k_max > L_max,
+ *    a misaligned pointer, a negative or non-finite scale, a stride not a
+ *    multiple of 8 elements or smaller than the block it steps over, a
+ *    non-zero `reserved`.  SPEC_ERR_UNSUPPORTED:
+ *    d != 128, d_r not 64 or 128, H_r > 16, G = H_q/H_kv not in
+ *    {1,2,4,8,16}, H_kv > 16, n_sets != 1, B or n_layers > 65535, and for
+ *    elastic loading L_cap > 245760.  SPEC_ERR_WORKSPACE: ws_bytes
+ *    below spec_workspace_size().  SPEC_ERR_HIP: a launch failed; the HIP
+ *    error code is kept (per thread) for spec_last_hip_error().
+ *  - Calls are reentrant; concurrent calls must not share a workspace.
+ */
+#ifndef SPEC_H_
+#define SPEC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPEC_API __attribute__((visibility("default")))
+
+typedef enum spec_status {
+  SPEC_OK = 0,
+  SPEC_ERR_INVALID = 1,
+  SPEC_ERR_UNSUPPORTED = 2,
+  SPEC_ERR_WORKSPACE = 3,
+  SPEC_ERR_HIP = 4
+} spec_status;
+
+typedef enum spec_op {
+  SPEC_OP_SCORE = 0,
+  SPEC_OP_TOPK = 1,
+  SPEC_OP_GATHER = 2,
+  SPEC_OP_ATTN = 3,
+  SPEC_OP_DELTA = 4,
+  SPEC_OP_STEP = 5
+} spec_op;
+
+/* A hipStream_t handle; NULL selects the null stream. */
+typedef void* spec_stream;
+
+/* Problem dimensions (host struct). */
+typedef struct spec_dims {
+  int32_t B;        /* sequences in the batch                                 */
+  int32_t L_cap;    /* token capacity of every cache row                      */
+  int32_t L_max;    /* host upper bound on seq_lens (sizes grids), <= L_cap   */
+  int32_t k_max;    /* host upper bound on ks (row length of idx), <= L_max   */
+  int32_t H_r;      /* retrieval-head heads                                   */
+  int32_t d_r;      /* retrieval-head head dimension (64 or 128)              */
+  int32_t n_layers; /* LLM layers attended with one selection                 */
+  int32_t H_q;      /* LLM query heads                                        */
+  int32_t H_kv;     /* LLM KV heads; query head h reads KV head h / (H_q/H_kv) */
+  int32_t d;        /* LLM head dimension (128)                               */
+  int64_t kr_stride_b;     /* elements between sequences of K_r; 0 = L_cap*H_r*d_r */
+  int64_t kv_stride_layer; /* elements between layers of K/V; 0 = B*kv_stride_b   */
+  int64_t kv_stride_b;     /* elements between sequences of K/V; 0 = L_cap*H_kv*d */
+  float scale_r;    /* retrieval softmax scale; 0 = 1/sqrt(d_r)               */
+  float scale;      /* LLM attention scale; 0 = 1/sqrt(d)                     */
+  int32_t n_sets;   /* index sets per sequence; must be 1 (one set shared by
+                       every head and layer)                                  */
+  int32_t reserved; /* must be 0                                              */
+} spec_dims;
+
+/* Device-resident elastic-loading state (host struct of device pointers).
+ *   slot_tok  [B][k_max] int32: token held by each slot, -1 = empty (S_last);
+ *   kbuf,vbuf [n_layers][B][k_max][H_kv][d] bf16: the rows held by the slots;
+ *   n_changed [B] int32 (output): rows loaded by the last update.           */
+typedef struct spec_elastic {
+  int32_t* slot_tok;
+  uint16_t* kbuf;
+  uint16_t* vbuf;
+  int32_t* n_changed;
+} spec_elastic;
+
+/* Retrieval scoring (Sec. 4.3 "Implementation Details"; Eq. 1 per head;
+ * batch-level mapping of Sec. 4.2).  For t < L_b:
+ *     l[h,t]      = scale_r * dot(q_r[b,h,:], K_r[b,t,h,:])
+ *     scores[b,t] = sum_h exp(l[h,t] - M_h) / Z_h,
+ * with M_h = max_t l[h,t] and Z_h = sum_t exp(l[h,t] - M_h) (softmax per head
+ * over all cached tokens, then the sum over heads).  scores[b,t] = -inf for
+ * L_b <= t < L_max.  Computed in fp32 from bf16 inputs.  Needs workspace
+ * spec_workspace_size(SPEC_OP_SCORE).                                       */
+SPEC_API spec_status spec_score(const spec_dims* dm, const uint16_t* q_r,
+                       const uint16_t* k_r, const int32_t* seq_lens,
+                       float* scores, void* ws, size_t ws_bytes,
+                       spec_stream stream);
+
+/* Token selection (Sec. 4.3: the important tokens are selected from the
+ * attention weights).  For each sequence, the k_b tokens t < L_b with the
+ * largest scores[b,t]; among equal scores the lower token index wins.
+ * idx[b, 0..k_b) receives them in ascending token order and idx[b, k_b..k_max)
+ * is set to -1.  counts (nullable) receives k_b.  The selection is exact on
+ * the fp32 keys.  Needs workspace spec_workspace_size(SPEC_OP_TOPK).          */
+SPEC_API spec_status spec_topk(const spec_dims* dm, const float* scores,
+                      const int32_t* seq_lens, const int32_t* ks,
+                      int32_t* idx, int32_t* counts, void* ws, size_t ws_bytes,
+                      spec_stream stream);
+
+/* Materialised KV gather (Sec. 4.3 "Support for MHA": the selected KV is
+ * loaded per head).  For every layer, sequence and j < counts[b]:
+ *     k_sel[l,b,j,:,:] = K[l,b,idx[b,j],:,:],  v_sel likewise,
+ * a bit-exact copy.  k_sel/v_sel are dense [n_layers][B][k_max][H_kv][d];
+ * rows j >= counts[b] are left unchanged.  idx entries must lie in [0, L_b);
+ * out-of-range entries are clamped into [0, L_cap).  No workspace.           */
+SPEC_API spec_status spec_gather(const spec_dims* dm, const uint16_t* k_cache,
+                        const uint16_t* v_cache, const int32_t* idx,
+                        const int32_t* counts, uint16_t* k_sel,
+                        uint16_t* v_sel, spec_stream stream);
+
+/* Sparse GQA decode attention (Eq. 1 over the selected rows; Sec. 4.3
+ * "Support for GQA": the G = H_q/H_kv query heads of a group share KV head
+ * g = h / G).  For every layer l, sequence b and query head h:
+ *     s_j = scale * dot(q[l,b,h,:], Kj[g,:]),   j < counts[b]
+ *     out[l,b,h,:] = sum_j softmax_j(s) * Vj[g,:],  lse[l,b,h] = log sum_j e^{s_j}
+ * Indexed mode (idx != NULL): Kj = K[l,b,idx[b,j]] read from the caches (the
+ * gather is fused; indices outside [0, L_cap) are clamped into it).
+ * Compact mode (idx == NULL): k/v are dense [n_layers][B][k_max][H_kv][d]
+ * buffers and Kj = k[l,b,j].  With counts[b] = 0 the output is 0 and lse is
+ * -inf.  fp32 accumulation and output; lse is nullable.  For one layer of a
+ * model, pass n_layers = 1 with layer-offset pointers.  Needs workspace
+ * spec_workspace_size(SPEC_OP_ATTN).                                        */
+SPEC_API spec_status spec_sparse_decode_attn(const spec_dims* dm, const uint16_t* q,
+                                    const uint16_t* k, const uint16_t* v,
+                                    const int32_t* idx, const int32_t* counts,
+                                    float* out, float* lse, void* ws,
+                                    size_t ws_bytes, spec_stream stream);
+
+/* Elastic loading on the device (Sec. 5.4).  S_now = idx_now[b, 0..c) with
+ * c = min(counts[b], k_max): distinct tokens in ascending order, as spec_topk
+ * writes them.  S_last = the tokens held in el->slot_tok[b, 0..k_max).  Slots
+ * whose token is not in S_now are freed; the tokens of S_now - S_last are
+ * copied, for every layer, K and V, from the caches into freed slots (the
+ * i-th smallest freed slot receives the i-th smallest new token); freed
+ * slots left over are set to -1.  With the budget c kept fixed between calls
+ * (the paper's |S_last| = |S_now|) slots [0, c) hold exactly S_now afterwards
+ * and the rest are -1; if c shrank so that a kept token sits at a slot >= c,
+ * the sequence is reloaded in full to restore that layout.
+ * el->n_changed[b] = number of rows loaded.  Start from slot_tok = -1
+ * everywhere for a full load.  Needs workspace
+ * spec_workspace_size(SPEC_OP_DELTA).                                       */
+SPEC_API spec_status spec_delta_gather(const spec_dims* dm, const int32_t* idx_now,
+                              const int32_t* counts, const uint16_t* k_cache,
+                              const uint16_t* v_cache, const spec_elastic* el,
+                              void* ws, size_t ws_bytes, spec_stream stream);
+
+/* One fused decode step: spec_score -> spec_topk -> [spec_delta_gather when
+ * el != NULL] -> spec_sparse_decode_attn (indexed over the caches, or compact
+ * over el->kbuf/vbuf when el != NULL), all enqueued on `stream` with no host
+ * synchronisation.  idx_out [B][k_max] and counts_out [B] receive the
+ * selection; out/lse as for spec_sparse_decode_attn (lse nullable);
+ * scores_out [B][L_max] (nullable) receives the retrieval scores.  Needs
+ * workspace spec_workspace_size(SPEC_OP_STEP).                              */
+SPEC_API spec_status spec_step(const spec_dims* dm, const uint16_t* q_r,
+                      const uint16_t* k_r, const int32_t* seq_lens,
+                      const int32_t* ks, const uint16_t* q,
+                      const uint16_t* k_cache, const uint16_t* v_cache,
+                      int32_t* idx_out, int32_t* counts_out, float* out,
+                      float* lse, float* scores_out, const spec_elastic* el,
+                      void* ws, size_t ws_bytes, spec_stream stream);
+
+/* Workspace bytes needed by `op` for dimensions `dm` (0 for SPEC_OP_GATHER).
+ * Returns the same validation status as the op itself.                      */
+SPEC_API spec_status spec_workspace_size(const spec_dims* dm, spec_op op,
+                                size_t* bytes);
+
+/* Static description of a status code (never NULL).                         */
+SPEC_API const char* spec_status_string(spec_status s);
+
+/* HIP error code of the last SPEC_ERR_HIP on the calling thread (0 = none). */
+SPEC_API int spec_last_hip_error(void);
+
+/* Library version string.                                                   */
+SPEC_API const char* spec_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPEC_H_ */

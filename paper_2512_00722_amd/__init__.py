@@ -1,0 +1,385 @@
+"""SpeContext decode-step hot path on MI355X: thin Python binding of libspecctx.
+
+Every step runs in the HIP kernels of libspecctx.so (gfx950); this module
+only marshals torch tensors (device memory, the current HIP stream) into the
+C ABI declared in include/spec.h.  There is no fallback: if the library is
+missing, importing the ops raises.
+
+    import paper_2512_00722_amd as spec
+    scores = spec.score(q_r, K_r, seq_lens)
+    idx, counts = spec.topk(scores, seq_lens, ks, k_max)
+    out, lse = spec.sparse_decode_attn(q, K, V, counts, idx=idx)
+    res = spec.step(q_r, K_r, seq_lens, ks, q, K, V, k_max)
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+__all__ = [
+    "SpecError", "load_library", "lib_path", "Dims", "workspace_size", "score", "topk",
+    "gather", "sparse_decode_attn", "delta_gather", "ElasticState", "step",
+    "OP_SCORE", "OP_TOPK", "OP_GATHER", "OP_ATTN", "OP_DELTA", "OP_STEP",
+    "EXPORTED_SYMBOLS",
+]
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+lib_path = os.path.join(_PKG, "libspecctx.so")
+
+OP_SCORE, OP_TOPK, OP_GATHER, OP_ATTN, OP_DELTA, OP_STEP = range(6)
+STATUS = {0: "SPEC_OK", 1: "SPEC_ERR_INVALID", 2: "SPEC_ERR_UNSUPPORTED",
+          3: "SPEC_ERR_WORKSPACE", 4: "SPEC_ERR_HIP"}
+
+EXPORTED_SYMBOLS = ["spec_score", "spec_topk", "spec_gather", "spec_sparse_decode_attn",
+                    "spec_delta_gather", "spec_step", "spec_workspace_size",
+                    "spec_status_string", "spec_last_hip_error", "spec_version"]
+
+
+class SpecError(RuntimeError):
+    def __init__(self, status: int, where: str, lib=None):
+        self.status = status
+        msg = STATUS.get(status, str(status))
+        if lib is not None:
+            msg += ": " + lib.spec_status_string(status).decode()
+            if status == 4:
+                msg += f" (hip error {lib.spec_last_hip_error()})"
+        super().__init__(f"{where}: {msg}")
+
+
+class Dims(ctypes.Structure):
+    """Mirror of `spec_dims` (include/spec.h)."""
+    _fields_ = [
+        ("B", ctypes.c_int32), ("L_cap", ctypes.c_int32), ("L_max", ctypes.c_int32),
+        ("k_max", ctypes.c_int32), ("H_r", ctypes.c_int32), ("d_r", ctypes.c_int32),
+        ("n_layers", ctypes.c_int32), ("H_q", ctypes.c_int32), ("H_kv", ctypes.c_int32),
+        ("d", ctypes.c_int32),
+        ("kr_stride_b", ctypes.c_int64), ("kv_stride_layer", ctypes.c_int64),
+        ("kv_stride_b", ctypes.c_int64),
+        ("scale_r", ctypes.c_float), ("scale", ctypes.c_float),
+        ("n_sets", ctypes.c_int32), ("reserved", ctypes.c_int32),
+    ]
+
+    @classmethod
+    def make(cls, B, L_cap, L_max, k_max, H_r=8, d_r=64, n_layers=1, H_q=8, H_kv=8, d=128,
+             kr_stride_b=0, kv_stride_layer=0, kv_stride_b=0, scale_r=0.0, scale=0.0,
+             n_sets=1):
+        return cls(B, L_cap, L_max, k_max, H_r, d_r, n_layers, H_q, H_kv, d, kr_stride_b,
+                   kv_stride_layer, kv_stride_b, scale_r, scale, n_sets, 0)
+
+
+class Elastic(ctypes.Structure):
+    """Mirror of `spec_elastic`."""
+    _fields_ = [("slot_tok", ctypes.c_void_p), ("kbuf", ctypes.c_void_p),
+                ("vbuf", ctypes.c_void_p), ("n_changed", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load_library(path: Optional[str] = None):
+    """Load libspecctx.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or lib_path
+    if not os.path.exists(p):
+        raise ImportError(f"{p} not found: build it with `python -m paper_2512_00722_amd.build` "
+                          "(or __graft_entry__.build())")
+    lib = ctypes.CDLL(p)
+    P, I, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    D = ctypes.POINTER(Dims)
+    E = ctypes.POINTER(Elastic)
+    sig = {
+        "spec_score": [D, P, P, P, P, P, S, P],
+        "spec_topk": [D, P, P, P, P, P, P, S, P],
+        "spec_gather": [D, P, P, P, P, P, P, P],
+        "spec_sparse_decode_attn": [D, P, P, P, P, P, P, P, P, S, P],
+        "spec_delta_gather": [D, P, P, P, P, E, P, S, P],
+        "spec_step": [D, P, P, P, P, P, P, P, P, P, P, P, P, E, P, S, P],
+        "spec_workspace_size": [D, I, ctypes.POINTER(S)],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = ctypes.c_int
+    lib.spec_status_string.argtypes = [ctypes.c_int]
+    lib.spec_status_string.restype = ctypes.c_char_p
+    lib.spec_last_hip_error.argtypes = []
+    lib.spec_last_hip_error.restype = ctypes.c_int
+    lib.spec_version.argtypes = []
+    lib.spec_version.restype = ctypes.c_char_p
+    if path is None:
+        _lib = lib
+    return lib
+
+
+# ------------------------------------------------------------------ helpers
+
+def _check(st: int, where: str):
+    if st != 0:
+        raise SpecError(st, where, _lib)
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, dtype, ndim: int):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got shape {tuple(t.shape)}")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor")
+
+
+def _inner_contig(t: torch.Tensor, name: str, n_inner: int):
+    """The last n_inner dims must be densely packed (row-major)."""
+    exp = 1
+    for dim in range(t.dim() - 1, t.dim() - 1 - n_inner, -1):
+        if t.shape[dim] != 1 and t.stride(dim) != exp:
+            raise ValueError(f"{name}: inner {n_inner} dims must be contiguous")
+        exp *= t.shape[dim]
+
+
+def _i32(t: torch.Tensor, name: str, n: int):
+    _need(t, name, torch.int32, 1)
+    if t.shape[0] != n or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous int32 [{n}] tensor")
+
+
+def workspace_size(dims: Dims, op: int) -> int:
+    lib = load_library()
+    n = ctypes.c_size_t(0)
+    _check(lib.spec_workspace_size(ctypes.byref(dims), op, ctypes.byref(n)), "spec_workspace_size")
+    return int(n.value)
+
+
+def _workspace(dims: Dims, op: int, device, ws: Optional[torch.Tensor]):
+    need = workspace_size(dims, op)
+    if ws is not None:
+        if ws.numel() * ws.element_size() < need:
+            raise ValueError(f"workspace too small: {need} bytes needed")
+        return ws, need
+    return torch.empty(max(need, 16), dtype=torch.uint8, device=device), need
+
+
+def _dims_retrieval(K_r: torch.Tensor, L_max: int, k_max: int, scale_r: float, **llm):
+    B, L_cap, H_r, d_r = K_r.shape
+    base = dict(n_layers=1, H_q=1, H_kv=1, d=128)
+    base.update(llm)
+    return Dims.make(B=B, L_cap=L_cap, L_max=L_max, k_max=k_max, H_r=H_r, d_r=d_r,
+                     kr_stride_b=K_r.stride(0), scale_r=scale_r, **base)
+
+
+# ------------------------------------------------------------------ ops
+
+def score(q_r: torch.Tensor, K_r: torch.Tensor, seq_lens: torch.Tensor,
+          L_max: Optional[int] = None, scale_r: float = 0.0,
+          out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Retrieval scores [B, L_max] fp32: softmax per head over the cached
+    tokens of q_r.K_r^T * scale_r, summed over heads; -inf beyond seq_lens."""
+    lib = load_library()
+    _need(q_r, "q_r", torch.bfloat16, 3)
+    _need(K_r, "K_r", torch.bfloat16, 4)
+    B, L_cap, H_r, d_r = K_r.shape
+    if tuple(q_r.shape) != (B, H_r, d_r) or not q_r.is_contiguous():
+        raise ValueError("q_r must be contiguous [B, H_r, d_r]")
+    _inner_contig(K_r, "K_r", 3)
+    _i32(seq_lens, "seq_lens", B)
+    L_max = L_cap if L_max is None else int(L_max)
+    dims = _dims_retrieval(K_r, L_max, 1, scale_r)
+    ws, nws = _workspace(dims, OP_SCORE, K_r.device, ws)
+    if out is None:
+        out = torch.empty((B, L_max), dtype=torch.float32, device=K_r.device)
+    _check(lib.spec_score(ctypes.byref(dims), _p(q_r), _p(K_r), _p(seq_lens), _p(out), _p(ws),
+                          nws, _stream(K_r)), "spec_score")
+    return out
+
+
+def topk(scores: torch.Tensor, seq_lens: torch.Tensor, ks: torch.Tensor, k_max: int,
+         idx: Optional[torch.Tensor] = None, counts: Optional[torch.Tensor] = None):
+    """Exact top-k of each score row (ties to the lower index), ascending
+    indices [B, k_max] int32 padded with -1, and counts [B] int32."""
+    lib = load_library()
+    _need(scores, "scores", torch.float32, 2)
+    if not scores.is_contiguous():
+        raise ValueError("scores must be contiguous")
+    B, L_max = scores.shape
+    _i32(seq_lens, "seq_lens", B)
+    _i32(ks, "ks", B)
+    dims = Dims.make(B=B, L_cap=L_max, L_max=L_max, k_max=int(k_max))
+    ws, nws = _workspace(dims, OP_TOPK, scores.device, None)
+    if idx is None:
+        idx = torch.empty((B, int(k_max)), dtype=torch.int32, device=scores.device)
+    if counts is None:
+        counts = torch.empty((B,), dtype=torch.int32, device=scores.device)
+    _check(lib.spec_topk(ctypes.byref(dims), _p(scores), _p(seq_lens), _p(ks), _p(idx),
+                         _p(counts), _p(ws), nws, _stream(scores)), "spec_topk")
+    return idx, counts
+
+
+def _dims_llm(q: torch.Tensor, K: torch.Tensor, k_max: int, scale: float, L_max=None, **extra):
+    n_layers, B, L_cap, H_kv, d = K.shape
+    _, _, H_q, _ = q.shape
+    return Dims.make(B=B, L_cap=L_cap, L_max=L_cap if L_max is None else L_max, k_max=k_max,
+                     n_layers=n_layers, H_q=H_q, H_kv=H_kv, d=d,
+                     kv_stride_layer=K.stride(0), kv_stride_b=K.stride(1), scale=scale, **extra)
+
+
+def _check_cache(K: torch.Tensor, V: torch.Tensor):
+    _need(K, "K", torch.bfloat16, 5)
+    _need(V, "V", torch.bfloat16, 5)
+    if K.shape != V.shape or K.stride() != V.stride():
+        raise ValueError("K and V must have the same shape and strides")
+    _inner_contig(K, "K", 3)
+
+
+def gather(K: torch.Tensor, V: torch.Tensor, idx: torch.Tensor, counts: torch.Tensor):
+    """Materialised gather: (K_sel, V_sel) [n_layers, B, k_max, H_kv, d] with
+    rows j < counts[b] = K/V[layer, b, idx[b, j]] (rows beyond are zero)."""
+    lib = load_library()
+    _check_cache(K, V)
+    n_layers, B, L_cap, H_kv, d = K.shape
+    _need(idx, "idx", torch.int32, 2)
+    k_max = idx.shape[1]
+    _i32(counts, "counts", B)
+    dims = Dims.make(B=B, L_cap=L_cap, L_max=L_cap, k_max=k_max, n_layers=n_layers, H_q=H_kv,
+                     H_kv=H_kv, d=d, kv_stride_layer=K.stride(0), kv_stride_b=K.stride(1))
+    ks = torch.zeros((n_layers, B, k_max, H_kv, d), dtype=torch.bfloat16, device=K.device)
+    vs = torch.zeros_like(ks)
+    _check(lib.spec_gather(ctypes.byref(dims), _p(K), _p(V), _p(idx.contiguous()), _p(counts),
+                           _p(ks), _p(vs), _stream(K)), "spec_gather")
+    return ks, vs
+
+
+def sparse_decode_attn(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, counts: torch.Tensor,
+                       idx: Optional[torch.Tensor] = None, scale: float = 0.0,
+                       out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                       with_lse: bool = True, ws: Optional[torch.Tensor] = None):
+    """GQA decode attention over the selected rows.  Indexed mode (idx given):
+    K/V are caches [n_layers, B, L_cap, H_kv, d].  Compact mode (idx None):
+    K/V are [n_layers, B, k_max, H_kv, d] and rows [0, counts[b]) are used.
+    Returns (out fp32 [n_layers, B, H_q, d], lse fp32 [n_layers, B, H_q] or None)."""
+    lib = load_library()
+    _need(q, "q", torch.bfloat16, 4)
+    _check_cache(K, V)
+    n_layers, B, L_cap, H_kv, d = K.shape
+    if q.shape[0] != n_layers or q.shape[1] != B or q.shape[3] != d or not q.is_contiguous():
+        raise ValueError("q must be contiguous [n_layers, B, H_q, d]")
+    _i32(counts, "counts", B)
+    if idx is not None:
+        _need(idx, "idx", torch.int32, 2)
+        idx = idx.contiguous()
+        k_max = idx.shape[1]
+        dims = _dims_llm(q, K, k_max, scale)
+    else:
+        k_max = L_cap
+        if not K.is_contiguous():
+            raise ValueError("compact K/V must be contiguous")
+        dims = _dims_llm(q, K, k_max, scale)
+    ws, nws = _workspace(dims, OP_ATTN, q.device, ws)
+    if out is None:
+        out = torch.empty((n_layers, B, q.shape[2], d), dtype=torch.float32, device=q.device)
+    if lse is None and with_lse:
+        lse = torch.empty((n_layers, B, q.shape[2]), dtype=torch.float32, device=q.device)
+    _check(lib.spec_sparse_decode_attn(ctypes.byref(dims), _p(q), _p(K), _p(V), _p(idx),
+                                       _p(counts), _p(out), _p(lse), _p(ws), nws, _stream(q)),
+           "spec_sparse_decode_attn")
+    return out, lse
+
+
+class ElasticState:
+    """Device-resident elastic-loading state: the slot->token map (S_last) and
+    the compact K/V rows it holds for every layer."""
+
+    def __init__(self, n_layers: int, B: int, k_max: int, H_kv: int, d: int, device):
+        self.slot_tok = torch.full((B, k_max), -1, dtype=torch.int32, device=device)
+        self.kbuf = torch.zeros((n_layers, B, k_max, H_kv, d), dtype=torch.bfloat16, device=device)
+        self.vbuf = torch.zeros_like(self.kbuf)
+        self.n_changed = torch.zeros((B,), dtype=torch.int32, device=device)
+
+    def reset(self):
+        self.slot_tok.fill_(-1)
+
+    def c_struct(self) -> Elastic:
+        return Elastic(self.slot_tok.data_ptr(), self.kbuf.data_ptr(), self.vbuf.data_ptr(),
+                       self.n_changed.data_ptr())
+
+
+def delta_gather(idx_now: torch.Tensor, counts: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
+                 state: ElasticState, L_max: Optional[int] = None):
+    """Elastic loading: copy only S_now - S_last rows into freed slots."""
+    lib = load_library()
+    _check_cache(K, V)
+    n_layers, B, L_cap, H_kv, d = K.shape
+    _need(idx_now, "idx_now", torch.int32, 2)
+    k_max = idx_now.shape[1]
+    _i32(counts, "counts", B)
+    if tuple(state.kbuf.shape) != (n_layers, B, k_max, H_kv, d):
+        raise ValueError("elastic state shape does not match")
+    dims = Dims.make(B=B, L_cap=L_cap, L_max=L_cap if L_max is None else L_max, k_max=k_max,
+                     n_layers=n_layers, H_q=H_kv, H_kv=H_kv, d=d,
+                     kv_stride_layer=K.stride(0), kv_stride_b=K.stride(1))
+    ws, nws = _workspace(dims, OP_DELTA, K.device, None)
+    el = state.c_struct()
+    _check(lib.spec_delta_gather(ctypes.byref(dims), _p(idx_now.contiguous()), _p(counts),
+                                 _p(K), _p(V), ctypes.byref(el), _p(ws), nws, _stream(K)),
+           "spec_delta_gather")
+    return state
+
+
+def step(q_r, K_r, seq_lens, ks, q, K, V, k_max: int, L_max: Optional[int] = None,
+         scale_r: float = 0.0, scale: float = 0.0, elastic: Optional[ElasticState] = None,
+         with_scores: bool = False, with_lse: bool = False, ws: Optional[torch.Tensor] = None,
+         outputs: Optional[dict] = None):
+    """One fused decode step (score -> top-k -> [elastic load] -> attention).
+    Returns a dict with idx, counts, out and optionally lse and scores."""
+    lib = load_library()
+    _need(q_r, "q_r", torch.bfloat16, 3)
+    _need(K_r, "K_r", torch.bfloat16, 4)
+    _need(q, "q", torch.bfloat16, 4)
+    _check_cache(K, V)
+    _inner_contig(K_r, "K_r", 3)
+    n_layers, B, L_cap_kv, H_kv, d = K.shape
+    _, L_cap_r, H_r, d_r = K_r.shape
+    if K_r.shape[0] != B or tuple(q_r.shape) != (B, H_r, d_r) or not q_r.is_contiguous():
+        raise ValueError("q_r / K_r shapes do not match")
+    if q.shape[0] != n_layers or q.shape[1] != B or q.shape[3] != d or not q.is_contiguous():
+        raise ValueError("q must be contiguous [n_layers, B, H_q, d]")
+    _i32(seq_lens, "seq_lens", B)
+    _i32(ks, "ks", B)
+    L_cap = min(L_cap_r, L_cap_kv)
+    L_max = L_cap if L_max is None else int(L_max)
+    dims = Dims.make(B=B, L_cap=L_cap, L_max=L_max, k_max=int(k_max), H_r=H_r, d_r=d_r,
+                     n_layers=n_layers, H_q=q.shape[2], H_kv=H_kv, d=d,
+                     kr_stride_b=K_r.stride(0), kv_stride_layer=K.stride(0),
+                     kv_stride_b=K.stride(1), scale_r=scale_r, scale=scale)
+    ws, nws = _workspace(dims, OP_STEP, q.device, ws)
+    dev = q.device
+    o = outputs if outputs is not None else {}
+    if "idx" not in o:
+        o["idx"] = torch.empty((B, int(k_max)), dtype=torch.int32, device=dev)
+        o["counts"] = torch.empty((B,), dtype=torch.int32, device=dev)
+        o["out"] = torch.empty((n_layers, B, q.shape[2], d), dtype=torch.float32, device=dev)
+        o["lse"] = (torch.empty((n_layers, B, q.shape[2]), dtype=torch.float32, device=dev)
+                    if with_lse else None)
+        o["scores"] = (torch.empty((B, L_max), dtype=torch.float32, device=dev)
+                       if with_scores else None)
+    el = elastic.c_struct() if elastic is not None else None
+    _check(lib.spec_step(ctypes.byref(dims), _p(q_r), _p(K_r), _p(seq_lens), _p(ks), _p(q),
+                         _p(K), _p(V), _p(o["idx"]), _p(o["counts"]), _p(o["out"]),
+                         _p(o.get("lse")), _p(o.get("scores")),
+                         ctypes.byref(el) if el is not None else None, _p(ws), nws,
+                         _stream(q)), "spec_step")
+    return o

@@ -1,0 +1,75 @@
+// Internal host-side interface between the C ABI layer and the kernel files.
+// Nothing here is exported from the shared library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace spec {
+
+// Dimensions after validation, with defaults resolved and derived values.
+struct Dims {
+  int B, L_cap, L_max, k_max;
+  int H_r, d_r;
+  int n_layers, H_q, H_kv, d, G;
+  int64_t kr_stride_b, kv_stride_layer, kv_stride_b;
+  float scale_r, scale;
+};
+
+// ---- workspace geometry (every region aligned to 256 bytes) -------------
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Retrieval scoring: tokens per workgroup of the logits kernel.
+constexpr int kScoreTokensPerBlock = 128;
+// Softmax/head-sum kernel: tokens per workgroup.
+constexpr int kSoftTokensPerBlock = 2048;
+
+inline int score_blocks(const Dims& d) {
+  return (d.L_max + kScoreTokensPerBlock - 1) / kScoreTokensPerBlock;
+}
+// logits [B][L_max][H_r] fp32 + per-block (max, sum) [B][n_blk][H_r][2] fp32
+inline size_t score_ws_bytes(const Dims& d) {
+  return align_up(sizeof(float) * (size_t)d.B * d.L_max * d.H_r) +
+         align_up(sizeof(float) * 2 * (size_t)d.B * score_blocks(d) * d.H_r);
+}
+
+inline size_t topk_ws_bytes(const Dims&) { return 0; }
+
+// Attention split size (tokens of the selection per wave work item).
+int attn_split_tokens(const Dims& d);
+inline int attn_n_split(const Dims& d) {
+  const int s = attn_split_tokens(d);
+  return (d.k_max + s - 1) / s;
+}
+// partial acc [n_layers*B][n_split][H_q][d] + (m, l) [n_layers*B][n_split][H_q][2]
+inline size_t attn_ws_bytes(const Dims& d) {
+  const size_t rows = (size_t)d.n_layers * d.B * attn_n_split(d) * d.H_q;
+  return align_up(sizeof(float) * rows * d.d) + align_up(sizeof(float) * rows * 2);
+}
+
+// Elastic loading: per sequence the list of (slot, token) copies.
+inline size_t delta_ws_bytes(const Dims& d) {
+  return align_up(sizeof(int32_t) * 2 * (size_t)d.B * d.k_max);
+}
+
+// ---- launchers (return the HIP launch status) --------------------------
+hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
+                        const int32_t* seq_lens, float* scores, void* ws,
+                        hipStream_t s);
+hipError_t launch_topk(const Dims& d, const float* scores, const int32_t* seq_lens,
+                       const int32_t* ks, int32_t* idx, int32_t* counts, void* ws,
+                       hipStream_t s);
+hipError_t launch_gather(const Dims& d, const uint16_t* k_cache, const uint16_t* v_cache,
+                         const int32_t* idx, const int32_t* counts, uint16_t* k_sel,
+                         uint16_t* v_sel, hipStream_t s);
+hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
+                       const uint16_t* v, const int32_t* idx, const int32_t* counts,
+                       float* out, float* lse, void* ws, hipStream_t s);
+hipError_t launch_delta(const Dims& d, const int32_t* idx_now, const int32_t* counts,
+                        const uint16_t* k_cache, const uint16_t* v_cache,
+                        int32_t* slot_tok, uint16_t* kbuf, uint16_t* vbuf,
+                        int32_t* n_changed, void* ws, hipStream_t s);
+
+}  // namespace spec

@@ -1,0 +1,183 @@
+// Retrieval scoring on gfx950 (SpeContext Sec. 4.3; Eq. 1 per retrieval head,
+// then the sum over heads of Sec. 4.2's batch-level mapping).
+//
+// Two launches:
+//  1. logits_kernel streams K_r once.  Each lane holds 8 bf16 of one
+//     (token, head) row slice in one 16-byte load; the d_r/8 lanes of a head
+//     reduce their partial dot products with cross-lane shuffles.  A
+//     workgroup covers 128 tokens; it writes the logits (log2 units, the
+//     scale and log2(e) folded into q_r) and its per-head (max, sum exp2).
+//  2. softmax_headsum_kernel merges the per-block pairs into each head's
+//     normaliser c_h = M_h + log2 Z_h and writes
+//     score[t] = sum_h exp2(l[h,t] - c_h), -inf beyond the sequence length.
+// The softmax needs every head's global max and sum before any score can be
+// formed, hence the logits round trip (1/(d_r/2) of the K_r bytes).
+#include "device_common.h"
+#include "internal.h"
+
+namespace spec {
+namespace {
+
+constexpr int T1 = kScoreTokensPerBlock;
+constexpr int T2 = kSoftTokensPerBlock;
+constexpr int kUnroll = 4;  // rows in flight per lane
+
+struct LogitsArgs {
+  const uint16_t* q_r;
+  const uint16_t* k_r;
+  const int32_t* seq_lens;
+  float* logits;  // [B][L_max][H_r], log2 units
+  float* part;    // [B][n_blk][H_r][2]: block max, block sum of exp2(l - max)
+  int64_t kr_stride_b;
+  int L_max, H_r, n_blk;
+  float qscale;   // scale_r * log2(e)
+};
+
+template <int LPH>  // lanes per head = d_r / 8
+__global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
+  constexpr int d_r = LPH * 8;
+  const int b = blockIdx.y;
+  const int blk = blockIdx.x;
+  const int L_b = clampi(a.seq_lens[b], 0, a.L_max);
+  const int t_begin = blk * T1;
+  if (t_begin >= L_b) return;  // uniform for the workgroup
+  const int n_tok = min(T1, L_b - t_begin);
+
+  const int cpt = a.H_r * LPH;  // 16-byte chunks per token row
+  const int tpi = 256 / cpt;    // tokens per pass of the workgroup
+  const int tid = threadIdx.x;
+  const int slot = tid / cpt;
+  const int c = tid - slot * cpt;
+  const int h = c / LPH;
+  const int part = c - h * LPH;
+
+  __shared__ float lg[T1 * 16];  // [token][head], H_r <= 16
+
+  if (slot < tpi) {  // whole LPH lane groups are in or out together
+    float qv[8];
+    unpack8(ldg16(a.q_r + ((size_t)b * a.H_r + h) * d_r + part * 8), qv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) qv[e] *= a.qscale;
+    const size_t row = (size_t)a.H_r * d_r;
+    const uint16_t* base =
+        a.k_r + (size_t)b * a.kr_stride_b + (size_t)t_begin * row + (size_t)h * d_r + part * 8;
+    float* lout = a.logits + ((size_t)b * a.L_max + t_begin) * a.H_r + h;
+    for (int i0 = slot; i0 < n_tok; i0 += tpi * kUnroll) {
+      uint4 kv[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int i = min(i0 + u * tpi, n_tok - 1);
+        kv[u] = ldg16_stream(base + (size_t)i * row);
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        float kf[8];
+        unpack8(kv[u], kf);
+        float acc = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc = fmaf(qv[e], kf[e], acc);
+#pragma unroll
+        for (int off = 1; off < LPH; off <<= 1) acc += __shfl_xor(acc, off, LPH);
+        const int i = i0 + u * tpi;
+        if (part == 0 && i < n_tok) {
+          lg[i * 16 + h] = acc;
+          lout[(size_t)i * a.H_r] = acc;
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // Per-head block maximum and sum of exp2(l - max): 16 lanes per head.
+  const int hh = tid >> 4;
+  const int j = tid & 15;
+  if (hh < a.H_r) {
+    float m = -INFINITY;
+    for (int i = j; i < n_tok; i += 16) m = fmaxf(m, lg[i * 16 + hh]);
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 16));
+    float s = 0.f;
+    for (int i = j; i < n_tok; i += 16) s += exp2f(lg[i * 16 + hh] - m);
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) s += __shfl_xor(s, off, 16);
+    if (j == 0) {
+      float* p = a.part + (((size_t)b * a.n_blk + blk) * a.H_r + hh) * 2;
+      p[0] = m;
+      p[1] = s;
+    }
+  }
+}
+
+struct SoftArgs {
+  const float* logits;
+  const float* part;
+  const int32_t* seq_lens;
+  float* scores;  // [B][L_max]
+  int L_max, H_r, n_blk;
+};
+
+__global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
+  const int b = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int t0 = blockIdx.x * T2;
+  const int t1 = min(t0 + T2, a.L_max);
+  const int L_b = clampi(a.seq_lens[b], 0, a.L_max);
+  float* out = a.scores + (size_t)b * a.L_max;
+  if (t0 >= L_b) {
+    for (int t = t0 + tid; t < t1; t += 256) out[t] = -INFINITY;
+    return;
+  }
+  __shared__ float c_h[16];
+  const int nb = (L_b + T1 - 1) / T1;
+  const int hh = tid >> 4;
+  const int j = tid & 15;
+  if (hh < a.H_r) {
+    float m = -INFINITY, s = 0.f;
+    for (int i = j; i < nb; i += 16) {
+      const float* p = a.part + (((size_t)b * a.n_blk + i) * a.H_r + hh) * 2;
+      ms_combine(m, s, p[0], p[1]);
+    }
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) {
+      const float m2 = __shfl_xor(m, off, 16);
+      const float s2 = __shfl_xor(s, off, 16);
+      ms_combine(m, s, m2, s2);
+    }
+    if (j == 0) c_h[hh] = m + log2f(s);
+  }
+  __syncthreads();
+  const int H_r = a.H_r;
+  for (int t = t0 + tid; t < t1; t += 256) {
+    float sc = -INFINITY;
+    if (t < L_b) {
+      const float* l = a.logits + ((size_t)b * a.L_max + t) * H_r;
+      sc = 0.f;
+      for (int h = 0; h < H_r; ++h) sc += exp2f(l[h] - c_h[h]);
+    }
+    out[t] = sc;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
+                        const int32_t* seq_lens, float* scores, void* ws,
+                        hipStream_t s) {
+  const int n_blk = score_blocks(d);
+  float* logits = static_cast<float*>(ws);
+  float* part = reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                         align_up(sizeof(float) * (size_t)d.B * d.L_max * d.H_r));
+  LogitsArgs la{q_r, k_r, seq_lens, logits, part, d.kr_stride_b,
+                d.L_max, d.H_r, n_blk, d.scale_r * kLog2e};
+  const dim3 g1(n_blk, d.B);
+  if (d.d_r == 64)
+    logits_kernel<8><<<g1, 256, 0, s>>>(la);
+  else
+    logits_kernel<16><<<g1, 256, 0, s>>>(la);
+  SoftArgs sa{logits, part, seq_lens, scores, d.L_max, d.H_r, n_blk};
+  const dim3 g2((d.L_max + T2 - 1) / T2, d.B);
+  softmax_headsum_kernel<<<g2, 256, 0, s>>>(sa);
+  return hipGetLastError();
+}
+
+}  // namespace spec

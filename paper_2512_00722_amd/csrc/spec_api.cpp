@@ -1,0 +1,261 @@
+// C ABI of the decode-step hot path: argument validation (host only, before
+// any HIP call), workspace carve-up and kernel dispatch on the caller's
+// stream.  The library holds no state except a per-thread last HIP error.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "../../include/spec.h"
+#include "internal.h"
+
+namespace spec {
+size_t elastic_plan_lds_bytes(const Dims& d);
+}
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+constexpr int kMaxElasticLcap = 245760;  // two LDS bitmaps of L_cap bits <= 60 KiB
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+bool is_pow2_group(int g) { return g == 1 || g == 2 || g == 4 || g == 8 || g == 16; }
+
+spec_status resolve(const spec_dims* dm, spec::Dims* o) {
+  if (!dm) return SPEC_ERR_INVALID;
+  if (dm->B <= 0 || dm->L_cap <= 0 || dm->L_max <= 0 || dm->k_max <= 0 || dm->H_r <= 0 ||
+      dm->d_r <= 0 || dm->n_layers <= 0 || dm->H_q <= 0 || dm->H_kv <= 0 || dm->d <= 0)
+    return SPEC_ERR_INVALID;
+  if (dm->reserved != 0) return SPEC_ERR_INVALID;
+  if (dm->L_max > dm->L_cap || dm->k_max > dm->L_max) return SPEC_ERR_INVALID;
+  if (dm->H_q % dm->H_kv != 0) return SPEC_ERR_INVALID;
+  if (dm->kr_stride_b < 0 || dm->kv_stride_layer < 0 || dm->kv_stride_b < 0)
+    return SPEC_ERR_INVALID;
+  if (!(isfinite(dm->scale_r) && isfinite(dm->scale)) || dm->scale_r < 0.f || dm->scale < 0.f)
+    return SPEC_ERR_INVALID;
+  if (dm->n_sets != 1) return SPEC_ERR_UNSUPPORTED;
+  if (dm->d != 128) return SPEC_ERR_UNSUPPORTED;
+  if (dm->d_r != 64 && dm->d_r != 128) return SPEC_ERR_UNSUPPORTED;
+  if (dm->H_r > 16) return SPEC_ERR_UNSUPPORTED;
+  if (dm->H_kv > 16) return SPEC_ERR_UNSUPPORTED;
+  if (!is_pow2_group(dm->H_q / dm->H_kv)) return SPEC_ERR_UNSUPPORTED;
+  if (dm->B > 65535 || dm->n_layers > 65535) return SPEC_ERR_UNSUPPORTED;
+
+  const int64_t kr_row = (int64_t)dm->L_cap * dm->H_r * dm->d_r;
+  const int64_t kv_row = (int64_t)dm->L_cap * dm->H_kv * dm->d;
+  o->B = dm->B;
+  o->L_cap = dm->L_cap;
+  o->L_max = dm->L_max;
+  o->k_max = dm->k_max;
+  o->H_r = dm->H_r;
+  o->d_r = dm->d_r;
+  o->n_layers = dm->n_layers;
+  o->H_q = dm->H_q;
+  o->H_kv = dm->H_kv;
+  o->d = dm->d;
+  o->G = dm->H_q / dm->H_kv;
+  o->kr_stride_b = dm->kr_stride_b ? dm->kr_stride_b : kr_row;
+  o->kv_stride_b = dm->kv_stride_b ? dm->kv_stride_b : kv_row;
+  o->kv_stride_layer = dm->kv_stride_layer ? dm->kv_stride_layer : (int64_t)dm->B * o->kv_stride_b;
+  if (o->kr_stride_b < kr_row || o->kr_stride_b % 8) return SPEC_ERR_INVALID;
+  if (o->kv_stride_b < kv_row || o->kv_stride_b % 8) return SPEC_ERR_INVALID;
+  if (o->kv_stride_layer < kv_row || o->kv_stride_layer % 8) return SPEC_ERR_INVALID;
+  o->scale_r = dm->scale_r > 0.f ? dm->scale_r : 1.0f / sqrtf((float)dm->d_r);
+  o->scale = dm->scale > 0.f ? dm->scale : 1.0f / sqrtf((float)dm->d);
+  return SPEC_OK;
+}
+
+size_t ws_bytes_for(const spec::Dims& d, spec_op op) {
+  switch (op) {
+    case SPEC_OP_SCORE: return spec::score_ws_bytes(d);
+    case SPEC_OP_TOPK: return spec::topk_ws_bytes(d);
+    case SPEC_OP_GATHER: return 0;
+    case SPEC_OP_ATTN: return spec::attn_ws_bytes(d);
+    case SPEC_OP_DELTA: return spec::delta_ws_bytes(d);
+    case SPEC_OP_STEP:
+      return spec::align_up(sizeof(float) * (size_t)d.B * d.L_max) + spec::score_ws_bytes(d) +
+             spec::topk_ws_bytes(d) + spec::attn_ws_bytes(d) + spec::delta_ws_bytes(d);
+  }
+  return 0;
+}
+
+spec_status check_ws(const spec::Dims& d, spec_op op, const void* ws, size_t ws_bytes) {
+  const size_t need = ws_bytes_for(d, op);
+  if (need == 0) return SPEC_OK;
+  if (!ws || ws_bytes < need) return SPEC_ERR_WORKSPACE;
+  if (!aligned16(ws)) return SPEC_ERR_INVALID;
+  return SPEC_OK;
+}
+
+spec_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return SPEC_OK;
+  g_last_hip_error = (int)e;
+  return SPEC_ERR_HIP;
+}
+
+hipStream_t as_stream(spec_stream s) { return reinterpret_cast<hipStream_t>(s); }
+
+spec_status check_elastic(const spec::Dims& d, const spec_elastic* el) {
+  if (!el || !el->slot_tok || !el->kbuf || !el->vbuf || !el->n_changed) return SPEC_ERR_INVALID;
+  if (!aligned4(el->slot_tok) || !aligned4(el->n_changed) || !aligned16(el->kbuf) ||
+      !aligned16(el->vbuf))
+    return SPEC_ERR_INVALID;
+  if (d.L_cap > kMaxElasticLcap) return SPEC_ERR_UNSUPPORTED;
+  return SPEC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+spec_status spec_workspace_size(const spec_dims* dm, spec_op op, size_t* bytes) {
+  if (!bytes) return SPEC_ERR_INVALID;
+  if ((int)op < SPEC_OP_SCORE || (int)op > SPEC_OP_STEP) return SPEC_ERR_INVALID;
+  spec::Dims d;
+  const spec_status st = resolve(dm, &d);
+  if (st != SPEC_OK) return st;
+  *bytes = ws_bytes_for(d, op);
+  return SPEC_OK;
+}
+
+spec_status spec_score(const spec_dims* dm, const uint16_t* q_r, const uint16_t* k_r,
+                       const int32_t* seq_lens, float* scores, void* ws, size_t ws_bytes,
+                       spec_stream stream) {
+  spec::Dims d;
+  spec_status st = resolve(dm, &d);
+  if (st != SPEC_OK) return st;
+  if (!q_r || !k_r || !seq_lens || !scores) return SPEC_ERR_INVALID;
+  if (!aligned16(q_r) || !aligned16(k_r) || !aligned4(seq_lens) || !aligned4(scores))
+    return SPEC_ERR_INVALID;
+  if ((st = check_ws(d, SPEC_OP_SCORE, ws, ws_bytes)) != SPEC_OK) return st;
+  return hip_status(spec::launch_score(d, q_r, k_r, seq_lens, scores, ws, as_stream(stream)));
+}
+
+spec_status spec_topk(const spec_dims* dm, const float* scores, const int32_t* seq_lens,
+                      const int32_t* ks, int32_t* idx, int32_t* counts, void* ws,
+                      size_t ws_bytes, spec_stream stream) {
+  spec::Dims d;
+  spec_status st = resolve(dm, &d);
+  if (st != SPEC_OK) return st;
+  if (!scores || !seq_lens || !ks || !idx) return SPEC_ERR_INVALID;
+  if (!aligned4(scores) || !aligned4(seq_lens) || !aligned4(ks) || !aligned4(idx) ||
+      (counts && !aligned4(counts)))
+    return SPEC_ERR_INVALID;
+  if ((st = check_ws(d, SPEC_OP_TOPK, ws, ws_bytes)) != SPEC_OK) return st;
+  return hip_status(
+      spec::launch_topk(d, scores, seq_lens, ks, idx, counts, ws, as_stream(stream)));
+}
+
+spec_status spec_gather(const spec_dims* dm, const uint16_t* k_cache, const uint16_t* v_cache,
+                        const int32_t* idx, const int32_t* counts, uint16_t* k_sel,
+                        uint16_t* v_sel, spec_stream stream) {
+  spec::Dims d;
+  spec_status st = resolve(dm, &d);
+  if (st != SPEC_OK) return st;
+  if (!k_cache || !v_cache || !idx || !counts || !k_sel || !v_sel) return SPEC_ERR_INVALID;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(k_sel) || !aligned16(v_sel) ||
+      !aligned4(idx) || !aligned4(counts))
+    return SPEC_ERR_INVALID;
+  return hip_status(
+      spec::launch_gather(d, k_cache, v_cache, idx, counts, k_sel, v_sel, as_stream(stream)));
+}
+
+spec_status spec_sparse_decode_attn(const spec_dims* dm, const uint16_t* q, const uint16_t* k,
+                                    const uint16_t* v, const int32_t* idx,
+                                    const int32_t* counts, float* out, float* lse, void* ws,
+                                    size_t ws_bytes, spec_stream stream) {
+  spec::Dims d;
+  spec_status st = resolve(dm, &d);
+  if (st != SPEC_OK) return st;
+  if (!q || !k || !v || !counts || !out) return SPEC_ERR_INVALID;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned4(counts) ||
+      !aligned16(out) || (idx && !aligned4(idx)) || (lse && !aligned4(lse)))
+    return SPEC_ERR_INVALID;
+  if ((st = check_ws(d, SPEC_OP_ATTN, ws, ws_bytes)) != SPEC_OK) return st;
+  return hip_status(
+      spec::launch_attn(d, q, k, v, idx, counts, out, lse, ws, as_stream(stream)));
+}
+
+spec_status spec_delta_gather(const spec_dims* dm, const int32_t* idx_now,
+                              const int32_t* counts, const uint16_t* k_cache,
+                              const uint16_t* v_cache, const spec_elastic* el, void* ws,
+                              size_t ws_bytes, spec_stream stream) {
+  spec::Dims d;
+  spec_status st = resolve(dm, &d);
+  if (st != SPEC_OK) return st;
+  if (!idx_now || !counts || !k_cache || !v_cache) return SPEC_ERR_INVALID;
+  if (!aligned4(idx_now) || !aligned4(counts) || !aligned16(k_cache) || !aligned16(v_cache))
+    return SPEC_ERR_INVALID;
+  if ((st = check_elastic(d, el)) != SPEC_OK) return st;
+  if ((st = check_ws(d, SPEC_OP_DELTA, ws, ws_bytes)) != SPEC_OK) return st;
+  return hip_status(spec::launch_delta(d, idx_now, counts, k_cache, v_cache, el->slot_tok,
+                                       el->kbuf, el->vbuf, el->n_changed, ws,
+                                       as_stream(stream)));
+}
+
+spec_status spec_step(const spec_dims* dm, const uint16_t* q_r, const uint16_t* k_r,
+                      const int32_t* seq_lens, const int32_t* ks, const uint16_t* q,
+                      const uint16_t* k_cache, const uint16_t* v_cache, int32_t* idx_out,
+                      int32_t* counts_out, float* out, float* lse, float* scores_out,
+                      const spec_elastic* el, void* ws, size_t ws_bytes,
+                      spec_stream stream) {
+  spec::Dims d;
+  spec_status st = resolve(dm, &d);
+  if (st != SPEC_OK) return st;
+  if (!q_r || !k_r || !seq_lens || !ks || !q || !k_cache || !v_cache || !idx_out ||
+      !counts_out || !out)
+    return SPEC_ERR_INVALID;
+  if (!aligned16(q_r) || !aligned16(k_r) || !aligned4(seq_lens) || !aligned4(ks) ||
+      !aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned4(idx_out) ||
+      !aligned4(counts_out) || !aligned16(out) || (lse && !aligned4(lse)) ||
+      (scores_out && !aligned4(scores_out)))
+    return SPEC_ERR_INVALID;
+  if (el && (st = check_elastic(d, el)) != SPEC_OK) return st;
+  if ((st = check_ws(d, SPEC_OP_STEP, ws, ws_bytes)) != SPEC_OK) return st;
+
+  char* p = static_cast<char*>(ws);
+  float* scores = reinterpret_cast<float*>(p);
+  p += spec::align_up(sizeof(float) * (size_t)d.B * d.L_max);
+  if (scores_out) scores = scores_out;
+  void* ws_score = p;
+  p += spec::score_ws_bytes(d);
+  void* ws_topk = p;
+  p += spec::topk_ws_bytes(d);
+  void* ws_attn = p;
+  p += spec::attn_ws_bytes(d);
+  void* ws_delta = p;
+
+  const hipStream_t s = as_stream(stream);
+  hipError_t e = spec::launch_score(d, q_r, k_r, seq_lens, scores, ws_score, s);
+  if (e != hipSuccess) return hip_status(e);
+  e = spec::launch_topk(d, scores, seq_lens, ks, idx_out, counts_out, ws_topk, s);
+  if (e != hipSuccess) return hip_status(e);
+  if (el) {
+    e = spec::launch_delta(d, idx_out, counts_out, k_cache, v_cache, el->slot_tok, el->kbuf,
+                           el->vbuf, el->n_changed, ws_delta, s);
+    if (e != hipSuccess) return hip_status(e);
+    e = spec::launch_attn(d, q, el->kbuf, el->vbuf, nullptr, counts_out, out, lse, ws_attn, s);
+  } else {
+    e = spec::launch_attn(d, q, k_cache, v_cache, idx_out, counts_out, out, lse, ws_attn, s);
+  }
+  return hip_status(e);
+}
+
+const char* spec_status_string(spec_status s) {
+  switch (s) {
+    case SPEC_OK: return "ok";
+    case SPEC_ERR_INVALID: return "invalid argument";
+    case SPEC_ERR_UNSUPPORTED: return "unsupported dimensions";
+    case SPEC_ERR_WORKSPACE: return "workspace missing or too small";
+    case SPEC_ERR_HIP: return "HIP launch failed";
+  }
+  return "unknown status";
+}
+
+int spec_last_hip_error(void) { return g_last_hip_error; }
+
+const char* spec_version(void) { return "specctx 0.1.0 (gfx950)"; }
+
+}  // extern "C"

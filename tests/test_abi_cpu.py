@@ -1,0 +1,135 @@
+"""The C ABI on a host without a GPU: the library loads, exports every symbol
+include/spec.h declares, and rejects bad arguments before any HIP call
+(fake pointers are never dereferenced because validation fails first)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2512_00722_amd as spec
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(spec.lib_path):
+        pytest.fail("libspecctx.so is not built (run __graft_entry__.build())")
+    return spec.load_library()
+
+
+def header_functions():
+    txt = open(os.path.join(ROOT, "include", "spec.h")).read()
+    return re.findall(r"SPEC_API\s+[\w\s\*]+?\b(spec_\w+)\s*\(", txt)
+
+
+def test_exports_every_declared_symbol(lib):
+    declared = header_functions()
+    assert len(declared) >= 10
+    assert sorted(declared) == sorted(spec.EXPORTED_SYMBOLS)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings(lib):
+    assert b"gfx950" in lib.spec_version()
+    for s in range(5):
+        assert lib.spec_status_string(s)
+    assert lib.spec_status_string(99) == b"unknown status"
+    assert lib.spec_last_hip_error() == 0
+
+
+FAKE = ctypes.c_void_p(0x7000_0000_0000)     # 16-byte aligned, never dereferenced
+FAKE_ODD = ctypes.c_void_p(0x7000_0000_0008)  # 8-byte aligned only
+
+
+def good_dims(**kw):
+    base = dict(B=2, L_cap=256, L_max=256, k_max=32, H_r=8, d_r=64, n_layers=2, H_q=32, H_kv=8, d=128)
+    base.update(kw)
+    return spec.Dims.make(**base)
+
+
+def ws_size(lib, dims, op):
+    n = ctypes.c_size_t(0)
+    st = lib.spec_workspace_size(ctypes.byref(dims), op, ctypes.byref(n))
+    return st, n.value
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("B", 0, 1), ("L_cap", -1, 1), ("k_max", 0, 1), ("H_r", 0, 1), ("d", 0, 1),
+    ("L_max", 300, 1),          # L_max > L_cap
+    ("k_max", 257, 1),          # k_max > L_max
+    ("H_q", 30, 1),             # H_q % H_kv != 0
+    ("d", 64, 2), ("d_r", 32, 2), ("H_r", 17, 2), ("H_kv", 32, 2),
+    ("H_q", 24, 2),             # G = 3
+    ("n_sets", 8, 2),
+    ("reserved", 1, 1),
+    ("kv_stride_b", 12, 1),     # smaller than a sequence's block
+    ("kr_stride_b", 256 * 8 * 64 + 3, 1),  # not a multiple of 8
+    ("scale", -1.0, 1),
+])
+def test_dims_validation(lib, field, value, status):
+    d = good_dims()
+    setattr(d, field, value)
+    for op in range(6):
+        st, _ = ws_size(lib, d, op)
+        assert st == status, (field, op, st)
+
+
+def test_workspace_sizes(lib):
+    d = good_dims()
+    sizes = {op: ws_size(lib, d, op) for op in range(6)}
+    assert all(st == 0 for st, _ in sizes.values())
+    assert sizes[spec.OP_GATHER][1] == 0
+    assert sizes[spec.OP_SCORE][1] >= 2 * 256 * 8 * 4        # the logits
+    assert sizes[spec.OP_STEP][1] >= sizes[spec.OP_SCORE][1] + sizes[spec.OP_ATTN][1]
+    assert lib.spec_workspace_size(None, 0, ctypes.byref(ctypes.c_size_t())) == 1
+    assert lib.spec_workspace_size(ctypes.byref(d), 9, ctypes.byref(ctypes.c_size_t())) == 1
+
+
+def test_entry_points_reject_before_hip(lib):
+    d = good_dims()
+    _, nws = ws_size(lib, d, spec.OP_STEP)
+    byref = ctypes.byref
+    # null pointers
+    assert lib.spec_score(byref(d), None, FAKE, FAKE, FAKE, FAKE, nws, None) == 1
+    assert lib.spec_topk(byref(d), FAKE, FAKE, None, FAKE, None, FAKE, nws, None) == 1
+    assert lib.spec_gather(byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == 1
+    assert lib.spec_sparse_decode_attn(byref(d), FAKE, FAKE, FAKE, None, None, FAKE, None,
+                                       FAKE, nws, None) == 1
+    # misaligned bf16 tensor
+    assert lib.spec_score(byref(d), FAKE_ODD, FAKE, FAKE, FAKE, FAKE, nws, None) == 1
+    assert lib.spec_sparse_decode_attn(byref(d), FAKE, FAKE_ODD, FAKE, FAKE, FAKE, FAKE, None,
+                                       FAKE, nws, None) == 1
+    # workspace missing or too small
+    assert lib.spec_score(byref(d), FAKE, FAKE, FAKE, FAKE, None, 0, None) == 3
+    assert lib.spec_sparse_decode_attn(byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                       FAKE, 16, None) == 3
+    assert lib.spec_step(byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                         None, None, None, FAKE, 64, None) == 3
+    # unsupported dims on every entry point
+    bad = good_dims(d=96)
+    assert lib.spec_score(byref(bad), FAKE, FAKE, FAKE, FAKE, FAKE, nws, None) == 2
+    assert lib.spec_step(byref(bad), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                         None, None, None, FAKE, nws, None) == 2
+    # elastic state with a null member
+    el = spec.Elastic(FAKE.value, FAKE.value, None, FAKE.value)
+    assert lib.spec_delta_gather(byref(d), FAKE, FAKE, FAKE, FAKE, byref(el), FAKE, nws,
+                                 None) == 1
+    # elastic loading caps L_cap
+    big = good_dims(L_cap=300000, L_max=300000)
+    el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value)
+    assert lib.spec_delta_gather(byref(big), FAKE, FAKE, FAKE, FAKE, byref(el), FAKE, 1 << 40,
+                                 None) == 2
+    assert lib.spec_last_hip_error() == 0
+
+
+def test_python_wrappers_refuse_cpu_tensors(lib):
+    import torch
+    q_r = torch.zeros((1, 8, 64), dtype=torch.bfloat16)
+    K_r = torch.zeros((1, 64, 8, 64), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        spec.score(q_r, K_r, torch.zeros(1, dtype=torch.int32))
+    with pytest.raises(TypeError):
+        spec.score(q_r.float(), K_r, torch.zeros(1, dtype=torch.int32))

@@ -1,0 +1,358 @@
+"""HIP path vs the fp64 oracle, element by element, at sizes the oracle
+finishes in seconds (several tiles plus ragged tails).  Calls go through the
+C ABI via the thin Python binding."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2512_00722_amd as spec
+from tests.gpu_helpers import SCORE_ABS, SCORE_REL, TOL_ATTN, announce, f64, need_gpu
+from workloads import generate, small_workload
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return need_gpu()
+
+
+def _rand_bf16(shape, gen, scale=1.0):
+    return (torch.randn(shape, generator=gen) * scale).to(torch.bfloat16)
+
+
+# ------------------------------------------------------------------ scoring
+
+SCORE_CASES = [
+    # B, L_cap, L_max, H_r, d_r, seq_lens
+    (1, 130, 130, 1, 64, [130]),
+    (2, 300, 300, 2, 64, [300, 1]),
+    (3, 1000, 1000, 8, 64, [1000, 777, 129]),
+    (2, 700, 640, 16, 64, [640, 513]),
+    (2, 520, 520, 8, 128, [520, 200]),
+    (1, 400, 400, 16, 128, [0]),
+    (4, 2500, 2400, 8, 64, [2400, 2048, 2047, 2049]),
+]
+
+
+@pytest.mark.parametrize("case", SCORE_CASES, ids=[str(c[:5]) for c in SCORE_CASES])
+def test_score_parity(dev, case):
+    B, L_cap, L_max, H_r, d_r, lens = case
+    announce(f"score {case}")
+    g = torch.Generator().manual_seed(1000 + B * L_cap + H_r)
+    q_r = _rand_bf16((B, H_r, d_r), g)
+    K_r = _rand_bf16((B, L_cap, H_r, d_r), g, 1.5)
+    seq = torch.tensor(lens, dtype=torch.int32)
+    got = spec.score(q_r.to(dev), K_r.to(dev), seq.to(dev), L_max=L_max)
+    torch.cuda.synchronize()
+    got = got.cpu().numpy().astype(np.float64)
+    qn, Kn = f64(q_r), f64(K_r)
+    for b in range(B):
+        L = min(lens[b], L_max)
+        want = oracle.retrieval_scores(qn[b], Kn[b], L)
+        err = np.abs(got[b, :L] - want)
+        assert np.all(err <= SCORE_ABS + SCORE_REL * want), (b, err.max())
+        assert np.all(np.isneginf(got[b, L:]))
+        if L:
+            assert abs(got[b, :L].sum() - H_r) < 1e-4 * H_r
+
+
+def test_score_strided_kr(dev):
+    """K_r as a slice of a larger buffer (sequence stride > L_cap*H_r*d_r)."""
+    announce("score strided")
+    g = torch.Generator().manual_seed(7)
+    big = _rand_bf16((3, 600, 8, 64), g)
+    K_r = big[:, :500]
+    q_r = _rand_bf16((3, 8, 64), g)
+    seq = torch.tensor([500, 499, 300], dtype=torch.int32)
+    got = spec.score(q_r.to(dev), big.to(dev)[:, :500], seq.to(dev)).cpu().numpy()
+    for b in range(3):
+        want = oracle.retrieval_scores(f64(q_r)[b], f64(K_r)[b], int(seq[b]))
+        np.testing.assert_allclose(got[b, :int(seq[b])], want, rtol=SCORE_REL, atol=SCORE_ABS)
+
+
+# ------------------------------------------------------------------ top-k
+
+def _topk_rows(kind, B, L, g):
+    if kind == "random":
+        return torch.rand((B, L), generator=g)
+    if kind == "ties":          # few distinct values: many exact ties
+        return torch.randint(0, 5, (B, L), generator=g).float() / 4.0
+    if kind == "equal":
+        return torch.full((B, L), 0.125)
+    if kind == "signed":        # negative keys and -inf too
+        x = torch.randn((B, L), generator=g)
+        x[:, ::7] = -float("inf")
+        return x
+    if kind == "narrow":        # scores packed in a narrow band (one radix bin)
+        return 1e-4 * (1.0 + 1e-6 * torch.randint(0, 300, (B, L), generator=g).float())
+    raise ValueError(kind)
+
+
+TOPK_CASES = [
+    # kind, B, L_max, k_max, seq_lens, ks
+    ("random", 2, 5000, 700, [5000, 4097], [700, 1]),
+    ("ties", 3, 3000, 512, [3000, 2999, 100], [512, 511, 100]),
+    ("equal", 2, 4096, 300, [4096, 300], [300, 300]),
+    ("signed", 2, 1500, 200, [1500, 1499], [200, 37]),
+    ("narrow", 2, 9000, 1000, [9000, 8191], [1000, 999]),
+    ("random", 4, 1024, 1024, [1024, 0, 5, 1024], [1024, 3, 9, 0]),
+    ("random", 1, 32768, 2048, [32768], [2048]),
+    ("ties", 1, 40000, 4096, [40000], [4096]),
+]
+
+
+@pytest.mark.parametrize("case", TOPK_CASES, ids=[f"{c[0]}-{c[2]}-{c[3]}" for c in TOPK_CASES])
+def test_topk_exact(dev, case):
+    """Same fp32 keys on both sides: the index sets must match bit-exactly,
+    including the -1 padding and the counts."""
+    kind, B, L_max, k_max, lens, ks = case
+    announce(f"topk {case[:4]}")
+    g = torch.Generator().manual_seed(B * L_max + k_max)
+    sc = _topk_rows(kind, B, L_max, g).float()
+    seq = torch.tensor(lens, dtype=torch.int32)
+    kt = torch.tensor(ks, dtype=torch.int32)
+    idx, cnt = spec.topk(sc.to(dev), seq.to(dev), kt.to(dev), k_max)
+    idx, cnt = idx.cpu().numpy(), cnt.cpu().numpy()
+    scn = sc.numpy().astype(np.float64)
+    for b in range(B):
+        L = min(lens[b], L_max)
+        kb = max(0, min(ks[b], L, k_max))
+        want = oracle.topk_indices(scn[b, :L], kb)
+        assert cnt[b] == kb
+        assert idx[b, :kb].tolist() == want.tolist(), b
+        assert np.all(idx[b, kb:] == -1)
+
+
+# ------------------------------------------------------------------ attention
+
+ATTN_CASES = [
+    # n_layers, B, L_cap, H_q, H_kv, counts, k_max
+    (1, 1, 300, 4, 1, [200], 256),
+    (2, 2, 700, 32, 8, [513, 64], 600),
+    (1, 3, 400, 16, 8, [1, 0, 17], 64),
+    (2, 1, 2000, 64, 8, [1500], 1600),
+    (1, 2, 500, 8, 8, [129, 300], 300),
+    (1, 1, 600, 32, 2, [520], 520),
+    (3, 2, 256, 16, 16, [256, 255], 256),
+]
+
+
+def _attn_inputs(case, g):
+    n_layers, B, L_cap, H_q, H_kv, counts, k_max = case
+    q = _rand_bf16((n_layers, B, H_q, 128), g)
+    K = _rand_bf16((n_layers, B, L_cap, H_kv, 128), g)
+    V = _rand_bf16((n_layers, B, L_cap, H_kv, 128), g)
+    idx = torch.full((B, k_max), -1, dtype=torch.int32)
+    for b in range(B):
+        c = counts[b]
+        sel = torch.randperm(L_cap, generator=g)[:c].sort().values
+        idx[b, :c] = sel.to(torch.int32)
+    return q, K, V, idx, torch.tensor(counts, dtype=torch.int32)
+
+
+def _check_attn(out, lse, q, K, V, idx, counts, case):
+    n_layers, B = case[0], case[1]
+    qn, Kn, Vn = f64(q), f64(K), f64(V)
+    worst = 0.0
+    for layer in range(n_layers):
+        for b in range(B):
+            sel = idx[b, :counts[b]].numpy()
+            want, wl = oracle.sparse_gqa_attention(qn[layer, b], Kn[layer, b], Vn[layer, b], sel)
+            err = np.abs(out[layer, b] - want).max()
+            worst = max(worst, err)
+            assert err <= TOL_ATTN, (layer, b, err)
+            if lse is not None:
+                if counts[b] == 0:
+                    assert np.all(np.isneginf(lse[layer, b]))
+                else:
+                    assert np.abs(lse[layer, b] - wl).max() <= TOL_ATTN
+    return worst
+
+
+@pytest.mark.parametrize("case", ATTN_CASES, ids=[str(c) for c in ATTN_CASES])
+def test_attention_indexed(dev, case):
+    announce(f"attn indexed {case}")
+    g = torch.Generator().manual_seed(sum(case[:5]))
+    q, K, V, idx, counts = _attn_inputs(case, g)
+    out, lse = spec.sparse_decode_attn(q.to(dev), K.to(dev), V.to(dev), counts.to(dev),
+                                       idx=idx.to(dev))
+    worst = _check_attn(out.cpu().numpy(), lse.cpu().numpy(), q, K, V, idx, counts, case)
+    print(f"max abs err {worst:.3e}")
+
+
+@pytest.mark.parametrize("case", ATTN_CASES[:4], ids=[str(c) for c in ATTN_CASES[:4]])
+def test_gather_then_compact_attention(dev, case):
+    """spec_gather is a bit-exact row copy; compact-mode attention over its
+    output equals the indexed result."""
+    announce(f"gather+compact {case}")
+    g = torch.Generator().manual_seed(3 + sum(case[:5]))
+    q, K, V, idx, counts = _attn_inputs(case, g)
+    Kd, Vd, idxd, cd = K.to(dev), V.to(dev), idx.to(dev), counts.to(dev)
+    ks, vs = spec.gather(Kd, Vd, idxd, cd)
+    ks, vs = ks.cpu(), vs.cpu()
+    n_layers, B = case[0], case[1]
+    for layer in range(n_layers):
+        for b in range(B):
+            c = int(counts[b])
+            sel = idx[b, :c].long()
+            assert torch.equal(ks[layer, b, :c].view(torch.int16), K[layer, b, sel].view(torch.int16))
+            assert torch.equal(vs[layer, b, :c].view(torch.int16), V[layer, b, sel].view(torch.int16))
+    out_c, lse_c = spec.sparse_decode_attn(q.to(dev), ks.to(dev), vs.to(dev), cd)
+    out_i, lse_i = spec.sparse_decode_attn(q.to(dev), Kd, Vd, cd, idx=idxd)
+    # same rows in the same order: identical arithmetic, identical bits
+    assert torch.equal(out_c, out_i)
+    _check_attn(out_c.cpu().numpy(), lse_c.cpu().numpy(), q, K, V, idx, counts, case)
+
+
+def test_full_budget_is_dense(dev):
+    """k = L selects every token: the fused step equals dense attention
+    (checked against torch SDPA in fp64 on the CPU)."""
+    announce("dense k=L")
+    w = small_workload(B=2, L=300, H_r=8, d_r=64, n_layers=2, H_q=32, H_kv=8, k=300)
+    x = generate(w, seed=5)
+    r = spec.step(x["q_r"].to(dev), x["K_r"].to(dev), x["seq_lens"].to(dev), x["ks"].to(dev),
+                  x["q"].to(dev), x["K"].to(dev), x["V"].to(dev), k_max=300)
+    idx = r["idx"].cpu().numpy()
+    assert (idx == np.arange(300)[None, :]).all()
+    out = r["out"].cpu().numpy()
+    qn, Kn, Vn = f64(x["q"]), f64(x["K"]), f64(x["V"])
+    for layer in range(2):
+        for b in range(2):
+            qt = torch.tensor(qn[layer, b]).reshape(1, 32, 1, 128)
+            kt = torch.tensor(Kn[layer, b]).permute(1, 0, 2).repeat_interleave(4, 0)[None].contiguous()
+            vt = torch.tensor(Vn[layer, b]).permute(1, 0, 2).repeat_interleave(4, 0)[None].contiguous()
+            want = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt).reshape(32, 128).numpy()
+            assert np.abs(out[layer, b] - want).max() <= TOL_ATTN
+
+
+# ------------------------------------------------------------------ fused step
+
+STEP_CASES = [
+    dict(B=2, L=1000, H_r=8, d_r=64, n_layers=2, H_q=32, H_kv=8, k=128, heavy_frac=0.05),
+    dict(B=3, L=3000, H_r=16, d_r=64, n_layers=1, H_q=32, H_kv=8, k=256, heavy_frac=0.01,
+         ragged_min=700),
+    dict(B=1, L=5000, H_r=8, d_r=128, n_layers=2, H_q=64, H_kv=8, k=600, n_clusters=3,
+         cluster_len=64),
+    dict(B=2, L=4000, H_r=8, d_r=64, n_layers=1, H_q=32, H_kv=8, k=512, heavy_frac=0.02,
+         recent=256),
+]
+
+
+@pytest.mark.parametrize("kw", STEP_CASES, ids=[str(i) for i in range(len(STEP_CASES))])
+def test_step_vs_oracle(dev, kw):
+    announce(f"step {kw}")
+    w = small_workload(**kw)
+    x = generate(w, seed=kw["B"] + kw["L"])
+    r = spec.step(x["q_r"].to(dev), x["K_r"].to(dev), x["seq_lens"].to(dev), x["ks"].to(dev),
+                  x["q"].to(dev), x["K"].to(dev), x["V"].to(dev), k_max=w.k, with_scores=True,
+                  with_lse=True)
+    idx, cnt = r["idx"].cpu().numpy(), r["counts"].cpu().numpy()
+    out, sc = r["out"].cpu().numpy(), r["scores"].cpu().numpy().astype(np.float64)
+    qrn, Krn = f64(x["q_r"]), f64(x["K_r"])
+    qn, Kn, Vn = f64(x["q"]), f64(x["K"]), f64(x["V"])
+    for b in range(w.B):
+        L = int(x["seq_lens"][b])
+        kb = min(int(x["ks"][b]), L)
+        s64 = oracle.retrieval_scores(qrn[b], Krn[b], L)
+        assert np.all(np.abs(sc[b, :L] - s64) <= SCORE_ABS + SCORE_REL * s64)
+        assert cnt[b] == kb
+        got = idx[b, :kb]
+        ok, info = oracle.accept_index_set(s64, kb, got)
+        assert ok, info
+        # exact on the kernel's own fp32 scores
+        assert got.tolist() == oracle.topk_indices(sc[b, :L], kb).tolist()
+        # planted heavy tokens are recovered when the budget covers them
+        heavy = x["heavy"][b]
+        if 0 < len(heavy) <= kb:
+            assert np.isin(heavy, got).mean() >= 0.99
+        for layer in range(w.n_layers):
+            want, _ = oracle.sparse_gqa_attention(qn[layer, b], Kn[layer, b], Vn[layer, b], got)
+            assert np.abs(out[layer, b] - want).max() <= TOL_ATTN
+
+
+def test_step_deterministic(dev):
+    """Two runs of the fused step give identical bits (no atomics-order
+    dependence, no uninitialised reads)."""
+    announce("determinism")
+    w = small_workload(B=2, L=3000, H_r=8, d_r=64, n_layers=2, H_q=32, H_kv=8, k=256,
+                       heavy_frac=0.02)
+    x = generate(w, seed=9)
+    args = [x[n].to(dev) for n in ("q_r", "K_r", "seq_lens", "ks", "q", "K", "V")]
+    r1 = spec.step(*args, k_max=w.k, with_scores=True, with_lse=True)
+    r2 = spec.step(*args, k_max=w.k, with_scores=True, with_lse=True)
+    for key in ("idx", "counts", "out", "lse", "scores"):
+        assert torch.equal(r1[key], r2[key]), key
+
+
+# ------------------------------------------------------------------ elastic loading
+
+def test_delta_gather_vs_oracle(dev):
+    """Several elastic updates with a fixed budget: slot->token maps equal
+    the oracle's, every held row is a bit-exact copy, and the rows loaded
+    equal |S_now - S_last|."""
+    announce("delta gather")
+    g = torch.Generator().manual_seed(21)
+    n_layers, B, L_cap, H_kv, k_max = 2, 3, 900, 8, 200
+    K = _rand_bf16((n_layers, B, L_cap, H_kv, 128), g)
+    V = _rand_bf16((n_layers, B, L_cap, H_kv, 128), g)
+    Kd, Vd = K.to(dev), V.to(dev)
+    st = spec.ElasticState(n_layers, B, k_max, H_kv, 128, dev)
+    budgets = [200, 150, 1]
+    slot_ref = [np.full(k_max, -1) for _ in range(B)]
+    prev = [np.sort(np.random.default_rng(b).choice(L_cap, budgets[b], replace=False)) for b in range(B)]
+    for it in range(4):
+        rng = np.random.default_rng(100 + it)
+        now = []
+        for b in range(B):
+            keep = prev[b][rng.random(len(prev[b])) < 0.8]
+            fresh = np.setdiff1d(np.arange(L_cap), prev[b])
+            add = rng.choice(fresh, budgets[b] - len(keep), replace=False)
+            now.append(np.sort(np.concatenate([keep, add])))
+        idx = torch.full((B, k_max), -1, dtype=torch.int32)
+        for b in range(B):
+            idx[b, :len(now[b])] = torch.tensor(now[b], dtype=torch.int32)
+        cnt = torch.tensor([len(s) for s in now], dtype=torch.int32)
+        spec.delta_gather(idx.to(dev), cnt.to(dev), Kd, Vd, st)
+        slots = st.slot_tok.cpu().numpy()
+        nch = st.n_changed.cpu().numpy()
+        kb, vb = st.kbuf.cpu(), st.vbuf.cpu()
+        for b in range(B):
+            ref, loads = oracle.elastic_update(slot_ref[b], now[b])
+            slot_ref[b] = ref
+            assert slots[b].tolist() == ref.tolist(), (it, b)
+            assert nch[b] == len(loads)
+            held = [(s, t) for s, t in enumerate(ref.tolist()) if t >= 0]
+            ss = torch.tensor([s for s, _ in held])
+            tt = torch.tensor([t for _, t in held])
+            assert torch.equal(kb[:, b, ss].view(torch.int16), K[:, b, tt].view(torch.int16))
+            assert torch.equal(vb[:, b, ss].view(torch.int16), V[:, b, tt].view(torch.int16))
+        prev = now
+
+
+def test_step_elastic_equals_indexed(dev):
+    """The fused step with elastic loading (compact attention over the slot
+    buffers) agrees with the indexed step, over a few appended tokens."""
+    announce("step elastic")
+    w = small_workload(B=2, L=2000, H_r=8, d_r=64, n_layers=2, H_q=32, H_kv=8, k=256,
+                       heavy_frac=0.02, extra_cap=8)
+    x = generate(w, seed=4)
+    dev_x = {n: x[n].to(dev) for n in ("q_r", "K_r", "seq_lens", "ks", "q", "K", "V")}
+    st = spec.ElasticState(w.n_layers, w.B, w.k, w.H_kv, w.d, dev)
+    g = torch.Generator().manual_seed(5)
+    for it in range(4):
+        dev_x["seq_lens"] += 1                       # one appended token per step
+        dev_x["q_r"] = (0.95 * dev_x["q_r"].float()
+                        + 0.31 * torch.randn(dev_x["q_r"].shape, generator=g).to(dev)).to(torch.bfloat16)
+        r_el = spec.step(**{k: dev_x[k] for k in ("q_r", "K_r", "seq_lens", "ks", "q")},
+                         K=dev_x["K"], V=dev_x["V"], k_max=w.k, elastic=st, with_lse=True)
+        r_ix = spec.step(**{k: dev_x[k] for k in ("q_r", "K_r", "seq_lens", "ks", "q")},
+                         K=dev_x["K"], V=dev_x["V"], k_max=w.k, with_lse=True)
+        assert torch.equal(r_el["idx"], r_ix["idx"])
+        assert torch.allclose(r_el["out"], r_ix["out"], atol=1e-5, rtol=0)
+        slots = st.slot_tok.cpu().numpy()
+        for b in range(w.B):
+            c = int(r_ix["counts"][b])
+            assert sorted(slots[b, :c].tolist()) == r_ix["idx"][b, :c].cpu().tolist()
+            assert np.all(slots[b, c:] == -1)
