@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--attn-iters", type=int, default=20)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run three 1 GiB device-to-device copies (known HBM bytes) so "
+                         "that PMC byte counters can be scaled")
     return ap.parse_args()
 
 
@@ -160,17 +163,17 @@ def main():
     torch.cuda.synchronize()
 
     # ---- timed region: exactly K steps between two device synchronisations
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    evs[0].record()
+    ev0.record()
     for i in range(args.steps):
         spec.step(**call, outputs=outputs, ws=ws)
-        evs[i + 1].record()
+    ev1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    step_ms = [evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)]
     ms_per_step = wall * 1e3 / args.steps
+    ev_ms_per_step = ev0.elapsed_time(ev1) / args.steps
     print(f"[bench] {args.steps} steps in {wall:.3f}s", file=sys.stderr, flush=True)
 
     # ---- per-op times (same inputs, same stream), HIP events
@@ -234,9 +237,16 @@ def main():
         "step_hbm_gbps": round(step_bytes * value / 1e9, 1),
         "step_frac_of_peak": round(step_bytes * value / 1e9 / PEAK_HBM_GBPS, 4),
         "step_algorithmic_bytes": step_bytes,
-        "step_ms_median_events": round(statistics.median(step_ms), 4),
+        "step_ms_events": round(ev_ms_per_step, 4),
         "op_us": {k: round(v, 2) for k, v in op_us.items()},
     }
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(w, x, res)

@@ -24,9 +24,37 @@
 namespace spec {
 namespace {
 
-constexpr int kWaves = 4;   // wavefronts per workgroup
-constexpr int kChunk = 64;  // selected tokens per inner step
-constexpr int kD = 128;     // head dimension
+#ifndef SPEC_ATTN_CHUNK
+#define SPEC_ATTN_CHUNK 32
+#endif
+#ifndef SPEC_ATTN_NT
+#define SPEC_ATTN_NT 1
+#endif
+#ifndef SPEC_ATTN_WPE
+#define SPEC_ATTN_WPE 2  // wavefronts per SIMD the register budget is sized for
+#endif
+#ifndef SPEC_ATTN_WAVES
+#define SPEC_ATTN_WAVES 4
+#endif
+constexpr int kWaves = SPEC_ATTN_WAVES;   // wavefronts per workgroup
+constexpr int kChunk = SPEC_ATTN_CHUNK;   // selected tokens per inner step (32 or 64)
+constexpr int kTiles = kChunk / 16;       // 16-token MFMA tiles per chunk
+constexpr int kVRows = kChunk / 4;        // V rows per lane per chunk
+constexpr int kD = 128;                   // head dimension
+constexpr int kMaxSplit = 2048;           // longest split (tokens per work item)
+#ifndef SPEC_ATTN_BLOCKS_PER_CU
+#define SPEC_ATTN_BLOCKS_PER_CU 2
+#endif
+constexpr int kBlocksPerCU = SPEC_ATTN_BLOCKS_PER_CU;  // resident workgroups per CU
+
+// K/V rows are read once per launch: stream them past the caches.
+__device__ __forceinline__ uint4 ldkv(const uint16_t* p) {
+#if SPEC_ATTN_NT
+  return ldg16_stream(p);
+#else
+  return ldg16(p);
+#endif
+}
 
 struct AttnArgs {
   const uint16_t* q;      // [n_layers][B][H_q][d]
@@ -36,9 +64,11 @@ struct AttnArgs {
   const int32_t* counts;  // [B]
   float* part_acc;        // [n_layers*B][n_split][H_q][d]
   float* part_ml;         // [n_layers*B][n_split][H_q][2]
+  float* out;             // [n_layers*B][H_q][d]: written directly when n_split == 1
+  float* lse;             // [n_layers*B][H_q] or null (n_split == 1)
   int64_t stride_layer;   // elements between layers (indexed mode)
   int64_t stride_b;       // elements between sequences (indexed mode)
-  int B, H_q, H_kv, k_max, L_cap, n_split, split_tokens, n_items;
+  int B, H_q, H_kv, G, k_max, L_cap, n_split, split_tokens, n_items;
   float scale_log2;       // scale * log2(e)
 };
 
@@ -48,23 +78,78 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <int G, bool INDEXED>
-__global__ __launch_bounds__(kWaves * 64) void attn_split_kernel(AttnArgs a) {
-  __shared__ float lds[kWaves][kChunk * G + 16];  // P[token][head], then alpha[G]
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int item = blockIdx.x * kWaves + wave;
-  if (item >= a.n_items) return;  // uniform per wavefront; no block barriers below
+// LDS row pitch of a staged V tile in bf16: 288 bytes, so that the rows of
+// one transpose read start 32 bytes apart and spread over the banks.
+constexpr int kVPitch = kD + 16;
+
+__device__ __forceinline__ uint32_t f2bf_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+// 8 probabilities -> bf16 hi part and bf16 lo part (p - hi), packed for MFMA.
+__device__ __forceinline__ void split_bf16x8(const float* p, bf16x8& hi, bf16x8& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t h0 = f2bf_rne(p[2 * j]), h1 = f2bf_rne(p[2 * j + 1]);
+    const uint32_t l0 = f2bf_rne(p[2 * j] - __uint_as_float(h0 << 16));
+    const uint32_t l1 = f2bf_rne(p[2 * j + 1] - __uint_as_float(h1 << 16));
+    h[j] = h0 | (h1 << 16);
+    l[j] = l0 | (l1 << 16);
+  }
+  hi = __builtin_bit_cast(bf16x8, make_uint4(h[0], h[1], h[2], h[3]));
+  lo = __builtin_bit_cast(bf16x8, make_uint4(l[0], l[1], l[2], l[3]));
+}
+
+// max / sum over the four lanes {l, l^16, l^32, l^48} (one head's lanes).
+__device__ __forceinline__ float xgroup_max(float v) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float xgroup_sum(float v) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// Transposing LDS read: within each 16-lane group, lane i receives element
+// (i & 3) of the 8-byte chunks read by lanes (i >> 2) + 4j, j = 0..3.
+__device__ __forceinline__ bf16x4 lds_read_tr(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (__attribute__((address_space(3))) bf16x4*)(p));
+}
+
+template <bool INDEXED>
+__device__ __forceinline__ void process_item(const AttnArgs& a, const int item, const int lane,
+                                             uint16_t* V, int* rows) {
+  const int G = a.G;
   const int g = item % a.H_kv;
   const int rest = item / a.H_kv;
   const int split = rest % a.n_split;
   const int lb = rest / a.n_split;  // layer * B + b
   const int b = lb % a.B;
   const int layer = lb / a.B;
-  const int count = clampi(a.counts[b], 0, a.k_max);
+  const int count = __builtin_amdgcn_readfirstlane(clampi(a.counts[b], 0, a.k_max));
   const int j0 = split * a.split_tokens;
-  if (j0 >= count) return;
-  const int j1 = min(j0 + a.split_tokens, count);
+  const int r16e = lane & 15;
+  if (j0 >= count) {  // uniform per wavefront
+    if (a.n_split == 1 && r16e < G) {  // no tokens: out = 0, lse = -inf
+      const size_t orow = (size_t)lb * a.H_q + (size_t)g * G + r16e;
+      float* dst = a.out + orow * kD + 4 * (lane >> 4);
+#pragma unroll
+      for (int db = 0; db < 8; ++db)
+        *reinterpret_cast<float4*>(dst + 16 * db) = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (a.lse && (lane >> 4) == 0) a.lse[orow] = -INFINITY;
+    }
+    return;
+  }
+  const int n_tok = min(a.split_tokens, count - j0);  // tokens of this work item
 
   const int64_t rs = (int64_t)a.H_kv * kD;  // elements per token row
   const uint16_t* kb;
@@ -78,11 +163,35 @@ __global__ __launch_bounds__(kWaves * 64) void attn_split_kernel(AttnArgs a) {
     kb = a.k + off;
     vb = a.v + off;
   }
-  const int32_t* idx_b = INDEXED ? a.idx + (size_t)b * a.k_max : nullptr;
 
-  const int r16 = lane & 15;  // MFMA row/column index of this lane
-  const int kg = lane >> 4;   // MFMA k-group of this lane
-  // A operand: query head g*G + r16, dims 32s + 8kg .. +8 (zero rows >= G).
+  // Stage the rows of this item's tokens in LDS (masked tokens read row 0),
+  // so that no chunk waits on an index load from memory.
+  wave_sync_lds();  // the previous item's reads of rows/V are done
+  {
+    // All index loads are issued before any is used (one round trip), and
+    // one chunk of padding follows the end: the software pipeline always
+    // prefetches the next chunk, and padding rows all read row 0 (cache hits).
+    const int32_t* idx_b = INDEXED ? a.idx + (size_t)b * a.k_max + j0 : nullptr;
+    const int n_pad = (n_tok + kChunk - 1) / kChunk * kChunk + kChunk;
+    constexpr int kRowLoads = (kMaxSplit + kChunk + 63) / 64;
+    int rv[kRowLoads];
+#pragma unroll
+    for (int m = 0; m < kRowLoads; ++m) {
+      const int j = lane + 64 * m;
+      rv[m] = 0;
+      if (j < n_tok) rv[m] = INDEXED ? idx_b[j] : j0 + j;
+    }
+#pragma unroll
+    for (int m = 0; m < kRowLoads; ++m) {
+      const int j = lane + 64 * m;
+      if (j < n_pad) rows[j] = clampi(rv[m], 0, a.L_cap - 1);
+    }
+  }
+
+  const int r16 = lane & 15;  // head of this lane (MFMA column); token of a K tile row
+  const int kg = lane >> 4;   // MFMA k-group; also the token phase of V loads
+  // B operand of S^T = K Q^T: Q^T column r16 = query head g*G + r16 (zero if >= G),
+  // dims 32s + 8kg .. +8.
   bf16x8 qf[4];
   {
     const uint16_t* qp = a.q + ((size_t)lb * a.H_q + g * G + (r16 < G ? r16 : 0)) * kD + 8 * kg;
@@ -92,141 +201,156 @@ __global__ __launch_bounds__(kWaves * 64) void attn_split_kernel(AttnArgs a) {
       qf[s] = __builtin_bit_cast(bf16x8, w);
     }
   }
+  wave_sync_lds();
 
-  float m_run[4], l_run[4];
+  // K rows in the MFMA A-operand layout: tile t, token 16t + r16, dims
+  // 32s + 8kg .. +8.  V rows: load r brings token 4r + kg, dims 8 r16 .. +8,
+  // i.e. four whole 256-byte rows per instruction.
+  auto load_k = [&](int c, uint4 (&kr)[kTiles][4]) {
+    const int* rc = rows + c;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    m_run[i] = -INFINITY;
-    l_run[i] = 0.f;
-  }
-  float acc[G][8];
+    for (int t = 0; t < kTiles; ++t) {
+      const uint16_t* p = kb + (int64_t)rc[16 * t + r16] * rs + 8 * kg;
 #pragma unroll
-  for (int m = 0; m < G; ++m)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[m][e] = 0.f;
-
-  float* P = lds[wave];
-  const int vq = lane >> 4;  // P.V: token phase of this lane
-  const int vc = lane & 15;  // P.V: 8-dim column block of this lane
-
-  for (int c0 = j0; c0 < j1; c0 += kChunk) {
-    // Row of selected token c0 + lane (masked tokens read row 0).
-    const int jl = c0 + lane;
-    int myrow = 0;
-    if (jl < j1) myrow = INDEXED ? clampi(idx_b[jl], 0, a.L_cap - 1) : jl;
-
-    uint4 kraw[4][4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int row = __shfl(myrow, 16 * t + r16);
-      const uint16_t* p = kb + (int64_t)row * rs + 8 * kg;
-#pragma unroll
-      for (int s = 0; s < 4; ++s) kraw[t][s] = ldg16(p + 32 * s);
+      for (int s = 0; s < 4; ++s) kr[t][s] = ldkv(p + 32 * s);
     }
-    uint4 vraw[16];
+  };
+  auto load_v = [&](int c, uint4 (&vr)[kVRows]) {
+    const int* rc = rows + c;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = __shfl(myrow, vq + 4 * r);
-      vraw[r] = ldg16(vb + (int64_t)row * rs + 8 * vc);
-    }
+    for (int r = 0; r < kVRows; ++r) vr[r] = ldkv(vb + (int64_t)rc[4 * r + kg] * rs + 8 * r16);
+  };
 
-    // S = Q K^T for 4 tiles of 16 tokens; lane holds S[head 4kg+i][token r16].
-    float sv[4][4];
+  float m_run = -INFINITY, l_run = 0.f;  // head r16
+  floatx4 acc[8];                        // O^T[16db + 4kg + i][head r16]
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      floatx4 sacc = {0.f, 0.f, 0.f, 0.f};
+  for (int db = 0; db < 8; ++db) acc[db] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  // Single register buffers, refilled as soon as they are consumed: V(c+1)
+  // is requested right after V(c) is staged in LDS, K(c+1) right after the
+  // Q.K^T MFMAs have read K(c); both stay in flight through the softmax and
+  // the P.V MFMAs of chunk c.  Loads retire in issue order, so each wait is
+  // a partial one.  The prefetch past the last chunk reads padding rows
+  // (row 0, cache hits).
+  uint4 kraw[kTiles][4], vraw[kVRows];
+  load_v(0, vraw);
+  __builtin_amdgcn_sched_barrier(0);
+  load_k(0, kraw);
+  __builtin_amdgcn_sched_barrier(0);
+  for (int c = 0; c < n_tok; c += kChunk) {
+#pragma unroll
+    for (int r = 0; r < kVRows; ++r)
+      *reinterpret_cast<uint4*>(V + (4 * r + kg) * kVPitch + 8 * r16) = vraw[r];
+    load_v(c + kChunk, vraw);
+    __builtin_amdgcn_sched_barrier(0);  // keep the refill here: issue order = retire order
+
+    // S^T tiles: lane holds S[head r16][token 16t + 4kg + i].
+    floatx4 sacc[kTiles];
+#pragma unroll
+    for (int t = 0; t < kTiles; ++t) {
+      sacc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < 4; ++s)
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[s], __builtin_bit_cast(bf16x8, kraw[t][s]),
-                                                       sacc, 0, 0, 0);
-      const bool valid = c0 + 16 * t + r16 < j1;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) sv[t][i] = valid ? sacc[i] * a.scale_log2 : -INFINITY;
+        sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kraw[t][s]),
+                                                          qf[s], sacc[t], 0, 0, 0);
     }
-    float alpha[4];
+    load_k(c + kChunk, kraw);
+    __builtin_amdgcn_sched_barrier(0);
+
+    float sv[kTiles][4];
+    float mx = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float mx = fmaxf(fmaxf(sv[0][i], sv[1][i]), fmaxf(sv[2][i], sv[3][i]));
+    for (int t = 0; t < kTiles; ++t)
 #pragma unroll
-      for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 16));
-      const float mn = fmaxf(m_run[i], mx);
-      alpha[i] = exp2f(m_run[i] - mn);
-      float ls = 0.f;
+      for (int i = 0; i < 4; ++i) {
+        const bool valid = c + 16 * t + 4 * kg + i < n_tok;
+        sv[t][i] = valid ? sacc[t][i] * a.scale_log2 : -INFINITY;
+        mx = fmaxf(mx, sv[t][i]);
+      }
+    mx = xgroup_max(mx);
+    const float mn = fmaxf(m_run, mx);
+    const float alpha = exp2f(m_run - mn);
+    float ls = 0.f;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < kTiles; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
         sv[t][i] = exp2f(sv[t][i] - mn);
         ls += sv[t][i];
       }
-      l_run[i] = l_run[i] * alpha[i] + ls;
-      m_run[i] = mn;
-    }
-    // P (and alpha) to LDS for the P.V lane layout.
-    if (4 * kg < G) {
+    l_run = l_run * alpha + ls;
+    m_run = mn;
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (4 * kg + i < G) P[(16 * t + r16) * G + 4 * kg + i] = sv[t][i];
-      if (r16 == 0) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (4 * kg + i < G) P[kChunk * G + 4 * kg + i] = alpha[i];
-      }
-    }
+    for (int db = 0; db < 8; ++db) acc[db] *= alpha;
+
+    // O^T += V^T P^T on the matrix cores.  The k-slots 8kg..8kg+7 of a
+    // 32-token block are tokens 4kg..4kg+3 of its first tile and of its
+    // second tile: exactly the S^T entries this lane holds.
     wave_sync_lds();
-
 #pragma unroll
-    for (int m = 0; m < G; ++m) {
-      const float al = P[kChunk * G + m];
+    for (int kb2 = 0; kb2 < kChunk / 32; ++kb2) {
+      float pv[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[m][e] *= al;
-    }
+      for (int i = 0; i < 4; ++i) {
+        pv[i] = sv[2 * kb2][i];
+        pv[4 + i] = sv[2 * kb2 + 1][i];
+      }
+      bf16x8 phi, plo;
+      split_bf16x8(pv, phi, plo);
+      const uint16_t* r0 = V + (32 * kb2 + 4 * kg + (r16 >> 2)) * kVPitch + 4 * (r16 & 3);
+      const uint16_t* r1 = r0 + 16 * kVPitch;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      float vf[8];
-      unpack8(vraw[r], vf);
-      const float* pr = P + (vq + 4 * r) * G;
-#pragma unroll
-      for (int m = 0; m < G; ++m) {
-        const float pm = pr[m];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[m][e] = fmaf(pm, vf[e], acc[m][e]);
+      for (int db = 0; db < 8; ++db) {
+        const bf16x4 va = lds_read_tr(r0 + 16 * db);
+        const bf16x4 vb4 = lds_read_tr(r1 + 16 * db);
+        const bf16x8 vA = __builtin_shufflevector(va, vb4, 0, 1, 2, 3, 4, 5, 6, 7);
+        acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vA, phi, acc[db], 0, 0, 0);
+        acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vA, plo, acc[db], 0, 0, 0);
       }
     }
-    wave_sync_lds();  // P is rewritten by the next chunk
+    wave_sync_lds();  // the V tile is rewritten by the next chunk
   }
 
-  // Row sums over the 16 token lanes; accumulators over the 4 token phases.
+  l_run = xgroup_sum(l_run);
+  if (r16 < G) {
+    if (a.n_split == 1) {  // the whole selection: normalise and write the output
+      const size_t orow = (size_t)lb * a.H_q + (size_t)g * G + r16;
+      const float inv = 1.f / l_run;
+      float* dst = a.out + orow * kD + 4 * kg;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+      for (int db = 0; db < 8; ++db)
+        *reinterpret_cast<float4*>(dst + 16 * db) =
+            make_float4(acc[db][0] * inv, acc[db][1] * inv, acc[db][2] * inv, acc[db][3] * inv);
+      if (a.lse && kg == 0) a.lse[orow] = (m_run + log2f(l_run)) * kLn2;
+    } else {
+      const size_t prow = ((size_t)lb * a.n_split + split) * a.H_q + (size_t)g * G + r16;
+      float* dst = a.part_acc + prow * kD + 4 * kg;
 #pragma unroll
-    for (int off = 1; off < 16; off <<= 1) l_run[i] += __shfl_xor(l_run[i], off, 16);
-#pragma unroll
-  for (int m = 0; m < G; ++m)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      acc[m][e] += __shfl_xor(acc[m][e], 16);
-      acc[m][e] += __shfl_xor(acc[m][e], 32);
-    }
-
-  const size_t prow = ((size_t)lb * a.n_split + split) * a.H_q + (size_t)g * G;
-  if (vq == 0) {
-#pragma unroll
-    for (int m = 0; m < G; ++m) {
-      float4* dst = reinterpret_cast<float4*>(a.part_acc + (prow + m) * kD + 8 * vc);
-      dst[0] = make_float4(acc[m][0], acc[m][1], acc[m][2], acc[m][3]);
-      dst[1] = make_float4(acc[m][4], acc[m][5], acc[m][6], acc[m][7]);
-    }
-  }
-  if (r16 == 0) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if (4 * kg + i < G) {
-        float* ml = a.part_ml + (prow + 4 * kg + i) * 2;
-        ml[0] = m_run[i];
-        ml[1] = l_run[i];
+      for (int db = 0; db < 8; ++db)
+        *reinterpret_cast<float4*>(dst + 16 * db) =
+            make_float4(acc[db][0], acc[db][1], acc[db][2], acc[db][3]);
+      if (kg == 0) {
+        a.part_ml[prow * 2] = m_run;
+        a.part_ml[prow * 2 + 1] = l_run;
       }
     }
+  }
+}
+
+template <bool INDEXED>
+__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(SPEC_ATTN_WPE)))
+void attn_split_kernel(AttnArgs a) {
+  __shared__ __align__(16) uint16_t vlds[kWaves][kChunk * kVPitch];
+  __shared__ int rows_lds[kWaves][kMaxSplit + kChunk];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  // Persistent wavefronts: the grid is sized to the machine and each wave
+  // walks work items with a stride, so the partial-result stores of one item
+  // drain while the next item's rows are in flight (a wave that exits must
+  // first wait for its stores).  No block barriers are used.
+  const int stride = gridDim.x * kWaves;
+  for (int item = blockIdx.x * kWaves + wave; item < a.n_items; item += stride) {
+    process_item<INDEXED>(a, item, lane, vlds[wave], rows_lds[wave]);
   }
 }
 
@@ -274,29 +398,25 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(CombineArgs a) {
   if (a.lse && d4 == 0) a.lse[(size_t)lb * a.H_q + h] = (M + log2f(L)) * kLn2;
 }
 
-template <bool INDEXED>
-void launch_split(int G, dim3 grid, hipStream_t s, const AttnArgs& a) {
-  switch (G) {
-    case 1: attn_split_kernel<1, INDEXED><<<grid, kWaves * 64, 0, s>>>(a); break;
-    case 2: attn_split_kernel<2, INDEXED><<<grid, kWaves * 64, 0, s>>>(a); break;
-    case 4: attn_split_kernel<4, INDEXED><<<grid, kWaves * 64, 0, s>>>(a); break;
-    case 8: attn_split_kernel<8, INDEXED><<<grid, kWaves * 64, 0, s>>>(a); break;
-    default: attn_split_kernel<16, INDEXED><<<grid, kWaves * 64, 0, s>>>(a); break;
-  }
-}
-
 }  // namespace
 
 int attn_split_tokens(const Dims& d) {
-  // Longest split (fewest partials to write and merge) that still yields at
-  // least 2048 wavefront work items to spread over the 256 compute units.
+  // One work item per resident wavefront slot (2 per SIMD on 256 CUs): a
+  // wavefront that finishes an item must wait for its result stores before
+  // the slot can take the next one, so items should not queue behind each
+  // other.  Items are (layer, sequence, KV head) pairs, split only as far as
+  // needed to fill the slots; a split never exceeds kMaxSplit tokens and is
+  // a whole number of chunks.
+  constexpr int64_t kSlots = 2 * 4 * 256;
   const int64_t base = (int64_t)d.n_layers * d.B * d.H_kv;
-  const int cand[3] = {512, 256, 128};
-  for (int i = 0; i < 3; ++i) {
-    const int64_t ns = (d.k_max + cand[i] - 1) / cand[i];
-    if (base * ns >= 2048) return cand[i];
-  }
-  return 64;
+  int64_t n_split = (kSlots + base - 1) / base;
+  n_split = n_split < 1 ? 1 : n_split;
+  const int64_t min_split = (d.k_max + kMaxSplit - 1) / kMaxSplit;
+  if (n_split < min_split) n_split = min_split;
+  int64_t split = (d.k_max + n_split - 1) / n_split;
+  split = (split + kChunk - 1) / kChunk * kChunk;
+  if (split > kMaxSplit) split = kMaxSplit;
+  return (int)split;
 }
 
 hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
@@ -309,14 +429,22 @@ hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
   float* part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) +
                                             align_up(sizeof(float) * rows * d.d));
   const int64_t n_items = (int64_t)d.n_layers * d.B * n_split * d.H_kv;
-  AttnArgs a{q, k, v, idx, counts, part_acc, part_ml, d.kv_stride_layer, d.kv_stride_b,
-             d.B, d.H_q, d.H_kv, d.k_max, d.L_cap, n_split, split, (int)n_items,
+  AttnArgs a{q, k, v, idx, counts, part_acc, part_ml, out, lse, d.kv_stride_layer, d.kv_stride_b,
+             d.B, d.H_q, d.H_kv, d.G, d.k_max, d.L_cap, n_split, split, (int)n_items,
              d.scale * kLog2e};
-  const dim3 grid((unsigned)((n_items + kWaves - 1) / kWaves));
+  // Persistent grid: at most as many workgroups as the machine holds at once
+  // (the register budget allows 2 wavefronts per SIMD: 2 workgroups per CU).
+  int dev = 0, n_cu = 256;
+  if (hipGetDevice(&dev) == hipSuccess)
+    hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+  const int64_t want = (n_items + kWaves - 1) / kWaves;
+  const int64_t cap = (int64_t)n_cu * kBlocksPerCU;
+  const dim3 grid((unsigned)(want < cap ? want : cap));
   if (idx)
-    launch_split<true>(d.G, grid, s, a);
+    attn_split_kernel<true><<<grid, kWaves * 64, 0, s>>>(a);
   else
-    launch_split<false>(d.G, grid, s, a);
+    attn_split_kernel<false><<<grid, kWaves * 64, 0, s>>>(a);
+  if (n_split == 1) return hipGetLastError();  // the split kernel wrote out/lse
   CombineArgs c{part_acc, part_ml, counts, out, lse, d.B, d.H_q, d.k_max, n_split, split};
   const dim3 g2(d.n_layers * d.B, (d.H_q + 7) / 8);
   attn_combine_kernel<<<g2, 256, 0, s>>>(c);

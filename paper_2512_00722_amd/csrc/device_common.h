@@ -49,6 +49,32 @@ __device__ __forceinline__ int clampi(int x, int lo, int hi) {
   return x < lo ? lo : (x > hi ? hi : x);
 }
 
+// ---- cross-lane reductions inside a 16-lane DPP row (no LDS traffic) ----
+// DPP controls: quad_perm [1,0,3,2] = 0xB1, quad_perm [2,3,0,1] = 0x4E,
+// row_half_mirror = 0x141, row_mirror = 0x140.  After the four steps every
+// lane of the row holds the reduction over its 16 lanes (8 lanes: three).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
+}
+template <int N>  // N in {2, 4, 8, 16}
+__device__ __forceinline__ float row_sum(float v) {
+  v += dpp_f<0xB1>(v);
+  if (N >= 4) v += dpp_f<0x4E>(v);
+  if (N >= 8) v += dpp_f<0x141>(v);
+  if (N >= 16) v += dpp_f<0x140>(v);
+  return v;
+}
+template <int N>
+__device__ __forceinline__ float row_max(float v) {
+  v = fmaxf(v, dpp_f<0xB1>(v));
+  if (N >= 4) v = fmaxf(v, dpp_f<0x4E>(v));
+  if (N >= 8) v = fmaxf(v, dpp_f<0x141>(v));
+  if (N >= 16) v = fmaxf(v, dpp_f<0x140>(v));
+  return v;
+}
+
 // Combine two (max, sum-of-exp2) pairs; -inf max marks an empty pair.
 __device__ __forceinline__ void ms_combine(float& m, float& s, float m2, float s2) {
   if (m2 == -INFINITY) return;

@@ -24,18 +24,35 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 // Retrieval scoring: tokens per workgroup of the logits kernel.
 constexpr int kScoreTokensPerBlock = 128;
 // Softmax/head-sum kernel: tokens per workgroup.
-constexpr int kSoftTokensPerBlock = 2048;
+constexpr int kSoftTokensPerBlock = 1024;
 
 inline int score_blocks(const Dims& d) {
   return (d.L_max + kScoreTokensPerBlock - 1) / kScoreTokensPerBlock;
 }
-// logits [B][L_max][H_r] fp32 + per-block (max, sum) [B][n_blk][H_r][2] fp32
-inline size_t score_ws_bytes(const Dims& d) {
-  return align_up(sizeof(float) * (size_t)d.B * d.L_max * d.H_r) +
-         align_up(sizeof(float) * 2 * (size_t)d.B * score_blocks(d) * d.H_r);
+// Top-k: 4096-bin histogram of the top 12 bits of the score keys per sequence.
+constexpr int kTopkBins = 4096;
+inline size_t topk_hist_bytes(const Dims& d) {
+  return align_up(sizeof(int32_t) * (size_t)d.B * kTopkBins);
 }
 
-inline size_t topk_ws_bytes(const Dims&) { return 0; }
+// logits [B][L_max][H_r] fp32 + per-block (max, sum) [B][n_blk][H_r][2] fp32
+// + the top-k histogram of the scores written.
+inline size_t score_logits_bytes(const Dims& d) {
+  return align_up(sizeof(float) * (size_t)d.B * d.L_max * d.H_r);
+}
+inline size_t score_part_bytes(const Dims& d) {
+  return align_up(sizeof(float) * 2 * (size_t)d.B * score_blocks(d) * d.H_r);
+}
+inline size_t score_ws_bytes(const Dims& d) {
+  return score_logits_bytes(d) + score_part_bytes(d) + topk_hist_bytes(d);
+}
+// The histogram region inside a score workspace.
+inline int32_t* score_ws_hist(const Dims& d, void* ws) {
+  return reinterpret_cast<int32_t*>(static_cast<char*>(ws) + score_logits_bytes(d) +
+                                    score_part_bytes(d));
+}
+
+inline size_t topk_ws_bytes(const Dims& d) { return topk_hist_bytes(d); }
 
 // Attention split size (tokens of the selection per wave work item).
 int attn_split_tokens(const Dims& d);
@@ -44,8 +61,11 @@ inline int attn_n_split(const Dims& d) {
   return (d.k_max + s - 1) / s;
 }
 // partial acc [n_layers*B][n_split][H_q][d] + (m, l) [n_layers*B][n_split][H_q][2]
+// (none when every work item covers the whole selection: out is written directly)
 inline size_t attn_ws_bytes(const Dims& d) {
-  const size_t rows = (size_t)d.n_layers * d.B * attn_n_split(d) * d.H_q;
+  const int n_split = attn_n_split(d);
+  if (n_split == 1) return 0;
+  const size_t rows = (size_t)d.n_layers * d.B * n_split * d.H_q;
   return align_up(sizeof(float) * rows * d.d) + align_up(sizeof(float) * rows * 2);
 }
 
@@ -61,6 +81,10 @@ hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
 hipError_t launch_topk(const Dims& d, const float* scores, const int32_t* seq_lens,
                        const int32_t* ks, int32_t* idx, int32_t* counts, void* ws,
                        hipStream_t s);
+// Selection only, from a histogram already built over the same scores.
+hipError_t launch_topk_select(const Dims& d, const float* scores, const int32_t* seq_lens,
+                              const int32_t* ks, const int32_t* hist, int32_t* idx,
+                              int32_t* counts, hipStream_t s);
 hipError_t launch_gather(const Dims& d, const uint16_t* k_cache, const uint16_t* v_cache,
                          const int32_t* idx, const int32_t* counts, uint16_t* k_sel,
                          uint16_t* v_sel, hipStream_t s);

@@ -28,6 +28,7 @@ struct LogitsArgs {
   const int32_t* seq_lens;
   float* logits;  // [B][L_max][H_r], log2 units
   float* part;    // [B][n_blk][H_r][2]: block max, block sum of exp2(l - max)
+  int32_t* hist;  // [B][4096] top-k histogram, zeroed here for the next kernel
   int64_t kr_stride_b;
   int L_max, H_r, n_blk;
   float qscale;   // scale_r * log2(e)
@@ -39,6 +40,10 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
   const int b = blockIdx.y;
   const int blk = blockIdx.x;
   const int L_b = clampi(a.seq_lens[b], 0, a.L_max);
+  if (blk == 0) {
+    int32_t* h = a.hist + (size_t)b * kTopkBins;
+    for (int i = threadIdx.x; i < kTopkBins; i += 256) h[i] = 0;
+  }
   const int t_begin = blk * T1;
   if (t_begin >= L_b) return;  // uniform for the workgroup
   const int n_tok = min(T1, L_b - t_begin);
@@ -76,8 +81,7 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
         float acc = 0.f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc = fmaf(qv[e], kf[e], acc);
-#pragma unroll
-        for (int off = 1; off < LPH; off <<= 1) acc += __shfl_xor(acc, off, LPH);
+        acc = row_sum<LPH>(acc);
         const int i = i0 + u * tpi;
         if (part == 0 && i < n_tok) {
           lg[i * 16 + h] = acc;
@@ -94,12 +98,10 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
   if (hh < a.H_r) {
     float m = -INFINITY;
     for (int i = j; i < n_tok; i += 16) m = fmaxf(m, lg[i * 16 + hh]);
-#pragma unroll
-    for (int off = 8; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 16));
+    m = row_max<16>(m);
     float s = 0.f;
     for (int i = j; i < n_tok; i += 16) s += exp2f(lg[i * 16 + hh] - m);
-#pragma unroll
-    for (int off = 8; off > 0; off >>= 1) s += __shfl_xor(s, off, 16);
+    s = row_sum<16>(s);
     if (j == 0) {
       float* p = a.part + (((size_t)b * a.n_blk + blk) * a.H_r + hh) * 2;
       p[0] = m;
@@ -112,11 +114,15 @@ struct SoftArgs {
   const float* logits;
   const float* part;
   const int32_t* seq_lens;
-  float* scores;  // [B][L_max]
+  float* scores;   // [B][L_max]
+  int32_t* hist;   // [B][4096]: histogram of key bits 31..20 of the scores
   int L_max, H_r, n_blk;
 };
 
+// One workgroup per (T2 tokens, sequence); thread = 4 consecutive tokens.
 __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
+  __shared__ float c_h[16];
+  __shared__ int sh_hist[kTopkBins];
   const int b = blockIdx.y;
   const int tid = threadIdx.x;
   const int t0 = blockIdx.x * T2;
@@ -127,35 +133,68 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
     for (int t = t0 + tid; t < t1; t += 256) out[t] = -INFINITY;
     return;
   }
-  __shared__ float c_h[16];
+  for (int i = tid; i < kTopkBins; i += 256) sh_hist[i] = 0;
+
+  // Each head's normaliser c_h = M_h + log2 Z_h from the per-block pairs:
+  // 16 lanes per head, partial pairs loaded 8 at a time before combining.
   const int nb = (L_b + T1 - 1) / T1;
   const int hh = tid >> 4;
   const int j = tid & 15;
   if (hh < a.H_r) {
     float m = -INFINITY, s = 0.f;
-    for (int i = j; i < nb; i += 16) {
-      const float* p = a.part + (((size_t)b * a.n_blk + i) * a.H_r + hh) * 2;
-      ms_combine(m, s, p[0], p[1]);
+    const float* p = a.part + ((size_t)b * a.n_blk * a.H_r + hh) * 2;
+    for (int i0 = j; i0 < nb; i0 += 16 * 8) {
+      float pm[8], ps[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = i0 + 16 * u;
+        const bool v = i < nb;
+        pm[u] = v ? p[(size_t)i * a.H_r * 2] : -INFINITY;
+        ps[u] = v ? p[(size_t)i * a.H_r * 2 + 1] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) ms_combine(m, s, pm[u], ps[u]);
     }
 #pragma unroll
-    for (int off = 8; off > 0; off >>= 1) {
-      const float m2 = __shfl_xor(m, off, 16);
-      const float s2 = __shfl_xor(s, off, 16);
+    for (int ctrl = 0; ctrl < 4; ++ctrl) {
+      float m2, s2;
+      if (ctrl == 0) { m2 = dpp_f<0xB1>(m); s2 = dpp_f<0xB1>(s); }
+      else if (ctrl == 1) { m2 = dpp_f<0x4E>(m); s2 = dpp_f<0x4E>(s); }
+      else if (ctrl == 2) { m2 = dpp_f<0x141>(m); s2 = dpp_f<0x141>(s); }
+      else { m2 = dpp_f<0x140>(m); s2 = dpp_f<0x140>(s); }
       ms_combine(m, s, m2, s2);
     }
     if (j == 0) c_h[hh] = m + log2f(s);
   }
   __syncthreads();
+
   const int H_r = a.H_r;
-  for (int t = t0 + tid; t < t1; t += 256) {
+  const int tb = t0 + 4 * tid;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int t = tb + e;
+    if (t >= t1) break;
     float sc = -INFINITY;
     if (t < L_b) {
       const float* l = a.logits + ((size_t)b * a.L_max + t) * H_r;
       sc = 0.f;
-      for (int h = 0; h < H_r; ++h) sc += exp2f(l[h] - c_h[h]);
+      if ((H_r & 3) == 0) {
+        for (int h = 0; h < H_r; h += 4) {
+          const float4 v = *reinterpret_cast<const float4*>(l + h);
+          sc += exp2f(v.x - c_h[h]) + exp2f(v.y - c_h[h + 1]) + exp2f(v.z - c_h[h + 2]) +
+                exp2f(v.w - c_h[h + 3]);
+        }
+      } else {
+        for (int h = 0; h < H_r; ++h) sc += exp2f(l[h] - c_h[h]);
+      }
+      atomicAdd(&sh_hist[order_key(sc) >> 20], 1);
     }
     out[t] = sc;
   }
+  __syncthreads();
+  int32_t* gh = a.hist + (size_t)b * kTopkBins;
+  for (int i = tid; i < kTopkBins; i += 256)
+    if (sh_hist[i]) atomicAdd(&gh[i], sh_hist[i]);
 }
 
 }  // namespace
@@ -165,16 +204,16 @@ hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
                         hipStream_t s) {
   const int n_blk = score_blocks(d);
   float* logits = static_cast<float*>(ws);
-  float* part = reinterpret_cast<float*>(static_cast<char*>(ws) +
-                                         align_up(sizeof(float) * (size_t)d.B * d.L_max * d.H_r));
-  LogitsArgs la{q_r, k_r, seq_lens, logits, part, d.kr_stride_b,
+  float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + score_logits_bytes(d));
+  int32_t* hist = score_ws_hist(d, ws);
+  LogitsArgs la{q_r, k_r, seq_lens, logits, part, hist, d.kr_stride_b,
                 d.L_max, d.H_r, n_blk, d.scale_r * kLog2e};
   const dim3 g1(n_blk, d.B);
   if (d.d_r == 64)
     logits_kernel<8><<<g1, 256, 0, s>>>(la);
   else
     logits_kernel<16><<<g1, 256, 0, s>>>(la);
-  SoftArgs sa{logits, part, seq_lens, scores, d.L_max, d.H_r, n_blk};
+  SoftArgs sa{logits, part, seq_lens, scores, hist, d.L_max, d.H_r, n_blk};
   const dim3 g2((d.L_max + T2 - 1) / T2, d.B);
   softmax_headsum_kernel<<<g2, 256, 0, s>>>(sa);
   return hipGetLastError();

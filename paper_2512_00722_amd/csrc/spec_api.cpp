@@ -230,7 +230,9 @@ spec_status spec_step(const spec_dims* dm, const uint16_t* q_r, const uint16_t* 
   const hipStream_t s = as_stream(stream);
   hipError_t e = spec::launch_score(d, q_r, k_r, seq_lens, scores, ws_score, s);
   if (e != hipSuccess) return hip_status(e);
-  e = spec::launch_topk(d, scores, seq_lens, ks, idx_out, counts_out, ws_topk, s);
+  (void)ws_topk;  // the score kernels already built the selection histogram
+  e = spec::launch_topk_select(d, scores, seq_lens, ks, spec::score_ws_hist(d, ws_score),
+                               idx_out, counts_out, s);
   if (e != hipSuccess) return hip_status(e);
   if (el) {
     e = spec::launch_delta(d, idx_out, counts_out, k_cache, v_cache, el->slot_tok, el->kbuf,

@@ -1,15 +1,25 @@
 // Exact top-k token selection on gfx950 (SpeContext Sec. 4.3: the important
 // tokens are chosen from the retrieval head's attention weights).
 //
-// One 1024-thread workgroup per sequence.  The fp32 scores are mapped to
-// order-preserving 32-bit keys and the k-th largest key T is found by a
-// radix select over three digits (bits 31..20, 19..8, 7..0) with LDS
-// histograms; only keys that share the digits chosen so far are counted in
-// later passes.  The select also yields r, the number of keys equal to T that
-// belong to the set (the lowest-index ones: ties go to the lower index).
-// A final ordered compaction walks the row in index order; one workgroup
-// scan of the pair (#keys > T, #keys == T) gives every selected token its
-// output slot, so the indices come out ascending with no sort.
+// Scores are mapped to order-preserving 32-bit keys.  The k-th largest key T
+// is located from the top 12 key bits first: a 4096-bin histogram of every
+// sequence (built while the scores are written, or by topk_hist_kernel for a
+// standalone call) names the bin b1 holding the k-th key, the number c1 of
+// keys in higher bins (all selected) and the bin's population n1.
+//
+// topk_select_kernel, one 1024-thread workgroup per sequence:
+//  * fast path (c1 <= 8192, n1 <= 12288): a single pass over the row in
+//    per-thread contiguous segments appends, in token order, the tokens of
+//    higher bins to an LDS list and the bin-b1 candidates (key, token) to a
+//    second list; the remaining 20 key bits of T are resolved among the
+//    candidates only (two 10-bit LDS histogram passes), which also gives r,
+//    the number of keys equal to T to take (the lowest-index ones); the
+//    selected candidates are compacted in order and the two ascending lists
+//    are merged by binary search.  The row is read once.
+//  * general path: two more radix passes (bits 19..8, 7..0) over the row,
+//    then an ordered compaction with one workgroup scan of (#keys > T,
+//    #keys == T) per 4096 tokens.
+// Both paths write the indices ascending, so no sort is needed.
 #include "device_common.h"
 #include "internal.h"
 
@@ -18,20 +28,14 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
-
-struct TopkArgs {
-  const float* scores;  // [B][L_max]
-  const int32_t* seq_lens;
-  const int32_t* ks;
-  int32_t* idx;         // [B][k_max]
-  int32_t* counts;      // [B] or null
-  int L_max, k_max;
-};
+constexpr int kBins = kTopkBins;  // 4096: key bits 31..20
+constexpr int kGtCap = 8192;
+constexpr int kCandCap = 12288;
 
 // Exclusive scan of two ints over the workgroup; returns the totals too.
 // Must be called by all threads.
 __device__ __forceinline__ void block_scan2(int a, int b, int& ea, int& eb, int& ta, int& tb,
-                                            int* sh /* [2*kWaves + 2] */) {
+                                            int* sh /* [2*kWaves] */) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   int ia = a, ib = b;
@@ -76,7 +80,68 @@ __device__ __forceinline__ void block_scan2(int a, int b, int& ea, int& eb, int&
   __syncthreads();  // sh is reused by the next call
 }
 
-__global__ __launch_bounds__(kThreads) void topk_kernel(TopkArgs a) {
+// Among `nbins` descending bins held by the workgroup (thread i owns bins
+// nbins-1-i*bpt .. with bpt = max(1, nbins/1024)), find the bin where the
+// running count from the top first reaches `need`.  Writes the bin and the
+// count of keys in higher bins to sel[0], sel[1] and the bin's count to
+// sel[2].  All threads must call; the result is valid after the call.
+__device__ __forceinline__ void find_bin(const int* hist, int nbins, int need, int* sh,
+                                         int* sel) {
+  const int tid = threadIdx.x;
+  const int bpt = nbins >= kThreads ? nbins / kThreads : 1;
+  const bool owns = tid * bpt < nbins;
+  int cnt[4] = {0, 0, 0, 0};
+  int local = 0;
+  if (owns) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (e < bpt) {
+        cnt[e] = hist[nbins - 1 - (tid * bpt + e)];
+        local += cnt[e];
+      }
+    }
+  }
+  int before, d0, t0, t1;
+  block_scan2(local, 0, before, d0, t0, t1, sh);
+  if (owns) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (e < bpt) {
+        if (before < need && need <= before + cnt[e]) {
+          sel[0] = nbins - 1 - (tid * bpt + e);
+          sel[1] = before;
+          sel[2] = cnt[e];
+        }
+        before += cnt[e];
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// Key of row[t] (t may be out of range: returns 0, below every real key).
+__device__ __forceinline__ uint32_t key_at(const float* row, int t, int L) {
+  return t < L ? order_key(row[t]) : 0u;
+}
+
+struct SelArgs {
+  const float* scores;  // [B][L_max]
+  const int32_t* seq_lens;
+  const int32_t* ks;
+  const int32_t* hist;  // [B][4096] of key bits 31..20 over t < L_b
+  int32_t* idx;         // [B][k_max]
+  int32_t* counts;      // [B] or null
+  int L_max, k_max;
+};
+
+__global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
+  __shared__ int s_hist[kBins];
+  __shared__ int s_gt[kGtCap];
+  __shared__ uint32_t s_ckey[kCandCap];
+  __shared__ int s_cidx[kCandCap];
+  __shared__ int s_scan[2 * kWaves];
+  __shared__ int s_sel[4];
+
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   const int L_b = clampi(a.seq_lens[b], 0, a.L_max);
@@ -91,60 +156,168 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(TopkArgs a) {
     return;
   }
 
-  __shared__ int hist[4096];
-  __shared__ int scan_sh[2 * kWaves + 2];
-  __shared__ int sel_digit, sel_above;
+  // ---- the bin of the k-th key from the 12-bit histogram
+  const int32_t* gh = a.hist + (size_t)b * kBins;
+  for (int i = tid; i < kBins; i += kThreads) s_hist[i] = gh[i];
+  if (tid == 0) s_sel[0] = s_sel[1] = s_sel[2] = -1;
+  __syncthreads();
+  find_bin(s_hist, kBins, k_b, s_scan, s_sel);
+  const int b1i = s_sel[0];
+  const int c1 = s_sel[1];  // keys in higher bins: all selected
+  const int n1 = s_sel[2];  // keys in bin b1
+  const int r1 = k_b - c1;  // keys still to take from bin b1 (1 <= r1 <= n1)
+  const uint32_t b1 = (uint32_t)b1i;
+  // A histogram that does not describe this row (never produced by this
+  // library) sends the sequence down the general path from scratch.
+  const bool hist_ok = b1i >= 0 && c1 >= 0 && c1 < k_b && r1 <= n1;
+  __syncthreads();
 
-  uint32_t prefix = 0, mask = 0;
-  int remaining = k_b;  // keys still to take at or below the current prefix
+  if (hist_ok && c1 <= kGtCap && n1 <= kCandCap) {
+    // ---------------- fast path: one pass over the row ----------------
+    const int seg = (L_b + kThreads - 1) / kThreads;
+    const int s0 = min(tid * seg, L_b);
+    const int s1 = min(s0 + seg, L_b);
+    int ngt = 0, ncand = 0;
+    for (int t0 = s0; t0 < s1; t0 += 8) {
+      uint32_t k8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) k8[e] = key_at(row, t0 + e, s1);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t dg = k8[e] >> 20;
+        ngt += (t0 + e < s1) && dg > b1;
+        ncand += (t0 + e < s1) && dg == b1;
+      }
+    }
+    int gt_pos, cand_pos, gt_tot, cand_tot;
+    block_scan2(ngt, ncand, gt_pos, cand_pos, gt_tot, cand_tot, s_scan);
+    for (int t0 = s0; t0 < s1; t0 += 8) {
+      uint32_t k8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) k8[e] = key_at(row, t0 + e, s1);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (t0 + e < s1) {
+          const uint32_t dg = k8[e] >> 20;
+          if (dg > b1) {
+            if (gt_pos < kGtCap) s_gt[gt_pos] = t0 + e;
+            ++gt_pos;
+          } else if (dg == b1) {
+            if (cand_pos < kCandCap) {
+              s_ckey[cand_pos] = k8[e];
+              s_cidx[cand_pos] = t0 + e;
+            }
+            ++cand_pos;
+          }
+        }
+      }
+    }
+    __syncthreads();
+
+    // ---- resolve the low 20 bits of T among the n1 candidates
+    int remaining = r1;
+    uint32_t T = b1 << 20;
 #pragma unroll 1
-  for (int pass = 0; pass < 3; ++pass) {
+    for (int pass = 0; pass < 2; ++pass) {
+      const int shift = pass == 0 ? 10 : 0;
+      for (int i = tid; i < 1024; i += kThreads) s_hist[i] = 0;
+      __syncthreads();
+      const uint32_t hi_mask = pass == 0 ? 0xFFF00000u : 0xFFFFFC00u;
+      for (int i = tid; i < n1; i += kThreads) {
+        const uint32_t kk = s_ckey[i];
+        if ((kk & hi_mask) == T) atomicAdd(&s_hist[(kk >> shift) & 1023], 1);
+      }
+      __syncthreads();
+      find_bin(s_hist, 1024, remaining, s_scan, s_sel);
+      T |= (uint32_t)s_sel[0] << shift;
+      remaining -= s_sel[1];
+      __syncthreads();
+    }
+    const int r = remaining;  // keys equal to T to take, lowest index first
+
+    // ---- selected candidates, in token order, into s_ckey (as ints)
+    const int cseg = (n1 + kThreads - 1) / kThreads;  // <= 12
+    const int c0 = min(tid * cseg, n1);
+    const int cend = min(c0 + cseg, n1);
+    uint32_t ck[12];
+    int ci[12];
+    int ngtT = 0, neqT = 0;
+#pragma unroll
+    for (int e = 0; e < 12; ++e) {
+      const bool v = c0 + e < cend;
+      ck[e] = v ? s_ckey[c0 + e] : 0u;
+      ci[e] = v ? s_cidx[c0 + e] : 0;
+      ngtT += v && ck[e] > T;
+      neqT += v && ck[e] == T;
+    }
+    int gbef, ebef, gtot, etot;
+    block_scan2(ngtT, neqT, gbef, ebef, gtot, etot, s_scan);  // also orders the reads above
+    int* s_selv = reinterpret_cast<int*>(s_ckey);
+#pragma unroll
+    for (int e = 0; e < 12; ++e) {
+      if (c0 + e < cend) {
+        if (ck[e] > T) {
+          s_selv[gbef + min(ebef, r)] = ci[e];
+          ++gbef;
+        } else if (ck[e] == T) {
+          if (ebef < r) s_selv[gbef + ebef] = ci[e];
+          ++ebef;
+        }
+      }
+    }
+    __syncthreads();
+
+    // ---- merge the two ascending lists (c1 + r1 = k_b entries)
+    for (int i = tid; i < c1; i += kThreads) {
+      const int v = s_gt[i];
+      int lo = 0, hi = r1;  // count of selected candidates below v
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (s_selv[mid] < v) lo = mid + 1; else hi = mid;
+      }
+      out[i + lo] = v;
+    }
+    for (int j = tid; j < r1; j += kThreads) {
+      const int v = s_selv[j];
+      int lo = 0, hi = c1;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (s_gt[mid] < v) lo = mid + 1; else hi = mid;
+      }
+      out[j + lo] = v;
+    }
+    return;
+  }
+
+  // ---------------- general path: radix passes over the row ----------------
+  uint32_t prefix = hist_ok ? b1 << 20 : 0u;
+  uint32_t mask = hist_ok ? 0xFFF00000u : 0u;
+  int remaining = hist_ok ? r1 : k_b;
+#pragma unroll 1
+  for (int pass = hist_ok ? 1 : 0; pass < 3; ++pass) {
     const int shift = pass == 0 ? 20 : (pass == 1 ? 8 : 0);
     const int nbins = pass < 2 ? 4096 : 256;
-    for (int i = tid; i < nbins; i += kThreads) hist[i] = 0;
+    for (int i = tid; i < nbins; i += kThreads) s_hist[i] = 0;
     __syncthreads();
-    for (int t = tid; t < L_b; t += kThreads) {
-      const uint32_t key = order_key(row[t]);
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & (nbins - 1)], 1);
-    }
-    __syncthreads();
-    // Thread i owns bins in descending order: digits nbins-1-i*bpt ... .
-    const int bpt = nbins >= kThreads ? nbins / kThreads : 1;
-    const bool owns = tid * bpt < nbins;
-    int cnt[4] = {0, 0, 0, 0};
-    int local = 0;
-    if (owns) {
+    for (int t0 = 0; t0 < L_b; t0 += 8 * kThreads) {
+      uint32_t k8[8];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (e < bpt) {
-          cnt[e] = hist[nbins - 1 - (tid * bpt + e)];
-          local += cnt[e];
-        }
-      }
-    }
-    int before, dummy, tot, tot2;
-    block_scan2(local, 0, before, dummy, tot, tot2, scan_sh);
-    if (owns) {
+      for (int e = 0; e < 8; ++e) k8[e] = key_at(row, t0 + e * kThreads + tid, L_b);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (e >= bpt) break;
-        if (before < remaining && remaining <= before + cnt[e]) {
-          sel_digit = nbins - 1 - (tid * bpt + e);
-          sel_above = before;
-        }
-        before += cnt[e];
-      }
+      for (int e = 0; e < 8; ++e)
+        if (t0 + e * kThreads + tid < L_b && (k8[e] & mask) == prefix)
+          atomicAdd(&s_hist[(k8[e] >> shift) & (nbins - 1)], 1);
     }
     __syncthreads();
-    prefix |= (uint32_t)sel_digit << shift;
+    find_bin(s_hist, nbins, remaining, s_scan, s_sel);
+    prefix |= (uint32_t)s_sel[0] << shift;
     mask |= (uint32_t)(nbins - 1) << shift;
-    remaining -= sel_above;
-    __syncthreads();  // sel_* are rewritten by the next pass
+    remaining -= s_sel[1];
+    __syncthreads();
   }
-  const uint32_t T = prefix;  // key of the k_b-th largest score
-  const int r = remaining;    // keys equal to T that are taken (lowest indices)
+  const uint32_t T = prefix;
+  const int r = remaining;
 
-  // Ordered compaction: thread tid covers 4 consecutive tokens per chunk.
   int carry_gt = 0, carry_eq = 0;
   for (int base = 0; base < L_b; base += 4 * kThreads) {
     const int t0 = base + 4 * tid;
@@ -152,13 +325,13 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(TopkArgs a) {
     int ngt = 0, neq = 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      key[e] = (t0 + e < L_b) ? order_key(row[t0 + e]) : 0u;
+      key[e] = key_at(row, t0 + e, L_b);
       const bool valid = t0 + e < L_b;
       ngt += (valid && key[e] > T);
       neq += (valid && key[e] == T);
     }
     int gt_before, eq_before, gt_tot, eq_tot;
-    block_scan2(ngt, neq, gt_before, eq_before, gt_tot, eq_tot, scan_sh);
+    block_scan2(ngt, neq, gt_before, eq_before, gt_tot, eq_tot, s_scan);
     gt_before += carry_gt;
     eq_before += carry_eq;
 #pragma unroll
@@ -177,14 +350,50 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(TopkArgs a) {
   }
 }
 
+// Standalone histogram of key bits 31..20 (the score kernels build the same
+// histogram on the fly).  grid (ceil(L_max / 4096), B); hist pre-zeroed.
+__global__ __launch_bounds__(256) void topk_hist_kernel(const float* scores,
+                                                        const int32_t* seq_lens,
+                                                        int32_t* hist, int L_max) {
+  __shared__ int sh[kBins];
+  const int b = blockIdx.y;
+  const int L_b = clampi(seq_lens[b], 0, L_max);
+  const int t0 = blockIdx.x * 4096;
+  if (t0 >= L_b) return;
+  for (int i = threadIdx.x; i < kBins; i += 256) sh[i] = 0;
+  __syncthreads();
+  const float* row = scores + (size_t)b * L_max;
+  const int t1 = min(t0 + 4096, L_b);
+  for (int t = t0 + threadIdx.x; t < t1; t += 256) atomicAdd(&sh[order_key(row[t]) >> 20], 1);
+  __syncthreads();
+  int32_t* gh = hist + (size_t)b * kBins;
+  for (int i = threadIdx.x; i < kBins; i += 256)
+    if (sh[i]) atomicAdd(&gh[i], sh[i]);
+}
+
+__global__ __launch_bounds__(256) void zero_kernel(int32_t* p, int n) {
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0;
+}
+
 }  // namespace
 
-hipError_t launch_topk(const Dims& d, const float* scores, const int32_t* seq_lens,
-                       const int32_t* ks, int32_t* idx, int32_t* counts, void* /*ws*/,
-                       hipStream_t s) {
-  TopkArgs a{scores, seq_lens, ks, idx, counts, d.L_max, d.k_max};
-  topk_kernel<<<d.B, kThreads, 0, s>>>(a);
+hipError_t launch_topk_select(const Dims& d, const float* scores, const int32_t* seq_lens,
+                              const int32_t* ks, const int32_t* hist, int32_t* idx,
+                              int32_t* counts, hipStream_t s) {
+  SelArgs a{scores, seq_lens, ks, hist, idx, counts, d.L_max, d.k_max};
+  topk_select_kernel<<<d.B, kThreads, 0, s>>>(a);
   return hipGetLastError();
+}
+
+hipError_t launch_topk(const Dims& d, const float* scores, const int32_t* seq_lens,
+                       const int32_t* ks, int32_t* idx, int32_t* counts, void* ws,
+                       hipStream_t s) {
+  int32_t* hist = static_cast<int32_t*>(ws);
+  const int n = d.B * kBins;
+  zero_kernel<<<(n + 255) / 256, 256, 0, s>>>(hist, n);
+  const dim3 g((d.L_max + 4095) / 4096, d.B);
+  topk_hist_kernel<<<g, 256, 0, s>>>(scores, seq_lens, hist, d.L_max);
+  return launch_topk_select(d, scores, seq_lens, ks, hist, idx, counts, s);
 }
 
 }  // namespace spec

@@ -136,6 +136,7 @@ ATTN_CASES = [
     (1, 2, 500, 8, 8, [129, 300], 300),
     (1, 1, 600, 32, 2, [520], 520),
     (3, 2, 256, 16, 16, [256, 255], 256),
+    (2, 3, 300, 32, 8, [32, 0, 7], 32),      # one split per item: direct output path
 ]
 
 
