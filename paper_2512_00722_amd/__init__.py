@@ -208,7 +208,8 @@ def score(q_r: torch.Tensor, K_r: torch.Tensor, seq_lens: torch.Tensor,
 
 
 def topk(scores: torch.Tensor, seq_lens: torch.Tensor, ks: torch.Tensor, k_max: int,
-         idx: Optional[torch.Tensor] = None, counts: Optional[torch.Tensor] = None):
+         idx: Optional[torch.Tensor] = None, counts: Optional[torch.Tensor] = None,
+         ws: Optional[torch.Tensor] = None):
     """Exact top-k of each score row (ties to the lower index), ascending
     indices [B, k_max] int32 padded with -1, and counts [B] int32."""
     lib = load_library()
@@ -219,7 +220,7 @@ def topk(scores: torch.Tensor, seq_lens: torch.Tensor, ks: torch.Tensor, k_max: 
     _i32(seq_lens, "seq_lens", B)
     _i32(ks, "ks", B)
     dims = Dims.make(B=B, L_cap=L_max, L_max=L_max, k_max=int(k_max))
-    ws, nws = _workspace(dims, OP_TOPK, scores.device, None)
+    ws, nws = _workspace(dims, OP_TOPK, scores.device, ws)
     if idx is None:
         idx = torch.empty((B, int(k_max)), dtype=torch.int32, device=scores.device)
     if counts is None:

@@ -52,7 +52,15 @@ inline int32_t* score_ws_hist(const Dims& d, void* ws) {
                                     score_part_bytes(d));
 }
 
-inline size_t topk_ws_bytes(const Dims& d) { return topk_hist_bytes(d); }
+// Per-tile lists of the selection (tokens per tile: kTopkTile): counts, the
+// tokens above the threshold bin, and the bin's candidates (key, token).
+constexpr int kTopkTile = 2048;
+inline int topk_tiles(const Dims& d) { return (d.L_max + kTopkTile - 1) / kTopkTile; }
+inline size_t topk_lists_bytes(const Dims& d) {
+  const size_t n = (size_t)d.B * topk_tiles(d);
+  return align_up(sizeof(int32_t) * 2 * n) + 3 * align_up(sizeof(int32_t) * n * kTopkTile);
+}
+inline size_t topk_ws_bytes(const Dims& d) { return topk_hist_bytes(d) + topk_lists_bytes(d); }
 
 // Attention split size (tokens of the selection per wave work item).
 int attn_split_tokens(const Dims& d);
@@ -83,7 +91,7 @@ hipError_t launch_topk(const Dims& d, const float* scores, const int32_t* seq_le
                        hipStream_t s);
 // Selection only, from a histogram already built over the same scores.
 hipError_t launch_topk_select(const Dims& d, const float* scores, const int32_t* seq_lens,
-                              const int32_t* ks, const int32_t* hist, int32_t* idx,
+                              const int32_t* ks, const int32_t* hist, void* lists, int32_t* idx,
                               int32_t* counts, hipStream_t s);
 hipError_t launch_gather(const Dims& d, const uint16_t* k_cache, const uint16_t* v_cache,
                          const int32_t* idx, const int32_t* counts, uint16_t* k_sel,

@@ -20,7 +20,7 @@ namespace {
 
 constexpr int T1 = kScoreTokensPerBlock;
 constexpr int T2 = kSoftTokensPerBlock;
-constexpr int kUnroll = 4;  // rows in flight per lane
+constexpr int kUnroll = 8;  // rows in flight per lane
 
 struct LogitsArgs {
   const uint16_t* q_r;
@@ -66,7 +66,6 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
     const size_t row = (size_t)a.H_r * d_r;
     const uint16_t* base =
         a.k_r + (size_t)b * a.kr_stride_b + (size_t)t_begin * row + (size_t)h * d_r + part * 8;
-    float* lout = a.logits + ((size_t)b * a.L_max + t_begin) * a.H_r + h;
     for (int i0 = slot; i0 < n_tok; i0 += tpi * kUnroll) {
       uint4 kv[kUnroll];
 #pragma unroll
@@ -83,14 +82,22 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
         for (int e = 0; e < 8; ++e) acc = fmaf(qv[e], kf[e], acc);
         acc = row_sum<LPH>(acc);
         const int i = i0 + u * tpi;
-        if (part == 0 && i < n_tok) {
-          lg[i * 16 + h] = acc;
-          lout[(size_t)i * a.H_r] = acc;
-        }
+        if (part == 0 && i < n_tok) lg[i * 16 + h] = acc;
       }
     }
   }
   __syncthreads();
+
+  // The block's logits leave in one coalesced burst after the stream: stores
+  // issued between the K_r loads would hold up every later load wait (the
+  // vector memory counter retires loads and stores in order).
+  {
+    float* lout = a.logits + ((size_t)b * a.L_max + t_begin) * a.H_r;
+    for (int e = threadIdx.x; e < n_tok * a.H_r; e += 256) {
+      const int i = e / a.H_r;
+      lout[e] = lg[i * 16 + (e - i * a.H_r)];
+    }
+  }
 
   // Per-head block maximum and sum of exp2(l - max): 16 lanes per head.
   const int hh = tid >> 4;

@@ -230,9 +230,10 @@ spec_status spec_step(const spec_dims* dm, const uint16_t* q_r, const uint16_t* 
   const hipStream_t s = as_stream(stream);
   hipError_t e = spec::launch_score(d, q_r, k_r, seq_lens, scores, ws_score, s);
   if (e != hipSuccess) return hip_status(e);
-  (void)ws_topk;  // the score kernels already built the selection histogram
+  // The score kernels already built the selection histogram.
   e = spec::launch_topk_select(d, scores, seq_lens, ks, spec::score_ws_hist(d, ws_score),
-                               idx_out, counts_out, s);
+                               static_cast<char*>(ws_topk) + spec::topk_hist_bytes(d), idx_out,
+                               counts_out, s);
   if (e != hipSuccess) return hip_status(e);
   if (el) {
     e = spec::launch_delta(d, idx_out, counts_out, k_cache, v_cache, el->slot_tok, el->kbuf,

@@ -7,18 +7,21 @@
 // standalone call) names the bin b1 holding the k-th key, the number c1 of
 // keys in higher bins (all selected) and the bin's population n1.
 //
-// topk_select_kernel, one 1024-thread workgroup per sequence:
-//  * fast path (c1 <= 8192, n1 <= 12288): a single pass over the row in
-//    per-thread contiguous segments appends, in token order, the tokens of
-//    higher bins to an LDS list and the bin-b1 candidates (key, token) to a
-//    second list; the remaining 20 key bits of T are resolved among the
-//    candidates only (two 10-bit LDS histogram passes), which also gives r,
-//    the number of keys equal to T to take (the lowest-index ones); the
-//    selected candidates are compacted in order and the two ascending lists
-//    are merged by binary search.  The row is read once.
-//  * general path: two more radix passes (bits 19..8, 7..0) over the row,
-//    then an ordered compaction with one workgroup scan of (#keys > T,
-//    #keys == T) per 4096 tokens.
+// Two kernels follow the histogram:
+//  * topk_classify_kernel, one 256-thread workgroup per 2048-token tile,
+//    recomputes b1 from the histogram and appends, in token order, the tile's
+//    tokens of higher bins and its bin-b1 candidates (key, token) to per-tile
+//    lists (wave-ordered appends with ballots, coalesced loads);
+//  * topk_select_kernel, one 1024-thread workgroup per sequence, gathers the
+//    per-tile lists into LDS by prefix sums, resolves the remaining 20 key
+//    bits of T among the candidates only (two 10-bit LDS histogram passes),
+//    which also gives r, the number of keys equal to T to take (the
+//    lowest-index ones), compacts the selected candidates in order and
+//    merges the two ascending lists by binary search.
+//  * When the lists would not fit (more than 8192 tokens above the bin or
+//    12288 candidates) the select kernel falls back to a general path: two
+//    more radix passes over the row (bits 19..8, 7..0) and an ordered
+//    compaction with one workgroup scan per 4096 tokens.
 // Both paths write the indices ascending, so no sort is needed.
 #include "device_common.h"
 #include "internal.h"
@@ -31,11 +34,15 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kBins = kTopkBins;  // 4096: key bits 31..20
 constexpr int kGtCap = 8192;
 constexpr int kCandCap = 12288;
+constexpr int kTile = kTopkTile;  // tokens per classify workgroup
+constexpr int kMaxTiles = 1024;   // fast path: at most one tile per select thread
 
-// Exclusive scan of two ints over the workgroup; returns the totals too.
-// Must be called by all threads.
+// Exclusive scan of two ints over a workgroup of NT threads; returns the
+// totals too.  Must be called by all threads.
+template <int NT>
 __device__ __forceinline__ void block_scan2(int a, int b, int& ea, int& eb, int& ta, int& tb,
-                                            int* sh /* [2*kWaves] */) {
+                                            int* sh /* [2*NT/64] */) {
+  constexpr int NW = NT / 64;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   int ia = a, ib = b;
@@ -50,14 +57,14 @@ __device__ __forceinline__ void block_scan2(int a, int b, int& ea, int& eb, int&
   }
   if (lane == 63) {
     sh[wave] = ia;
-    sh[kWaves + wave] = ib;
+    sh[NW + wave] = ib;
   }
   __syncthreads();
   if (wave == 0) {
-    int wa = lane < kWaves ? sh[lane] : 0;
-    int wb = lane < kWaves ? sh[kWaves + lane] : 0;
+    int wa = lane < NW ? sh[lane] : 0;
+    int wb = lane < NW ? sh[NW + lane] : 0;
 #pragma unroll
-    for (int off = 1; off < kWaves; off <<= 1) {
+    for (int off = 1; off < NW; off <<= 1) {
       const int na = __shfl_up(wa, off);
       const int nb = __shfl_up(wb, off);
       if (lane >= off) {
@@ -65,47 +72,45 @@ __device__ __forceinline__ void block_scan2(int a, int b, int& ea, int& eb, int&
         wb += nb;
       }
     }
-    if (lane < kWaves) {
+    if (lane < NW) {
       sh[lane] = wa;  // inclusive prefix over waves
-      sh[kWaves + lane] = wb;
+      sh[NW + lane] = wb;
     }
   }
   __syncthreads();
   const int pa = wave > 0 ? sh[wave - 1] : 0;
-  const int pb = wave > 0 ? sh[kWaves + wave - 1] : 0;
+  const int pb = wave > 0 ? sh[NW + wave - 1] : 0;
   ea = pa + ia - a;
   eb = pb + ib - b;
-  ta = sh[kWaves - 1];
-  tb = sh[2 * kWaves - 1];
+  ta = sh[NW - 1];
+  tb = sh[2 * NW - 1];
   __syncthreads();  // sh is reused by the next call
 }
 
 // Among `nbins` descending bins held by the workgroup (thread i owns bins
-// nbins-1-i*bpt .. with bpt = max(1, nbins/1024)), find the bin where the
+// nbins-1-i*bpt .. with bpt = max(1, nbins/NT)), find the bin where the
 // running count from the top first reaches `need`.  Writes the bin and the
 // count of keys in higher bins to sel[0], sel[1] and the bin's count to
 // sel[2].  All threads must call; the result is valid after the call.
+template <int NT>
 __device__ __forceinline__ void find_bin(const int* hist, int nbins, int need, int* sh,
                                          int* sel) {
+  constexpr int kMaxBpt = kBins / NT;
   const int tid = threadIdx.x;
-  const int bpt = nbins >= kThreads ? nbins / kThreads : 1;
+  const int bpt = nbins >= NT ? nbins / NT : 1;
   const bool owns = tid * bpt < nbins;
-  int cnt[4] = {0, 0, 0, 0};
+  int cnt[kMaxBpt];
   int local = 0;
-  if (owns) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (e < bpt) {
-        cnt[e] = hist[nbins - 1 - (tid * bpt + e)];
-        local += cnt[e];
-      }
-    }
+  for (int e = 0; e < kMaxBpt; ++e) {
+    cnt[e] = (owns && e < bpt) ? hist[nbins - 1 - (tid * bpt + e)] : 0;
+    local += cnt[e];
   }
   int before, d0, t0, t1;
-  block_scan2(local, 0, before, d0, t0, t1, sh);
+  block_scan2<NT>(local, 0, before, d0, t0, t1, sh);
   if (owns) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
+    for (int e = 0; e < kMaxBpt; ++e) {
       if (e < bpt) {
         if (before < need && need <= before + cnt[e]) {
           sel[0] = nbins - 1 - (tid * bpt + e);
@@ -124,6 +129,15 @@ __device__ __forceinline__ uint32_t key_at(const float* row, int t, int L) {
   return t < L ? order_key(row[t]) : 0u;
 }
 
+// Per-tile lists written by the classify kernel (workspace).
+struct TileLists {
+  int32_t* cnt;     // [B][n_tiles][2]: tokens above bin b1, candidates in b1
+  int32_t* gt;      // [B][n_tiles][kTile]
+  uint32_t* ckey;   // [B][n_tiles][kTile]
+  int32_t* cidx;    // [B][n_tiles][kTile]
+  int n_tiles;      // ceil(L_max / kTile)
+};
+
 struct SelArgs {
   const float* scores;  // [B][L_max]
   const int32_t* seq_lens;
@@ -131,6 +145,7 @@ struct SelArgs {
   const int32_t* hist;  // [B][4096] of key bits 31..20 over t < L_b
   int32_t* idx;         // [B][k_max]
   int32_t* counts;      // [B] or null
+  TileLists tl;
   int L_max, k_max;
 };
 
@@ -161,7 +176,7 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
   for (int i = tid; i < kBins; i += kThreads) s_hist[i] = gh[i];
   if (tid == 0) s_sel[0] = s_sel[1] = s_sel[2] = -1;
   __syncthreads();
-  find_bin(s_hist, kBins, k_b, s_scan, s_sel);
+  find_bin<kThreads>(s_hist, kBins, k_b, s_scan, s_sel);
   const int b1i = s_sel[0];
   const int c1 = s_sel[1];  // keys in higher bins: all selected
   const int n1 = s_sel[2];  // keys in bin b1
@@ -172,44 +187,60 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
   const bool hist_ok = b1i >= 0 && c1 >= 0 && c1 < k_b && r1 <= n1;
   __syncthreads();
 
-  if (hist_ok && c1 <= kGtCap && n1 <= kCandCap) {
-    // ---------------- fast path: one pass over the row ----------------
-    const int seg = (L_b + kThreads - 1) / kThreads;
-    const int s0 = min(tid * seg, L_b);
-    const int s1 = min(s0 + seg, L_b);
-    int ngt = 0, ncand = 0;
-    for (int t0 = s0; t0 < s1; t0 += 8) {
-      uint32_t k8[8];
+  const int n_tiles_b = (L_b + kTile - 1) / kTile;
+  if (hist_ok && c1 <= kGtCap && n1 <= kCandCap && n_tiles_b <= kMaxTiles) {
+    // ---------------- fast path: gather the per-tile lists ----------------
+    const int32_t* tcnt = a.tl.cnt + (size_t)b * a.tl.n_tiles * 2;
+    int* s_toff = s_cidx;  // borrowed until the candidates are gathered below
+    int tg = 0, tc = 0;
+    if (tid < n_tiles_b) {
+      tg = tcnt[2 * tid];
+      tc = tcnt[2 * tid + 1];
+    }
+    int og, oc, sum_g, sum_c;
+    block_scan2<kThreads>(tg, tc, og, oc, sum_g, sum_c, s_scan);
+    if (tid < n_tiles_b) {
+      s_toff[tid] = og;
+      s_toff[kMaxTiles + tid] = oc;
+    }
+    __syncthreads();
+    // Token p of a list lives in the tile whose offset is the last one <= p.
+    auto tile_of = [&](const int* off, int p) {
+      int lo = 0, hi = n_tiles_b - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (off[mid] <= p) lo = mid; else hi = mid - 1;
+      }
+      return lo;
+    };
+    const int ng = min(sum_g, kGtCap);
+    const int nc = min(sum_c, kCandCap);
+    int32_t* tgt = a.tl.gt + (size_t)b * a.tl.n_tiles * kTile;
+    for (int p = tid; p < ng; p += kThreads) {
+      const int t = tile_of(s_toff, p);
+      s_gt[p] = tgt[(size_t)t * kTile + (p - s_toff[t])];
+    }
+    const uint32_t* tck = a.tl.ckey + (size_t)b * a.tl.n_tiles * kTile;
+    const int32_t* tci = a.tl.cidx + (size_t)b * a.tl.n_tiles * kTile;
+    uint32_t ck_l[kCandCap / kThreads];
+    int ci_l[kCandCap / kThreads];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) k8[e] = key_at(row, t0 + e, s1);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t dg = k8[e] >> 20;
-        ngt += (t0 + e < s1) && dg > b1;
-        ncand += (t0 + e < s1) && dg == b1;
+    for (int e = 0; e < kCandCap / kThreads; ++e) {
+      const int p = tid + e * kThreads;
+      if (p < nc) {
+        const int t = tile_of(s_toff + kMaxTiles, p);
+        const size_t q = (size_t)t * kTile + (p - s_toff[kMaxTiles + t]);
+        ck_l[e] = tck[q];
+        ci_l[e] = tci[q];
       }
     }
-    int gt_pos, cand_pos, gt_tot, cand_tot;
-    block_scan2(ngt, ncand, gt_pos, cand_pos, gt_tot, cand_tot, s_scan);
-    for (int t0 = s0; t0 < s1; t0 += 8) {
-      uint32_t k8[8];
+    __syncthreads();  // s_toff (inside s_cidx) is no longer read
 #pragma unroll
-      for (int e = 0; e < 8; ++e) k8[e] = key_at(row, t0 + e, s1);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        if (t0 + e < s1) {
-          const uint32_t dg = k8[e] >> 20;
-          if (dg > b1) {
-            if (gt_pos < kGtCap) s_gt[gt_pos] = t0 + e;
-            ++gt_pos;
-          } else if (dg == b1) {
-            if (cand_pos < kCandCap) {
-              s_ckey[cand_pos] = k8[e];
-              s_cidx[cand_pos] = t0 + e;
-            }
-            ++cand_pos;
-          }
-        }
+    for (int e = 0; e < kCandCap / kThreads; ++e) {
+      const int p = tid + e * kThreads;
+      if (p < nc) {
+        s_ckey[p] = ck_l[e];
+        s_cidx[p] = ci_l[e];
       }
     }
     __syncthreads();
@@ -228,7 +259,7 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
         if ((kk & hi_mask) == T) atomicAdd(&s_hist[(kk >> shift) & 1023], 1);
       }
       __syncthreads();
-      find_bin(s_hist, 1024, remaining, s_scan, s_sel);
+      find_bin<kThreads>(s_hist, 1024, remaining, s_scan, s_sel);
       T |= (uint32_t)s_sel[0] << shift;
       remaining -= s_sel[1];
       __syncthreads();
@@ -251,7 +282,7 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
       neqT += v && ck[e] == T;
     }
     int gbef, ebef, gtot, etot;
-    block_scan2(ngtT, neqT, gbef, ebef, gtot, etot, s_scan);  // also orders the reads above
+    block_scan2<kThreads>(ngtT, neqT, gbef, ebef, gtot, etot, s_scan);  // also orders the reads above
     int* s_selv = reinterpret_cast<int*>(s_ckey);
 #pragma unroll
     for (int e = 0; e < 12; ++e) {
@@ -309,7 +340,7 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
           atomicAdd(&s_hist[(k8[e] >> shift) & (nbins - 1)], 1);
     }
     __syncthreads();
-    find_bin(s_hist, nbins, remaining, s_scan, s_sel);
+    find_bin<kThreads>(s_hist, nbins, remaining, s_scan, s_sel);
     prefix |= (uint32_t)s_sel[0] << shift;
     mask |= (uint32_t)(nbins - 1) << shift;
     remaining -= s_sel[1];
@@ -331,7 +362,7 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
       neq += (valid && key[e] == T);
     }
     int gt_before, eq_before, gt_tot, eq_tot;
-    block_scan2(ngt, neq, gt_before, eq_before, gt_tot, eq_tot, s_scan);
+    block_scan2<kThreads>(ngt, neq, gt_before, eq_before, gt_tot, eq_tot, s_scan);
     gt_before += carry_gt;
     eq_before += carry_eq;
 #pragma unroll
@@ -347,6 +378,105 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
     }
     carry_gt += gt_tot;
     carry_eq += eq_tot;
+  }
+}
+
+constexpr int kClsThreads = 256;
+constexpr int kClsWaves = kClsThreads / 64;
+constexpr int kClsPerLane = kTile / kClsThreads;  // 8 tokens per lane
+
+struct ClsArgs {
+  const float* scores;
+  const int32_t* seq_lens;
+  const int32_t* ks;
+  const int32_t* hist;
+  TileLists tl;
+  int L_max, k_max;
+};
+
+// grid (n_tiles, B).  Wave w of a tile owns tokens [t0 + 512w, t0 + 512w + 512);
+// lane i reads tokens base + 64j + i.  An element's list slot is its wave's
+// offset plus the flagged elements before it in (j, lane) order.
+__global__ __launch_bounds__(kClsThreads) void topk_classify_kernel(ClsArgs a) {
+  __shared__ int s_hist[kBins];
+  __shared__ int s_scan[2 * kClsWaves];
+  __shared__ int s_sel[4];
+  __shared__ int s_wcnt[2 * kClsWaves];
+  const int b = blockIdx.y;
+  const int tile = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int L_b = clampi(a.seq_lens[b], 0, a.L_max);
+  const int k_b = clampi(a.ks[b], 0, min(L_b, a.k_max));
+  const int t0 = tile * kTile;
+  if (k_b == 0 || k_b == L_b || t0 >= L_b) return;  // uniform: nothing to classify
+
+  const int32_t* gh = a.hist + (size_t)b * kBins;
+  for (int i = tid; i < kBins; i += kClsThreads) s_hist[i] = gh[i];
+  if (tid == 0) s_sel[0] = s_sel[1] = s_sel[2] = -1;
+  __syncthreads();
+  find_bin<kClsThreads>(s_hist, kBins, k_b, s_scan, s_sel);
+  const int b1i = s_sel[0], c1 = s_sel[1], n1 = s_sel[2];
+  // Same decision as the select kernel: it only reads the lists on its fast path.
+  if (!(b1i >= 0 && c1 >= 0 && c1 < k_b && k_b - c1 <= n1) || c1 > kGtCap || n1 > kCandCap)
+    return;
+  const uint32_t b1 = (uint32_t)b1i;
+
+  const float* row = a.scores + (size_t)b * a.L_max;
+  const int lane = tid & 63;
+  const int wv = tid >> 6;
+  const int w0 = min(t0 + wv * (kTile / kClsWaves), L_b);
+  const int w1 = min(w0 + kTile / kClsWaves, L_b);
+  uint32_t kk[kClsPerLane];
+#pragma unroll
+  for (int j = 0; j < kClsPerLane; ++j) kk[j] = key_at(row, w0 + 64 * j + lane, w1);
+  int wgt = 0, wcand = 0;
+#pragma unroll
+  for (int j = 0; j < kClsPerLane; ++j) {
+    const bool in = w0 + 64 * j + lane < w1;
+    const uint32_t dg = kk[j] >> 20;
+    wgt += __popcll(__ballot(in && dg > b1));
+    wcand += __popcll(__ballot(in && dg == b1));
+  }
+  if (lane == 0) {
+    s_wcnt[wv] = wgt;
+    s_wcnt[kClsWaves + wv] = wcand;
+  }
+  __syncthreads();
+  int gpos = 0, cpos = 0, gtot = 0, ctot = 0;
+#pragma unroll
+  for (int i = 0; i < kClsWaves; ++i) {
+    if (i < wv) {
+      gpos += s_wcnt[i];
+      cpos += s_wcnt[kClsWaves + i];
+    }
+    gtot += s_wcnt[i];
+    ctot += s_wcnt[kClsWaves + i];
+  }
+  const size_t tb = ((size_t)b * a.tl.n_tiles + tile);
+  int32_t* gt = a.tl.gt + tb * kTile;
+  uint32_t* ck = a.tl.ckey + tb * kTile;
+  int32_t* ci = a.tl.cidx + tb * kTile;
+  const uint64_t lt_mask = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int j = 0; j < kClsPerLane; ++j) {
+    const int t = w0 + 64 * j + lane;
+    const bool in = t < w1;
+    const uint32_t dg = kk[j] >> 20;
+    const uint64_t mg = __ballot(in && dg > b1);
+    const uint64_t mc = __ballot(in && dg == b1);
+    if (in && dg > b1) {
+      gt[gpos + __popcll(mg & lt_mask)] = t;
+    } else if (in && dg == b1) {
+      const int q = cpos + __popcll(mc & lt_mask);
+      ck[q] = kk[j];
+      ci[q] = t;
+    }
+    gpos += __popcll(mg);
+    cpos += __popcll(mc);
+  }
+  if (tid == 0) {
+    a.tl.cnt[tb * 2] = gtot;
+    a.tl.cnt[tb * 2 + 1] = ctot;
   }
 }
 
@@ -375,12 +505,31 @@ __global__ __launch_bounds__(256) void zero_kernel(int32_t* p, int n) {
   for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0;
 }
 
+TileLists tile_lists(const Dims& d, void* lists) {
+  TileLists tl;
+  const int n_tiles = topk_tiles(d);
+  const size_t n = (size_t)d.B * n_tiles;
+  char* p = static_cast<char*>(lists);
+  tl.cnt = reinterpret_cast<int32_t*>(p);
+  p += align_up(sizeof(int32_t) * 2 * n);
+  tl.gt = reinterpret_cast<int32_t*>(p);
+  p += align_up(sizeof(int32_t) * n * kTile);
+  tl.ckey = reinterpret_cast<uint32_t*>(p);
+  p += align_up(sizeof(uint32_t) * n * kTile);
+  tl.cidx = reinterpret_cast<int32_t*>(p);
+  tl.n_tiles = n_tiles;
+  return tl;
+}
+
 }  // namespace
 
 hipError_t launch_topk_select(const Dims& d, const float* scores, const int32_t* seq_lens,
-                              const int32_t* ks, const int32_t* hist, int32_t* idx,
+                              const int32_t* ks, const int32_t* hist, void* lists, int32_t* idx,
                               int32_t* counts, hipStream_t s) {
-  SelArgs a{scores, seq_lens, ks, hist, idx, counts, d.L_max, d.k_max};
+  const TileLists tl = tile_lists(d, lists);
+  ClsArgs c{scores, seq_lens, ks, hist, tl, d.L_max, d.k_max};
+  topk_classify_kernel<<<dim3(tl.n_tiles, d.B), kClsThreads, 0, s>>>(c);
+  SelArgs a{scores, seq_lens, ks, hist, idx, counts, tl, d.L_max, d.k_max};
   topk_select_kernel<<<d.B, kThreads, 0, s>>>(a);
   return hipGetLastError();
 }
@@ -393,7 +542,8 @@ hipError_t launch_topk(const Dims& d, const float* scores, const int32_t* seq_le
   zero_kernel<<<(n + 255) / 256, 256, 0, s>>>(hist, n);
   const dim3 g((d.L_max + 4095) / 4096, d.B);
   topk_hist_kernel<<<g, 256, 0, s>>>(scores, seq_lens, hist, d.L_max);
-  return launch_topk_select(d, scores, seq_lens, ks, hist, idx, counts, s);
+  return launch_topk_select(d, scores, seq_lens, ks, hist,
+                            static_cast<char*>(ws) + topk_hist_bytes(d), idx, counts, s);
 }
 
 }  // namespace spec
