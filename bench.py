@@ -27,7 +27,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decode steps/s of retrieve+top-k+sparse attn; achieved HBM GB/s vs peak"
 PEAK_HBM_GBPS = 8000.0  # MI355X published HBM3E bandwidth
-ATTN_SRC = os.path.join(ROOT, "paper_2512_00722_amd", "csrc", "attn.hip")
+CSRC = os.path.join(ROOT, "paper_2512_00722_amd", "csrc")
+ATTN_SOURCES = ("attn.hip", "device_common.h", "internal.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
 
 
@@ -53,14 +54,27 @@ def attn_bytes(w, counts):
     return w.n_layers * (kb * w.H_kv * w.d * 2 * 2 + w.B * w.H_q * w.d * 2 + w.B * w.H_q * w.d * 4)
 
 
+def attn_source_digest():
+    """sha256 of the attention kernel's sources with comments and blank
+    lines removed: it changes when the code does, not when a comment does."""
+    import re
+    h = hashlib.sha256()
+    for name in ATTN_SOURCES:
+        txt = open(os.path.join(CSRC, name)).read()
+        txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+        txt = re.sub(r"//[^\n]*", "", txt)
+        lines = [ln.rstrip() for ln in txt.splitlines() if ln.strip()]
+        h.update(("\n".join(lines) + "\n").encode())
+    return h.hexdigest()
+
+
 def stored_traffic():
     """Per-launch HBM bytes of the attention kernels measured with rocprofv3
-    PMC counters, valid only for the attention source they were taken on."""
+    PMC counters, valid only for the attention code they were taken on."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
-        sha = hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()
-        if t.get("attn_source_sha256") != sha:
+        if t.get("attn_code_sha256") != attn_source_digest():
             return None
         return t.get("bytes_per_launch")
     except (OSError, ValueError):

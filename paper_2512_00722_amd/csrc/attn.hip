@@ -3,21 +3,26 @@
 // KV head, which is read directly -- no repeat_kv copy).
 //
 // Split-K flash decode.  One wavefront owns a work item (layer, sequence,
-// KV head g, split of the selection) and walks it in chunks of 64 selected
+// KV head g, split of the selection) and walks it in chunks of 32 selected
 // tokens:
-//  * Q.K^T on the matrix cores: v_mfma_f32_16x16x32_bf16 with A = the G
-//    query heads of the group (rows >= G are zero) and B = 16 selected K rows,
-//    each lane feeding one 16-byte slice of one row straight from HBM, so K
-//    needs no LDS staging and no bf16->fp32 conversion.  The useful fraction
-//    of the tile is G/16, irrelevant here: the op is HBM-bound by two orders
-//    of magnitude.
-//  * online softmax in log2 units (the scale and log2(e) are folded into one
-//    multiply), P and the rescale factors go through a 4 KB LDS slice;
-//  * P.V on the vector ALUs: lane (q, c) owns the 8 dims 8c..8c+7 of every
-//    4th token of the chunk, accumulating G x 8 fp32 values; V rows arrive as
-//    16-byte loads, four full 256-byte rows per load instruction.
-// A second kernel merges the per-split (max, sum, acc) partials with a
-// log-sum-exp combine and writes fp32 out and lse.
+//  * the item's row indices are staged in LDS first, so no chunk waits on an
+//    index load;
+//  * S^T = K Q^T on the matrix cores (v_mfma_f32_16x16x32_bf16): A = 16
+//    selected K rows, each lane feeding one 16-byte slice of one row straight
+//    from HBM (no LDS staging, no conversion); B = Q^T with the G query heads
+//    of the group as columns (columns >= G are zero).  Only G/16 of the tile
+//    is useful, which does not matter: the op is HBM-bound;
+//  * online softmax in log2 units (scale and log2(e) folded into one
+//    multiply); the four lanes that hold one head combine with permlane swaps;
+//  * O^T += V^T P^T on the matrix cores: V rows arrive as 16-byte loads (four
+//    whole 256-byte rows per instruction), are staged in LDS and read back
+//    transposed with ds_read_b64_tr_b16; P is split into a bf16 high part and
+//    a bf16 low part (two MFMAs), which keeps it to ~2^-16 relative;
+//  * K and V of chunk c+1 are requested as soon as chunk c's registers are
+//    consumed and stay in flight through chunk c's softmax and MFMAs.
+// When one split covers the whole selection the wavefront normalises and
+// writes out/lse itself; otherwise a second kernel merges the per-split
+// (max, sum, acc) partials with a log-sum-exp combine.
 #include "device_common.h"
 #include "internal.h"
 
@@ -434,9 +439,11 @@ hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
              d.scale * kLog2e};
   // Persistent grid: at most as many workgroups as the machine holds at once
   // (the register budget allows 2 wavefronts per SIMD: 2 workgroups per CU).
-  int dev = 0, n_cu = 256;
-  if (hipGetDevice(&dev) == hipSuccess)
-    hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+  int dev = 0, n_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n_cu <= 0)
+    n_cu = 256;
   const int64_t want = (n_items + kWaves - 1) / kWaves;
   const int64_t cap = (int64_t)n_cu * kBlocksPerCU;
   const dim3 grid((unsigned)(want < cap ? want : cap));

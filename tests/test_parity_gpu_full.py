@@ -1,0 +1,77 @@
+"""Full-size decode-step workloads through the fused step (the launch
+configuration the benchmark times), checked against the fp64 oracle on
+sampled sequences and layers, and by properties that hold at any size on all
+sequences."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2512_00722_amd as spec
+from tests.gpu_helpers import SCORE_ABS, SCORE_REL, TOL_ATTN, announce, f64, need_gpu
+from workloads import WORKLOADS, generate
+
+pytestmark = pytest.mark.gpu
+
+FIXED = ["b1_l4096_k512_1layer", "b8_l32768_k2048_32layers", "b32_l16384_k1024_hr16",
+         "b1_l131072_k4096_g8"]
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return need_gpu()
+
+
+def _sample_layers(n):
+    return sorted({0, n // 2, n - 1})
+
+
+@pytest.mark.parametrize("name", FIXED)
+def test_full_size_step(dev, name):
+    w = WORKLOADS[name]
+    announce(f"full-size step {name}")
+    x = generate(w, seed=0, device=dev)
+    r = spec.step(x["q_r"], x["K_r"], x["seq_lens"], x["ks"], x["q"], x["K"], x["V"], k_max=w.k,
+                  with_scores=True, with_lse=True)
+    torch.cuda.synchronize()
+    idx = r["idx"].cpu().numpy()
+    cnt = r["counts"].cpu().numpy()
+    sc = r["scores"].cpu().numpy().astype(np.float64)
+    lens = x["seq_lens"].cpu().numpy()
+    ks = x["ks"].cpu().numpy()
+
+    # properties on every sequence
+    for b in range(w.B):
+        L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
+        assert cnt[b] == kb
+        sel = idx[b, :kb]
+        assert np.all(np.diff(sel) > 0) and sel[0] >= 0 and sel[-1] < L
+        assert np.all(idx[b, kb:] == -1)
+        assert abs(sc[b, :L].sum() - w.H_r) < 1e-3 * w.H_r       # softmax rows sum to 1
+        assert sel.tolist() == oracle.topk_indices(sc[b, :L], kb).tolist()  # exact on fp32 keys
+    assert np.all(np.isfinite(r["out"].cpu().numpy()))
+
+    # element-wise parity on sampled sequences and layers
+    for b in sorted({0, w.B - 1}):
+        L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
+        s64 = oracle.retrieval_scores(f64(x["q_r"][b]), f64(x["K_r"][b, :L]), L)
+        err = np.abs(sc[b, :L] - s64)
+        assert np.all(err <= SCORE_ABS + SCORE_REL * s64), err.max()
+        ok, info = oracle.accept_index_set(s64, kb, idx[b, :kb])
+        assert ok, info
+        print(f"b={b}: tie-band population {info['band_pop']}, set difference {info['sym_diff']}")
+        heavy = x["heavy"][b]
+        if len(heavy):
+            recall = np.isin(heavy, idx[b, :kb]).mean()
+            print(f"b={b}: planted-token recall {recall:.4f}")
+            assert recall >= 0.99
+        sel_t = torch.as_tensor(idx[b, :kb], device=dev, dtype=torch.long)
+        for layer in _sample_layers(w.n_layers):
+            Ks = f64(x["K"][layer, b, sel_t])
+            Vs = f64(x["V"][layer, b, sel_t])
+            want, wl = oracle.sparse_gqa_attention(f64(x["q"][layer, b]), Ks, Vs, np.arange(kb))
+            got = r["out"][layer, b].cpu().numpy()
+            assert np.abs(got - want).max() <= TOL_ATTN, (layer, np.abs(got - want).max())
+            assert np.abs(r["lse"][layer, b].cpu().numpy() - wl).max() <= TOL_ATTN
+    del x, r
+    torch.cuda.empty_cache()
