@@ -22,30 +22,78 @@ struct GatherArgs {
   uint16_t* k_sel;        // [n_layers][B][k_max][H_kv][d]
   uint16_t* v_sel;
   int64_t stride_layer, stride_b, row_elems;
-  int B, k_max, L_cap;
+  int B, k_max, L_cap, n_layers;
 };
 
-// grid (ceil(k_max / 16), B, n_layers)
+// 16-byte store that bypasses cache retention (the rows are consumed later,
+// by another launch, and exceed the caches anyway).
+__device__ __forceinline__ void stg16_stream(uint16_t* p, const uint4& v) {
+  uint4* q = reinterpret_cast<uint4*>(p);
+  __builtin_nontemporal_store(v.x, &q->x);
+  __builtin_nontemporal_store(v.y, &q->y);
+  __builtin_nontemporal_store(v.z, &q->z);
+  __builtin_nontemporal_store(v.w, &q->w);
+}
+
+// Copies of whole rows.  The block's (source row, destination row) pairs are
+// staged in LDS first (one index round trip), then every lane issues all its
+// loads (kCopyUnroll K and V chunks) before its first store, so each lane
+// keeps 2*kCopyUnroll 16-byte loads in flight.
+constexpr int kCopyUnroll = 8;
+
+__device__ __forceinline__ void copy_rows(const uint16_t* __restrict__ ks,
+                                          const uint16_t* __restrict__ vs,
+                                          uint16_t* __restrict__ kd, uint16_t* __restrict__ vd,
+                                          int nrows, int cpr, int64_t row_elems,
+                                          const int64_t* src_row, const int64_t* dst_row) {
+  const int total = nrows * cpr;
+  for (int x0 = threadIdx.x; x0 < total; x0 += 256 * kCopyUnroll) {
+    uint4 kr[kCopyUnroll], vr[kCopyUnroll];
+    int64_t dst[kCopyUnroll];
+#pragma unroll
+    for (int u = 0; u < kCopyUnroll; ++u) {
+      const int x = x0 + 256 * u;
+      dst[u] = -1;
+      if (x < total) {
+        const int r = x / cpr;
+        const int c = x - r * cpr;
+        const int64_t src = src_row[r] * row_elems + 8 * c;
+        dst[u] = dst_row[r] * row_elems + 8 * c;
+        kr[u] = ldg16_stream(ks + src);
+        vr[u] = ldg16_stream(vs + src);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kCopyUnroll; ++u) {
+      if (dst[u] >= 0) {
+        stg16_stream(kd + dst[u], kr[u]);
+        stg16_stream(vd + dst[u], vr[u]);
+      }
+    }
+  }
+}
+
+// grid (ceil(k_max / 16), B): 16 selected rows of one sequence, every layer.
 __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
   const int b = blockIdx.y;
-  const int layer = blockIdx.z;
   const int count = clampi(a.counts[b], 0, a.k_max);
   const int j0 = blockIdx.x * kRowsPerBlock;
   if (j0 >= count) return;
   const int nrows = min(kRowsPerBlock, count - j0);
   const int cpr = (int)(a.row_elems / 8);  // 16-byte chunks per row
-  const uint16_t* ks = a.k + (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b;
-  const uint16_t* vs = a.v + (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b;
-  const int64_t dst0 = ((int64_t)layer * a.B + b) * a.k_max * a.row_elems;
-  for (int x = threadIdx.x; x < nrows * cpr; x += 256) {
-    const int r = x / cpr;
-    const int c = x - r * cpr;
-    const int j = j0 + r;
-    const int tok = clampi(a.idx[(size_t)b * a.k_max + j], 0, a.L_cap - 1);
-    const int64_t src = (int64_t)tok * a.row_elems + 8 * c;
-    const int64_t dst = dst0 + (int64_t)j * a.row_elems + 8 * c;
-    *reinterpret_cast<uint4*>(a.k_sel + dst) = ldg16(ks + src);
-    *reinterpret_cast<uint4*>(a.v_sel + dst) = ldg16(vs + src);
+  __shared__ int64_t src_row[kRowsPerBlock], dst_row[kRowsPerBlock];
+  if (threadIdx.x < nrows) {
+    const int j = j0 + threadIdx.x;
+    src_row[threadIdx.x] = clampi(a.idx[(size_t)b * a.k_max + j], 0, a.L_cap - 1);
+    dst_row[threadIdx.x] = (int64_t)b * a.k_max + j;
+  }
+  __syncthreads();
+  const int64_t layer_rows = (int64_t)a.B * a.k_max;  // rows per layer of the output
+  for (int layer = 0; layer < a.n_layers; ++layer) {
+    const int64_t off = (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b;
+    const int64_t doff = layer * layer_rows * a.row_elems;
+    copy_rows(a.k + off, a.v + off, a.k_sel + doff, a.v_sel + doff, nrows, cpr, a.row_elems,
+              src_row, dst_row);
   }
 }
 
@@ -188,32 +236,31 @@ struct CopyArgs {
   uint16_t* kbuf;
   uint16_t* vbuf;
   int64_t stride_layer, stride_b, row_elems;
-  int B, k_max, L_cap;
+  int B, k_max, L_cap, n_layers;
 };
 
-// grid (ceil(k_max / 16), B, n_layers): copy the loaded rows into their slots.
+// grid (ceil(k_max / 16), B): copy 16 loaded rows of one sequence into their
+// slots, every layer.
 __global__ __launch_bounds__(256) void elastic_copy_kernel(CopyArgs a) {
   const int b = blockIdx.y;
-  const int layer = blockIdx.z;
   const int n = clampi(a.n_changed[b], 0, a.k_max);
   const int i0 = blockIdx.x * kRowsPerBlock;
   if (i0 >= n) return;
   const int nrows = min(kRowsPerBlock, n - i0);
   const int cpr = (int)(a.row_elems / 8);
-  const int32_t* loads = a.loads + (size_t)b * a.k_max * 2;
-  const uint16_t* ks = a.k + (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b;
-  const uint16_t* vs = a.v + (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b;
-  const int64_t dst0 = ((int64_t)layer * a.B + b) * a.k_max * a.row_elems;
-  for (int x = threadIdx.x; x < nrows * cpr; x += 256) {
-    const int r = x / cpr;
-    const int c = x - r * cpr;
-    const int i = i0 + r;
-    const int slot = clampi(loads[2 * i], 0, a.k_max - 1);
-    const int tok = clampi(loads[2 * i + 1], 0, a.L_cap - 1);
-    const int64_t src = (int64_t)tok * a.row_elems + 8 * c;
-    const int64_t dst = dst0 + (int64_t)slot * a.row_elems + 8 * c;
-    *reinterpret_cast<uint4*>(a.kbuf + dst) = ldg16(ks + src);
-    *reinterpret_cast<uint4*>(a.vbuf + dst) = ldg16(vs + src);
+  __shared__ int64_t src_row[kRowsPerBlock], dst_row[kRowsPerBlock];
+  if (threadIdx.x < nrows) {
+    const int32_t* ld = a.loads + ((size_t)b * a.k_max + i0 + threadIdx.x) * 2;
+    dst_row[threadIdx.x] = (int64_t)b * a.k_max + clampi(ld[0], 0, a.k_max - 1);
+    src_row[threadIdx.x] = clampi(ld[1], 0, a.L_cap - 1);
+  }
+  __syncthreads();
+  const int64_t layer_rows = (int64_t)a.B * a.k_max;
+  for (int layer = 0; layer < a.n_layers; ++layer) {
+    const int64_t off = (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b;
+    const int64_t doff = layer * layer_rows * a.row_elems;
+    copy_rows(a.k + off, a.v + off, a.kbuf + doff, a.vbuf + doff, nrows, cpr, a.row_elems,
+              src_row, dst_row);
   }
 }
 
@@ -223,8 +270,8 @@ hipError_t launch_gather(const Dims& d, const uint16_t* k_cache, const uint16_t*
                          const int32_t* idx, const int32_t* counts, uint16_t* k_sel,
                          uint16_t* v_sel, hipStream_t s) {
   GatherArgs a{k_cache, v_cache, idx, counts, k_sel, v_sel, d.kv_stride_layer, d.kv_stride_b,
-               (int64_t)d.H_kv * d.d, d.B, d.k_max, d.L_cap};
-  const dim3 grid((d.k_max + kRowsPerBlock - 1) / kRowsPerBlock, d.B, d.n_layers);
+               (int64_t)d.H_kv * d.d, d.B, d.k_max, d.L_cap, d.n_layers};
+  const dim3 grid((d.k_max + kRowsPerBlock - 1) / kRowsPerBlock, d.B);
   gather_kernel<<<grid, 256, 0, s>>>(a);
   return hipGetLastError();
 }
@@ -241,8 +288,8 @@ hipError_t launch_delta(const Dims& d, const int32_t* idx_now, const int32_t* co
   PlanArgs p{idx_now, counts, slot_tok, n_changed, loads, d.k_max, d.L_cap};
   elastic_plan_kernel<<<d.B, kPlanThreads, elastic_plan_lds_bytes(d), s>>>(p);
   CopyArgs c{k_cache, v_cache, loads, n_changed, kbuf, vbuf, d.kv_stride_layer, d.kv_stride_b,
-             (int64_t)d.H_kv * d.d, d.B, d.k_max, d.L_cap};
-  const dim3 grid((d.k_max + kRowsPerBlock - 1) / kRowsPerBlock, d.B, d.n_layers);
+             (int64_t)d.H_kv * d.d, d.B, d.k_max, d.L_cap, d.n_layers};
+  const dim3 grid((d.k_max + kRowsPerBlock - 1) / kRowsPerBlock, d.B);
   elastic_copy_kernel<<<grid, 256, 0, s>>>(c);
   return hipGetLastError();
 }

@@ -9,7 +9,7 @@ import torch
 import oracle
 import paper_2512_00722_amd as spec
 from tests.gpu_helpers import SCORE_ABS, SCORE_REL, TOL_ATTN, announce, f64, need_gpu
-from workloads import WORKLOADS, generate
+from workloads import WORKLOADS, elastic_sequence, generate
 
 pytestmark = pytest.mark.gpu
 
@@ -74,4 +74,76 @@ def test_full_size_step(dev, name):
             assert np.abs(got - want).max() <= TOL_ATTN, (layer, np.abs(got - want).max())
             assert np.abs(r["lse"][layer, b].cpu().numpy() - wl).max() <= TOL_ATTN
     del x, r
+    torch.cuda.empty_cache()
+
+
+def test_full_size_elastic_sequence(dev):
+    """The ragged 64-sequence workload over its 16 appended-token steps with
+    elastic loading.  Every sequence, every step: the slot buffer holds
+    exactly the selected set, and the rows loaded equal |S_now - S_last|.
+    Sampled sequences: scores vs fp64, index-set acceptance, the slot->token
+    map equals the oracle's elastic update of the previous map, held K/V rows
+    are bit-exact copies, and attention matches the oracle on sampled layers."""
+    w = WORKLOADS["b64_ragged_l2k_16k_elastic"]
+    announce(f"full-size elastic sequence {w.name}")
+    x = generate(w, seed=0, device=dev)
+    e = elastic_sequence(w, x, seed=0, device=dev)
+    st = spec.ElasticState(w.n_layers, w.B, w.k, w.H_kv, w.d, dev)
+    ks = x["ks"].cpu().numpy()
+    sample = sorted({0, w.B // 2, w.B - 1})
+    slot_ref = {b: np.full(w.k, -1, dtype=np.int64) for b in sample}
+    prev = [np.zeros(0, dtype=np.int64) for _ in range(w.B)]
+    overlap = []
+    for s in range(w.steps):
+        lens_t = e["seq_lens"][s]
+        r = spec.step(q_r=e["q_r"][s], K_r=x["K_r"], seq_lens=lens_t, ks=x["ks"], q=e["q"][s],
+                      K=x["K"], V=x["V"], k_max=w.k, elastic=st, with_scores=True, with_lse=True)
+        torch.cuda.synchronize()
+        lens = lens_t.cpu().numpy()
+        idx = r["idx"].cpu().numpy()
+        cnt = r["counts"].cpu().numpy()
+        sc = r["scores"].cpu().numpy().astype(np.float64)
+        slots = st.slot_tok.cpu().numpy()
+        nch = st.n_changed.cpu().numpy()
+        for b in range(w.B):
+            L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
+            sel = idx[b, :kb].astype(np.int64)
+            assert cnt[b] == kb
+            assert sel.tolist() == oracle.topk_indices(sc[b, :L], kb).tolist(), (s, b)
+            assert sorted(slots[b, :kb].tolist()) == sel.tolist(), (s, b)
+            assert np.all(slots[b, kb:] == -1)
+            assert nch[b] == len(np.setdiff1d(sel, prev[b])), (s, b)
+            if s > 0:
+                overlap.append(len(np.intersect1d(sel, prev[b])) / kb)
+            prev[b] = sel
+        for b in sample:
+            L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
+            s64 = oracle.retrieval_scores(f64(e["q_r"][s, b]), f64(x["K_r"][b, :L]), L)
+            err = np.abs(sc[b, :L] - s64)
+            assert np.all(err <= SCORE_ABS + SCORE_REL * s64), (s, b, err.max())
+            ok, info = oracle.accept_index_set(s64, kb, idx[b, :kb])
+            assert ok, (s, b, info)
+            slot_ref[b], loads = oracle.elastic_update(slot_ref[b], idx[b, :kb])
+            assert slots[b].tolist() == slot_ref[b].tolist(), (s, b)
+            assert len(loads) == nch[b]
+            held = torch.as_tensor(np.nonzero(slot_ref[b] >= 0)[0], device=dev)
+            toks = torch.as_tensor(slot_ref[b][slot_ref[b] >= 0], device=dev)
+            for layer in (0, w.n_layers - 1):
+                assert torch.equal(st.kbuf[layer, b, held].view(torch.int16),
+                                   x["K"][layer, b, toks].view(torch.int16)), (s, b, layer)
+                assert torch.equal(st.vbuf[layer, b, held].view(torch.int16),
+                                   x["V"][layer, b, toks].view(torch.int16)), (s, b, layer)
+            if s in (0, w.steps - 1):
+                sel_t = torch.as_tensor(idx[b, :kb], device=dev, dtype=torch.long)
+                for layer in _sample_layers(w.n_layers):
+                    Ks = f64(x["K"][layer, b, sel_t])
+                    Vs = f64(x["V"][layer, b, sel_t])
+                    want, wl = oracle.sparse_gqa_attention(f64(e["q"][s, layer, b]), Ks, Vs,
+                                                           np.arange(kb))
+                    got = r["out"][layer, b].cpu().numpy()
+                    assert np.abs(got - want).max() <= TOL_ATTN, (s, b, layer)
+                    assert np.abs(r["lse"][layer, b].cpu().numpy() - wl).max() <= TOL_ATTN
+    print(f"adjacent-step overlap: min {min(overlap):.3f} mean {np.mean(overlap):.3f}")
+    assert np.mean(overlap) > 0.7
+    del x, e, st, r
     torch.cuda.empty_cache()

@@ -31,7 +31,7 @@ import numpy as np
 import torch
 
 __all__ = ["Workload", "WORKLOADS", "BENCH_WORKLOAD", "tensor_seed",
-           "generate", "algorithmic_bytes", "small_workload"]
+           "generate", "elastic_sequence", "algorithmic_bytes", "small_workload"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -194,6 +194,42 @@ def generate(w: Workload, seed: int = 0, device="cpu", with_kv: bool = True,
             V[i].normal_(generator=_gen(device, seed, f"V.{layer}"))
         out["K"], out["V"] = K, V
     return out
+
+
+def elastic_sequence(w: Workload, x: dict, seed: int = 0, device=None):
+    """Per-step inputs of a run of `w.steps` decode steps on the inputs `x`
+    drawn by `generate` (one appended token per step).
+
+    Step s sees seq_lens + s tokens: the rows past the initial lengths were
+    drawn N(0,1) and unplanted by `generate`, so appending a token only moves
+    the length.  The retrieval query drifts as an AR(1) process,
+    q_r(s+1) = drift * q_r(s) + sqrt(1 - drift^2) * xi_s with xi_s ~ N(0,1),
+    carried in fp32 and rounded to bf16 per step; the LLM queries are fresh
+    N(0,1) draws each step.  The budgets stay those of the initial lengths.
+
+    Returns q_r [S, B, H_r, d_r] bf16, q [S, n_layers, B, H_q, d] bf16 and
+    seq_lens [S, B] int32 (S = w.steps).
+    """
+    device = torch.device(device if device is not None else x["q_r"].device)
+    S = w.steps
+    lens0 = x["seq_lens"].to(device=device, dtype=torch.int64)
+    if int((lens0 + S - 1).max()) > w.L_cap:
+        raise ValueError("the appended tokens do not fit the capacity")
+    qr = x["q_r"].to(device).float()
+    c = float(np.sqrt(1.0 - w.drift * w.drift))
+    q_r_steps = torch.empty((S,) + tuple(qr.shape), dtype=torch.bfloat16, device=device)
+    q_steps = torch.empty((S, w.n_layers, w.B, w.H_q, w.d), dtype=torch.bfloat16, device=device)
+    for s in range(S):
+        if s > 0:
+            xi = torch.randn(qr.shape, generator=_gen(device, seed, f"q_r.drift.{s}"),
+                             device=device, dtype=torch.float32)
+            qr = w.drift * qr + c * xi
+        q_r_steps[s] = qr.to(torch.bfloat16)
+        q_steps[s] = torch.randn((w.n_layers, w.B, w.H_q, w.d),
+                                 generator=_gen(device, seed, f"q.step.{s}"), device=device,
+                                 dtype=torch.float32).to(torch.bfloat16)
+    lens = (lens0[None, :] + torch.arange(S, device=device)[:, None]).to(torch.int32)
+    return {"q_r": q_r_steps, "q": q_steps, "seq_lens": lens}
 
 
 def algorithmic_bytes(w: Workload, seq_lens, ks, delta_rows: int = 0) -> int:
