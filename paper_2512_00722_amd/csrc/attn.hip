@@ -2,10 +2,11 @@
 // tokens; Sec. 4.3 "Support for GQA": the G query heads of a group share one
 // KV head, which is read directly -- no repeat_kv copy).
 //
-// Split-K flash decode.  One wavefront owns a work item (layer, sequence,
-// KV head g, split of the selection) and walks it in chunks of 32 selected
-// tokens:
-//  * the item's row indices are staged in LDS first, so no chunk waits on an
+// Flash decode over work units (layer, sequence, KV head g, split of the
+// selection).  One workgroup per CU runs one wavefront per SIMD; its
+// wavefronts take units from a contiguous range on demand.  A wavefront walks
+// its unit in chunks of 32 selected tokens:
+//  * the unit's row indices are staged in LDS first, so no chunk waits on an
 //    index load;
 //  * S^T = K Q^T on the matrix cores (v_mfma_f32_16x16x32_bf16): A = 16
 //    selected K rows, each lane feeding one 16-byte slice of one row straight
@@ -20,9 +21,9 @@
 //    a bf16 low part (two MFMAs), which keeps it to ~2^-16 relative;
 //  * K and V of chunk c+1 are requested as soon as chunk c's registers are
 //    consumed and stay in flight through chunk c's softmax and MFMAs.
-// When one split covers the whole selection the wavefront normalises and
-// writes out/lse itself; otherwise a second kernel merges the per-split
-// (max, sum, acc) partials with a log-sum-exp combine.
+// A unit that covers a whole selection normalises and writes out/lse itself;
+// split selections leave (max, sum, acc) partials that a second kernel merges
+// with a log-sum-exp combine.
 #include "device_common.h"
 #include "internal.h"
 
@@ -47,10 +48,10 @@ constexpr int kTiles = kChunk / 16;       // 16-token MFMA tiles per chunk
 constexpr int kVRows = kChunk / 4;        // V rows per lane per chunk
 constexpr int kD = 128;                   // head dimension
 constexpr int kMaxSplit = 2048;           // longest split (tokens per work item)
-#ifndef SPEC_ATTN_BLOCKS_PER_CU
-#define SPEC_ATTN_BLOCKS_PER_CU 2
+#ifndef SPEC_ATTN_MIN_SPLIT
+#define SPEC_ATTN_MIN_SPLIT 256
 #endif
-constexpr int kBlocksPerCU = SPEC_ATTN_BLOCKS_PER_CU;  // resident workgroups per CU
+constexpr int kMinSplitTokens = SPEC_ATTN_MIN_SPLIT;
 
 // K/V rows are read once per launch: stream them past the caches.
 __device__ __forceinline__ uint4 ldkv(const uint16_t* p) {
@@ -61,6 +62,13 @@ __device__ __forceinline__ uint4 ldkv(const uint16_t* p) {
 #endif
 }
 
+// How the selection of a (layer, sequence, KV head) group is covered:
+//  kDirect:         one work unit per group; the wave writes out/lse.
+//  kGlobalPartials: the selection is split over several units; partial
+//                   results go to the workspace and a second kernel merges
+//                   them.
+enum AttnMode { kDirect = 0, kGlobalPartials = 1 };
+
 struct AttnArgs {
   const uint16_t* q;      // [n_layers][B][H_q][d]
   const uint16_t* k;      // indexed: cache; compact: [n_layers][B][k_max][H_kv][d]
@@ -69,11 +77,12 @@ struct AttnArgs {
   const int32_t* counts;  // [B]
   float* part_acc;        // [n_layers*B][n_split][H_q][d]
   float* part_ml;         // [n_layers*B][n_split][H_q][2]
-  float* out;             // [n_layers*B][H_q][d]: written directly when n_split == 1
-  float* lse;             // [n_layers*B][H_q] or null (n_split == 1)
+  float* out;             // [n_layers*B][H_q][d]
+  float* lse;             // [n_layers*B][H_q] or null
   int64_t stride_layer;   // elements between layers (indexed mode)
   int64_t stride_b;       // elements between sequences (indexed mode)
   int B, H_q, H_kv, G, k_max, L_cap, n_split, split_tokens, n_items;
+  int mode;               // kDirect or kGlobalPartials
   float scale_log2;       // scale * log2(e)
 };
 
@@ -144,7 +153,7 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
   const int j0 = split * a.split_tokens;
   const int r16e = lane & 15;
   if (j0 >= count) {  // uniform per wavefront
-    if (a.n_split == 1 && r16e < G) {  // no tokens: out = 0, lse = -inf
+    if (a.mode == kDirect && r16e < G) {  // no tokens: out = 0, lse = -inf
       const size_t orow = (size_t)lb * a.H_q + (size_t)g * G + r16e;
       float* dst = a.out + orow * kD + 4 * (lane >> 4);
 #pragma unroll
@@ -318,7 +327,7 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
 
   l_run = xgroup_sum(l_run);
   if (r16 < G) {
-    if (a.n_split == 1) {  // the whole selection: normalise and write the output
+    if (a.mode == kDirect) {  // the whole selection: normalise and write the output
       const size_t orow = (size_t)lb * a.H_q + (size_t)g * G + r16;
       const float inv = 1.f / l_run;
       float* dst = a.out + orow * kD + 4 * kg;
@@ -342,20 +351,38 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
   }
 }
 
+// Dynamic LDS requested on top of the static arrays so that one workgroup
+// takes more than half of a CU's 160 KiB: exactly one per CU.
+constexpr size_t kLdsPerCU = 160 * 1024;
+constexpr size_t kStaticLds =
+    sizeof(uint16_t) * kWaves * kChunk * kVPitch + sizeof(int) * kWaves * (kMaxSplit + kChunk) + 16;
+constexpr size_t kLdsReserve = kLdsPerCU / 2 + 1024 > kStaticLds ? kLdsPerCU / 2 + 1024 - kStaticLds : 0;
+
 template <bool INDEXED>
 __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(SPEC_ATTN_WPE)))
 void attn_split_kernel(AttnArgs a) {
   __shared__ __align__(16) uint16_t vlds[kWaves][kChunk * kVPitch];
   __shared__ int rows_lds[kWaves][kMaxSplit + kChunk];
+  __shared__ int next_unit;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  // Persistent wavefronts: the grid is sized to the machine and each wave
-  // walks work items with a stride, so the partial-result stores of one item
-  // drain while the next item's rows are in flight (a wave that exits must
-  // first wait for its stores).  No block barriers are used.
-  const int stride = gridDim.x * kWaves;
-  for (int item = blockIdx.x * kWaves + wave; item < a.n_items; item += stride) {
-    process_item<INDEXED>(a, item, lane, vlds[wave], rows_lds[wave]);
+  // One workgroup per CU, one wavefront per SIMD.  Two wavefronts on a SIMD
+  // do not progress at equal rates (the older one wins instruction issue), and
+  // they add no bandwidth over one wavefront with its loads in flight, so the
+  // CU runs one per SIMD.  The workgroup owns a contiguous range of work
+  // units; its wavefronts take them on demand from an LDS counter, which also
+  // evens out units of unequal length (ragged selections).
+  const int per_block = (a.n_items + gridDim.x - 1) / gridDim.x;
+  const int u0 = blockIdx.x * per_block;
+  const int u1 = min(u0 + per_block, a.n_items);
+  if (threadIdx.x == 0) next_unit = u0;
+  __syncthreads();
+  for (;;) {
+    int t = 0;
+    if (lane == 0) t = atomicAdd(&next_unit, 1);
+    const int unit = __builtin_amdgcn_readfirstlane(t);
+    if (unit >= u1) break;  // uniform per wave: every wave ends here
+    process_item<INDEXED>(a, unit, lane, vlds[wave], rows_lds[wave]);
   }
 }
 
@@ -403,56 +430,75 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(CombineArgs a) {
   if (a.lse && d4 == 0) a.lse[(size_t)lb * a.H_q + h] = (M + log2f(L)) * kLn2;
 }
 
+// Resident wavefront slots the work is sized for: one per SIMD on 256 CUs.
+constexpr int64_t kWaveSlots = (int64_t)kWaves * 256;
+
+struct AttnPlan {
+  int mode, n_split, split;
+};
+
+// Work units are (layer, sequence, KV head, split of the selection).  With at
+// least one (layer, sequence, KV head) group per wavefront slot there is no
+// split and each unit writes its output (kDirect).  With fewer groups the
+// selections are split until there is about one unit per slot, but not below
+// kMinSplitTokens (each unit pays a start-up latency and a partial-result
+// store) nor above kMaxSplit (the index staging area) (kGlobalPartials).
+// Units are numbered KV head fastest, so that the wavefronts of a workgroup
+// read the same selected tokens' rows for neighbouring heads at the same time:
+// those pieces share DRAM pages.  A split is a whole number of chunks.
+AttnPlan attn_plan(const Dims& d) {
+  const int64_t base = (int64_t)d.n_layers * d.B * d.H_kv;
+  auto round_chunk = [](int64_t t) { return (t + kChunk - 1) / kChunk * kChunk; };
+  int64_t n_split = (kWaveSlots + base - 1) / base;
+  int64_t split = round_chunk((d.k_max + n_split - 1) / n_split);
+  if (split < kMinSplitTokens) split = kMinSplitTokens;
+  if (split > kMaxSplit) split = kMaxSplit;
+  n_split = (d.k_max + split - 1) / split;
+  if (n_split == 1) return {kDirect, 1, (int)round_chunk(d.k_max)};
+  return {kGlobalPartials, (int)n_split, (int)split};
+}
+
 }  // namespace
 
-int attn_split_tokens(const Dims& d) {
-  // One work item per resident wavefront slot (2 per SIMD on 256 CUs): a
-  // wavefront that finishes an item must wait for its result stores before
-  // the slot can take the next one, so items should not queue behind each
-  // other.  Items are (layer, sequence, KV head) pairs, split only as far as
-  // needed to fill the slots; a split never exceeds kMaxSplit tokens and is
-  // a whole number of chunks.
-  constexpr int64_t kSlots = 2 * 4 * 256;
-  const int64_t base = (int64_t)d.n_layers * d.B * d.H_kv;
-  int64_t n_split = (kSlots + base - 1) / base;
-  n_split = n_split < 1 ? 1 : n_split;
-  const int64_t min_split = (d.k_max + kMaxSplit - 1) / kMaxSplit;
-  if (n_split < min_split) n_split = min_split;
-  int64_t split = (d.k_max + n_split - 1) / n_split;
-  split = (split + kChunk - 1) / kChunk * kChunk;
-  if (split > kMaxSplit) split = kMaxSplit;
-  return (int)split;
+int attn_split_tokens(const Dims& d) { return attn_plan(d).split; }
+
+size_t attn_ws_bytes(const Dims& d) {
+  const AttnPlan pl = attn_plan(d);
+  if (pl.mode != kGlobalPartials) return 0;
+  const size_t rows = (size_t)d.n_layers * d.B * pl.n_split * d.H_q;
+  return align_up(sizeof(float) * rows * d.d) + align_up(sizeof(float) * rows * 2);
 }
 
 hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
                        const uint16_t* v, const int32_t* idx, const int32_t* counts,
                        float* out, float* lse, void* ws, hipStream_t s) {
-  const int split = attn_split_tokens(d);
-  const int n_split = attn_n_split(d);
-  const size_t rows = (size_t)d.n_layers * d.B * n_split * d.H_q;
+  const AttnPlan pl = attn_plan(d);
+  const size_t rows = (size_t)d.n_layers * d.B * pl.n_split * d.H_q;
   float* part_acc = static_cast<float*>(ws);
-  float* part_ml = reinterpret_cast<float*>(static_cast<char*>(ws) +
-                                            align_up(sizeof(float) * rows * d.d));
-  const int64_t n_items = (int64_t)d.n_layers * d.B * n_split * d.H_kv;
+  float* part_ml = pl.mode == kGlobalPartials
+                       ? reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                                  align_up(sizeof(float) * rows * d.d))
+                       : nullptr;
+  const int64_t n_groups = (int64_t)d.n_layers * d.B * d.H_kv;
+  const int64_t n_items = n_groups * pl.n_split;
+  if (n_items > INT32_MAX / 2) return hipErrorInvalidValue;
   AttnArgs a{q, k, v, idx, counts, part_acc, part_ml, out, lse, d.kv_stride_layer, d.kv_stride_b,
-             d.B, d.H_q, d.H_kv, d.G, d.k_max, d.L_cap, n_split, split, (int)n_items,
-             d.scale * kLog2e};
-  // Persistent grid: at most as many workgroups as the machine holds at once
-  // (the register budget allows 2 wavefronts per SIMD: 2 workgroups per CU).
+             d.B, d.H_q, d.H_kv, d.G, d.k_max, d.L_cap, pl.n_split, pl.split, (int)n_items,
+             pl.mode, d.scale * kLog2e};
+  // One workgroup per CU, fewer when there are fewer units than wavefronts.
   int dev = 0, n_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       n_cu <= 0)
     n_cu = 256;
   const int64_t want = (n_items + kWaves - 1) / kWaves;
-  const int64_t cap = (int64_t)n_cu * kBlocksPerCU;
-  const dim3 grid((unsigned)(want < cap ? want : cap));
+  const dim3 grid((unsigned)(want < n_cu ? want : n_cu));
   if (idx)
-    attn_split_kernel<true><<<grid, kWaves * 64, 0, s>>>(a);
+    attn_split_kernel<true><<<grid, kWaves * 64, kLdsReserve, s>>>(a);
   else
-    attn_split_kernel<false><<<grid, kWaves * 64, 0, s>>>(a);
-  if (n_split == 1) return hipGetLastError();  // the split kernel wrote out/lse
-  CombineArgs c{part_acc, part_ml, counts, out, lse, d.B, d.H_q, d.k_max, n_split, split};
+    attn_split_kernel<false><<<grid, kWaves * 64, kLdsReserve, s>>>(a);
+  if (pl.mode != kGlobalPartials) return hipGetLastError();
+  CombineArgs c{part_acc, part_ml, counts, out, lse, d.B, d.H_q, d.k_max, pl.n_split, pl.split};
   const dim3 g2(d.n_layers * d.B, (d.H_q + 7) / 8);
   attn_combine_kernel<<<g2, 256, 0, s>>>(c);
   return hipGetLastError();

@@ -62,20 +62,10 @@ inline size_t topk_lists_bytes(const Dims& d) {
 }
 inline size_t topk_ws_bytes(const Dims& d) { return topk_hist_bytes(d) + topk_lists_bytes(d); }
 
-// Attention split size (tokens of the selection per wave work item).
+// Attention: tokens of the selection per work unit, and the workspace for
+// partial results (zero unless a selection is split across workgroups).
 int attn_split_tokens(const Dims& d);
-inline int attn_n_split(const Dims& d) {
-  const int s = attn_split_tokens(d);
-  return (d.k_max + s - 1) / s;
-}
-// partial acc [n_layers*B][n_split][H_q][d] + (m, l) [n_layers*B][n_split][H_q][2]
-// (none when every work item covers the whole selection: out is written directly)
-inline size_t attn_ws_bytes(const Dims& d) {
-  const int n_split = attn_n_split(d);
-  if (n_split == 1) return 0;
-  const size_t rows = (size_t)d.n_layers * d.B * n_split * d.H_q;
-  return align_up(sizeof(float) * rows * d.d) + align_up(sizeof(float) * rows * 2);
-}
+size_t attn_ws_bytes(const Dims& d);
 
 // Elastic loading: per sequence the list of (slot, token) copies.
 inline size_t delta_ws_bytes(const Dims& d) {

@@ -27,7 +27,7 @@ struct LogitsArgs {
   const uint16_t* k_r;
   const int32_t* seq_lens;
   float* logits;  // [B][L_max][H_r], log2 units
-  float* part;    // [B][n_blk][H_r][2]: block max, block sum of exp2(l - max)
+  float* part;    // [B][H_r][n_blk][2]: block max, block sum of exp2(l - max)
   int32_t* hist;  // [B][4096] top-k histogram, zeroed here for the next kernel
   int64_t kr_stride_b;
   int L_max, H_r, n_blk;
@@ -110,7 +110,7 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
     for (int i = j; i < n_tok; i += 16) s += exp2f(lg[i * 16 + hh] - m);
     s = row_sum<16>(s);
     if (j == 0) {
-      float* p = a.part + (((size_t)b * a.n_blk + blk) * a.H_r + hh) * 2;
+      float* p = a.part + (((size_t)b * a.H_r + hh) * a.n_blk + blk) * 2;
       p[0] = m;
       p[1] = s;
     }
@@ -129,6 +129,7 @@ struct SoftArgs {
 // One workgroup per (T2 tokens, sequence); thread = 4 consecutive tokens.
 __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
   __shared__ float c_h[16];
+  __shared__ float2 wred[4];
   __shared__ int sh_hist[kTopkBins];
   const int b = blockIdx.y;
   const int tid = threadIdx.x;
@@ -142,40 +143,51 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
   }
   for (int i = tid; i < kTopkBins; i += 256) sh_hist[i] = 0;
 
-  // Each head's normaliser c_h = M_h + log2 Z_h from the per-block pairs:
-  // 16 lanes per head, partial pairs loaded 8 at a time before combining.
+  // Each head's normaliser c_h = M_h + log2 Z_h from the per-block pairs
+  // (head-major, so a head's pairs are contiguous): 256/P lanes per head (P =
+  // H_r rounded up to a power of two), 16 pairs in flight per lane, then a
+  // butterfly over the head's lanes of the wave and, for heads wider than a
+  // wave, a combine of the per-wave results.
   const int nb = (L_b + T1 - 1) / T1;
-  const int hh = tid >> 4;
-  const int j = tid & 15;
-  if (hh < a.H_r) {
-    float m = -INFINITY, s = 0.f;
-    const float* p = a.part + ((size_t)b * a.n_blk * a.H_r + hh) * 2;
-    for (int i0 = j; i0 < nb; i0 += 16 * 8) {
-      float pm[8], ps[8];
+  const int H_r = a.H_r;
+  const int P = H_r <= 1 ? 1 : H_r <= 2 ? 2 : H_r <= 4 ? 4 : H_r <= 8 ? 8 : 16;
+  const int LPH = 256 / P;
+  const int hh = tid / LPH;
+  const int j = tid - hh * LPH;
+  float m = -INFINITY, s = 0.f;
+  if (hh < H_r) {
+    const float2* p = reinterpret_cast<const float2*>(a.part) + ((size_t)b * H_r + hh) * a.n_blk;
+    for (int i0 = j; i0 < nb; i0 += LPH * 16) {
+      float2 v[16];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int i = i0 + 16 * u;
-        const bool v = i < nb;
-        pm[u] = v ? p[(size_t)i * a.H_r * 2] : -INFINITY;
-        ps[u] = v ? p[(size_t)i * a.H_r * 2 + 1] : 0.f;
+      for (int u = 0; u < 16; ++u) {
+        const int i = i0 + LPH * u;
+        v[u] = i < nb ? p[i] : make_float2(-INFINITY, 0.f);
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) ms_combine(m, s, pm[u], ps[u]);
+      for (int u = 0; u < 16; ++u) ms_combine(m, s, v[u].x, v[u].y);
     }
-#pragma unroll
-    for (int ctrl = 0; ctrl < 4; ++ctrl) {
-      float m2, s2;
-      if (ctrl == 0) { m2 = dpp_f<0xB1>(m); s2 = dpp_f<0xB1>(s); }
-      else if (ctrl == 1) { m2 = dpp_f<0x4E>(m); s2 = dpp_f<0x4E>(s); }
-      else if (ctrl == 2) { m2 = dpp_f<0x141>(m); s2 = dpp_f<0x141>(s); }
-      else { m2 = dpp_f<0x140>(m); s2 = dpp_f<0x140>(s); }
-      ms_combine(m, s, m2, s2);
+  }
+  const int width = LPH < 64 ? LPH : 64;
+  for (int off = 1; off < width; off <<= 1) {
+    const float m2 = __shfl_xor(m, off);
+    const float s2 = __shfl_xor(s, off);
+    ms_combine(m, s, m2, s2);
+  }
+  if (LPH <= 64) {
+    if (j == 0 && hh < H_r) c_h[hh] = m + log2f(s);
+  } else {
+    if ((tid & 63) == 0) wred[tid >> 6] = make_float2(m, s);
+    __syncthreads();
+    if (tid < H_r) {
+      const int wpw = LPH / 64;  // waves per head
+      float mm = -INFINITY, ss = 0.f;
+      for (int w = tid * wpw; w < (tid + 1) * wpw; ++w) ms_combine(mm, ss, wred[w].x, wred[w].y);
+      c_h[tid] = mm + log2f(ss);
     }
-    if (j == 0) c_h[hh] = m + log2f(s);
   }
   __syncthreads();
 
-  const int H_r = a.H_r;
   const int tb = t0 + 4 * tid;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {

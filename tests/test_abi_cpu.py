@@ -45,8 +45,10 @@ FAKE_ODD = ctypes.c_void_p(0x7000_0000_0008)  # 8-byte aligned only
 
 
 def good_dims(**kw):
-    base = dict(B=2, L_cap=4096, L_max=4096, k_max=1024, H_r=8, d_r=64, n_layers=2, H_q=32, H_kv=8,
-                d=128)
+    # k_max above 4 x 2048 makes the attention split its selection across
+    # workgroups, so that its workspace is not empty
+    base = dict(B=2, L_cap=16384, L_max=16384, k_max=12288, H_r=8, d_r=64, n_layers=2, H_q=32,
+                H_kv=8, d=128)
     base.update(kw)
     return spec.Dims.make(**base)
 
@@ -59,15 +61,15 @@ def ws_size(lib, dims, op):
 
 @pytest.mark.parametrize("field,value,status", [
     ("B", 0, 1), ("L_cap", -1, 1), ("k_max", 0, 1), ("H_r", 0, 1), ("d", 0, 1),
-    ("L_max", 4097, 1),         # L_max > L_cap
-    ("k_max", 4097, 1),         # k_max > L_max
+    ("L_max", 16385, 1),        # L_max > L_cap
+    ("k_max", 16385, 1),        # k_max > L_max
     ("H_q", 30, 1),             # H_q % H_kv != 0
     ("d", 64, 2), ("d_r", 32, 2), ("H_r", 17, 2), ("H_kv", 32, 2),
     ("H_q", 24, 2),             # G = 3
     ("n_sets", 8, 2),
     ("reserved", 1, 1),
     ("kv_stride_b", 12, 1),     # smaller than a sequence's block
-    ("kr_stride_b", 4096 * 8 * 64 + 3, 1),  # not a multiple of 8
+    ("kr_stride_b", 16384 * 8 * 64 + 3, 1),  # not a multiple of 8
     ("scale", -1.0, 1),
 ])
 def test_dims_validation(lib, field, value, status):
@@ -83,7 +85,7 @@ def test_workspace_sizes(lib):
     sizes = {op: ws_size(lib, d, op) for op in range(6)}
     assert all(st == 0 for st, _ in sizes.values())
     assert sizes[spec.OP_GATHER][1] == 0
-    assert sizes[spec.OP_SCORE][1] >= 2 * 4096 * 8 * 4       # the logits
+    assert sizes[spec.OP_SCORE][1] >= 2 * 16384 * 8 * 4      # the logits
     assert sizes[spec.OP_STEP][1] >= sizes[spec.OP_SCORE][1] + sizes[spec.OP_ATTN][1]
     assert lib.spec_workspace_size(None, 0, ctypes.byref(ctypes.c_size_t())) == 1
     assert lib.spec_workspace_size(ctypes.byref(d), 9, ctypes.byref(ctypes.c_size_t())) == 1

@@ -33,6 +33,10 @@ SCORE_CASES = [
     (2, 520, 520, 8, 128, [520, 200]),
     (1, 400, 400, 16, 128, [0]),
     (4, 2500, 2400, 8, 64, [2400, 2048, 2047, 2049]),
+    (2, 900, 900, 3, 64, [900, 450]),
+    (1, 600, 600, 5, 128, [600]),
+    # more per-block softmax pairs per head than one pass of the merge holds
+    (1, 40000, 40000, 16, 64, [40000]),
 ]
 
 
@@ -136,7 +140,13 @@ ATTN_CASES = [
     (1, 2, 500, 8, 8, [129, 300], 300),
     (1, 1, 600, 32, 2, [520], 520),
     (3, 2, 256, 16, 16, [256, 255], 256),
-    (2, 3, 300, 32, 8, [32, 0, 7], 32),      # one split per item: direct output path
+    (2, 3, 300, 32, 8, [32, 0, 7], 32),
+    # >= 1024 (layer, sequence, KV head) groups: one work unit per group, the
+    # wavefront writes the output itself
+    (4, 32, 160, 32, 8, [(37 * b) % 129 for b in range(32)], 128),
+    # selections longer than 4 x 2048: splits merged by the second kernel
+    (1, 2, 12000, 8, 2, [9000, 8193], 9000),
+    (1, 3, 9000, 8, 1, [8400, 0, 3], 8400),
 ]
 
 
