@@ -51,6 +51,7 @@ constexpr int kMaxSplit = 2048;           // longest split (tokens per work item
 #ifndef SPEC_ATTN_MIN_SPLIT
 #define SPEC_ATTN_MIN_SPLIT 256
 #endif
+
 constexpr int kMinSplitTokens = SPEC_ATTN_MIN_SPLIT;
 
 // K/V rows are read once per launch: stream them past the caches.

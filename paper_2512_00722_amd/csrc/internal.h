@@ -22,7 +22,10 @@ constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Retrieval scoring: tokens per workgroup of the logits kernel.
-constexpr int kScoreTokensPerBlock = 128;
+#ifndef SPEC_SCORE_TPB
+#define SPEC_SCORE_TPB 128
+#endif
+constexpr int kScoreTokensPerBlock = SPEC_SCORE_TPB;
 // Softmax/head-sum kernel: tokens per workgroup.
 constexpr int kSoftTokensPerBlock = 1024;
 

@@ -20,7 +20,10 @@ namespace {
 
 constexpr int T1 = kScoreTokensPerBlock;
 constexpr int T2 = kSoftTokensPerBlock;
-constexpr int kUnroll = 8;  // rows in flight per lane
+#ifndef SPEC_LOGITS_UNROLL
+#define SPEC_LOGITS_UNROLL 8
+#endif
+constexpr int kUnroll = SPEC_LOGITS_UNROLL;  // rows in flight per lane
 
 struct LogitsArgs {
   const uint16_t* q_r;
@@ -150,6 +153,29 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
   // wave, a combine of the per-wave results.
   const int nb = (L_b + T1 - 1) / T1;
   const int H_r = a.H_r;
+  // This thread's logits (4 tokens x H_r heads, H_r <= 16) are loaded before
+  // the normalisers are merged: the two loads are independent.
+  const int tb = t0 + 4 * tid;
+  float lv[4][16];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int t = tb + e;
+    const float* l = a.logits + ((size_t)b * a.L_max + t) * H_r;
+    if (t < L_b && (H_r & 3) == 0) {
+#pragma unroll
+      for (int h = 0; h < 16; h += 4)
+        if (h < H_r) {
+          const float4 v = *reinterpret_cast<const float4*>(l + h);
+          lv[e][h] = v.x;
+          lv[e][h + 1] = v.y;
+          lv[e][h + 2] = v.z;
+          lv[e][h + 3] = v.w;
+        }
+    } else {
+#pragma unroll
+      for (int h = 0; h < 16; ++h) lv[e][h] = (t < L_b && h < H_r) ? l[h] : 0.f;
+    }
+  }
   const int P = H_r <= 1 ? 1 : H_r <= 2 ? 2 : H_r <= 4 ? 4 : H_r <= 8 ? 8 : 16;
   const int LPH = 256 / P;
   const int hh = tid / LPH;
@@ -188,24 +214,16 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
   }
   __syncthreads();
 
-  const int tb = t0 + 4 * tid;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int t = tb + e;
     if (t >= t1) break;
     float sc = -INFINITY;
     if (t < L_b) {
-      const float* l = a.logits + ((size_t)b * a.L_max + t) * H_r;
       sc = 0.f;
-      if ((H_r & 3) == 0) {
-        for (int h = 0; h < H_r; h += 4) {
-          const float4 v = *reinterpret_cast<const float4*>(l + h);
-          sc += exp2f(v.x - c_h[h]) + exp2f(v.y - c_h[h + 1]) + exp2f(v.z - c_h[h + 2]) +
-                exp2f(v.w - c_h[h + 3]);
-        }
-      } else {
-        for (int h = 0; h < H_r; ++h) sc += exp2f(l[h] - c_h[h]);
-      }
+#pragma unroll
+      for (int h = 0; h < 16; ++h)
+        if (h < H_r) sc += exp2f(lv[e][h] - c_h[h]);
       atomicAdd(&sh_hist[order_key(sc) >> 20], 1);
     }
     out[t] = sc;

@@ -173,6 +173,15 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
 
   // ---- the bin of the k-th key from the 12-bit histogram
   const int32_t* gh = a.hist + (size_t)b * kBins;
+  const int n_tiles_b = (L_b + kTile - 1) / kTile;
+  // The per-tile list counts are loaded with the histogram (one round trip);
+  // they are only used on the fast path.
+  const int32_t* tcnt = a.tl.cnt + (size_t)b * a.tl.n_tiles * 2;
+  int tg = 0, tc = 0;
+  if (tid < n_tiles_b && n_tiles_b <= kMaxTiles) {
+    tg = tcnt[2 * tid];
+    tc = tcnt[2 * tid + 1];
+  }
   for (int i = tid; i < kBins; i += kThreads) s_hist[i] = gh[i];
   if (tid == 0) s_sel[0] = s_sel[1] = s_sel[2] = -1;
   __syncthreads();
@@ -187,16 +196,9 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
   const bool hist_ok = b1i >= 0 && c1 >= 0 && c1 < k_b && r1 <= n1;
   __syncthreads();
 
-  const int n_tiles_b = (L_b + kTile - 1) / kTile;
   if (hist_ok && c1 <= kGtCap && n1 <= kCandCap && n_tiles_b <= kMaxTiles) {
     // ---------------- fast path: gather the per-tile lists ----------------
-    const int32_t* tcnt = a.tl.cnt + (size_t)b * a.tl.n_tiles * 2;
     int* s_toff = s_cidx;  // borrowed until the candidates are gathered below
-    int tg = 0, tc = 0;
-    if (tid < n_tiles_b) {
-      tg = tcnt[2 * tid];
-      tc = tcnt[2 * tid + 1];
-    }
     int og, oc, sum_g, sum_c;
     block_scan2<kThreads>(tg, tc, og, oc, sum_g, sum_c, s_scan);
     if (tid < n_tiles_b) {
@@ -410,6 +412,16 @@ __global__ __launch_bounds__(kClsThreads) void topk_classify_kernel(ClsArgs a) {
   const int t0 = tile * kTile;
   if (k_b == 0 || k_b == L_b || t0 >= L_b) return;  // uniform: nothing to classify
 
+  // The tile's keys and the histogram are independent: both loads are in
+  // flight before either is used.
+  const float* row = a.scores + (size_t)b * a.L_max;
+  const int lane = tid & 63;
+  const int wv = tid >> 6;
+  const int w0 = min(t0 + wv * (kTile / kClsWaves), L_b);
+  const int w1 = min(w0 + kTile / kClsWaves, L_b);
+  uint32_t kk[kClsPerLane];
+#pragma unroll
+  for (int j = 0; j < kClsPerLane; ++j) kk[j] = key_at(row, w0 + 64 * j + lane, w1);
   const int32_t* gh = a.hist + (size_t)b * kBins;
   for (int i = tid; i < kBins; i += kClsThreads) s_hist[i] = gh[i];
   if (tid == 0) s_sel[0] = s_sel[1] = s_sel[2] = -1;
@@ -420,15 +432,6 @@ __global__ __launch_bounds__(kClsThreads) void topk_classify_kernel(ClsArgs a) {
   if (!(b1i >= 0 && c1 >= 0 && c1 < k_b && k_b - c1 <= n1) || c1 > kGtCap || n1 > kCandCap)
     return;
   const uint32_t b1 = (uint32_t)b1i;
-
-  const float* row = a.scores + (size_t)b * a.L_max;
-  const int lane = tid & 63;
-  const int wv = tid >> 6;
-  const int w0 = min(t0 + wv * (kTile / kClsWaves), L_b);
-  const int w1 = min(w0 + kTile / kClsWaves, L_b);
-  uint32_t kk[kClsPerLane];
-#pragma unroll
-  for (int j = 0; j < kClsPerLane; ++j) kk[j] = key_at(row, w0 + 64 * j + lane, w1);
   int wgt = 0, wcand = 0;
 #pragma unroll
   for (int j = 0; j < kClsPerLane; ++j) {

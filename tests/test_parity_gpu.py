@@ -104,6 +104,14 @@ TOPK_CASES = [
     ("random", 4, 1024, 1024, [1024, 0, 5, 1024], [1024, 3, 9, 0]),
     ("random", 1, 32768, 2048, [32768], [2048]),
     ("ties", 1, 40000, 4096, [40000], [4096]),
+    # rows whose start is not 16-byte aligned (row length not a multiple of 4)
+    ("random", 3, 5001, 600, [5001, 4999, 17], [600, 600, 5]),
+    # a row longer than one workgroup classifies (tiles classified across
+    # workgroups) next to one it classifies itself
+    ("random", 2, 140000, 3000, [140000, 131072], [3000, 2999]),
+    # a threshold bin too crowded for the candidate lists: the general path
+    ("narrow", 1, 131072, 4096, [131072], [4096]),
+    ("ties", 1, 150000, 4096, [150000], [4096]),
 ]
 
 
