@@ -68,15 +68,16 @@ def attn_source_digest():
     return h.hexdigest()
 
 
-def stored_traffic():
-    """Per-launch HBM bytes of the attention kernels measured with rocprofv3
-    PMC counters, valid only for the attention code they were taken on."""
+def stored_traffic(workload):
+    """Per-launch HBM bytes of the attention kernels on `workload`, measured
+    with rocprofv3 PMC counters; valid only for the attention code they were
+    taken on."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
         if t.get("attn_code_sha256") != attn_source_digest():
             return None
-        return t.get("bytes_per_launch")
+        return t.get("workloads", {}).get(workload, {}).get("bytes_per_launch")
     except (OSError, ValueError):
         return None
 
@@ -244,7 +245,7 @@ def main():
     a_bytes = attn_bytes(w, counts)
     attn_s = op_us["attn"] * 1e-6
     achieved = a_bytes / attn_s / 1e9
-    traffic = stored_traffic()
+    traffic = stored_traffic(name)
     value = args.steps / wall
     line = {
         "metric": METRIC,
