@@ -179,6 +179,20 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
     vb = a.v + off;
   }
 
+  const int r16 = lane & 15;  // head of this lane (MFMA column); token of a K tile row
+  const int kg = lane >> 4;   // MFMA k-group; also the token phase of V loads
+  // B operand of S^T = K Q^T: Q^T column r16 = query head g*G + r16 (zero if >= G),
+  // dims 32s + 8kg .. +8.  Loaded together with the row indices.
+  bf16x8 qf[4];
+  {
+    const uint16_t* qp = a.q + ((size_t)lb * a.H_q + g * G + (r16 < G ? r16 : 0)) * kD + 8 * kg;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      uint4 w = r16 < G ? ldg16(qp + 32 * s) : make_uint4(0, 0, 0, 0);
+      qf[s] = __builtin_bit_cast(bf16x8, w);
+    }
+  }
+
   // Stage the rows of this item's tokens in LDS (masked tokens read row 0),
   // so that no chunk waits on an index load from memory.
   wave_sync_lds();  // the previous item's reads of rows/V are done
@@ -203,19 +217,6 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
     }
   }
 
-  const int r16 = lane & 15;  // head of this lane (MFMA column); token of a K tile row
-  const int kg = lane >> 4;   // MFMA k-group; also the token phase of V loads
-  // B operand of S^T = K Q^T: Q^T column r16 = query head g*G + r16 (zero if >= G),
-  // dims 32s + 8kg .. +8.
-  bf16x8 qf[4];
-  {
-    const uint16_t* qp = a.q + ((size_t)lb * a.H_q + g * G + (r16 < G ? r16 : 0)) * kD + 8 * kg;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      uint4 w = r16 < G ? ldg16(qp + 32 * s) : make_uint4(0, 0, 0, 0);
-      qf[s] = __builtin_bit_cast(bf16x8, w);
-    }
-  }
   wave_sync_lds();
 
   // K rows in the MFMA A-operand layout: tile t, token 16t + r16, dims

@@ -23,7 +23,7 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Retrieval scoring: tokens per workgroup of the logits kernel.
 #ifndef SPEC_SCORE_TPB
-#define SPEC_SCORE_TPB 128
+#define SPEC_SCORE_TPB 256
 #endif
 constexpr int kScoreTokensPerBlock = SPEC_SCORE_TPB;
 // Softmax/head-sum kernel: tokens per workgroup.

@@ -124,9 +124,26 @@ __device__ __forceinline__ void find_bin(const int* hist, int nbins, int need, i
   __syncthreads();
 }
 
-// Key of row[t] (t may be out of range: returns 0, below every real key).
-__device__ __forceinline__ uint32_t key_at(const float* row, int t, int L) {
-  return t < L ? order_key(row[t]) : 0u;
+// Key of row[t] for t < L, else 0 (below every real key).  The load is
+// unconditional, from an index clamped into [0, row_len): a conditional load
+// makes the compiler wait for each one before the next is issued.
+__device__ __forceinline__ uint32_t key_at(const float* row, int t, int L, int row_len) {
+  const float v = row[min(max(t, 0), row_len - 1)];
+  // a mask, not a select: a select lets the compiler sink the load into a branch
+  const uint32_t keep = 0u - (uint32_t)(t < L);
+  return order_key(v) & keep;
+}
+
+// Copy a [kBins] int array from global memory to LDS with NT threads: all
+// loads of a thread are issued before the first LDS write.
+template <int NT>
+__device__ __forceinline__ void load_hist(const int32_t* g, int* sh) {
+  constexpr int kPer = kBins / NT;
+  int v[kPer];
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) v[e] = g[threadIdx.x + e * NT];
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) sh[threadIdx.x + e * NT] = v[e];
 }
 
 // Per-tile lists written by the classify kernel (workspace).
@@ -177,12 +194,11 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
   // The per-tile list counts are loaded with the histogram (one round trip);
   // they are only used on the fast path.
   const int32_t* tcnt = a.tl.cnt + (size_t)b * a.tl.n_tiles * 2;
-  int tg = 0, tc = 0;
-  if (tid < n_tiles_b && n_tiles_b <= kMaxTiles) {
-    tg = tcnt[2 * tid];
-    tc = tcnt[2 * tid + 1];
-  }
-  for (int i = tid; i < kBins; i += kThreads) s_hist[i] = gh[i];
+  const int tcl = min(tid, a.tl.n_tiles - 1);  // clamped: the load is unconditional
+  int tg = tcnt[2 * tcl];
+  int tc = tcnt[2 * tcl + 1];
+  if (!(tid < n_tiles_b && n_tiles_b <= kMaxTiles)) tg = tc = 0;
+  load_hist<kThreads>(gh, s_hist);
   if (tid == 0) s_sel[0] = s_sel[1] = s_sel[2] = -1;
   __syncthreads();
   find_bin<kThreads>(s_hist, kBins, k_b, s_scan, s_sel);
@@ -198,51 +214,56 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
 
   if (hist_ok && c1 <= kGtCap && n1 <= kCandCap && n_tiles_b <= kMaxTiles) {
     // ---------------- fast path: gather the per-tile lists ----------------
-    int* s_toff = s_cidx;  // borrowed until the candidates are gathered below
+    // Per-tile offsets and counts go to the histogram's LDS (no longer
+    // needed); then each wave copies whole tiles, four at a time, with
+    // coalesced, unconditional loads.
+    int* s_off_g = s_hist;
+    int* s_off_c = s_hist + kMaxTiles;
+    int* s_cnt_g = s_hist + 2 * kMaxTiles;
+    int* s_cnt_c = s_hist + 3 * kMaxTiles;
     int og, oc, sum_g, sum_c;
     block_scan2<kThreads>(tg, tc, og, oc, sum_g, sum_c, s_scan);
     if (tid < n_tiles_b) {
-      s_toff[tid] = og;
-      s_toff[kMaxTiles + tid] = oc;
+      s_off_g[tid] = og;
+      s_off_c[tid] = oc;
+      s_cnt_g[tid] = tg;
+      s_cnt_c[tid] = tc;
     }
     __syncthreads();
-    // Token p of a list lives in the tile whose offset is the last one <= p.
-    auto tile_of = [&](const int* off, int p) {
-      int lo = 0, hi = n_tiles_b - 1;
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (off[mid] <= p) lo = mid; else hi = mid - 1;
-      }
-      return lo;
-    };
-    const int ng = min(sum_g, kGtCap);
-    const int nc = min(sum_c, kCandCap);
-    int32_t* tgt = a.tl.gt + (size_t)b * a.tl.n_tiles * kTile;
-    for (int p = tid; p < ng; p += kThreads) {
-      const int t = tile_of(s_toff, p);
-      s_gt[p] = tgt[(size_t)t * kTile + (p - s_toff[t])];
-    }
+    const int lane = tid & 63;
+    const int wv = tid >> 6;
+    const int32_t* tgt = a.tl.gt + (size_t)b * a.tl.n_tiles * kTile;
     const uint32_t* tck = a.tl.ckey + (size_t)b * a.tl.n_tiles * kTile;
     const int32_t* tci = a.tl.cidx + (size_t)b * a.tl.n_tiles * kTile;
-    uint32_t ck_l[kCandCap / kThreads];
-    int ci_l[kCandCap / kThreads];
-#pragma unroll
-    for (int e = 0; e < kCandCap / kThreads; ++e) {
-      const int p = tid + e * kThreads;
-      if (p < nc) {
-        const int t = tile_of(s_toff + kMaxTiles, p);
-        const size_t q = (size_t)t * kTile + (p - s_toff[kMaxTiles + t]);
-        ck_l[e] = tck[q];
-        ci_l[e] = tci[q];
+    auto put = [&](int t, int i, int gv, uint32_t kv, int iv) {
+      if (i < s_cnt_g[t] && s_off_g[t] + i < kGtCap) s_gt[s_off_g[t] + i] = gv;
+      if (i < s_cnt_c[t] && s_off_c[t] + i < kCandCap) {
+        s_ckey[s_off_c[t] + i] = kv;
+        s_cidx[s_off_c[t] + i] = iv;
       }
-    }
-    __syncthreads();  // s_toff (inside s_cidx) is no longer read
+    };
+    for (int t0 = wv; t0 < n_tiles_b; t0 += 4 * kWaves) {
+      int gv[4], iv[4];
+      uint32_t kv[4];
 #pragma unroll
-    for (int e = 0; e < kCandCap / kThreads; ++e) {
-      const int p = tid + e * kThreads;
-      if (p < nc) {
-        s_ckey[p] = ck_l[e];
-        s_cidx[p] = ci_l[e];
+      for (int u = 0; u < 4; ++u) {
+        const size_t q = (size_t)min(t0 + u * kWaves, n_tiles_b - 1) * kTile + lane;
+        gv[u] = tgt[q];
+        kv[u] = tck[q];
+        iv[u] = tci[q];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int t = t0 + u * kWaves;
+        if (t < n_tiles_b) {
+          put(t, lane, gv[u], kv[u], iv[u]);
+          // tiles with more than 64 entries in a list (rare)
+          const int n = max(s_cnt_g[t], s_cnt_c[t]);
+          for (int i = lane + 64; i < n; i += 64) {
+            const size_t q = (size_t)t * kTile + i;
+            put(t, i, tgt[q], tck[q], tci[q]);
+          }
+        }
       }
     }
     __syncthreads();
@@ -335,7 +356,7 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
     for (int t0 = 0; t0 < L_b; t0 += 8 * kThreads) {
       uint32_t k8[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) k8[e] = key_at(row, t0 + e * kThreads + tid, L_b);
+      for (int e = 0; e < 8; ++e) k8[e] = key_at(row, t0 + e * kThreads + tid, L_b, a.L_max);
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         if (t0 + e * kThreads + tid < L_b && (k8[e] & mask) == prefix)
@@ -358,7 +379,7 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
     int ngt = 0, neq = 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      key[e] = key_at(row, t0 + e, L_b);
+      key[e] = key_at(row, t0 + e, L_b, a.L_max);
       const bool valid = t0 + e < L_b;
       ngt += (valid && key[e] > T);
       neq += (valid && key[e] == T);
@@ -421,9 +442,8 @@ __global__ __launch_bounds__(kClsThreads) void topk_classify_kernel(ClsArgs a) {
   const int w1 = min(w0 + kTile / kClsWaves, L_b);
   uint32_t kk[kClsPerLane];
 #pragma unroll
-  for (int j = 0; j < kClsPerLane; ++j) kk[j] = key_at(row, w0 + 64 * j + lane, w1);
-  const int32_t* gh = a.hist + (size_t)b * kBins;
-  for (int i = tid; i < kBins; i += kClsThreads) s_hist[i] = gh[i];
+  for (int j = 0; j < kClsPerLane; ++j) kk[j] = key_at(row, w0 + 64 * j + lane, w1, a.L_max);
+  load_hist<kClsThreads>(a.hist + (size_t)b * kBins, s_hist);
   if (tid == 0) s_sel[0] = s_sel[1] = s_sel[2] = -1;
   __syncthreads();
   find_bin<kClsThreads>(s_hist, kBins, k_b, s_scan, s_sel);
@@ -497,7 +517,12 @@ __global__ __launch_bounds__(256) void topk_hist_kernel(const float* scores,
   __syncthreads();
   const float* row = scores + (size_t)b * L_max;
   const int t1 = min(t0 + 4096, L_b);
-  for (int t = t0 + threadIdx.x; t < t1; t += 256) atomicAdd(&sh[order_key(row[t]) >> 20], 1);
+  float v[16];  // 4096 / 256 tokens per thread, all loads in flight
+#pragma unroll
+  for (int e = 0; e < 16; ++e) v[e] = row[min(t0 + (int)threadIdx.x + 256 * e, t1 - 1)];
+#pragma unroll
+  for (int e = 0; e < 16; ++e)
+    if (t0 + (int)threadIdx.x + 256 * e < t1) atomicAdd(&sh[order_key(v[e]) >> 20], 1);
   __syncthreads();
   int32_t* gh = hist + (size_t)b * kBins;
   for (int i = threadIdx.x; i < kBins; i += 256)

@@ -36,7 +36,7 @@ SCORE_CASES = [
     (2, 900, 900, 3, 64, [900, 450]),
     (1, 600, 600, 5, 128, [600]),
     # more per-block softmax pairs per head than one pass of the merge holds
-    (1, 40000, 40000, 16, 64, [40000]),
+    (1, 70000, 70000, 16, 64, [70000]),
 ]
 
 
