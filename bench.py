@@ -41,6 +41,10 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--attn-iters", type=int, default=20)
+    ap.add_argument("--variants", action="store_true",
+                    help="also time the secondary schedules: steps with a 1 GiB cache flush "
+                         "before each, per-layer attention launches, and the unfused "
+                         "score / top-k / gather / compact-attention sequence")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run three 1 GiB device-to-device copies (known HBM bytes) so "
                          "that PMC byte counters can be scaled")
@@ -279,6 +283,8 @@ def main():
         "step_ms_events": round(ev_ms_per_step, 4),
         "op_us": {k: round(v, 2) for k, v in op_us.items()},
     }
+    if args.variants:
+        line["variants"] = run_variants(args, spec, w, x, call, outputs, ws, step_bytes)
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
@@ -401,6 +407,117 @@ def run_elastic(args, spec, w, x, e, algorithmic_bytes):
         "first_step_us": round(step_us[0], 1),
         "later_steps_us_mean": round(statistics.mean(step_us[1:]), 1) if S > 1 else None,
     }
+
+
+def run_variants(args, spec, w, x, call, outputs, ws, step_bytes):
+    """Secondary schedules of the same step (µs per step, HIP events on the
+    launch stream).
+
+    flushed_step: each step alone, after a 1 GiB write that evicts the L2 and
+    the 256 MB last-level cache (outside the events): median, p10, p90.
+    per_layer_attention: score, top-k, then one attention launch per layer
+    (the schedule of a model that attends layer by layer).
+    unfused: score, top-k, materialised gather of the selected rows of every
+    layer, attention over the compact rows.
+    fused_step_graph: the fused step, replayed from a HIP graph.
+    The last three are captured in HIP graphs and replayed.
+    """
+    import torch
+
+    dev = x["K"].device
+    n = max(args.steps // 2, 5)
+
+    def ev_loop(fn, iters):
+        """µs per call of fn, captured once in a HIP graph and replayed
+        (the many small launches of these schedules would otherwise time the
+        Python launch path, not the GPU)."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for _ in range(3):
+                fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            fn()
+        graph.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        del graph
+        return e0.elapsed_time(e1) * 1e3 / iters
+
+    res = {}
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    times = []
+    for i in range(n):
+        flush.fill_(i & 255)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        spec.step(**call, outputs=outputs, ws=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e3)
+    del flush
+    times.sort()
+    med = statistics.median(times)
+    res["flushed_step"] = {"median_us": round(med, 1), "p10_us": round(times[len(times) // 10], 1),
+                           "p90_us": round(times[(9 * len(times)) // 10], 1),
+                           "steps_per_s": round(1e6 / med, 1),
+                           "frac_of_peak": round(step_bytes / (med * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4)}
+
+    scores = torch.empty((w.B, w.L_cap), dtype=torch.float32, device=dev)
+    idx, counts = outputs["idx"], outputs["counts"]
+    dims_s = _dims_of(spec, w, x)
+    ws_s = torch.zeros(spec.workspace_size(dims_s, spec.OP_SCORE), dtype=torch.uint8, device=dev)
+    ws_t = torch.zeros(max(16, spec.workspace_size(dims_s, spec.OP_TOPK)), dtype=torch.uint8,
+                       device=dev)
+    out = torch.empty_like(outputs["out"])
+
+    def score_topk():
+        spec.score(x["q_r"], x["K_r"], x["seq_lens"], out=scores, ws=ws_s)
+        spec.topk(scores, x["seq_lens"], x["ks"], w.k, idx=idx, counts=counts, ws=ws_t)
+
+    dims_l = spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, n_layers=1,
+                            H_q=w.H_q, H_kv=w.H_kv, d=w.d, kv_stride_layer=x["K"].stride(0),
+                            kv_stride_b=x["K"].stride(1))
+    ws_l = torch.zeros(max(16, spec.workspace_size(dims_l, spec.OP_ATTN)), dtype=torch.uint8,
+                       device=dev)
+
+    def per_layer():
+        score_topk()
+        for layer in range(w.n_layers):
+            spec.sparse_decode_attn(x["q"][layer:layer + 1], x["K"][layer:layer + 1],
+                                    x["V"][layer:layer + 1], counts, idx=idx,
+                                    out=out[layer:layer + 1], with_lse=False, ws=ws_l)
+
+    us = ev_loop(per_layer, n)
+    res["per_layer_attention"] = {"us_per_step": round(us, 1), "steps_per_s": round(1e6 / us, 1)}
+
+    ks = torch.empty((w.n_layers, w.B, w.k, w.H_kv, w.d), dtype=torch.bfloat16, device=dev)
+    vs = torch.empty_like(ks)
+    dims_c = spec.Dims.make(B=w.B, L_cap=w.k, L_max=w.k, k_max=w.k, n_layers=w.n_layers,
+                            H_q=w.H_q, H_kv=w.H_kv, d=w.d)
+    ws_c = torch.zeros(max(16, spec.workspace_size(dims_c, spec.OP_ATTN)), dtype=torch.uint8,
+                       device=dev)
+
+    def unfused():
+        score_topk()
+        spec.gather(x["K"], x["V"], idx, counts, out=(ks, vs))
+        spec.sparse_decode_attn(x["q"], ks, vs, counts, out=out, with_lse=False, ws=ws_c)
+
+    us = ev_loop(unfused, n)
+    res["unfused_with_gather"] = {"us_per_step": round(us, 1), "steps_per_s": round(1e6 / us, 1)}
+    us = ev_loop(lambda: spec.step(**call, outputs=outputs, ws=ws), n)
+    res["fused_step_graph"] = {"us_per_step": round(us, 1), "steps_per_s": round(1e6 / us, 1)}
+    del ks, vs
+    torch.cuda.empty_cache()
+    return res
 
 
 def _dims_of(spec, w, x):

@@ -246,9 +246,12 @@ def _check_cache(K: torch.Tensor, V: torch.Tensor):
     _inner_contig(K, "K", 3)
 
 
-def gather(K: torch.Tensor, V: torch.Tensor, idx: torch.Tensor, counts: torch.Tensor):
+def gather(K: torch.Tensor, V: torch.Tensor, idx: torch.Tensor, counts: torch.Tensor,
+           out: Optional[tuple] = None):
     """Materialised gather: (K_sel, V_sel) [n_layers, B, k_max, H_kv, d] with
-    rows j < counts[b] = K/V[layer, b, idx[b, j]] (rows beyond are zero)."""
+    rows j < counts[b] = K/V[layer, b, idx[b, j]].  Rows beyond counts[b]
+    are left as they are (zero when the outputs are allocated here); `out`
+    takes preallocated contiguous outputs."""
     lib = load_library()
     _check_cache(K, V)
     n_layers, B, L_cap, H_kv, d = K.shape
@@ -257,8 +260,15 @@ def gather(K: torch.Tensor, V: torch.Tensor, idx: torch.Tensor, counts: torch.Te
     _i32(counts, "counts", B)
     dims = Dims.make(B=B, L_cap=L_cap, L_max=L_cap, k_max=k_max, n_layers=n_layers, H_q=H_kv,
                      H_kv=H_kv, d=d, kv_stride_layer=K.stride(0), kv_stride_b=K.stride(1))
-    ks = torch.zeros((n_layers, B, k_max, H_kv, d), dtype=torch.bfloat16, device=K.device)
-    vs = torch.zeros_like(ks)
+    if out is None:
+        ks = torch.zeros((n_layers, B, k_max, H_kv, d), dtype=torch.bfloat16, device=K.device)
+        vs = torch.zeros_like(ks)
+    else:
+        ks, vs = out
+        for t, nm in ((ks, "K_sel"), (vs, "V_sel")):
+            _need(t, nm, torch.bfloat16, 5)
+            if tuple(t.shape) != (n_layers, B, k_max, H_kv, d) or not t.is_contiguous():
+                raise ValueError(f"{nm} must be contiguous [n_layers, B, k_max, H_kv, d]")
     _check(lib.spec_gather(ctypes.byref(dims), _p(K), _p(V), _p(idx.contiguous()), _p(counts),
                            _p(ks), _p(vs), _stream(K)), "spec_gather")
     return ks, vs

@@ -1,0 +1,51 @@
+"""The fused step captured in a HIP graph (through torch's graph capture on
+the launch stream): several replays, with eager work and synchronisations
+between them, each match the eager result bit for bit.  The library records
+no memset nodes: every scratch clear is a kernel."""
+import pytest
+import torch
+
+import paper_2512_00722_amd as spec
+from tests.gpu_helpers import announce, need_gpu
+from workloads import generate, small_workload
+
+pytestmark = pytest.mark.gpu
+
+
+def test_step_graph_replays_match_eager():
+    dev = need_gpu()
+    announce("graph replay of the fused step")
+    w = small_workload(B=3, L=3000, H_r=8, d_r=64, n_layers=3, H_q=32, H_kv=8, k=512,
+                       heavy_frac=0.02, ragged_min=1500)
+    x = generate(w, seed=11, device=dev)
+    args = dict(q_r=x["q_r"], K_r=x["K_r"], seq_lens=x["seq_lens"], ks=x["ks"], q=x["q"],
+                K=x["K"], V=x["V"], k_max=w.k)
+    dims = spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, H_r=w.H_r, d_r=w.d_r,
+                          n_layers=w.n_layers, H_q=w.H_q, H_kv=w.H_kv, d=w.d,
+                          kr_stride_b=x["K_r"].stride(0), kv_stride_layer=x["K"].stride(0),
+                          kv_stride_b=x["K"].stride(1))
+    ws = torch.zeros(spec.workspace_size(dims, spec.OP_STEP), dtype=torch.uint8, device=dev)
+    eager = spec.step(**args, with_scores=True, with_lse=True)
+    torch.cuda.synchronize()
+    ref = {k: v.clone() for k, v in eager.items() if v is not None}
+
+    outputs = {}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        spec.step(**args, with_scores=True, with_lse=True, outputs=outputs, ws=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        spec.step(**args, with_scores=True, with_lse=True, outputs=outputs, ws=ws)
+    for rep in range(4):
+        for v in outputs.values():
+            if v is not None:
+                v.fill_(7)                      # stale values must be overwritten
+        spec.score(x["q_r"], x["K_r"], x["seq_lens"])   # eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k, v in ref.items():
+            assert torch.equal(outputs[k], v), (rep, k)
