@@ -52,7 +52,9 @@ __all__ = [
     "retrieval_scores",
     "topk_indices",
     "group_max_scores",
+    "head_level_scores",
     "sparse_gqa_attention",
+    "sparse_gqa_attention_sets",
     "dense_gqa_attention",
     "elastic_update",
     "decode_step",
@@ -137,6 +139,20 @@ def group_max_scores(p: np.ndarray, n_groups: int) -> np.ndarray:
     return np.stack([p[g * per:(g + 1) * per].max(axis=0) for g in range(n_groups)])
 
 
+def head_level_scores(q_r, K_r, L: int, n_sets: int, scale: float | None = None) -> np.ndarray:
+    """Head-level importance (Sec. 4.2 head-level mapping; Sec. 4.3 "Support
+    for GQA"): the per-head softmax weights of the retrieval head, reduced by
+    an element-wise maximum within each group of heads that shares one KV
+    head.  Returns [n_sets, L]: one row of weights per KV head, from which
+    that KV head's tokens are chosen.
+    """
+    H_r = np.asarray(q_r).shape[0]
+    if L == 0:
+        return np.zeros((n_sets, 0), dtype=np.float64)
+    assert H_r % n_sets == 0
+    return group_max_scores(head_softmax(retrieval_logits(q_r, K_r, L, scale)), n_sets)
+
+
 # ---------------------------------------------------------------------------
 # Token selection
 # ---------------------------------------------------------------------------
@@ -193,6 +209,28 @@ def sparse_gqa_attention(q: np.ndarray, K: np.ndarray, V: np.ndarray,
         z = w.sum()
         out[h] = (w / z) @ Vs[:, g, :]
         lse[h] = m + math.log(z)
+    return out, lse
+
+
+def sparse_gqa_attention_sets(q: np.ndarray, K: np.ndarray, V: np.ndarray, idx_sets,
+                              scale: float | None = None):
+    """Decode attention with one token set per KV head (head-level selection,
+    Sec. 4.3): the query heads of group g attend over KV head g's rows at
+    idx_sets[g] only.  Same shapes and returns as sparse_gqa_attention.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    H_q, d = q.shape
+    H_kv = K.shape[1]
+    assert len(idx_sets) == H_kv and H_q % H_kv == 0
+    G = H_q // H_kv
+    out = np.zeros((H_q, d), dtype=np.float64)
+    lse = np.full((H_q,), -np.inf, dtype=np.float64)
+    for g in range(H_kv):
+        # group g alone, as an MHA/GQA problem with one KV head
+        o, l_ = sparse_gqa_attention(q[g * G:(g + 1) * G], K[:, g:g + 1], V[:, g:g + 1],
+                                     idx_sets[g], scale)
+        out[g * G:(g + 1) * G] = o
+        lse[g * G:(g + 1) * G] = l_
     return out, lse
 
 

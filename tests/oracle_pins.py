@@ -258,6 +258,80 @@ def pin_group_max_bruteforce(o):
             assert gm[g, t] == max(p[h, t] for h in range(g * 4, g * 4 + 4))
 
 
+def _sp_softmax(x):
+    import scipy.special
+    return scipy.special.softmax(x, axis=-1)
+
+
+def _torch_logits(q_r, K_r, L):
+    """q_r . K_r^T / sqrt(d_r) per head with torch in float64 (independent of the oracle)."""
+    q = torch.as_tensor(q_r, dtype=torch.float64)          # [H, d]
+    k = torch.as_tensor(K_r[:L], dtype=torch.float64)      # [L, H, d]
+    return (torch.einsum("lhd,hd->hl", k, q) / math.sqrt(q.shape[1])).numpy()
+
+
+def pin_head_level_one_head_per_set(o):
+    # H_r = n_sets: each set's weights are one head's softmax (scipy)
+    rng = np.random.default_rng(23)
+    q_r = rng.standard_normal((4, 16))
+    K_r = rng.standard_normal((30, 4, 16))
+    got = o.head_level_scores(q_r, K_r, 25, 4)
+    np.testing.assert_allclose(got, _sp_softmax(_torch_logits(q_r, K_r, 25)), rtol=1e-12,
+                               atol=1e-15)
+
+
+def pin_head_level_identical_heads(o):
+    # two identical heads per set: the group maximum is that head's softmax
+    rng = np.random.default_rng(29)
+    q1 = rng.standard_normal((3, 8))
+    K1 = rng.standard_normal((17, 3, 8))
+    q_r = np.repeat(q1, 2, axis=0)                 # heads 2g, 2g+1 equal
+    K_r = np.repeat(K1, 2, axis=1)
+    got = o.head_level_scores(q_r, K_r, 17, 3)
+    np.testing.assert_allclose(got, _sp_softmax(_torch_logits(q1, K1, 17)), rtol=1e-12,
+                               atol=1e-15)
+
+
+def pin_head_level_bounds(o):
+    # a maximum of `per` distributions: at least each of them, at most 1, and
+    # a row sum between 1 and `per`
+    rng = np.random.default_rng(31)
+    q_r = rng.standard_normal((8, 16))
+    K_r = rng.standard_normal((40, 8, 16)) * 2
+    got = o.head_level_scores(q_r, K_r, 40, 2)
+    p = _sp_softmax(_torch_logits(q_r, K_r, 40))
+    for g in range(2):
+        assert np.all(got[g] >= p[4 * g:4 * g + 4].max(axis=0) - 1e-15)
+        assert np.all(got[g] <= 1.0)
+        assert 1.0 - 1e-12 <= got[g].sum() <= 4.0 + 1e-12
+    assert o.head_level_scores(q_r, K_r, 0, 2).shape == (2, 0)
+
+
+def pin_attention_sets_per_group_sdpa(o):
+    # each group's heads against torch's SDPA over that group's own rows
+    rng = np.random.default_rng(37)
+    H_q, H_kv, d, L = 8, 2, 16, 30
+    q = rng.standard_normal((H_q, d))
+    K = rng.standard_normal((L, H_kv, d))
+    V = rng.standard_normal((L, H_kv, d))
+    sets = [np.array([1, 4, 9, 22]), np.array([0, 2, 3, 5, 28, 29])]
+    out, lse = o.sparse_gqa_attention_sets(q, K, V, sets)
+    G = H_q // H_kv
+    for g in range(H_kv):
+        Ks = torch.as_tensor(K[sets[g], g], dtype=torch.float64)
+        Vs = torch.as_tensor(V[sets[g], g], dtype=torch.float64)
+        qq = torch.as_tensor(q[g * G:(g + 1) * G], dtype=torch.float64)
+        want = torch.nn.functional.scaled_dot_product_attention(qq[None], Ks[None], Vs[None])[0]
+        np.testing.assert_allclose(out[g * G:(g + 1) * G], want.numpy(), rtol=1e-12, atol=1e-13)
+        s = (qq @ Ks.T) / math.sqrt(d)
+        np.testing.assert_allclose(lse[g * G:(g + 1) * G], torch.logsumexp(s, 1).numpy(),
+                                   rtol=1e-12)
+    # an empty set gives zero output and -inf lse for that group only
+    out2, lse2 = o.sparse_gqa_attention_sets(q, K, V, [np.array([], dtype=np.int64), sets[1]])
+    assert np.all(out2[:G] == 0) and np.all(np.isneginf(lse2[:G]))
+    np.testing.assert_allclose(out2[G:], out[G:], rtol=0, atol=0)
+
+
 # --------------------------------------------------------------- elastic
 
 def pin_elastic_worked_example(o):

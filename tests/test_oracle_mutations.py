@@ -26,6 +26,11 @@ MUTANTS = {
     "group_mean_not_max": ("return np.stack([p[g * per:(g + 1) * per].max(axis=0)", "return np.stack([p[g * per:(g + 1) * per].mean(axis=0)"),
     "accept_no_band_low": ("if np.any(inset & (score < s_k - band)):", "if False:"),
     "bf16_wrong_shift": ("<< np.uint32(16)", "<< np.uint32(15)"),
+    "head_level_sum_not_max": ("return group_max_scores(head_softmax(retrieval_logits(q_r, K_r, L, scale)), n_sets)",
+                               "return group_max_scores(head_softmax(retrieval_logits(q_r, K_r, L, scale)), 1)[[0] * n_sets]"),
+    "sets_all_use_first": ("                                     idx_sets[g], scale)", "                                     idx_sets[0], scale)"),
+    "sets_wrong_kv_head": ("o, l_ = sparse_gqa_attention(q[g * G:(g + 1) * G], K[:, g:g + 1], V[:, g:g + 1],",
+                           "o, l_ = sparse_gqa_attention(q[g * G:(g + 1) * G], K[:, 0:1], V[:, g:g + 1],"),
 }
 
 
