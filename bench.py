@@ -41,6 +41,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--attn-iters", type=int, default=20)
+    ap.add_argument("--head-level", action="store_true",
+                    help="one token set per KV head (the group maximum of the retrieval "
+                         "heads' weights) instead of one per sequence")
     ap.add_argument("--variants", action="store_true",
                     help="also time the secondary schedules: steps with a 1 GiB cache flush "
                          "before each, per-layer attention launches, and the unfused "
@@ -177,6 +180,10 @@ def main():
     t_gen = time.perf_counter() - t_gen
     print(f"[bench] workload {name} generated in {t_gen:.1f}s", file=sys.stderr, flush=True)
 
+    if w.steps > 1 and args.head_level:
+        print("bench.py: elastic loading keeps one token set per sequence; --head-level does "
+              "not apply to this workload", file=sys.stderr)
+        sys.exit(2)
     if w.steps > 1:
         line = run_elastic(args, spec, w, x, elastic_sequence(w, x, seed=args.seed, device=dev),
                            algorithmic_bytes)
@@ -184,11 +191,11 @@ def main():
         return
 
     call = dict(q_r=x["q_r"], K_r=x["K_r"], seq_lens=x["seq_lens"], ks=x["ks"], q=x["q"],
-                K=x["K"], V=x["V"], k_max=w.k)
+                K=x["K"], V=x["V"], k_max=w.k, head_level=args.head_level)
     outputs = {}
     res = spec.step(**call, outputs=outputs)
     torch.cuda.synchronize()
-    ws = torch.zeros(spec.workspace_size(_dims_of(spec, w, x), spec.OP_STEP),
+    ws = torch.zeros(spec.workspace_size(_dims_of(spec, w, x, args.head_level), spec.OP_STEP),
                      dtype=torch.uint8, device=dev)
 
     for _ in range(args.warmup):
@@ -217,7 +224,9 @@ def main():
     dims_a = _dims_attn(spec, w, x, outputs)
     ws_attn = torch.zeros(max(16, spec.workspace_size(dims_a, spec.OP_ATTN)), dtype=torch.uint8,
                           device=dev)
-    scores = torch.empty((w.B, w.L_cap), dtype=torch.float32, device=dev)
+    n_sets = w.H_kv if args.head_level else 1
+    sets = (n_sets,) if args.head_level else ()
+    scores = torch.empty((w.B,) + sets + (w.L_cap,), dtype=torch.float32, device=dev)
     # Each op is timed over n_it back-to-back launches between two events on
     # the launch stream (no host synchronisation inside the window).
     def timed(fn):
@@ -231,13 +240,14 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / n_it
 
-    ws_score = torch.zeros(spec.workspace_size(_dims_of(spec, w, x), spec.OP_SCORE),
-                           dtype=torch.uint8, device=dev)
-    ws_topk = torch.zeros(max(16, spec.workspace_size(_dims_of(spec, w, x), spec.OP_TOPK)),
+    dims_hl = _dims_of(spec, w, x, args.head_level)
+    ws_score = torch.zeros(spec.workspace_size(dims_hl, spec.OP_SCORE), dtype=torch.uint8,
+                           device=dev)
+    ws_topk = torch.zeros(max(16, spec.workspace_size(dims_hl, spec.OP_TOPK)),
                           dtype=torch.uint8, device=dev)
     op_us = {
         "score": timed(lambda: spec.score(x["q_r"], x["K_r"], x["seq_lens"], out=scores,
-                                          ws=ws_score)),
+                                          ws=ws_score, n_sets=n_sets)),
         "topk": timed(lambda: spec.topk(scores, x["seq_lens"], x["ks"], w.k, idx=outputs["idx"],
                                         counts=outputs["counts"], ws=ws_topk)),
         "attn": timed(lambda: spec.sparse_decode_attn(x["q"], x["K"], x["V"], outputs["counts"],
@@ -265,7 +275,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": name, "B": w.B, "L": w.L, "H_r": w.H_r, "d_r": w.d_r,
-                   "n_layers": w.n_layers, "H_q": w.H_q, "H_kv": w.H_kv, "d": w.d, "k": w.k},
+                   "n_layers": w.n_layers, "H_q": w.H_q, "H_kv": w.H_kv, "d": w.d, "k": w.k,
+                   "token_sets": "per_kv_head" if args.head_level else "per_sequence"},
         "roofline": {
             "bound": "hbm",
             "achieved": round(achieved, 1),
@@ -284,7 +295,7 @@ def main():
         "op_us": {k: round(v, 2) for k, v in op_us.items()},
     }
     if args.variants:
-        line["variants"] = run_variants(args, spec, w, x, call, outputs, ws, step_bytes)
+        line["variants"] = run_variants(args, spec, w, x, call, outputs, ws, step_bytes, n_sets)
     if args.copy_calibration:
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
@@ -409,7 +420,7 @@ def run_elastic(args, spec, w, x, e, algorithmic_bytes):
     }
 
 
-def run_variants(args, spec, w, x, call, outputs, ws, step_bytes):
+def run_variants(args, spec, w, x, call, outputs, ws, step_bytes, n_sets=1):
     """Secondary schedules of the same step (µs per step, HIP events on the
     launch stream).
 
@@ -471,16 +482,17 @@ def run_variants(args, spec, w, x, call, outputs, ws, step_bytes):
                            "steps_per_s": round(1e6 / med, 1),
                            "frac_of_peak": round(step_bytes / (med * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4)}
 
-    scores = torch.empty((w.B, w.L_cap), dtype=torch.float32, device=dev)
+    sets = (n_sets,) if n_sets > 1 else ()
+    scores = torch.empty((w.B,) + sets + (w.L_cap,), dtype=torch.float32, device=dev)
     idx, counts = outputs["idx"], outputs["counts"]
-    dims_s = _dims_of(spec, w, x)
+    dims_s = _dims_of(spec, w, x, n_sets > 1)
     ws_s = torch.zeros(spec.workspace_size(dims_s, spec.OP_SCORE), dtype=torch.uint8, device=dev)
     ws_t = torch.zeros(max(16, spec.workspace_size(dims_s, spec.OP_TOPK)), dtype=torch.uint8,
                        device=dev)
     out = torch.empty_like(outputs["out"])
 
     def score_topk():
-        spec.score(x["q_r"], x["K_r"], x["seq_lens"], out=scores, ws=ws_s)
+        spec.score(x["q_r"], x["K_r"], x["seq_lens"], out=scores, ws=ws_s, n_sets=n_sets)
         spec.topk(scores, x["seq_lens"], x["ks"], w.k, idx=idx, counts=counts, ws=ws_t)
 
     dims_l = spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, n_layers=1,
@@ -520,11 +532,11 @@ def run_variants(args, spec, w, x, call, outputs, ws, step_bytes):
     return res
 
 
-def _dims_of(spec, w, x):
+def _dims_of(spec, w, x, head_level=False):
     return spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, H_r=w.H_r, d_r=w.d_r,
                           n_layers=w.n_layers, H_q=w.H_q, H_kv=w.H_kv, d=w.d,
                           kr_stride_b=x["K_r"].stride(0), kv_stride_layer=x["K"].stride(0),
-                          kv_stride_b=x["K"].stride(1))
+                          kv_stride_b=x["K"].stride(1), n_sets=w.H_kv if head_level else 1)
 
 
 def _dims_attn(spec, w, x, outputs):

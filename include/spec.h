@@ -22,9 +22,17 @@
  *                                              kv_stride_b; the inner
  *                                              [token][head][dim] block is
  *                                              contiguous)
- *        scores  [B][L_max] fp32
- *        idx     [B][k_max] int32, out [n_layers][B][H_q][d] fp32,
- *        lse     [n_layers][B][H_q] fp32.
+ *        scores  [B][n_sets][L_max] fp32
+ *        idx     [B][n_sets][k_max] int32, counts [B] int32,
+ *        out     [n_layers][B][H_q][d] fp32, lse [n_layers][B][H_q] fp32.
+ *  - Token sets (spec_dims.n_sets): n_sets = 1 is the batch-level mapping of
+ *    Sec. 4.2, one set per sequence from the retrieval heads' softmax weights
+ *    summed over heads, shared by every KV head and layer.  n_sets = H_kv is
+ *    the head-level mapping of Sec. 4.2/4.3 ("Support for GQA"): set g is
+ *    chosen from the element-wise maximum, per token, of the weights of
+ *    retrieval heads g*H_r/H_kv .. (g+1)*H_r/H_kv - 1, and KV head g (with
+ *    its G query heads) attends over set g only.  Every set of a sequence has
+ *    the same size k_b.
  *  - Per-sequence lengths live on the device and are clamped in the kernels,
  *    not validated: L_b = min(seq_lens[b], L_max) (negative -> 0) and
  *    k_b = min(ks[b], L_b, k_max) (negative -> 0).
@@ -42,8 +50,9 @@
  *    multiple of 8 elements or smaller than the block it steps over, a
  *    non-zero `reserved`.  SPEC_ERR_UNSUPPORTED:
  *    d != 128, d_r not 64 or 128, H_r > 16, G = H_q/H_kv not in
- *    {1,2,4,8,16}, H_kv > 16, n_sets != 1, B or n_layers > 65535, and for
- *    elastic loading L_cap > 245760.  SPEC_ERR_WORKSPACE: ws_bytes
+ *    {1,2,4,8,16}, H_kv > 16, n_sets not 1 or H_kv, n_sets = H_kv with H_r
+ *    not a multiple of H_kv or B*n_sets > 65535, B or n_layers > 65535, and
+ *    for elastic loading L_cap > 245760 or n_sets != 1.  SPEC_ERR_WORKSPACE: ws_bytes
  *    below spec_workspace_size().  SPEC_ERR_HIP: a launch failed; the HIP
  *    error code is kept (per thread) for spec_last_hip_error().
  *  - Calls are reentrant; concurrent calls must not share a workspace.
@@ -97,8 +106,8 @@ typedef struct spec_dims {
   int64_t kv_stride_b;     /* elements between sequences of K/V; 0 = L_cap*H_kv*d */
   float scale_r;    /* retrieval softmax scale; 0 = 1/sqrt(d_r)               */
   float scale;      /* LLM attention scale; 0 = 1/sqrt(d)                     */
-  int32_t n_sets;   /* index sets per sequence; must be 1 (one set shared by
-                       every head and layer)                                  */
+  int32_t n_sets;   /* token sets per sequence: 1 (one set for every KV head,
+                       summed heads) or H_kv (one per KV head, group maximum) */
   int32_t reserved; /* must be 0                                              */
 } spec_dims;
 
@@ -114,35 +123,40 @@ typedef struct spec_elastic {
 } spec_elastic;
 
 /* Retrieval scoring (Sec. 4.3 "Implementation Details"; Eq. 1 per head;
- * batch-level mapping of Sec. 4.2).  For t < L_b:
- *     l[h,t]      = scale_r * dot(q_r[b,h,:], K_r[b,t,h,:])
- *     scores[b,t] = sum_h exp(l[h,t] - M_h) / Z_h,
+ * the mappings of Sec. 4.2).  For t < L_b:
+ *     l[h,t] = scale_r * dot(q_r[b,h,:], K_r[b,t,h,:]),
+ *     p[h,t] = exp(l[h,t] - M_h) / Z_h
  * with M_h = max_t l[h,t] and Z_h = sum_t exp(l[h,t] - M_h) (softmax per head
- * over all cached tokens, then the sum over heads).  scores[b,t] = -inf for
- * L_b <= t < L_max.  Computed in fp32 from bf16 inputs.  Needs workspace
- * spec_workspace_size(SPEC_OP_SCORE).                                       */
+ * over all cached tokens), then
+ *     n_sets = 1:    scores[b,0,t] = sum_h p[h,t]
+ *     n_sets = H_kv: scores[b,g,t] = max over the heads h of group g of p[h,t].
+ * scores[b,g,t] = -inf for L_b <= t < L_max.  Computed in fp32 from bf16
+ * inputs.  Needs workspace spec_workspace_size(SPEC_OP_SCORE).             */
 SPEC_API spec_status spec_score(const spec_dims* dm, const uint16_t* q_r,
                        const uint16_t* k_r, const int32_t* seq_lens,
                        float* scores, void* ws, size_t ws_bytes,
                        spec_stream stream);
 
 /* Token selection (Sec. 4.3: the important tokens are selected from the
- * attention weights).  For each sequence, the k_b tokens t < L_b with the
- * largest scores[b,t]; among equal scores the lower token index wins.
- * idx[b, 0..k_b) receives them in ascending token order and idx[b, k_b..k_max)
- * is set to -1.  counts (nullable) receives k_b.  The selection is exact on
- * the fp32 keys.  Needs workspace spec_workspace_size(SPEC_OP_TOPK).          */
+ * attention weights).  For each sequence b and set g, the k_b tokens t < L_b
+ * with the largest scores[b,g,t]; among equal scores the lower token index
+ * wins.  idx[b,g, 0..k_b) receives them in ascending token order and
+ * idx[b,g, k_b..k_max) is set to -1.  counts (nullable) receives k_b.  The
+ * selection is exact on the fp32 keys.  Needs workspace
+ * spec_workspace_size(SPEC_OP_TOPK).                                          */
 SPEC_API spec_status spec_topk(const spec_dims* dm, const float* scores,
                       const int32_t* seq_lens, const int32_t* ks,
                       int32_t* idx, int32_t* counts, void* ws, size_t ws_bytes,
                       spec_stream stream);
 
 /* Materialised KV gather (Sec. 4.3 "Support for MHA": the selected KV is
- * loaded per head).  For every layer, sequence and j < counts[b]:
- *     k_sel[l,b,j,:,:] = K[l,b,idx[b,j],:,:],  v_sel likewise,
- * a bit-exact copy.  k_sel/v_sel are dense [n_layers][B][k_max][H_kv][d];
- * rows j >= counts[b] are left unchanged.  idx entries must lie in [0, L_b);
- * out-of-range entries are clamped into [0, L_cap).  No workspace.           */
+ * loaded per head).  For every layer, sequence, KV head g and j < counts[b]:
+ *     k_sel[l,b,j,g,:] = K[l,b,idx[b,s,j],g,:],  v_sel likewise,
+ * with s = 0 (n_sets = 1: whole rows move) or s = g (n_sets = H_kv: each
+ * head's piece comes from its own set), a bit-exact copy.  k_sel/v_sel are
+ * dense [n_layers][B][k_max][H_kv][d], the layout compact-mode attention
+ * reads; rows j >= counts[b] are left unchanged.  idx entries must lie in
+ * [0, L_b); out-of-range entries are clamped into [0, L_cap).  No workspace. */
 SPEC_API spec_status spec_gather(const spec_dims* dm, const uint16_t* k_cache,
                         const uint16_t* v_cache, const int32_t* idx,
                         const int32_t* counts, uint16_t* k_sel,
@@ -153,8 +167,9 @@ SPEC_API spec_status spec_gather(const spec_dims* dm, const uint16_t* k_cache,
  * g = h / G).  For every layer l, sequence b and query head h:
  *     s_j = scale * dot(q[l,b,h,:], Kj[g,:]),   j < counts[b]
  *     out[l,b,h,:] = sum_j softmax_j(s) * Vj[g,:],  lse[l,b,h] = log sum_j e^{s_j}
- * Indexed mode (idx != NULL): Kj = K[l,b,idx[b,j]] read from the caches (the
- * gather is fused; indices outside [0, L_cap) are clamped into it).
+ * Indexed mode (idx != NULL): Kj = K[l,b,idx[b,s,j]] read from the caches,
+ * s = 0 for n_sets = 1 and s = g for n_sets = H_kv (the gather is fused;
+ * indices outside [0, L_cap) are clamped into it).
  * Compact mode (idx == NULL): k/v are dense [n_layers][B][k_max][H_kv][d]
  * buffers and Kj = k[l,b,j].  With counts[b] = 0 the output is 0 and lse is
  * -inf.  fp32 accumulation and output; lse is nullable.  For one layer of a
@@ -187,10 +202,11 @@ SPEC_API spec_status spec_delta_gather(const spec_dims* dm, const int32_t* idx_n
 /* One fused decode step: spec_score -> spec_topk -> [spec_delta_gather when
  * el != NULL] -> spec_sparse_decode_attn (indexed over the caches, or compact
  * over el->kbuf/vbuf when el != NULL), all enqueued on `stream` with no host
- * synchronisation.  idx_out [B][k_max] and counts_out [B] receive the
- * selection; out/lse as for spec_sparse_decode_attn (lse nullable);
- * scores_out [B][L_max] (nullable) receives the retrieval scores.  Needs
- * workspace spec_workspace_size(SPEC_OP_STEP).                              */
+ * synchronisation.  idx_out [B][n_sets][k_max] and counts_out [B] receive
+ * the selection; out/lse as for spec_sparse_decode_attn (lse nullable);
+ * scores_out [B][n_sets][L_max] (nullable) receives the retrieval scores.
+ * Elastic loading needs n_sets = 1.  Needs workspace
+ * spec_workspace_size(SPEC_OP_STEP).                                        */
 SPEC_API spec_status spec_step(const spec_dims* dm, const uint16_t* q_r,
                       const uint16_t* k_r, const int32_t* seq_lens,
                       const int32_t* ks, const uint16_t* q,

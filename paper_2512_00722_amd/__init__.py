@@ -186,9 +186,12 @@ def _dims_retrieval(K_r: torch.Tensor, L_max: int, k_max: int, scale_r: float, *
 
 def score(q_r: torch.Tensor, K_r: torch.Tensor, seq_lens: torch.Tensor,
           L_max: Optional[int] = None, scale_r: float = 0.0,
-          out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Retrieval scores [B, L_max] fp32: softmax per head over the cached
-    tokens of q_r.K_r^T * scale_r, summed over heads; -inf beyond seq_lens."""
+          out: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+          n_sets: int = 1) -> torch.Tensor:
+    """Retrieval scores fp32: softmax per head over the cached tokens of
+    q_r.K_r^T * scale_r, then summed over heads ([B, L_max], n_sets = 1) or,
+    with n_sets > 1 sets (one per KV head), the maximum over each group of
+    H_r / n_sets heads ([B, n_sets, L_max]); -inf beyond seq_lens."""
     lib = load_library()
     _need(q_r, "q_r", torch.bfloat16, 3)
     _need(K_r, "K_r", torch.bfloat16, 4)
@@ -198,10 +201,13 @@ def score(q_r: torch.Tensor, K_r: torch.Tensor, seq_lens: torch.Tensor,
     _inner_contig(K_r, "K_r", 3)
     _i32(seq_lens, "seq_lens", B)
     L_max = L_cap if L_max is None else int(L_max)
-    dims = _dims_retrieval(K_r, L_max, 1, scale_r)
+    dims = _dims_retrieval(K_r, L_max, 1, scale_r, H_q=n_sets, H_kv=n_sets, n_sets=n_sets)
     ws, nws = _workspace(dims, OP_SCORE, K_r.device, ws)
+    shape = (B, L_max) if n_sets == 1 else (B, n_sets, L_max)
     if out is None:
-        out = torch.empty((B, L_max), dtype=torch.float32, device=K_r.device)
+        out = torch.empty(shape, dtype=torch.float32, device=K_r.device)
+    elif tuple(out.shape) != shape or not out.is_contiguous() or out.dtype != torch.float32:
+        raise ValueError(f"out must be contiguous fp32 {shape}")
     _check(lib.spec_score(ctypes.byref(dims), _p(q_r), _p(K_r), _p(seq_lens), _p(out), _p(ws),
                           nws, _stream(K_r)), "spec_score")
     return out
@@ -210,19 +216,27 @@ def score(q_r: torch.Tensor, K_r: torch.Tensor, seq_lens: torch.Tensor,
 def topk(scores: torch.Tensor, seq_lens: torch.Tensor, ks: torch.Tensor, k_max: int,
          idx: Optional[torch.Tensor] = None, counts: Optional[torch.Tensor] = None,
          ws: Optional[torch.Tensor] = None):
-    """Exact top-k of each score row (ties to the lower index), ascending
-    indices [B, k_max] int32 padded with -1, and counts [B] int32."""
+    """Exact top-k of each score row (ties to the lower index): scores
+    [B, L_max] (one set per sequence) or [B, n_sets, L_max]; ascending
+    indices of the same leading shape [.., k_max] int32 padded with -1, and
+    counts [B] int32."""
     lib = load_library()
-    _need(scores, "scores", torch.float32, 2)
+    if scores.dim() == 3:
+        _need(scores, "scores", torch.float32, 3)
+        B, n_sets, L_max = scores.shape
+    else:
+        _need(scores, "scores", torch.float32, 2)
+        (B, L_max), n_sets = scores.shape, 1
     if not scores.is_contiguous():
         raise ValueError("scores must be contiguous")
-    B, L_max = scores.shape
     _i32(seq_lens, "seq_lens", B)
     _i32(ks, "ks", B)
-    dims = Dims.make(B=B, L_cap=L_max, L_max=L_max, k_max=int(k_max))
+    dims = Dims.make(B=B, L_cap=L_max, L_max=L_max, k_max=int(k_max), H_q=n_sets, H_kv=n_sets,
+                     n_sets=n_sets)
     ws, nws = _workspace(dims, OP_TOPK, scores.device, ws)
     if idx is None:
-        idx = torch.empty((B, int(k_max)), dtype=torch.int32, device=scores.device)
+        shape = (B, int(k_max)) if n_sets == 1 else (B, n_sets, int(k_max))
+        idx = torch.empty(shape, dtype=torch.int32, device=scores.device)
     if counts is None:
         counts = torch.empty((B,), dtype=torch.int32, device=scores.device)
     _check(lib.spec_topk(ctypes.byref(dims), _p(scores), _p(seq_lens), _p(ks), _p(idx),
@@ -246,6 +260,18 @@ def _check_cache(K: torch.Tensor, V: torch.Tensor):
     _inner_contig(K, "K", 3)
 
 
+def _sets_of(idx: torch.Tensor, H_kv: int) -> int:
+    """Token sets per sequence of an index tensor: [B, k_max] -> 1,
+    [B, H_kv, k_max] -> H_kv (one set per KV head)."""
+    if idx.dim() == 3:
+        _need(idx, "idx", torch.int32, 3)
+        if idx.shape[1] != H_kv:
+            raise ValueError("idx with one set per KV head must be [B, H_kv, k_max]")
+        return H_kv
+    _need(idx, "idx", torch.int32, 2)
+    return 1
+
+
 def gather(K: torch.Tensor, V: torch.Tensor, idx: torch.Tensor, counts: torch.Tensor,
            out: Optional[tuple] = None):
     """Materialised gather: (K_sel, V_sel) [n_layers, B, k_max, H_kv, d] with
@@ -255,11 +281,12 @@ def gather(K: torch.Tensor, V: torch.Tensor, idx: torch.Tensor, counts: torch.Te
     lib = load_library()
     _check_cache(K, V)
     n_layers, B, L_cap, H_kv, d = K.shape
-    _need(idx, "idx", torch.int32, 2)
-    k_max = idx.shape[1]
+    n_sets = _sets_of(idx, H_kv)
+    k_max = idx.shape[-1]
     _i32(counts, "counts", B)
     dims = Dims.make(B=B, L_cap=L_cap, L_max=L_cap, k_max=k_max, n_layers=n_layers, H_q=H_kv,
-                     H_kv=H_kv, d=d, kv_stride_layer=K.stride(0), kv_stride_b=K.stride(1))
+                     H_kv=H_kv, d=d, kv_stride_layer=K.stride(0), kv_stride_b=K.stride(1),
+                     n_sets=n_sets)
     if out is None:
         ks = torch.zeros((n_layers, B, k_max, H_kv, d), dtype=torch.bfloat16, device=K.device)
         vs = torch.zeros_like(ks)
@@ -290,10 +317,10 @@ def sparse_decode_attn(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, counts
         raise ValueError("q must be contiguous [n_layers, B, H_q, d]")
     _i32(counts, "counts", B)
     if idx is not None:
-        _need(idx, "idx", torch.int32, 2)
+        n_sets = _sets_of(idx, H_kv)
         idx = idx.contiguous()
-        k_max = idx.shape[1]
-        dims = _dims_llm(q, K, k_max, scale)
+        k_max = idx.shape[-1]
+        dims = _dims_llm(q, K, k_max, scale, n_sets=n_sets)
     else:
         k_max = L_cap
         if not K.is_contiguous():
@@ -353,9 +380,11 @@ def delta_gather(idx_now: torch.Tensor, counts: torch.Tensor, K: torch.Tensor, V
 def step(q_r, K_r, seq_lens, ks, q, K, V, k_max: int, L_max: Optional[int] = None,
          scale_r: float = 0.0, scale: float = 0.0, elastic: Optional[ElasticState] = None,
          with_scores: bool = False, with_lse: bool = False, ws: Optional[torch.Tensor] = None,
-         outputs: Optional[dict] = None):
+         outputs: Optional[dict] = None, head_level: bool = False):
     """One fused decode step (score -> top-k -> [elastic load] -> attention).
-    Returns a dict with idx, counts, out and optionally lse and scores."""
+    Returns a dict with idx, counts, out and optionally lse and scores.
+    head_level selects one token set per KV head (idx [B, H_kv, k_max],
+    scores [B, H_kv, L_max]) instead of one per sequence."""
     lib = load_library()
     _need(q_r, "q_r", torch.bfloat16, 3)
     _need(K_r, "K_r", torch.bfloat16, 4)
@@ -375,18 +404,22 @@ def step(q_r, K_r, seq_lens, ks, q, K, V, k_max: int, L_max: Optional[int] = Non
     dims = Dims.make(B=B, L_cap=L_cap, L_max=L_max, k_max=int(k_max), H_r=H_r, d_r=d_r,
                      n_layers=n_layers, H_q=q.shape[2], H_kv=H_kv, d=d,
                      kr_stride_b=K_r.stride(0), kv_stride_layer=K.stride(0),
-                     kv_stride_b=K.stride(1), scale_r=scale_r, scale=scale)
+                     kv_stride_b=K.stride(1), scale_r=scale_r, scale=scale,
+                     n_sets=H_kv if head_level else 1)
     ws, nws = _workspace(dims, OP_STEP, q.device, ws)
     dev = q.device
+    sets = (H_kv,) if head_level else ()
     o = outputs if outputs is not None else {}
     if "idx" not in o:
-        o["idx"] = torch.empty((B, int(k_max)), dtype=torch.int32, device=dev)
+        o["idx"] = torch.empty((B,) + sets + (int(k_max),), dtype=torch.int32, device=dev)
         o["counts"] = torch.empty((B,), dtype=torch.int32, device=dev)
         o["out"] = torch.empty((n_layers, B, q.shape[2], d), dtype=torch.float32, device=dev)
         o["lse"] = (torch.empty((n_layers, B, q.shape[2]), dtype=torch.float32, device=dev)
                     if with_lse else None)
-        o["scores"] = (torch.empty((B, L_max), dtype=torch.float32, device=dev)
+        o["scores"] = (torch.empty((B,) + sets + (L_max,), dtype=torch.float32, device=dev)
                        if with_scores else None)
+    elif tuple(o["idx"].shape) != (B,) + sets + (int(k_max),):
+        raise ValueError("outputs do not match the selection layout")
     el = elastic.c_struct() if elastic is not None else None
     _check(lib.spec_step(ctypes.byref(dims), _p(q_r), _p(K_r), _p(seq_lens), _p(ks), _p(q),
                          _p(K), _p(V), _p(o["idx"]), _p(o["counts"]), _p(o["out"]),

@@ -84,6 +84,7 @@ struct AttnArgs {
   int64_t stride_b;       // elements between sequences (indexed mode)
   int B, H_q, H_kv, G, k_max, L_cap, n_split, split_tokens, n_items;
   int mode;               // kDirect or kGlobalPartials
+  int n_sets;             // 1: idx [B][k_max]; H_kv: idx [B][H_kv][k_max], one set per KV head
   float scale_log2;       // scale * log2(e)
 };
 
@@ -200,7 +201,9 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
     // All index loads are issued before any is used (one round trip), and
     // one chunk of padding follows the end: the software pipeline always
     // prefetches the next chunk, and padding rows all read row 0 (cache hits).
-    const int32_t* idx_b = INDEXED ? a.idx + (size_t)b * a.k_max + j0 : nullptr;
+    const int32_t* idx_b =
+        INDEXED ? a.idx + ((size_t)b * a.n_sets + (a.n_sets > 1 ? g : 0)) * a.k_max + j0
+                : nullptr;
     const int n_pad = (n_tok + kChunk - 1) / kChunk * kChunk + kChunk;
     constexpr int kRowLoads = (kMaxSplit + kChunk + 63) / 64;
     int rv[kRowLoads];
@@ -486,7 +489,7 @@ hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
   if (n_items > INT32_MAX / 2) return hipErrorInvalidValue;
   AttnArgs a{q, k, v, idx, counts, part_acc, part_ml, out, lse, d.kv_stride_layer, d.kv_stride_b,
              d.B, d.H_q, d.H_kv, d.G, d.k_max, d.L_cap, pl.n_split, pl.split, (int)n_items,
-             pl.mode, d.scale * kLog2e};
+             pl.mode, d.n_sets, d.scale * kLog2e};
   // One workgroup per CU, fewer when there are fewer units than wavefronts.
   int dev = 0, n_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||

@@ -22,7 +22,7 @@ struct GatherArgs {
   uint16_t* k_sel;        // [n_layers][B][k_max][H_kv][d]
   uint16_t* v_sel;
   int64_t stride_layer, stride_b, row_elems;
-  int B, k_max, L_cap, n_layers;
+  int B, k_max, L_cap, n_layers, n_sets;
 };
 
 // 16-byte store that bypasses cache retention (the rows are consumed later,
@@ -41,11 +41,14 @@ __device__ __forceinline__ void stg16_stream(uint16_t* p, const uint4& v) {
 // keeps 2*kCopyUnroll 16-byte loads in flight.
 constexpr int kCopyUnroll = 8;
 
+// src_row holds `nsrc` source rows per destination row: one (the row moves
+// whole) or one per KV head (head h's cph chunks come from its own row).
 __device__ __forceinline__ void copy_rows(const uint16_t* __restrict__ ks,
                                           const uint16_t* __restrict__ vs,
                                           uint16_t* __restrict__ kd, uint16_t* __restrict__ vd,
                                           int nrows, int cpr, int64_t row_elems,
-                                          const int64_t* src_row, const int64_t* dst_row) {
+                                          const int64_t* src_row, const int64_t* dst_row,
+                                          int nsrc = 1, int cph = 1) {
   const int total = nrows * cpr;
   for (int x0 = threadIdx.x; x0 < total; x0 += 256 * kCopyUnroll) {
     uint4 kr[kCopyUnroll], vr[kCopyUnroll];
@@ -57,7 +60,7 @@ __device__ __forceinline__ void copy_rows(const uint16_t* __restrict__ ks,
       if (x < total) {
         const int r = x / cpr;
         const int c = x - r * cpr;
-        const int64_t src = src_row[r] * row_elems + 8 * c;
+        const int64_t src = src_row[r * nsrc + (nsrc > 1 ? c / cph : 0)] * row_elems + 8 * c;
         dst[u] = dst_row[r] * row_elems + 8 * c;
         kr[u] = ldg16_stream(ks + src);
         vr[u] = ldg16_stream(vs + src);
@@ -74,6 +77,8 @@ __device__ __forceinline__ void copy_rows(const uint16_t* __restrict__ ks,
 }
 
 // grid (ceil(k_max / 16), B): 16 selected rows of one sequence, every layer.
+// With one token set per KV head (n_sets = H_kv), row j of the output holds,
+// for each head g, the head-g piece of token idx[b][g][j].
 __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
   const int b = blockIdx.y;
   const int count = clampi(a.counts[b], 0, a.k_max);
@@ -81,19 +86,20 @@ __global__ __launch_bounds__(256) void gather_kernel(GatherArgs a) {
   if (j0 >= count) return;
   const int nrows = min(kRowsPerBlock, count - j0);
   const int cpr = (int)(a.row_elems / 8);  // 16-byte chunks per row
-  __shared__ int64_t src_row[kRowsPerBlock], dst_row[kRowsPerBlock];
-  if (threadIdx.x < nrows) {
-    const int j = j0 + threadIdx.x;
-    src_row[threadIdx.x] = clampi(a.idx[(size_t)b * a.k_max + j], 0, a.L_cap - 1);
-    dst_row[threadIdx.x] = (int64_t)b * a.k_max + j;
+  const int ns = a.n_sets;                 // source rows per output row
+  __shared__ int64_t src_row[kRowsPerBlock * 16], dst_row[kRowsPerBlock];
+  for (int e = threadIdx.x; e < nrows * ns; e += 256) {
+    const int r = e / ns, g = e - r * ns;
+    src_row[e] = clampi(a.idx[((size_t)b * ns + g) * a.k_max + j0 + r], 0, a.L_cap - 1);
   }
+  if (threadIdx.x < nrows) dst_row[threadIdx.x] = (int64_t)b * a.k_max + j0 + threadIdx.x;
   __syncthreads();
   const int64_t layer_rows = (int64_t)a.B * a.k_max;  // rows per layer of the output
   for (int layer = 0; layer < a.n_layers; ++layer) {
     const int64_t off = (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b;
     const int64_t doff = layer * layer_rows * a.row_elems;
     copy_rows(a.k + off, a.v + off, a.k_sel + doff, a.v_sel + doff, nrows, cpr, a.row_elems,
-              src_row, dst_row);
+              src_row, dst_row, ns, cpr / (ns > 1 ? ns : 1));
   }
 }
 
@@ -270,7 +276,7 @@ hipError_t launch_gather(const Dims& d, const uint16_t* k_cache, const uint16_t*
                          const int32_t* idx, const int32_t* counts, uint16_t* k_sel,
                          uint16_t* v_sel, hipStream_t s) {
   GatherArgs a{k_cache, v_cache, idx, counts, k_sel, v_sel, d.kv_stride_layer, d.kv_stride_b,
-               (int64_t)d.H_kv * d.d, d.B, d.k_max, d.L_cap, d.n_layers};
+               (int64_t)d.H_kv * d.d, d.B, d.k_max, d.L_cap, d.n_layers, d.n_sets};
   const dim3 grid((d.k_max + kRowsPerBlock - 1) / kRowsPerBlock, d.B);
   gather_kernel<<<grid, 256, 0, s>>>(a);
   return hipGetLastError();

@@ -13,6 +13,7 @@ struct Dims {
   int B, L_cap, L_max, k_max;
   int H_r, d_r;
   int n_layers, H_q, H_kv, d, G;
+  int n_sets;  // token sets per sequence: 1 (summed heads) or H_kv (one per KV head)
   int64_t kr_stride_b, kv_stride_layer, kv_stride_b;
   float scale_r, scale;
 };
@@ -32,10 +33,11 @@ constexpr int kSoftTokensPerBlock = 1024;
 inline int score_blocks(const Dims& d) {
   return (d.L_max + kScoreTokensPerBlock - 1) / kScoreTokensPerBlock;
 }
-// Top-k: 4096-bin histogram of the top 12 bits of the score keys per sequence.
+// Top-k: 4096-bin histogram of the top 12 bits of the score keys per score
+// row (B * n_sets rows).
 constexpr int kTopkBins = 4096;
 inline size_t topk_hist_bytes(const Dims& d) {
-  return align_up(sizeof(int32_t) * (size_t)d.B * kTopkBins);
+  return align_up(sizeof(int32_t) * (size_t)d.B * d.n_sets * kTopkBins);
 }
 
 // logits [B][L_max][H_r] fp32 + per-block (max, sum) [B][n_blk][H_r][2] fp32
@@ -60,7 +62,7 @@ inline int32_t* score_ws_hist(const Dims& d, void* ws) {
 constexpr int kTopkTile = 2048;
 inline int topk_tiles(const Dims& d) { return (d.L_max + kTopkTile - 1) / kTopkTile; }
 inline size_t topk_lists_bytes(const Dims& d) {
-  const size_t n = (size_t)d.B * topk_tiles(d);
+  const size_t n = (size_t)d.B * d.n_sets * topk_tiles(d);
   return align_up(sizeof(int32_t) * 2 * n) + 3 * align_up(sizeof(int32_t) * n * kTopkTile);
 }
 inline size_t topk_ws_bytes(const Dims& d) { return topk_hist_bytes(d) + topk_lists_bytes(d); }

@@ -29,11 +29,11 @@ struct LogitsArgs {
   const uint16_t* q_r;
   const uint16_t* k_r;
   const int32_t* seq_lens;
-  float* logits;  // [B][L_max][H_r], log2 units
+  float* logits;  // [B][H_r][L_max], log2 units
   float* part;    // [B][H_r][n_blk][2]: block max, block sum of exp2(l - max)
-  int32_t* hist;  // [B][4096] top-k histogram, zeroed here for the next kernel
+  int32_t* hist;  // [B][n_sets][4096] top-k histograms, zeroed here for the next kernel
   int64_t kr_stride_b;
-  int L_max, H_r, n_blk;
+  int L_max, H_r, n_blk, n_sets;
   float qscale;   // scale_r * log2(e)
 };
 
@@ -44,8 +44,8 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
   const int blk = blockIdx.x;
   const int L_b = clampi(a.seq_lens[b], 0, a.L_max);
   if (blk == 0) {
-    int32_t* h = a.hist + (size_t)b * kTopkBins;
-    for (int i = threadIdx.x; i < kTopkBins; i += 256) h[i] = 0;
+    int32_t* h = a.hist + (size_t)b * a.n_sets * kTopkBins;
+    for (int i = threadIdx.x; i < a.n_sets * kTopkBins; i += 256) h[i] = 0;
   }
   const int t_begin = blk * T1;
   if (t_begin >= L_b) return;  // uniform for the workgroup
@@ -59,7 +59,7 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
   const int h = c / LPH;
   const int part = c - h * LPH;
 
-  __shared__ float lg[T1 * 16];  // [token][head], H_r <= 16
+  __shared__ float lg[T1 * 17];  // [token][head], H_r <= 16; pitch 17 spreads the banks
 
   if (slot < tpi) {  // whole LPH lane groups are in or out together
     float qv[8];
@@ -85,7 +85,7 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
         for (int e = 0; e < 8; ++e) acc = fmaf(qv[e], kf[e], acc);
         acc = row_sum<LPH>(acc);
         const int i = i0 + u * tpi;
-        if (part == 0 && i < n_tok) lg[i * 16 + h] = acc;
+        if (part == 0 && i < n_tok) lg[i * 17 + h] = acc;
       }
     }
   }
@@ -95,10 +95,11 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
   // issued between the K_r loads would hold up every later load wait (the
   // vector memory counter retires loads and stores in order).
   {
-    float* lout = a.logits + ((size_t)b * a.L_max + t_begin) * a.H_r;
+    // head-major: each head's logits of the block are one contiguous run
     for (int e = threadIdx.x; e < n_tok * a.H_r; e += 256) {
-      const int i = e / a.H_r;
-      lout[e] = lg[i * 16 + (e - i * a.H_r)];
+      const int h = e / n_tok;
+      const int i = e - h * n_tok;
+      a.logits[((size_t)b * a.H_r + h) * a.L_max + t_begin + i] = lg[i * 17 + h];
     }
   }
 
@@ -107,10 +108,10 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
   const int j = tid & 15;
   if (hh < a.H_r) {
     float m = -INFINITY;
-    for (int i = j; i < n_tok; i += 16) m = fmaxf(m, lg[i * 16 + hh]);
+    for (int i = j; i < n_tok; i += 16) m = fmaxf(m, lg[i * 17 + hh]);
     m = row_max<16>(m);
     float s = 0.f;
-    for (int i = j; i < n_tok; i += 16) s += exp2f(lg[i * 16 + hh] - m);
+    for (int i = j; i < n_tok; i += 16) s += exp2f(lg[i * 17 + hh] - m);
     s = row_sum<16>(s);
     if (j == 0) {
       float* p = a.part + (((size_t)b * a.H_r + hh) * a.n_blk + blk) * 2;
@@ -124,22 +125,29 @@ struct SoftArgs {
   const float* logits;
   const float* part;
   const int32_t* seq_lens;
-  float* scores;   // [B][L_max]
-  int32_t* hist;   // [B][4096]: histogram of key bits 31..20 of the scores
-  int L_max, H_r, n_blk;
+  float* scores;   // [B][n_sets][L_max]
+  int32_t* hist;   // [B][n_sets][4096]: histogram of key bits 31..20 of the scores
+  int L_max, H_r, n_blk, n_sets;
 };
 
-// One workgroup per (T2 tokens, sequence); thread = 4 consecutive tokens.
+// One workgroup per (T2 tokens, score row); thread = 4 consecutive tokens.
+// A score row is a sequence (n_sets = 1: the heads' weights summed) or one
+// KV head of a sequence (n_sets = H_kv: the maximum over the H_r / n_sets
+// heads of its group).
 __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
   __shared__ float c_h[16];
   __shared__ float2 wred[4];
   __shared__ int sh_hist[kTopkBins];
-  const int b = blockIdx.y;
+  const int row = blockIdx.y;
+  const int b = row / a.n_sets;
+  const int per = a.H_r / a.n_sets;         // heads of this row
+  const int h0 = (row - b * a.n_sets) * per;  // its first head
+  const bool sum_heads = a.n_sets == 1;
   const int tid = threadIdx.x;
   const int t0 = blockIdx.x * T2;
   const int t1 = min(t0 + T2, a.L_max);
   const int L_b = clampi(a.seq_lens[b], 0, a.L_max);
-  float* out = a.scores + (size_t)b * a.L_max;
+  float* out = a.scores + (size_t)row * a.L_max;
   if (t0 >= L_b) {
     for (int t = t0 + tid; t < t1; t += 256) out[t] = -INFINITY;
     return;
@@ -148,41 +156,44 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
 
   // Each head's normaliser c_h = M_h + log2 Z_h from the per-block pairs
   // (head-major, so a head's pairs are contiguous): 256/P lanes per head (P =
-  // H_r rounded up to a power of two), 16 pairs in flight per lane, then a
-  // butterfly over the head's lanes of the wave and, for heads wider than a
-  // wave, a combine of the per-wave results.
+  // the row's head count rounded up to a power of two), 16 pairs in flight
+  // per lane, then a butterfly over the head's lanes of the wave and, for
+  // heads wider than a wave, a combine of the per-wave results.
   const int nb = (L_b + T1 - 1) / T1;
   const int H_r = a.H_r;
-  // This thread's logits (4 tokens x H_r heads, H_r <= 16) are loaded before
-  // the normalisers are merged: the two loads are independent.
+  // This thread's logits (4 tokens x the row's heads, at most 16) are loaded
+  // before the normalisers are merged: the two loads are independent.
+  // Logits are head-major: one float4 holds this thread's 4 tokens of a head.
   const int tb = t0 + 4 * tid;
   float lv[4][16];
+  const bool vec = (a.L_max & 3) == 0 && tb + 3 < L_b;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int t = tb + e;
-    const float* l = a.logits + ((size_t)b * a.L_max + t) * H_r;
-    if (t < L_b && (H_r & 3) == 0) {
+  for (int h = 0; h < 16; ++h) {
+    if (h < per) {
+      const float* l = a.logits + ((size_t)b * H_r + h0 + h) * a.L_max;  // head row
+      if (vec) {
+        const float4 v = *reinterpret_cast<const float4*>(l + tb);
+        lv[0][h] = v.x;
+        lv[1][h] = v.y;
+        lv[2][h] = v.z;
+        lv[3][h] = v.w;
+      } else {  // row tail: clamp into [0, L_b) (L_b >= 1 here); unused values
 #pragma unroll
-      for (int h = 0; h < 16; h += 4)
-        if (h < H_r) {
-          const float4 v = *reinterpret_cast<const float4*>(l + h);
-          lv[e][h] = v.x;
-          lv[e][h + 1] = v.y;
-          lv[e][h + 2] = v.z;
-          lv[e][h + 3] = v.w;
-        }
+        for (int e = 0; e < 4; ++e) lv[e][h] = l[min(tb + e, L_b - 1)];
+      }
     } else {
 #pragma unroll
-      for (int h = 0; h < 16; ++h) lv[e][h] = (t < L_b && h < H_r) ? l[h] : 0.f;
+      for (int e = 0; e < 4; ++e) lv[e][h] = 0.f;
     }
   }
-  const int P = H_r <= 1 ? 1 : H_r <= 2 ? 2 : H_r <= 4 ? 4 : H_r <= 8 ? 8 : 16;
+  const int P = per <= 1 ? 1 : per <= 2 ? 2 : per <= 4 ? 4 : per <= 8 ? 8 : 16;
   const int LPH = 256 / P;
   const int hh = tid / LPH;
   const int j = tid - hh * LPH;
   float m = -INFINITY, s = 0.f;
-  if (hh < H_r) {
-    const float2* p = reinterpret_cast<const float2*>(a.part) + ((size_t)b * H_r + hh) * a.n_blk;
+  if (hh < per) {
+    const float2* p =
+        reinterpret_cast<const float2*>(a.part) + ((size_t)b * H_r + h0 + hh) * a.n_blk;
     for (int i0 = j; i0 < nb; i0 += LPH * 16) {
       float2 v[16];
 #pragma unroll
@@ -201,11 +212,11 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
     ms_combine(m, s, m2, s2);
   }
   if (LPH <= 64) {
-    if (j == 0 && hh < H_r) c_h[hh] = m + log2f(s);
+    if (j == 0 && hh < per) c_h[hh] = m + log2f(s);
   } else {
     if ((tid & 63) == 0) wred[tid >> 6] = make_float2(m, s);
     __syncthreads();
-    if (tid < H_r) {
+    if (tid < per) {
       const int wpw = LPH / 64;  // waves per head
       float mm = -INFINITY, ss = 0.f;
       for (int w = tid * wpw; w < (tid + 1) * wpw; ++w) ms_combine(mm, ss, wred[w].x, wred[w].y);
@@ -223,13 +234,16 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
       sc = 0.f;
 #pragma unroll
       for (int h = 0; h < 16; ++h)
-        if (h < H_r) sc += exp2f(lv[e][h] - c_h[h]);
+        if (h < per) {
+          const float w = exp2f(lv[e][h] - c_h[h]);
+          sc = sum_heads ? sc + w : fmaxf(sc, w);
+        }
       atomicAdd(&sh_hist[order_key(sc) >> 20], 1);
     }
     out[t] = sc;
   }
   __syncthreads();
-  int32_t* gh = a.hist + (size_t)b * kTopkBins;
+  int32_t* gh = a.hist + (size_t)row * kTopkBins;
   for (int i = tid; i < kTopkBins; i += 256)
     if (sh_hist[i]) atomicAdd(&gh[i], sh_hist[i]);
 }
@@ -244,14 +258,14 @@ hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
   float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + score_logits_bytes(d));
   int32_t* hist = score_ws_hist(d, ws);
   LogitsArgs la{q_r, k_r, seq_lens, logits, part, hist, d.kr_stride_b,
-                d.L_max, d.H_r, n_blk, d.scale_r * kLog2e};
+                d.L_max, d.H_r, n_blk, d.n_sets, d.scale_r * kLog2e};
   const dim3 g1(n_blk, d.B);
   if (d.d_r == 64)
     logits_kernel<8><<<g1, 256, 0, s>>>(la);
   else
     logits_kernel<16><<<g1, 256, 0, s>>>(la);
-  SoftArgs sa{logits, part, seq_lens, scores, hist, d.L_max, d.H_r, n_blk};
-  const dim3 g2((d.L_max + T2 - 1) / T2, d.B);
+  SoftArgs sa{logits, part, seq_lens, scores, hist, d.L_max, d.H_r, n_blk, d.n_sets};
+  const dim3 g2((d.L_max + T2 - 1) / T2, d.B * d.n_sets);
   softmax_headsum_kernel<<<g2, 256, 0, s>>>(sa);
   return hipGetLastError();
 }

@@ -35,7 +35,11 @@ spec_status resolve(const spec_dims* dm, spec::Dims* o) {
     return SPEC_ERR_INVALID;
   if (!(isfinite(dm->scale_r) && isfinite(dm->scale)) || dm->scale_r < 0.f || dm->scale < 0.f)
     return SPEC_ERR_INVALID;
-  if (dm->n_sets != 1) return SPEC_ERR_UNSUPPORTED;
+  // One token set per sequence (the heads' weights summed), or one per KV
+  // head (the maximum over the retrieval heads of its group).
+  if (dm->n_sets != 1 && dm->n_sets != dm->H_kv) return SPEC_ERR_UNSUPPORTED;
+  if (dm->n_sets > 1 && (dm->H_r % dm->n_sets != 0 || (int64_t)dm->B * dm->n_sets > 65535))
+    return SPEC_ERR_UNSUPPORTED;
   if (dm->d != 128) return SPEC_ERR_UNSUPPORTED;
   if (dm->d_r != 64 && dm->d_r != 128) return SPEC_ERR_UNSUPPORTED;
   if (dm->H_r > 16) return SPEC_ERR_UNSUPPORTED;
@@ -56,6 +60,7 @@ spec_status resolve(const spec_dims* dm, spec::Dims* o) {
   o->H_kv = dm->H_kv;
   o->d = dm->d;
   o->G = dm->H_q / dm->H_kv;
+  o->n_sets = dm->n_sets;
   o->kr_stride_b = dm->kr_stride_b ? dm->kr_stride_b : kr_row;
   o->kv_stride_b = dm->kv_stride_b ? dm->kv_stride_b : kv_row;
   o->kv_stride_layer = dm->kv_stride_layer ? dm->kv_stride_layer : (int64_t)dm->B * o->kv_stride_b;
@@ -75,7 +80,8 @@ size_t ws_bytes_for(const spec::Dims& d, spec_op op) {
     case SPEC_OP_ATTN: return spec::attn_ws_bytes(d);
     case SPEC_OP_DELTA: return spec::delta_ws_bytes(d);
     case SPEC_OP_STEP:
-      return spec::align_up(sizeof(float) * (size_t)d.B * d.L_max) + spec::score_ws_bytes(d) +
+      return spec::align_up(sizeof(float) * (size_t)d.B * d.n_sets * d.L_max) +
+             spec::score_ws_bytes(d) +
              spec::topk_ws_bytes(d) + spec::attn_ws_bytes(d) + spec::delta_ws_bytes(d);
   }
   return 0;
@@ -99,6 +105,8 @@ hipStream_t as_stream(spec_stream s) { return reinterpret_cast<hipStream_t>(s); 
 
 spec_status check_elastic(const spec::Dims& d, const spec_elastic* el) {
   if (!el || !el->slot_tok || !el->kbuf || !el->vbuf || !el->n_changed) return SPEC_ERR_INVALID;
+  // the compact slot buffers hold one token per slot for every KV head
+  if (d.n_sets != 1) return SPEC_ERR_UNSUPPORTED;
   if (!aligned4(el->slot_tok) || !aligned4(el->n_changed) || !aligned16(el->kbuf) ||
       !aligned16(el->vbuf))
     return SPEC_ERR_INVALID;
@@ -217,7 +225,7 @@ spec_status spec_step(const spec_dims* dm, const uint16_t* q_r, const uint16_t* 
 
   char* p = static_cast<char*>(ws);
   float* scores = reinterpret_cast<float*>(p);
-  p += spec::align_up(sizeof(float) * (size_t)d.B * d.L_max);
+  p += spec::align_up(sizeof(float) * (size_t)d.B * d.n_sets * d.L_max);
   if (scores_out) scores = scores_out;
   void* ws_score = p;
   p += spec::score_ws_bytes(d);

@@ -163,7 +163,7 @@ struct SelArgs {
   int32_t* idx;         // [B][k_max]
   int32_t* counts;      // [B] or null
   TileLists tl;
-  int L_max, k_max;
+  int L_max, k_max, n_sets;  // score rows: B * n_sets, sequence = row / n_sets
 };
 
 __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
@@ -174,14 +174,15 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
   __shared__ int s_scan[2 * kWaves];
   __shared__ int s_sel[4];
 
-  const int b = blockIdx.x;
+  const int srow = blockIdx.x;      // score row
+  const int b = srow / a.n_sets;    // its sequence
   const int tid = threadIdx.x;
   const int L_b = clampi(a.seq_lens[b], 0, a.L_max);
   const int k_b = clampi(a.ks[b], 0, min(L_b, a.k_max));
-  const float* row = a.scores + (size_t)b * a.L_max;
-  int32_t* out = a.idx + (size_t)b * a.k_max;
+  const float* row = a.scores + (size_t)srow * a.L_max;
+  int32_t* out = a.idx + (size_t)srow * a.k_max;
 
-  if (tid == 0 && a.counts) a.counts[b] = k_b;
+  if (tid == 0 && a.counts && srow == b * a.n_sets) a.counts[b] = k_b;
   for (int j = k_b + tid; j < a.k_max; j += kThreads) out[j] = -1;
   if (k_b == 0 || k_b == L_b) {  // nothing, or every token, is selected
     for (int j = tid; j < k_b; j += kThreads) out[j] = j;
@@ -189,11 +190,11 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
   }
 
   // ---- the bin of the k-th key from the 12-bit histogram
-  const int32_t* gh = a.hist + (size_t)b * kBins;
+  const int32_t* gh = a.hist + (size_t)srow * kBins;
   const int n_tiles_b = (L_b + kTile - 1) / kTile;
   // The per-tile list counts are loaded with the histogram (one round trip);
   // they are only used on the fast path.
-  const int32_t* tcnt = a.tl.cnt + (size_t)b * a.tl.n_tiles * 2;
+  const int32_t* tcnt = a.tl.cnt + (size_t)srow * a.tl.n_tiles * 2;
   const int tcl = min(tid, a.tl.n_tiles - 1);  // clamped: the load is unconditional
   int tg = tcnt[2 * tcl];
   int tc = tcnt[2 * tcl + 1];
@@ -232,9 +233,9 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
     __syncthreads();
     const int lane = tid & 63;
     const int wv = tid >> 6;
-    const int32_t* tgt = a.tl.gt + (size_t)b * a.tl.n_tiles * kTile;
-    const uint32_t* tck = a.tl.ckey + (size_t)b * a.tl.n_tiles * kTile;
-    const int32_t* tci = a.tl.cidx + (size_t)b * a.tl.n_tiles * kTile;
+    const int32_t* tgt = a.tl.gt + (size_t)srow * a.tl.n_tiles * kTile;
+    const uint32_t* tck = a.tl.ckey + (size_t)srow * a.tl.n_tiles * kTile;
+    const int32_t* tci = a.tl.cidx + (size_t)srow * a.tl.n_tiles * kTile;
     auto put = [&](int t, int i, int gv, uint32_t kv, int iv) {
       if (i < s_cnt_g[t] && s_off_g[t] + i < kGtCap) s_gt[s_off_g[t] + i] = gv;
       if (i < s_cnt_c[t] && s_off_c[t] + i < kCandCap) {
@@ -414,7 +415,7 @@ struct ClsArgs {
   const int32_t* ks;
   const int32_t* hist;
   TileLists tl;
-  int L_max, k_max;
+  int L_max, k_max, n_sets;  // score rows: B * n_sets, sequence = row / n_sets
 };
 
 // grid (n_tiles, B).  Wave w of a tile owns tokens [t0 + 512w, t0 + 512w + 512);
@@ -425,7 +426,8 @@ __global__ __launch_bounds__(kClsThreads) void topk_classify_kernel(ClsArgs a) {
   __shared__ int s_scan[2 * kClsWaves];
   __shared__ int s_sel[4];
   __shared__ int s_wcnt[2 * kClsWaves];
-  const int b = blockIdx.y;
+  const int srow = blockIdx.y;  // score row
+  const int b = srow / a.n_sets;
   const int tile = blockIdx.x;
   const int tid = threadIdx.x;
   const int L_b = clampi(a.seq_lens[b], 0, a.L_max);
@@ -435,7 +437,7 @@ __global__ __launch_bounds__(kClsThreads) void topk_classify_kernel(ClsArgs a) {
 
   // The tile's keys and the histogram are independent: both loads are in
   // flight before either is used.
-  const float* row = a.scores + (size_t)b * a.L_max;
+  const float* row = a.scores + (size_t)srow * a.L_max;
   const int lane = tid & 63;
   const int wv = tid >> 6;
   const int w0 = min(t0 + wv * (kTile / kClsWaves), L_b);
@@ -443,7 +445,7 @@ __global__ __launch_bounds__(kClsThreads) void topk_classify_kernel(ClsArgs a) {
   uint32_t kk[kClsPerLane];
 #pragma unroll
   for (int j = 0; j < kClsPerLane; ++j) kk[j] = key_at(row, w0 + 64 * j + lane, w1, a.L_max);
-  load_hist<kClsThreads>(a.hist + (size_t)b * kBins, s_hist);
+  load_hist<kClsThreads>(a.hist + (size_t)srow * kBins, s_hist);
   if (tid == 0) s_sel[0] = s_sel[1] = s_sel[2] = -1;
   __syncthreads();
   find_bin<kClsThreads>(s_hist, kBins, k_b, s_scan, s_sel);
@@ -475,7 +477,7 @@ __global__ __launch_bounds__(kClsThreads) void topk_classify_kernel(ClsArgs a) {
     gtot += s_wcnt[i];
     ctot += s_wcnt[kClsWaves + i];
   }
-  const size_t tb = ((size_t)b * a.tl.n_tiles + tile);
+  const size_t tb = ((size_t)srow * a.tl.n_tiles + tile);
   int32_t* gt = a.tl.gt + tb * kTile;
   uint32_t* ck = a.tl.ckey + tb * kTile;
   int32_t* ci = a.tl.cidx + tb * kTile;
@@ -507,15 +509,15 @@ __global__ __launch_bounds__(kClsThreads) void topk_classify_kernel(ClsArgs a) {
 // histogram on the fly).  grid (ceil(L_max / 4096), B); hist pre-zeroed.
 __global__ __launch_bounds__(256) void topk_hist_kernel(const float* scores,
                                                         const int32_t* seq_lens,
-                                                        int32_t* hist, int L_max) {
+                                                        int32_t* hist, int L_max, int n_sets) {
   __shared__ int sh[kBins];
-  const int b = blockIdx.y;
-  const int L_b = clampi(seq_lens[b], 0, L_max);
+  const int srow = blockIdx.y;  // score row; its sequence is srow / n_sets
+  const int L_b = clampi(seq_lens[srow / n_sets], 0, L_max);
   const int t0 = blockIdx.x * 4096;
   if (t0 >= L_b) return;
   for (int i = threadIdx.x; i < kBins; i += 256) sh[i] = 0;
   __syncthreads();
-  const float* row = scores + (size_t)b * L_max;
+  const float* row = scores + (size_t)srow * L_max;
   const int t1 = min(t0 + 4096, L_b);
   float v[16];  // 4096 / 256 tokens per thread, all loads in flight
 #pragma unroll
@@ -524,7 +526,7 @@ __global__ __launch_bounds__(256) void topk_hist_kernel(const float* scores,
   for (int e = 0; e < 16; ++e)
     if (t0 + (int)threadIdx.x + 256 * e < t1) atomicAdd(&sh[order_key(v[e]) >> 20], 1);
   __syncthreads();
-  int32_t* gh = hist + (size_t)b * kBins;
+  int32_t* gh = hist + (size_t)srow * kBins;
   for (int i = threadIdx.x; i < kBins; i += 256)
     if (sh[i]) atomicAdd(&gh[i], sh[i]);
 }
@@ -536,7 +538,7 @@ __global__ __launch_bounds__(256) void zero_kernel(int32_t* p, int n) {
 TileLists tile_lists(const Dims& d, void* lists) {
   TileLists tl;
   const int n_tiles = topk_tiles(d);
-  const size_t n = (size_t)d.B * n_tiles;
+  const size_t n = (size_t)d.B * d.n_sets * n_tiles;
   char* p = static_cast<char*>(lists);
   tl.cnt = reinterpret_cast<int32_t*>(p);
   p += align_up(sizeof(int32_t) * 2 * n);
@@ -555,10 +557,10 @@ hipError_t launch_topk_select(const Dims& d, const float* scores, const int32_t*
                               const int32_t* ks, const int32_t* hist, void* lists, int32_t* idx,
                               int32_t* counts, hipStream_t s) {
   const TileLists tl = tile_lists(d, lists);
-  ClsArgs c{scores, seq_lens, ks, hist, tl, d.L_max, d.k_max};
-  topk_classify_kernel<<<dim3(tl.n_tiles, d.B), kClsThreads, 0, s>>>(c);
-  SelArgs a{scores, seq_lens, ks, hist, idx, counts, tl, d.L_max, d.k_max};
-  topk_select_kernel<<<d.B, kThreads, 0, s>>>(a);
+  ClsArgs c{scores, seq_lens, ks, hist, tl, d.L_max, d.k_max, d.n_sets};
+  topk_classify_kernel<<<dim3(tl.n_tiles, d.B * d.n_sets), kClsThreads, 0, s>>>(c);
+  SelArgs a{scores, seq_lens, ks, hist, idx, counts, tl, d.L_max, d.k_max, d.n_sets};
+  topk_select_kernel<<<d.B * d.n_sets, kThreads, 0, s>>>(a);
   return hipGetLastError();
 }
 
@@ -566,10 +568,10 @@ hipError_t launch_topk(const Dims& d, const float* scores, const int32_t* seq_le
                        const int32_t* ks, int32_t* idx, int32_t* counts, void* ws,
                        hipStream_t s) {
   int32_t* hist = static_cast<int32_t*>(ws);
-  const int n = d.B * kBins;
+  const int n = d.B * d.n_sets * kBins;
   zero_kernel<<<(n + 255) / 256, 256, 0, s>>>(hist, n);
-  const dim3 g((d.L_max + 4095) / 4096, d.B);
-  topk_hist_kernel<<<g, 256, 0, s>>>(scores, seq_lens, hist, d.L_max);
+  const dim3 g((d.L_max + 4095) / 4096, d.B * d.n_sets);
+  topk_hist_kernel<<<g, 256, 0, s>>>(scores, seq_lens, hist, d.L_max, d.n_sets);
   return launch_topk_select(d, scores, seq_lens, ks, hist,
                             static_cast<char*>(ws) + topk_hist_bytes(d), idx, counts, s);
 }

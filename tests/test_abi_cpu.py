@@ -66,7 +66,8 @@ def ws_size(lib, dims, op):
     ("H_q", 30, 1),             # H_q % H_kv != 0
     ("d", 64, 2), ("d_r", 32, 2), ("H_r", 17, 2), ("H_kv", 32, 2),
     ("H_q", 24, 2),             # G = 3
-    ("n_sets", 8, 2),
+    ("n_sets", 4, 2),           # neither 1 nor H_kv
+    ("n_sets", 0, 2),
     ("reserved", 1, 1),
     ("kv_stride_b", 12, 1),     # smaller than a sequence's block
     ("kr_stride_b", 16384 * 8 * 64 + 3, 1),  # not a multiple of 8
@@ -78,6 +79,26 @@ def test_dims_validation(lib, field, value, status):
     for op in range(6):
         st, _ = ws_size(lib, d, op)
         assert st == status, (field, op, st)
+
+
+def test_head_level_sets(lib):
+    # one set per KV head: valid when H_r is a multiple of H_kv
+    d = good_dims(n_sets=8)
+    for op in range(6):
+        assert ws_size(lib, d, op)[0] == 0
+    st1, n1 = ws_size(lib, good_dims(), spec.OP_STEP)
+    st8, n8 = ws_size(lib, d, spec.OP_STEP)
+    assert n8 > n1                       # per-set scores, histograms and lists
+    assert ws_size(lib, good_dims(n_sets=8, H_r=12), spec.OP_SCORE)[0] == 2
+    assert ws_size(lib, good_dims(n_sets=8, B=9000), spec.OP_TOPK)[0] == 2   # B*n_sets rows
+    # elastic loading keeps one token per slot for every head: not with sets
+    el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value)
+    _, nws = ws_size(lib, d, spec.OP_STEP)
+    assert lib.spec_delta_gather(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, ctypes.byref(el), FAKE,
+                                 nws, None) == 2
+    assert lib.spec_step(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                         FAKE, None, None, ctypes.byref(el), FAKE, nws, None) == 2
+    assert lib.spec_last_hip_error() == 0
 
 
 def test_workspace_sizes(lib):

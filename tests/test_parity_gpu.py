@@ -375,3 +375,157 @@ def test_step_elastic_equals_indexed(dev):
             c = int(r_ix["counts"][b])
             assert sorted(slots[b, :c].tolist()) == r_ix["idx"][b, :c].cpu().tolist()
             assert np.all(slots[b, c:] == -1)
+
+
+# ------------------------------------------------------- head-level selection
+
+SET_SCORE_CASES = [
+    # B, L_cap, H_r, d_r, n_sets (= H_kv), seq_lens
+    (2, 700, 8, 64, 8, [700, 333]),       # one retrieval head per KV head
+    (2, 1000, 16, 64, 8, [1000, 600]),    # two heads per group: their maximum
+    (1, 520, 4, 128, 2, [520]),
+    (3, 300, 8, 64, 4, [300, 1, 0]),
+]
+
+
+@pytest.mark.parametrize("case", SET_SCORE_CASES, ids=[str(c[:5]) for c in SET_SCORE_CASES])
+def test_score_head_level(dev, case):
+    B, L_cap, H_r, d_r, n_sets, lens = case
+    announce(f"score head-level {case}")
+    g = torch.Generator().manual_seed(2000 + B * L_cap + H_r)
+    q_r = _rand_bf16((B, H_r, d_r), g)
+    K_r = _rand_bf16((B, L_cap, H_r, d_r), g, 1.5)
+    seq = torch.tensor(lens, dtype=torch.int32)
+    got = spec.score(q_r.to(dev), K_r.to(dev), seq.to(dev), n_sets=n_sets)
+    torch.cuda.synchronize()
+    assert tuple(got.shape) == (B, n_sets, L_cap)
+    got = got.cpu().numpy().astype(np.float64)
+    for b in range(B):
+        L = lens[b]
+        want = oracle.head_level_scores(f64(q_r)[b], f64(K_r)[b], L, n_sets)
+        err = np.abs(got[b, :, :L] - want)
+        assert np.all(err <= SCORE_ABS + SCORE_REL * want), (b, err.max())
+        assert np.all(np.isneginf(got[b, :, L:]))
+
+
+def test_topk_head_level_rows(dev):
+    """Every (sequence, set) row is an independent exact top-k with the
+    sequence's length and budget; counts hold one value per sequence."""
+    announce("topk head-level")
+    g = torch.Generator().manual_seed(77)
+    B, n_sets, L_max, k_max = 3, 4, 3000, 400
+    sc = torch.rand((B, n_sets, L_max), generator=g)
+    sc[1, 2] = torch.randint(0, 3, (L_max,), generator=g).float()   # ties in one row
+    lens, ks = [3000, 2500, 200], [400, 399, 400]
+    idx, cnt = spec.topk(sc.to(dev), torch.tensor(lens, dtype=torch.int32).to(dev),
+                         torch.tensor(ks, dtype=torch.int32).to(dev), k_max)
+    torch.cuda.synchronize()
+    assert tuple(idx.shape) == (B, n_sets, k_max)
+    idx, cnt = idx.cpu().numpy(), cnt.cpu().numpy()
+    scn = sc.numpy().astype(np.float64)
+    for b in range(B):
+        kb = min(ks[b], lens[b])
+        assert cnt[b] == kb
+        for s_ in range(n_sets):
+            want = oracle.topk_indices(scn[b, s_, :lens[b]], kb)
+            assert idx[b, s_, :kb].tolist() == want.tolist(), (b, s_)
+            assert np.all(idx[b, s_, kb:] == -1)
+
+
+def _attn_sets_inputs(n_layers, B, L_cap, H_q, H_kv, counts, k_max, g):
+    q = _rand_bf16((n_layers, B, H_q, 128), g)
+    K = _rand_bf16((n_layers, B, L_cap, H_kv, 128), g)
+    V = _rand_bf16((n_layers, B, L_cap, H_kv, 128), g)
+    idx = torch.full((B, H_kv, k_max), -1, dtype=torch.int32)
+    for b in range(B):
+        for h in range(H_kv):
+            c = counts[b]
+            idx[b, h, :c] = torch.randperm(L_cap, generator=g)[:c].sort().values.to(torch.int32)
+    return q, K, V, idx, torch.tensor(counts, dtype=torch.int32)
+
+
+SET_ATTN_CASES = [
+    # n_layers, B, L_cap, H_q, H_kv, counts, k_max
+    (2, 2, 700, 32, 8, [513, 64], 600),
+    (1, 3, 400, 16, 4, [1, 0, 17], 64),
+    (4, 32, 160, 32, 8, [(37 * b) % 129 for b in range(32)], 128),   # one unit per group
+    (1, 1, 12000, 8, 2, [9000], 9000),                               # split selections
+]
+
+
+@pytest.mark.parametrize("case", SET_ATTN_CASES, ids=[str(c[:5]) for c in SET_ATTN_CASES])
+def test_attention_head_level_sets(dev, case):
+    n_layers, B, L_cap, H_q, H_kv, counts, k_max = case
+    announce(f"attn head-level {case}")
+    g = torch.Generator().manual_seed(300 + sum(case[:5]))
+    q, K, V, idx, cnt = _attn_sets_inputs(*case, g)
+    out, lse = spec.sparse_decode_attn(q.to(dev), K.to(dev), V.to(dev), cnt.to(dev),
+                                       idx=idx.to(dev))
+    out, lse = out.cpu().numpy(), lse.cpu().numpy()
+    qn, Kn, Vn = f64(q), f64(K), f64(V)
+    for layer in range(n_layers):
+        for b in range(B):
+            sets = [idx[b, h, :counts[b]].numpy() for h in range(H_kv)]
+            want, wl = oracle.sparse_gqa_attention_sets(qn[layer, b], Kn[layer, b], Vn[layer, b],
+                                                        sets)
+            assert np.abs(out[layer, b] - want).max() <= TOL_ATTN, (layer, b)
+            if counts[b] == 0:
+                assert np.all(np.isneginf(lse[layer, b]))
+            else:
+                assert np.abs(lse[layer, b] - wl).max() <= TOL_ATTN
+
+
+def test_gather_head_level_then_compact(dev):
+    """With one set per KV head, row j of the gathered buffer holds each
+    head's piece of its own j-th token; compact attention over it equals the
+    indexed result bit for bit."""
+    announce("gather head-level + compact")
+    g = torch.Generator().manual_seed(91)
+    case = (2, 2, 500, 16, 4, [300, 77], 320)
+    q, K, V, idx, cnt = _attn_sets_inputs(*case, g)
+    Kd, Vd, idxd, cd = K.to(dev), V.to(dev), idx.to(dev), cnt.to(dev)
+    ks, vs = spec.gather(Kd, Vd, idxd, cd)
+    ksc, vsc = ks.cpu(), vs.cpu()
+    for layer in range(2):
+        for b in range(2):
+            for h in range(4):
+                c = int(cnt[b])
+                sel = idx[b, h, :c].long()
+                assert torch.equal(ksc[layer, b, :c, h].view(torch.int16),
+                                   K[layer, b, sel, h].view(torch.int16))
+                assert torch.equal(vsc[layer, b, :c, h].view(torch.int16),
+                                   V[layer, b, sel, h].view(torch.int16))
+    out_c, _ = spec.sparse_decode_attn(q.to(dev), ks, vs, cd)
+    out_i, _ = spec.sparse_decode_attn(q.to(dev), Kd, Vd, cd, idx=idxd)
+    assert torch.equal(out_c, out_i)
+
+
+def test_step_head_level_vs_oracle(dev):
+    announce("step head-level")
+    w = small_workload(B=3, L=2500, H_r=16, d_r=64, n_layers=2, H_q=32, H_kv=8, k=300,
+                       heavy_frac=0.02, ragged_min=800)
+    x = generate(w, seed=6)
+    d_x = {n: x[n].to(dev) for n in ("q_r", "K_r", "seq_lens", "ks", "q", "K", "V")}
+    r = spec.step(d_x["q_r"], d_x["K_r"], d_x["seq_lens"], d_x["ks"], d_x["q"], d_x["K"],
+                  d_x["V"], k_max=w.k, with_scores=True, with_lse=True, head_level=True)
+    torch.cuda.synchronize()
+    idx, cnt = r["idx"].cpu().numpy(), r["counts"].cpu().numpy()
+    sc = r["scores"].cpu().numpy().astype(np.float64)
+    lens, ks = x["seq_lens"].numpy(), x["ks"].numpy()
+    for b in range(w.B):
+        L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
+        assert cnt[b] == kb
+        s64 = oracle.head_level_scores(f64(x["q_r"][b]), f64(x["K_r"][b]), L, w.H_kv)
+        sets = []
+        for h in range(w.H_kv):
+            err = np.abs(sc[b, h, :L] - s64[h])
+            assert np.all(err <= SCORE_ABS + SCORE_REL * s64[h]), (b, h)
+            assert idx[b, h, :kb].tolist() == oracle.topk_indices(sc[b, h, :L], kb).tolist()
+            ok, info = oracle.accept_index_set(s64[h], kb, idx[b, h, :kb])
+            assert ok, (b, h, info)
+            sets.append(idx[b, h, :kb])
+        for layer in range(w.n_layers):
+            want, wl = oracle.sparse_gqa_attention_sets(f64(x["q"][layer, b]), f64(x["K"][layer, b]),
+                                                        f64(x["V"][layer, b]), sets)
+            assert np.abs(r["out"][layer, b].cpu().numpy() - want).max() <= TOL_ATTN
+            assert np.abs(r["lse"][layer, b].cpu().numpy() - wl).max() <= TOL_ATTN

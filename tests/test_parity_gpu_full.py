@@ -147,3 +147,48 @@ def test_full_size_elastic_sequence(dev):
     assert np.mean(overlap) > 0.7
     del x, e, st, r
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["b8_l32768_k2048_32layers", "b32_l16384_k1024_hr16"])
+def test_full_size_step_head_level(dev, name):
+    """One token set per KV head at full size: every row's selection is the
+    exact top-k of its fp32 scores; sampled sequences match the fp64 oracle
+    (scores, accepted sets, attention over each head's own set)."""
+    w = WORKLOADS[name]
+    announce(f"full-size head-level step {name}")
+    x = generate(w, seed=0, device=dev)
+    r = spec.step(x["q_r"], x["K_r"], x["seq_lens"], x["ks"], x["q"], x["K"], x["V"], k_max=w.k,
+                  with_scores=True, with_lse=True, head_level=True)
+    torch.cuda.synchronize()
+    idx = r["idx"].cpu().numpy()
+    cnt = r["counts"].cpu().numpy()
+    sc = r["scores"].cpu().numpy().astype(np.float64)
+    lens = x["seq_lens"].cpu().numpy()
+    ks = x["ks"].cpu().numpy()
+    for b in range(w.B):
+        L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
+        assert cnt[b] == kb
+        for h in range(w.H_kv):
+            assert idx[b, h, :kb].tolist() == oracle.topk_indices(sc[b, h, :L], kb).tolist()
+            assert np.all(idx[b, h, kb:] == -1)
+    for b in sorted({0, w.B - 1}):
+        L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
+        s64 = oracle.head_level_scores(f64(x["q_r"][b]), f64(x["K_r"][b, :L]), L, w.H_kv)
+        for h in range(w.H_kv):
+            err = np.abs(sc[b, h, :L] - s64[h])
+            assert np.all(err <= SCORE_ABS + SCORE_REL * s64[h]), (b, h, err.max())
+            ok, info = oracle.accept_index_set(s64[h], kb, idx[b, h, :kb])
+            assert ok, (b, h, info)
+        rows = sorted(set(np.concatenate([idx[b, h, :kb] for h in range(w.H_kv)]).tolist()))
+        rows_t = torch.as_tensor(rows, device=dev, dtype=torch.long)
+        pos = {t: i for i, t in enumerate(rows)}
+        sets = [np.array([pos[t] for t in idx[b, h, :kb]]) for h in range(w.H_kv)]
+        for layer in _sample_layers(w.n_layers):
+            Ks = f64(x["K"][layer, b, rows_t])      # only the rows some head selected
+            Vs = f64(x["V"][layer, b, rows_t])
+            want, wl = oracle.sparse_gqa_attention_sets(f64(x["q"][layer, b]), Ks, Vs, sets)
+            got = r["out"][layer, b].cpu().numpy()
+            assert np.abs(got - want).max() <= TOL_ATTN, (layer, np.abs(got - want).max())
+            assert np.abs(r["lse"][layer, b].cpu().numpy() - wl).max() <= TOL_ATTN
+    del x, r
+    torch.cuda.empty_cache()
