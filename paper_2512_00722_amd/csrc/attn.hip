@@ -490,14 +490,15 @@ hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
   AttnArgs a{q, k, v, idx, counts, part_acc, part_ml, out, lse, d.kv_stride_layer, d.kv_stride_b,
              d.B, d.H_q, d.H_kv, d.G, d.k_max, d.L_cap, pl.n_split, pl.split, (int)n_items,
              pl.mode, d.n_sets, d.scale * kLog2e};
-  // One workgroup per CU, fewer when there are fewer units than wavefronts.
+  // One workgroup per CU, fewer only when there are fewer units than CUs:
+  // with few units they are spread over all CUs (each CU's share of the
+  // bandwidth is limited) rather than packed four to a CU.
   int dev = 0, n_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       n_cu <= 0)
     n_cu = 256;
-  const int64_t want = (n_items + kWaves - 1) / kWaves;
-  const dim3 grid((unsigned)(want < n_cu ? want : n_cu));
+  const dim3 grid((unsigned)(n_items < n_cu ? n_items : n_cu));
   if (idx)
     attn_split_kernel<true><<<grid, kWaves * 64, kLdsReserve, s>>>(a);
   else
