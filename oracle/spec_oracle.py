@@ -60,6 +60,9 @@ __all__ = [
     "decode_step",
     "accept_index_set",
     "bf16_to_f64",
+    "yarn_frequencies",
+    "rope_rotate",
+    "retrieval_qk",
 ]
 
 
@@ -237,6 +240,63 @@ def sparse_gqa_attention_sets(q: np.ndarray, K: np.ndarray, V: np.ndarray, idx_s
 def dense_gqa_attention(q, K, V, L: int, scale: float | None = None):
     """Dense decode attention over all L cached tokens (for the k = L pin)."""
     return sparse_gqa_attention(q, K, V, np.arange(L), scale)
+
+
+# ---------------------------------------------------------------------------
+# The retrieval head's front end for the new token (Sec. 4.3 "Implementation
+# Details": the head keeps the draft model's embedding and Q/K projection
+# weights and extends its context with YaRN)
+# ---------------------------------------------------------------------------
+
+def yarn_frequencies(d_r: int, base: float, scale: float, orig_ctx: int,
+                     alpha: float = 1.0, beta: float = 32.0):
+    """Rotary frequencies of the d_r/2 dimension pairs after YaRN scaling
+    (Peng et al., YaRN: the published method, written out here), and the
+    magnitude factor applied to q and k.
+
+    theta_i = base^(-2i/d_r).  A pair whose wavelength 2*pi/theta_i fits r_i =
+    orig_ctx * theta_i / (2*pi) times into the original context is
+    interpolated by gamma(r_i): gamma = 0 below alpha (the frequency is
+    divided by `scale`), 1 above beta (kept), linear in between:
+        theta'_i = (1 - gamma) * theta_i / scale + gamma * theta_i.
+    Both q and k are multiplied by m = 0.1 * ln(scale) + 1 (so that the
+    logits carry m^2); scale <= 1 leaves the frequencies and m = 1 unchanged.
+    Returns (theta' [d_r/2], m).
+    """
+    i = np.arange(d_r // 2, dtype=np.float64)
+    theta = base ** (-2.0 * i / d_r)
+    if scale <= 1.0:
+        return theta, 1.0
+    r = orig_ctx * theta / (2.0 * math.pi)
+    gamma = np.clip((r - alpha) / (beta - alpha), 0.0, 1.0)
+    theta_s = (1.0 - gamma) * theta / scale + gamma * theta
+    return theta_s, 0.1 * math.log(scale) + 1.0
+
+
+def rope_rotate(v: np.ndarray, pos: int, theta: np.ndarray, m: float = 1.0) -> np.ndarray:
+    """Rotate one head vector v [d_r] to position `pos`: dimension pair
+    (i, i + d_r/2) turns by the angle pos * theta[i] (the half-split pairing),
+    and the result is scaled by m."""
+    v = np.asarray(v, dtype=np.float64)
+    h = v.shape[-1] // 2
+    ang = pos * np.asarray(theta, dtype=np.float64)
+    c, s_ = np.cos(ang), np.sin(ang)
+    x, y = v[..., :h], v[..., h:]
+    return m * np.concatenate([x * c - y * s_, x * s_ + y * c], axis=-1)
+
+
+def retrieval_qk(token: int, pos: int, emb: np.ndarray, w_q: np.ndarray, w_k: np.ndarray,
+                 H_r: int, theta: np.ndarray, m: float):
+    """The new token's retrieval query and key: its embedding row, the Q and
+    K projections (no bias; weights [H_r*d_r, hidden] as a linear layer
+    stores them), then each head's vector rotated to position `pos`.
+    Returns (q_r [H_r, d_r], k_r [H_r, d_r]); k_r is what the token appends
+    to the retrieval key cache."""
+    x = np.asarray(emb[token], dtype=np.float64)
+    q = (np.asarray(w_q, dtype=np.float64) @ x).reshape(H_r, -1)
+    k = (np.asarray(w_k, dtype=np.float64) @ x).reshape(H_r, -1)
+    return (np.stack([rope_rotate(q[h], pos, theta, m) for h in range(H_r)]),
+            np.stack([rope_rotate(k[h], pos, theta, m) for h in range(H_r)]))
 
 
 # ---------------------------------------------------------------------------

@@ -332,6 +332,63 @@ def pin_attention_sets_per_group_sdpa(o):
     np.testing.assert_allclose(out2[G:], out[G:], rtol=0, atol=0)
 
 
+# ------------------------------------------------- retrieval-head front end
+
+def pin_yarn_worked_example(o):
+    g = _load("yarn_worked_example.json")
+    theta, m = o.yarn_frequencies(g["d_r"], g["base"], g["scale"], g["orig_ctx"])
+    np.testing.assert_allclose(theta, g["theta"], rtol=1e-9)
+    assert abs(m - g["m"]) < 1e-9
+    got = o.rope_rotate(np.array(g["v"], dtype=np.float64), g["pos"], theta, m)
+    np.testing.assert_allclose(got, g["rotated"], atol=1e-9)
+    # no scaling: the plain rotary frequencies and no magnitude factor
+    theta1, m1 = o.yarn_frequencies(8, 10000.0, 1.0, 2048)
+    np.testing.assert_allclose(theta1, [1.0, 0.1, 0.01, 0.001], rtol=1e-12)
+    assert m1 == 1.0
+
+
+def pin_rope_is_complex_rotation(o):
+    # pair (i, i + d/2) as the complex number x + iy, multiplied by e^{i pos theta_i}
+    rng = np.random.default_rng(41)
+    v = rng.standard_normal(16)
+    theta = np.exp(-rng.random(8) * 5)
+    for pos in (0, 1, 7, 100000):
+        z = (v[:8] + 1j * v[8:]) * np.exp(1j * pos * theta)
+        np.testing.assert_allclose(o.rope_rotate(v, pos, theta, 1.5),
+                                   1.5 * np.concatenate([z.real, z.imag]), atol=1e-12)
+    np.testing.assert_array_equal(o.rope_rotate(v, 0, theta), v)
+
+
+def pin_rope_relative_position(o):
+    # rotated q.k depends on the positions only through their difference, and
+    # the rotation keeps the norm (times m)
+    rng = np.random.default_rng(43)
+    q, k = rng.standard_normal(64), rng.standard_normal(64)
+    theta, m = o.yarn_frequencies(64, 500000.0, 32.0, 2048)
+    a = o.rope_rotate(q, 1000, theta, m) @ o.rope_rotate(k, 900, theta, m)
+    b = o.rope_rotate(q, 5100, theta, m) @ o.rope_rotate(k, 5000, theta, m)
+    assert abs(a - b) < 1e-9 * (1 + abs(a))
+    assert abs(np.linalg.norm(o.rope_rotate(q, 777, theta, m)) - m * np.linalg.norm(q)) < 1e-12
+
+
+def pin_retrieval_qk_projection(o):
+    # embedding row -> torch linear layers (no bias) -> rotation as complex products
+    rng = np.random.default_rng(47)
+    V, hidden, H_r, d_r = 11, 32, 2, 8
+    emb = rng.standard_normal((V, hidden))
+    w_q = rng.standard_normal((H_r * d_r, hidden))
+    w_k = rng.standard_normal((H_r * d_r, hidden))
+    theta, m = o.yarn_frequencies(d_r, 10000.0, 4.0, 16)
+    q_r, k_r = o.retrieval_qk(7, 20, emb, w_q, w_k, H_r, theta, m)
+    x = torch.as_tensor(emb[7], dtype=torch.float64)
+    for w, got in ((w_q, q_r), (w_k, k_r)):
+        y = torch.nn.functional.linear(x, torch.as_tensor(w, dtype=torch.float64)).numpy()
+        y = y.reshape(H_r, d_r)
+        z = (y[:, :d_r // 2] + 1j * y[:, d_r // 2:]) * np.exp(1j * 20 * theta)
+        np.testing.assert_allclose(got, m * np.concatenate([z.real, z.imag], axis=1),
+                                   rtol=1e-12, atol=1e-12)
+
+
 # --------------------------------------------------------------- elastic
 
 def pin_elastic_worked_example(o):

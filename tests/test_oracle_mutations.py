@@ -29,6 +29,12 @@ MUTANTS = {
     "head_level_sum_not_max": ("return group_max_scores(head_softmax(retrieval_logits(q_r, K_r, L, scale)), n_sets)",
                                "return group_max_scores(head_softmax(retrieval_logits(q_r, K_r, L, scale)), 1)[[0] * n_sets]"),
     "sets_all_use_first": ("                                     idx_sets[g], scale)", "                                     idx_sets[0], scale)"),
+    "yarn_no_division": ("theta_s = (1.0 - gamma) * theta / scale + gamma * theta", "theta_s = theta"),
+    "yarn_ramp_reversed": ("theta_s = (1.0 - gamma) * theta / scale + gamma * theta", "theta_s = gamma * theta / scale + (1.0 - gamma) * theta"),
+    "yarn_no_magnitude": ("return theta_s, 0.1 * math.log(scale) + 1.0", "return theta_s, 1.0"),
+    "rope_exponent_over_d": ("theta = base ** (-2.0 * i / d_r)", "theta = base ** (-1.0 * i / d_r)"),
+    "rope_rotation_sign": ("return m * np.concatenate([x * c - y * s_, x * s_ + y * c], axis=-1)", "return m * np.concatenate([x * c + y * s_, -x * s_ + y * c], axis=-1)"),
+    "qk_swapped": ("k = (np.asarray(w_k, dtype=np.float64) @ x).reshape(H_r, -1)", "k = (np.asarray(w_q, dtype=np.float64) @ x).reshape(H_r, -1)"),
     "sets_wrong_kv_head": ("o, l_ = sparse_gqa_attention(q[g * G:(g + 1) * G], K[:, g:g + 1], V[:, g:g + 1],",
                            "o, l_ = sparse_gqa_attention(q[g * G:(g + 1) * G], K[:, 0:1], V[:, g:g + 1],"),
 }
