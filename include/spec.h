@@ -83,7 +83,8 @@ typedef enum spec_op {
   SPEC_OP_GATHER = 2,
   SPEC_OP_ATTN = 3,
   SPEC_OP_DELTA = 4,
-  SPEC_OP_STEP = 5
+  SPEC_OP_STEP = 5,
+  SPEC_OP_FRONTEND = 6
 } spec_op;
 
 /* A hipStream_t handle; NULL selects the null stream. */
@@ -214,6 +215,51 @@ SPEC_API spec_status spec_step(const spec_dims* dm, const uint16_t* q_r,
                       int32_t* idx_out, int32_t* counts_out, float* out,
                       float* lse, float* scores_out, const spec_elastic* el,
                       void* ws, size_t ws_bytes, spec_stream stream);
+
+/* Retrieval-head front end parameters (host struct).                        */
+typedef struct spec_frontend {
+  int32_t vocab;         /* rows of the embedding table                       */
+  int32_t hidden;        /* embedding width = input width of W_q and W_k; a
+                            multiple of 128                                   */
+  float rope_base;       /* rotary base: theta_i = rope_base^(-2i/d_r), > 0   */
+  float yarn_scale;      /* YaRN context-extension factor s; <= 1 = no scaling */
+  int32_t yarn_orig_ctx; /* context the model was trained at (> 0 if s > 1)   */
+  float yarn_alpha;      /* YaRN ramp bounds, in rotations over yarn_orig_ctx; */
+  float yarn_beta;       /* alpha = beta = 0 selects 1 and 32                  */
+  int32_t reserved;      /* must be 0                                         */
+} spec_frontend;
+
+/* Retrieval-head front end for the new token of every sequence (Sec. 4.3:
+ * the retrieval head is the distilled model's embedding and Q/K projection,
+ * with its 2K context extended by YaRN).  For each sequence b, with
+ * x = emb[tokens[b]] (ids clamped into [0, vocab)) and p = pos[b]:
+ *     q = W_q x,  k = W_k x                 (fp32 accumulation, [H_r][d_r])
+ *     q_r[b,h]        = m * rot(q[h], p)    bf16 (round to nearest even)
+ *     K_r[b, p, h]    = m * rot(k[h], p)    bf16, only when 0 <= p < L_cap
+ * rot turns dimension pair (i, i + d_r/2) by the angle p * theta'_i, with
+ * theta_i = rope_base^(-2i/d_r) and, when yarn_scale = s > 1 (YaRN), the
+ * pair's r_i = yarn_orig_ctx * theta_i / (2 pi) rotations over the original
+ * context giving gamma_i = clamp((r_i - alpha) / (beta - alpha), 0, 1) and
+ *     theta'_i = (1 - gamma_i) * theta_i / s + gamma_i * theta_i,
+ *     m = 0.1 ln(s) + 1;
+ * without scaling theta' = theta and m = 1.  Angles are formed in fp64.
+ * Layouts: tokens, pos [B] int32; emb [vocab][hidden] bf16; w_q, w_k
+ * [H_r * d_r][hidden] bf16 (a linear layer's [out][in], feature h*d_r + i
+ * being dimension i of head h); q_r [B][H_r][d_r]; K_r as for spec_score
+ * (dm->B, H_r, d_r, L_cap and kr_stride_b are used; the other dimensions
+ * are validated as everywhere).  In a decode step, p is the new token's
+ * index, so that seq_lens = p + 1 afterwards makes the scoring include it.
+ * SPEC_ERR_INVALID also for a null fe, vocab or hidden <= 0, a non-finite
+ * or non-positive rope_base, a non-finite yarn_scale, and with s > 1
+ * yarn_orig_ctx <= 0 or alpha >= beta; SPEC_ERR_UNSUPPORTED for hidden not
+ * a multiple of 128.  The result is deterministic (fixed summation order).
+ * Needs workspace spec_workspace_size(SPEC_OP_FRONTEND) (fp32 partial sums
+ * of the projection; any contents on entry).                                */
+SPEC_API spec_status spec_retrieval_qk(const spec_dims* dm, const spec_frontend* fe,
+                              const int32_t* tokens, const int32_t* pos,
+                              const uint16_t* emb, const uint16_t* w_q,
+                              const uint16_t* w_k, uint16_t* q_r, uint16_t* k_r,
+                              void* ws, size_t ws_bytes, spec_stream stream);
 
 /* Workspace bytes needed by `op` for dimensions `dm` (0 for SPEC_OP_GATHER).
  * Returns the same validation status as the op itself.                      */

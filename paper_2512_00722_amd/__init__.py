@@ -22,20 +22,21 @@ import torch
 
 __all__ = [
     "SpecError", "load_library", "lib_path", "Dims", "workspace_size", "score", "topk",
-    "gather", "sparse_decode_attn", "delta_gather", "ElasticState", "step",
-    "OP_SCORE", "OP_TOPK", "OP_GATHER", "OP_ATTN", "OP_DELTA", "OP_STEP",
+    "gather", "sparse_decode_attn", "delta_gather", "ElasticState", "step", "Frontend",
+    "retrieval_qk",
+    "OP_SCORE", "OP_TOPK", "OP_GATHER", "OP_ATTN", "OP_DELTA", "OP_STEP", "OP_FRONTEND",
     "EXPORTED_SYMBOLS",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 lib_path = os.path.join(_PKG, "libspecctx.so")
 
-OP_SCORE, OP_TOPK, OP_GATHER, OP_ATTN, OP_DELTA, OP_STEP = range(6)
+OP_SCORE, OP_TOPK, OP_GATHER, OP_ATTN, OP_DELTA, OP_STEP, OP_FRONTEND = range(7)
 STATUS = {0: "SPEC_OK", 1: "SPEC_ERR_INVALID", 2: "SPEC_ERR_UNSUPPORTED",
           3: "SPEC_ERR_WORKSPACE", 4: "SPEC_ERR_HIP"}
 
 EXPORTED_SYMBOLS = ["spec_score", "spec_topk", "spec_gather", "spec_sparse_decode_attn",
-                    "spec_delta_gather", "spec_step", "spec_workspace_size",
+                    "spec_delta_gather", "spec_step", "spec_retrieval_qk", "spec_workspace_size",
                     "spec_status_string", "spec_last_hip_error", "spec_version"]
 
 
@@ -77,6 +78,14 @@ class Elastic(ctypes.Structure):
                 ("vbuf", ctypes.c_void_p), ("n_changed", ctypes.c_void_p)]
 
 
+class Frontend(ctypes.Structure):
+    """Mirror of `spec_frontend`."""
+    _fields_ = [("vocab", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("rope_base", ctypes.c_float), ("yarn_scale", ctypes.c_float),
+                ("yarn_orig_ctx", ctypes.c_int32), ("yarn_alpha", ctypes.c_float),
+                ("yarn_beta", ctypes.c_float), ("reserved", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -93,6 +102,7 @@ def load_library(path: Optional[str] = None):
     P, I, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
     D = ctypes.POINTER(Dims)
     E = ctypes.POINTER(Elastic)
+    F = ctypes.POINTER(Frontend)
     sig = {
         "spec_score": [D, P, P, P, P, P, S, P],
         "spec_topk": [D, P, P, P, P, P, P, S, P],
@@ -100,6 +110,7 @@ def load_library(path: Optional[str] = None):
         "spec_sparse_decode_attn": [D, P, P, P, P, P, P, P, P, S, P],
         "spec_delta_gather": [D, P, P, P, P, E, P, S, P],
         "spec_step": [D, P, P, P, P, P, P, P, P, P, P, P, P, E, P, S, P],
+        "spec_retrieval_qk": [D, F, P, P, P, P, P, P, P, P, S, P],
         "spec_workspace_size": [D, I, ctypes.POINTER(S)],
     }
     for name, args in sig.items():
@@ -427,3 +438,44 @@ def step(q_r, K_r, seq_lens, ks, q, K, V, k_max: int, L_max: Optional[int] = Non
                          ctypes.byref(el) if el is not None else None, _p(ws), nws,
                          _stream(q)), "spec_step")
     return o
+
+
+def retrieval_qk(tokens: torch.Tensor, pos: torch.Tensor, emb: torch.Tensor, w_q: torch.Tensor,
+                 w_k: torch.Tensor, K_r: torch.Tensor, rope_base: float = 500000.0,
+                 yarn_scale: float = 1.0, yarn_orig_ctx: int = 2048, yarn_alpha: float = 0.0,
+                 yarn_beta: float = 0.0, q_r: Optional[torch.Tensor] = None,
+                 ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Retrieval-head front end of the new token of every sequence: embedding
+    row, Q/K projection, rotary embedding with YaRN scaling.  Returns q_r
+    [B, H_r, d_r] bf16 and writes each new key into K_r[b, pos[b]] in place
+    (nothing for positions outside [0, L_cap)).  tokens, pos: int32 [B];
+    emb [vocab, hidden]; w_q, w_k [H_r * d_r, hidden] (bf16)."""
+    lib = load_library()
+    _need(emb, "emb", torch.bfloat16, 2)
+    _need(w_q, "w_q", torch.bfloat16, 2)
+    _need(w_k, "w_k", torch.bfloat16, 2)
+    _need(K_r, "K_r", torch.bfloat16, 4)
+    _inner_contig(K_r, "K_r", 3)
+    B = tokens.shape[0]
+    _i32(tokens, "tokens", B)
+    _i32(pos, "pos", B)
+    if K_r.shape[0] != B:
+        raise ValueError("K_r must hold B sequences")
+    _, L_cap, H_r, d_r = K_r.shape
+    vocab, hidden = emb.shape
+    for t, nm in ((emb, "emb"), (w_q, "w_q"), (w_k, "w_k")):
+        if not t.is_contiguous():
+            raise ValueError(f"{nm} must be contiguous")
+    if tuple(w_q.shape) != (H_r * d_r, hidden) or tuple(w_k.shape) != (H_r * d_r, hidden):
+        raise ValueError("w_q / w_k must be [H_r * d_r, hidden]")
+    if q_r is None:
+        q_r = torch.empty((B, H_r, d_r), dtype=torch.bfloat16, device=K_r.device)
+    elif tuple(q_r.shape) != (B, H_r, d_r) or not q_r.is_contiguous() or q_r.dtype != torch.bfloat16:
+        raise ValueError("q_r must be contiguous bf16 [B, H_r, d_r]")
+    dims = _dims_retrieval(K_r, L_cap, 1, 0.0)
+    ws, nws = _workspace(dims, OP_FRONTEND, K_r.device, ws)
+    fe = Frontend(vocab, hidden, rope_base, yarn_scale, yarn_orig_ctx, yarn_alpha, yarn_beta, 0)
+    _check(lib.spec_retrieval_qk(ctypes.byref(dims), ctypes.byref(fe), _p(tokens), _p(pos),
+                                 _p(emb), _p(w_q), _p(w_k), _p(q_r), _p(K_r), _p(ws), nws,
+                                 _stream(K_r)), "spec_retrieval_qk")
+    return q_r

@@ -77,6 +77,19 @@ inline size_t delta_ws_bytes(const Dims& d) {
   return align_up(sizeof(int32_t) * 2 * (size_t)d.B * d.k_max);
 }
 
+// Retrieval-head front end: embedding width, vocabulary and the rotary /
+// YaRN parameters, validated (alpha < beta; orig_ctx > 0 when scale > 1).
+struct FrontDims {
+  int vocab, hidden;
+  float base, scale, alpha, beta;
+  int orig_ctx;
+};
+// The projection splits the hidden dimension over at most this many
+// workgroups per output tile; the workspace holds one fp32 partial result
+// [split][B][2 * H_r * d_r] per split.
+constexpr int kFrontMaxSplit = 16;
+size_t front_ws_bytes(const Dims& d);
+
 // ---- launchers (return the HIP launch status) --------------------------
 hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
                         const int32_t* seq_lens, float* scores, void* ws,
@@ -98,5 +111,9 @@ hipError_t launch_delta(const Dims& d, const int32_t* idx_now, const int32_t* co
                         const uint16_t* k_cache, const uint16_t* v_cache,
                         int32_t* slot_tok, uint16_t* kbuf, uint16_t* vbuf,
                         int32_t* n_changed, void* ws, hipStream_t s);
+hipError_t launch_retrieval_qk(const Dims& d, const FrontDims& f, const int32_t* tokens,
+                               const int32_t* pos, const uint16_t* emb, const uint16_t* w_q,
+                               const uint16_t* w_k, uint16_t* q_r, uint16_t* k_r, void* ws,
+                               hipStream_t s);
 
 }  // namespace spec

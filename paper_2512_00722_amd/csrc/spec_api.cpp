@@ -79,6 +79,7 @@ size_t ws_bytes_for(const spec::Dims& d, spec_op op) {
     case SPEC_OP_GATHER: return 0;
     case SPEC_OP_ATTN: return spec::attn_ws_bytes(d);
     case SPEC_OP_DELTA: return spec::delta_ws_bytes(d);
+    case SPEC_OP_FRONTEND: return spec::front_ws_bytes(d);
     case SPEC_OP_STEP:
       return spec::align_up(sizeof(float) * (size_t)d.B * d.n_sets * d.L_max) +
              spec::score_ws_bytes(d) +
@@ -114,13 +115,38 @@ spec_status check_elastic(const spec::Dims& d, const spec_elastic* el) {
   return SPEC_OK;
 }
 
+spec_status resolve_frontend(const spec_frontend* fe, spec::FrontDims* f) {
+  if (!fe || fe->reserved != 0) return SPEC_ERR_INVALID;
+  if (fe->vocab <= 0 || fe->hidden <= 0) return SPEC_ERR_INVALID;
+  if (!isfinite(fe->rope_base) || !(fe->rope_base > 0.f) || !isfinite(fe->yarn_scale))
+    return SPEC_ERR_INVALID;
+  if (fe->hidden % 128 != 0) return SPEC_ERR_UNSUPPORTED;
+  f->vocab = fe->vocab;
+  f->hidden = fe->hidden;
+  f->base = fe->rope_base;
+  f->scale = fe->yarn_scale;
+  f->orig_ctx = fe->yarn_orig_ctx;
+  f->alpha = fe->yarn_alpha;
+  f->beta = fe->yarn_beta;
+  if (fe->yarn_scale > 1.f) {
+    if (fe->yarn_orig_ctx <= 0) return SPEC_ERR_INVALID;
+    if (fe->yarn_alpha == 0.f && fe->yarn_beta == 0.f) {
+      f->alpha = 1.f;
+      f->beta = 32.f;
+    }
+    if (!isfinite(f->alpha) || !isfinite(f->beta) || !(f->alpha < f->beta))
+      return SPEC_ERR_INVALID;
+  }
+  return SPEC_OK;
+}
+
 }  // namespace
 
 extern "C" {
 
 spec_status spec_workspace_size(const spec_dims* dm, spec_op op, size_t* bytes) {
   if (!bytes) return SPEC_ERR_INVALID;
-  if ((int)op < SPEC_OP_SCORE || (int)op > SPEC_OP_STEP) return SPEC_ERR_INVALID;
+  if ((int)op < SPEC_OP_SCORE || (int)op > SPEC_OP_FRONTEND) return SPEC_ERR_INVALID;
   spec::Dims d;
   const spec_status st = resolve(dm, &d);
   if (st != SPEC_OK) return st;
@@ -252,6 +278,24 @@ spec_status spec_step(const spec_dims* dm, const uint16_t* q_r, const uint16_t* 
     e = spec::launch_attn(d, q, k_cache, v_cache, idx_out, counts_out, out, lse, ws_attn, s);
   }
   return hip_status(e);
+}
+
+spec_status spec_retrieval_qk(const spec_dims* dm, const spec_frontend* fe,
+                              const int32_t* tokens, const int32_t* pos, const uint16_t* emb,
+                              const uint16_t* w_q, const uint16_t* w_k, uint16_t* q_r,
+                              uint16_t* k_r, void* ws, size_t ws_bytes, spec_stream stream) {
+  spec::Dims d;
+  spec_status st = resolve(dm, &d);
+  if (st != SPEC_OK) return st;
+  spec::FrontDims f;
+  if ((st = resolve_frontend(fe, &f)) != SPEC_OK) return st;
+  if (!tokens || !pos || !emb || !w_q || !w_k || !q_r || !k_r) return SPEC_ERR_INVALID;
+  if (!aligned4(tokens) || !aligned4(pos) || !aligned16(emb) || !aligned16(w_q) ||
+      !aligned16(w_k) || !aligned16(q_r) || !aligned16(k_r))
+    return SPEC_ERR_INVALID;
+  if ((st = check_ws(d, SPEC_OP_FRONTEND, ws, ws_bytes)) != SPEC_OK) return st;
+  return hip_status(spec::launch_retrieval_qk(d, f, tokens, pos, emb, w_q, w_k, q_r, k_r, ws,
+                                              as_stream(stream)));
 }
 
 const char* spec_status_string(spec_status s) {

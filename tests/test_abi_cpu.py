@@ -76,7 +76,7 @@ def ws_size(lib, dims, op):
 def test_dims_validation(lib, field, value, status):
     d = good_dims()
     setattr(d, field, value)
-    for op in range(6):
+    for op in range(7):
         st, _ = ws_size(lib, d, op)
         assert st == status, (field, op, st)
 
@@ -84,7 +84,7 @@ def test_dims_validation(lib, field, value, status):
 def test_head_level_sets(lib):
     # one set per KV head: valid when H_r is a multiple of H_kv
     d = good_dims(n_sets=8)
-    for op in range(6):
+    for op in range(7):
         assert ws_size(lib, d, op)[0] == 0
     st1, n1 = ws_size(lib, good_dims(), spec.OP_STEP)
     st8, n8 = ws_size(lib, d, spec.OP_STEP)
@@ -103,13 +103,15 @@ def test_head_level_sets(lib):
 
 def test_workspace_sizes(lib):
     d = good_dims()
-    sizes = {op: ws_size(lib, d, op) for op in range(6)}
+    sizes = {op: ws_size(lib, d, op) for op in range(7)}
     assert all(st == 0 for st, _ in sizes.values())
     assert sizes[spec.OP_GATHER][1] == 0
     assert sizes[spec.OP_SCORE][1] >= 2 * 16384 * 8 * 4      # the logits
     assert sizes[spec.OP_STEP][1] >= sizes[spec.OP_SCORE][1] + sizes[spec.OP_ATTN][1]
     assert lib.spec_workspace_size(None, 0, ctypes.byref(ctypes.c_size_t())) == 1
     assert lib.spec_workspace_size(ctypes.byref(d), 9, ctypes.byref(ctypes.c_size_t())) == 1
+    # the front end's fp32 partial sums: up to 16 slices of [B][2 * H_r * d_r]
+    assert sizes[spec.OP_FRONTEND][1] >= 16 * 2 * 2 * 8 * 64 * 4
 
 
 def test_entry_points_reject_before_hip(lib):
@@ -150,6 +152,58 @@ def test_entry_points_reject_before_hip(lib):
     el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value)
     assert lib.spec_delta_gather(byref(big), FAKE, FAKE, FAKE, FAKE, byref(el), FAKE, 1 << 40,
                                  None) == 2
+    assert lib.spec_last_hip_error() == 0
+
+
+def good_frontend(**kw):
+    base = dict(vocab=128256, hidden=4096, rope_base=500000.0, yarn_scale=16.0,
+                yarn_orig_ctx=2048, yarn_alpha=0.0, yarn_beta=0.0, reserved=0)
+    base.update(kw)
+    return spec.Frontend(**base)
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("vocab", 0, 1), ("hidden", -128, 1), ("hidden", 4000, 2),   # not a multiple of 128
+    ("rope_base", 0.0, 1), ("rope_base", float("inf"), 1), ("yarn_scale", float("nan"), 1),
+    ("yarn_orig_ctx", 0, 1),                                      # needed when scaling
+    ("yarn_alpha", 40.0, 1),                                      # alpha >= beta = 32
+    ("reserved", 3, 1),
+])
+def test_frontend_validation(lib, field, value, status):
+    """Every rejection of spec_retrieval_qk happens on the host."""
+    d = good_dims()
+    fe = good_frontend()
+    setattr(fe, field, value)
+    if field == "yarn_alpha":
+        fe.yarn_beta = 32.0
+    args = (FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30)
+    assert lib.spec_retrieval_qk(ctypes.byref(d), ctypes.byref(fe), *args, None) == status
+    assert lib.spec_last_hip_error() == 0
+
+
+def test_frontend_rejects_before_hip(lib):
+    d = good_dims()
+    fe = good_frontend()
+    byref = ctypes.byref
+    _, nws = ws_size(lib, d, spec.OP_FRONTEND)
+    ws = (FAKE, nws)
+    assert lib.spec_retrieval_qk(byref(d), None, *(FAKE,) * 7, *ws, None) == 1
+    assert lib.spec_retrieval_qk(None, byref(fe), *(FAKE,) * 7, *ws, None) == 1
+    for i in range(7):              # each tensor null in turn, then misaligned
+        args = [FAKE] * 7
+        args[i] = None
+        assert lib.spec_retrieval_qk(byref(d), byref(fe), *args, *ws, None) == 1, i
+        args[i] = ctypes.c_void_p(FAKE.value + (2 if i < 2 else 8))
+        assert lib.spec_retrieval_qk(byref(d), byref(fe), *args, *ws, None) == 1, i
+    # workspace missing, too small, misaligned
+    assert lib.spec_retrieval_qk(byref(d), byref(fe), *(FAKE,) * 7, None, nws, None) == 3
+    assert lib.spec_retrieval_qk(byref(d), byref(fe), *(FAKE,) * 7, FAKE, nws - 1, None) == 3
+    assert lib.spec_retrieval_qk(byref(d), byref(fe), *(FAKE,) * 7, FAKE_ODD, nws, None) == 1
+    # the retrieval dimensions are validated as for every entry point
+    assert lib.spec_retrieval_qk(byref(good_dims(d_r=96)), byref(fe), *(FAKE,) * 7, *ws,
+                                 None) == 2
+    assert lib.spec_retrieval_qk(byref(good_dims(kr_stride_b=12)), byref(fe), *(FAKE,) * 7,
+                                 *ws, None) == 1
     assert lib.spec_last_hip_error() == 0
 
 

@@ -6,7 +6,8 @@ import numpy as np
 import torch
 
 import oracle
-from workloads import WORKLOADS, algorithmic_bytes, elastic_sequence, generate, small_workload
+from workloads import (WORKLOADS, algorithmic_bytes, elastic_sequence, frontend_bytes,
+                       frontend_inputs, generate, small_workload)
 
 
 def test_generate_is_seeded_and_shaped():
@@ -76,3 +77,29 @@ def test_algorithmic_bytes_formula():
     # elastic rows: read + write of K and V per changed row and layer
     assert (algorithmic_bytes(w, [32768] * 8, [2048] * 8, delta_rows=10)
             - algorithmic_bytes(w, [32768] * 8, [2048] * 8)) == 2 * 10 * 8 * 128 * 2 * 2 * 32
+
+
+def test_frontend_inputs_seeded_and_shaped():
+    w = small_workload(B=4, H_r=2, d_r=64, hidden=256, vocab=97)
+    lens = np.array([10, 1, 64, 33])
+    a, b = frontend_inputs(w, lens, seed=2), frontend_inputs(w, lens, seed=2)
+    for name in ("tokens", "pos", "emb", "w_q", "w_k"):
+        assert torch.equal(a[name], b[name]), name
+    assert a["pos"].tolist() == (lens - 1).tolist()
+    assert a["tokens"].dtype == torch.int32 and 0 <= int(a["tokens"].min())
+    assert int(a["tokens"].max()) < 97
+    assert tuple(a["emb"].shape) == (97, 256) and tuple(a["w_q"].shape) == (128, 256)
+    # projected vectors have about unit variance
+    x = a["emb"].float()[a["tokens"].long()]
+    assert 0.7 < float((x @ a["w_q"].float().T).std()) < 1.3
+    assert not torch.equal(a["w_q"], a["w_k"])
+    c = frontend_inputs(w, lens, seed=3)
+    assert not torch.equal(a["emb"], c["emb"])
+
+
+def test_frontend_scale_and_bytes():
+    w = WORKLOADS["b8_l32768_k2048_32layers"]
+    assert w.yarn_scale == 16.0 and WORKLOADS["b1_l131072_k4096_g8"].yarn_scale == 64.0
+    assert WORKLOADS["b1_l4096_k512_1layer"].yarn_scale == 2.0
+    # two 512 x 4096 bf16 matrices, 8 embedding rows, q_r and the new K_r row
+    assert frontend_bytes(w) == 2 * 512 * 4096 * 2 + 8 * 4096 * 2 + 2 * 8 * 512 * 2

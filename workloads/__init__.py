@@ -31,7 +31,8 @@ import numpy as np
 import torch
 
 __all__ = ["Workload", "WORKLOADS", "BENCH_WORKLOAD", "tensor_seed",
-           "generate", "elastic_sequence", "algorithmic_bytes", "small_workload"]
+           "generate", "elastic_sequence", "algorithmic_bytes", "small_workload",
+           "frontend_inputs", "frontend_bytes"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -57,6 +58,13 @@ class Workload:
     extra_cap: int = 0     # spare capacity for appended tokens
     steps: int = 1         # decode steps simulated (elastic workload)
     drift: float = 0.95    # AR(1) coefficient of q_r across steps
+    # retrieval-head front end (synthetic weights; an 8B-class model's
+    # embedding table and width, its rotary base, and the 2K training context
+    # of the distilled model that YaRN extends to L_cap)
+    hidden: int = 4096
+    vocab: int = 128256
+    rope_base: float = 500000.0
+    orig_ctx: int = 2048
 
     @property
     def L_cap(self) -> int:
@@ -65,6 +73,11 @@ class Workload:
     @property
     def G(self) -> int:
         return self.H_q // self.H_kv
+
+    @property
+    def yarn_scale(self) -> float:
+        """Context-extension factor from the training context to L_cap."""
+        return max(1.0, self.L_cap / self.orig_ctx)
 
 
 # The five decode-step workloads (shapes of the paper's cloud/edge settings).
@@ -80,7 +93,7 @@ WORKLOADS = {
         H_q=32, H_kv=8, d=128, k=1024, heavy_frac=0.01),
     "b1_l131072_k4096_g8": Workload(
         "b1_l131072_k4096_g8", B=1, L=131072, H_r=8, d_r=128, n_layers=32,
-        H_q=64, H_kv=8, d=128, k=4096, n_clusters=3, cluster_len=512),
+        H_q=64, H_kv=8, d=128, k=4096, n_clusters=3, cluster_len=512, hidden=8192),
     "b64_ragged_l2k_16k_elastic": Workload(
         "b64_ragged_l2k_16k_elastic", B=64, L=16384, H_r=8, d_r=64,
         n_layers=32, H_q=32, H_kv=8, d=128, k=2048, heavy_frac=0.02,
@@ -230,6 +243,45 @@ def elastic_sequence(w: Workload, x: dict, seed: int = 0, device=None):
                                  dtype=torch.float32).to(torch.bfloat16)
     lens = (lens0[None, :] + torch.arange(S, device=device)[:, None]).to(torch.int32)
     return {"q_r": q_r_steps, "q": q_steps, "seq_lens": lens}
+
+
+def frontend_inputs(w: Workload, seq_lens, seed: int = 0, device="cpu", vocab=None):
+    """Inputs of the retrieval head's front end for the new token of every
+    sequence: token ids uniform over the vocabulary (numpy PCG64), the
+    embedding table N(0,1), the Q/K projection weights N(0, 1/hidden) (so
+    that the projected vectors have unit variance), all rounded to bf16, and
+    each new token's position = seq_lens - 1 (its key is the last cached row).
+    `vocab` overrides the workload's (tests use small tables).
+
+    Returns tokens [B] int32, pos [B] int32, emb [vocab, hidden],
+    w_q, w_k [H_r * d_r, hidden] (bf16).
+    """
+    device = torch.device(device)
+    V = int(vocab) if vocab is not None else w.vocab
+    rng = np.random.default_rng(tensor_seed(seed, "tokens"))
+    tokens = rng.integers(0, V, size=w.B)
+    emb = torch.empty((V, w.hidden), dtype=torch.bfloat16, device=device)
+    step = max(1, (1 << 26) // w.hidden)            # rows per fp32 chunk (256 MiB)
+    g = _gen(device, seed, "emb")
+    for r0 in range(0, V, step):
+        r1 = min(V, r0 + step)
+        emb[r0:r1] = torch.randn((r1 - r0, w.hidden), generator=g, device=device,
+                                 dtype=torch.float32).to(torch.bfloat16)
+    sd = 1.0 / float(np.sqrt(w.hidden))
+    wq = (torch.randn((w.H_r * w.d_r, w.hidden), generator=_gen(device, seed, "w_q"),
+                      device=device, dtype=torch.float32) * sd).to(torch.bfloat16)
+    wk = (torch.randn((w.H_r * w.d_r, w.hidden), generator=_gen(device, seed, "w_k"),
+                      device=device, dtype=torch.float32) * sd).to(torch.bfloat16)
+    lens = torch.as_tensor(seq_lens).to(device=device, dtype=torch.int64)
+    return {"tokens": torch.as_tensor(tokens, dtype=torch.int32, device=device),
+            "pos": (lens - 1).to(torch.int32), "emb": emb, "w_q": wq, "w_k": wk}
+
+
+def frontend_bytes(w: Workload) -> int:
+    """Bytes the front end must move: both projection matrices, one
+    embedding row per sequence, and q_r and the new K_r row written."""
+    return (2 * w.H_r * w.d_r * w.hidden * 2 + w.B * w.hidden * 2
+            + 2 * w.B * w.H_r * w.d_r * 2)
 
 
 def algorithmic_bytes(w: Workload, seq_lens, ks, delta_rows: int = 0) -> int:
