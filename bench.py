@@ -30,6 +30,8 @@ PEAK_HBM_GBPS = 8000.0  # MI355X published HBM3E bandwidth
 CSRC = os.path.join(ROOT, "paper_2512_00722_amd", "csrc")
 ATTN_SOURCES = ("attn.hip", "device_common.h", "internal.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
+FRONT_SOURCES = ("frontend.hip", "device_common.h", "internal.h")
+FRONT_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "frontend_traffic.json")
 
 
 def parse():
@@ -48,6 +50,10 @@ def parse():
                     help="also time the secondary schedules: steps with a 1 GiB cache flush "
                          "before each, per-layer attention launches, and the unfused "
                          "score / top-k / gather / compact-attention sequence")
+    ap.add_argument("--frontend", action="store_true",
+                    help="time only the retrieval head's front end for the new token "
+                         "(embedding row, Q/K projection, YaRN rotary embedding, K_r append): "
+                         "--steps calls, replayed from HIP graphs of 20 calls")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run three 1 GiB device-to-device copies (known HBM bytes) so "
                          "that PMC byte counters can be scaled")
@@ -61,12 +67,13 @@ def attn_bytes(w, counts):
     return w.n_layers * (kb * w.H_kv * w.d * 2 * 2 + w.B * w.H_q * w.d * 2 + w.B * w.H_q * w.d * 4)
 
 
-def attn_source_digest():
-    """sha256 of the attention kernel's sources with comments and blank
-    lines removed: it changes when the code does, not when a comment does."""
+def attn_source_digest(sources=ATTN_SOURCES):
+    """sha256 of a kernel's sources (default: the attention's) with comments
+    and blank lines removed: it changes when the code does, not when a
+    comment does."""
     import re
     h = hashlib.sha256()
-    for name in ATTN_SOURCES:
+    for name in sources:
         txt = open(os.path.join(CSRC, name)).read()
         txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
         txt = re.sub(r"//[^\n]*", "", txt)
@@ -75,14 +82,14 @@ def attn_source_digest():
     return h.hexdigest()
 
 
-def stored_traffic(workload):
-    """Per-launch HBM bytes of the attention kernels on `workload`, measured
-    with rocprofv3 PMC counters; valid only for the attention code they were
-    taken on."""
+def stored_traffic(workload, path=TRAFFIC_FILE, sources=ATTN_SOURCES):
+    """Per-launch HBM bytes of a kernel (default: the attention) on
+    `workload`, measured with rocprofv3 PMC counters; valid only for the code
+    they were taken on."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             t = json.load(f)
-        if t.get("attn_code_sha256") != attn_source_digest():
+        if t.get("attn_code_sha256", t.get("code_sha256")) != attn_source_digest(sources):
             return None
         return t.get("workloads", {}).get(workload, {}).get("bytes_per_launch")
     except (OSError, ValueError):
@@ -175,11 +182,14 @@ def main():
     name = args.workload or BENCH_WORKLOAD
     w = WORKLOADS[name]
     t_gen = time.perf_counter()
-    x = generate(w, seed=args.seed, device=dev)
+    x = generate(w, seed=args.seed, device=dev, with_kv=not args.frontend)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
     print(f"[bench] workload {name} generated in {t_gen:.1f}s", file=sys.stderr, flush=True)
 
+    if args.frontend:
+        print(json.dumps(run_frontend(args, spec, w, x)), flush=True)
+        return
     if w.steps > 1 and args.head_level:
         print("bench.py: elastic loading keeps one token set per sequence; --head-level does "
               "not apply to this workload", file=sys.stderr)
@@ -297,12 +307,7 @@ def main():
     if args.variants:
         line["variants"] = run_variants(args, spec, w, x, call, outputs, ws, step_bytes, n_sets)
     if args.copy_calibration:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        copy_calibration(dev)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(w, x, res)
@@ -420,6 +425,94 @@ def run_elastic(args, spec, w, x, e, algorithmic_bytes):
     }
 
 
+def copy_calibration(dev):
+    """Three 1 GiB device-to-device copies (known HBM bytes) whose PMC byte
+    counts scale the counters of the kernels."""
+    import torch
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def run_frontend(args, spec, w, x):
+    """The retrieval head's front end alone: --steps calls on the workload's
+    synthetic weights (the whole embedding table), timed over graph replays
+    with HIP events on the launch stream."""
+    import torch
+    from workloads import frontend_bytes, frontend_inputs
+
+    dev = x["K_r"].device
+    fe = frontend_inputs(w, x["seq_lens"], seed=args.seed, device=dev)
+    q_r = torch.empty_like(x["q_r"])
+    dims = _dims_of_retrieval(spec, w, x)
+    ws = torch.zeros(spec.workspace_size(dims, spec.OP_FRONTEND), dtype=torch.uint8, device=dev)
+
+    def front():
+        spec.retrieval_qk(fe["tokens"], fe["pos"], fe["emb"], fe["w_q"], fe["w_k"], x["K_r"],
+                          rope_base=w.rope_base, yarn_scale=w.yarn_scale,
+                          yarn_orig_ctx=w.orig_ctx, q_r=q_r, ws=ws)
+
+    reps = 20
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(max(args.warmup, 1)):
+            front()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(reps):
+            front()
+    graph.replay()
+    torch.cuda.synchronize()
+    n_rep = max(1, (args.steps + reps - 1) // reps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(n_rep):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    calls = n_rep * reps
+    us = e0.elapsed_time(e1) * 1e3 / calls
+    fb = frontend_bytes(w)
+    achieved = fb / (us * 1e-6) / 1e9
+    kernels = ("qk_gemv_kernel" if w.B <= 16 else "qk_partial_kernel + qk_finish_kernel")
+    line = {
+        "metric": "retrieval head front-end calls/s (embedding, Q/K projection, YaRN RoPE, "
+                  "K_r append)",
+        "value": round(calls / wall, 1),
+        "unit": "calls/s",
+        "n_gpus": 1, "steps": calls, "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / calls, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H_r": w.H_r, "d_r": w.d_r,
+                   "hidden": w.hidden, "vocab": w.vocab, "rope_base": w.rope_base,
+                   "yarn_scale": w.yarn_scale, "orig_ctx": w.orig_ctx},
+        "roofline": {
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
+            "traffic": stored_traffic(w.name, FRONT_TRAFFIC_FILE, FRONT_SOURCES),
+            "kernel": kernels, "bytes_per_launch": fb, "avg_launch_us": round(us, 3),
+        },
+    }
+    del graph, fe
+    if args.copy_calibration:
+        copy_calibration(dev)
+    return line
+
+
+def _dims_of_retrieval(spec, w, x):
+    return spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=1, H_r=w.H_r, d_r=w.d_r,
+                          n_layers=1, H_q=1, H_kv=1, d=128, kr_stride_b=x["K_r"].stride(0))
+
+
 def run_variants(args, spec, w, x, call, outputs, ws, step_bytes, n_sets=1):
     """Secondary schedules of the same step (µs per step, HIP events on the
     launch stream).
@@ -431,7 +524,10 @@ def run_variants(args, spec, w, x, call, outputs, ws, step_bytes, n_sets=1):
     unfused: score, top-k, materialised gather of the selected rows of every
     layer, attention over the compact rows.
     fused_step_graph: the fused step, replayed from a HIP graph.
-    The last three are captured in HIP graphs and replayed.
+    retrieval_frontend: the retrieval head's front end for the new token
+    (per call, 20 calls per graph); frontend_then_step_graph: the front end
+    followed by the step on the q_r it produced.
+    These are captured in HIP graphs and replayed.
     """
     import torch
 
@@ -528,6 +624,45 @@ def run_variants(args, spec, w, x, call, outputs, ws, step_bytes, n_sets=1):
     us = ev_loop(lambda: spec.step(**call, outputs=outputs, ws=ws), n)
     res["fused_step_graph"] = {"us_per_step": round(us, 1), "steps_per_s": round(1e6 / us, 1)}
     del ks, vs
+
+    # The retrieval head's front end for the new token (embedding row, Q/K
+    # projection, YaRN rotary embedding, append to K_r), alone and ahead of
+    # the step.  It writes the new key over each sequence's last cached row.
+    from workloads import frontend_bytes, frontend_inputs
+    fe = frontend_inputs(w, x["seq_lens"], seed=0, device=dev)
+    q_r_new = torch.empty_like(x["q_r"])
+    ws_f = torch.zeros(spec.workspace_size(dims_s, spec.OP_FRONTEND), dtype=torch.uint8,
+                       device=dev)
+
+    def front():
+        spec.retrieval_qk(fe["tokens"], fe["pos"], fe["emb"], fe["w_q"], fe["w_k"], x["K_r"],
+                          rope_base=w.rope_base, yarn_scale=w.yarn_scale,
+                          yarn_orig_ctx=w.orig_ctx, q_r=q_r_new, ws=ws_f)
+
+    reps = 20
+
+    def front_rep():
+        for _ in range(reps):
+            front()
+
+    us = ev_loop(front_rep, n) / reps
+    fb = frontend_bytes(w)
+    res["retrieval_frontend"] = {
+        "us_per_call": round(us, 2), "algorithmic_bytes": fb,
+        "GBps": round(fb / (us * 1e-6) / 1e9, 1),
+        "frac_of_peak": round(fb / (us * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+        "vocab": w.vocab, "hidden": w.hidden, "yarn_scale": w.yarn_scale}
+    call_fe = dict(call)
+    call_fe["q_r"] = q_r_new
+
+    def front_step():
+        front()
+        spec.step(**call_fe, outputs=outputs, ws=ws)
+
+    us = ev_loop(front_step, n)
+    res["frontend_then_step_graph"] = {"us_per_step": round(us, 1),
+                                       "steps_per_s": round(1e6 / us, 1)}
+    del fe
     torch.cuda.empty_cache()
     return res
 

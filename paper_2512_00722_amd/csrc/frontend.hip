@@ -13,7 +13,22 @@
 // The projections are one skinny GEMM, [B x hidden] . [hidden x 2*H_r*d_r],
 // whose weights (2 * H_r * d_r * hidden bf16, 8-32 MiB) are read once per call
 // for the whole batch: the work is bound by HBM bandwidth on them, and one
-// CU streams only about 30 GB/s, so every CU must take part.  Two kernels:
+// CU streams only about 30 GB/s, so every CU must take part.
+//
+// Up to 16 sequences: one kernel, qk_gemv_kernel.  A workgroup owns two
+// rotary pairs (four features) of one head of Q or K over the whole hidden
+// dimension (2 * H_r * d_r / 4 workgroups: 256 for 8 heads of 64).  Its
+// waves take 512-element slabs of the hidden dimension in turn; per slab a
+// load instruction reads 1 KiB of one weight or embedding row, and each lane
+// forms fp32 dot products over its 8 elements (vector ALU: with at most 16
+// tokens the matrix cores would idle on padding; v_dot2_f32_bf16 takes the
+// bf16 pairs as loaded).  Lane sums are reduced
+// within 16-lane rows by DPP, then over rows and waves in LDS; the pairs are
+// rotated in the workgroup.  Every weight byte is read once; the embedding
+// rows come from L2.
+//
+// More sequences: two kernels, since a narrow tile per workgroup would make
+// every workgroup re-read all embedding rows.
 //
 //  1. qk_partial_kernel (matrix cores, v_mfma_f32_16x16x32_bf16, tokens on
 //     the M side): a workgroup owns 16 output features of Q or K -- the
@@ -26,10 +41,14 @@
 //     load instruction; all loads of a chunk of steps are issued before the
 //     first MFMA.  The waves' tiles are summed in LDS and the fp32 partial
 //     tile is written to the workspace, [KS][B][2*H_r*d_r].
+//     One workgroup also computes the YaRN frequencies and m (fp64) into the
+//     workspace while its loads are in flight.
 //  2. qk_finish_kernel: one thread per (sequence, Q/K, head, pair) sums the
 //     KS partials of both pair members in slice order (deterministic), forms
-//     the angle in fp64 (positions reach 2^17 and beyond), rotates, scales,
-//     rounds to bf16 and stores q_r or the new K_r row.
+//     the angle pos * theta'_i in fp64 (positions reach 2^17 and beyond) and
+//     reduces it modulo 2 pi in fp64 with a two-term 2 pi, takes sin and cos
+//     of the reduced angle, rotates, scales, rounds to bf16 and stores q_r or
+//     the new K_r row.
 #include <math.h>
 
 #include "device_common.h"
@@ -52,7 +71,8 @@ struct FrontArgs {
   const uint16_t* w_k;
   uint16_t* q_r;
   uint16_t* k_r;
-  float* part;  // [KS][B][2 * H_r * d_r]
+  float* part;     // [KS][B][2 * H_r * d_r]
+  double* theta;   // [d_r / 2] YaRN frequencies, then the magnitude factor m
   int64_t kr_stride_b;
   int B, vocab, hidden, H_r, d_r, L_cap;
   int ks, steps_per_split;
@@ -79,6 +99,30 @@ __device__ double yarn_theta(const FrontArgs& a, int i) {
   double gamma = (turns - (double)a.alpha) / ((double)a.beta - (double)a.alpha);
   gamma = gamma < 0.0 ? 0.0 : (gamma > 1.0 ? 1.0 : gamma);
   return (1.0 - gamma) * theta / (double)a.scale + gamma * theta;
+}
+
+// Rotate one pair, scale, round and store (q_r, or the new K_r row).
+__device__ __forceinline__ void store_pair(const FrontArgs& a, int mat, int b, int h, int i,
+                                           float x, float y, double theta, float m) {
+  const int pos = a.pos[b];
+  // angle in fp64, reduced modulo 2 pi (hi + lo parts of 2 pi; |k| < 2^29
+  // leaves the reduced angle accurate to about 1e-15)
+  const double ang = (double)pos * theta;
+  const double k = rint(ang * 0.15915494309189535);
+  double red = fma(-k, 6.283185307179586, ang);
+  red = fma(-k, 2.4492935982947064e-16, red);
+  float sn, cs;
+  sincosf((float)red, &sn, &cs);
+  const float c = m * cs, s = m * sn;
+  uint16_t* dst;
+  if (mat == 0) {
+    dst = a.q_r + ((size_t)b * a.H_r + h) * a.d_r;
+  } else {
+    if (pos < 0 || pos >= a.L_cap) return;  // nothing appended outside the cache
+    dst = a.k_r + (size_t)b * a.kr_stride_b + ((size_t)pos * a.H_r + h) * a.d_r;
+  }
+  dst[i] = to_bf16(x * c - y * s);
+  dst[i + a.d_r / 2] = to_bf16(x * s + y * c);
 }
 
 // T: 16-token row tiles per workgroup.  CH: wave steps whose loads are
@@ -138,6 +182,10 @@ __global__ __launch_bounds__(kFeThreads) void qk_partial_kernel(FrontArgs a) {
         for (int j = 0; j < 4; ++j) e[c][t][j] = ldg16(erow[t] + off + 32 * j);
     }
     __builtin_amdgcn_sched_barrier(0);  // no MFMA (and its wait) moves above a load
+    if (blockIdx.x == 0 && blockIdx.y == 0 && s0 == s_begin + wave && wave == 0) {
+      if (lane < a.d_r / 2) a.theta[lane] = yarn_theta(a, lane);
+      if (lane == 0) a.theta[a.d_r / 2] = a.scale > 1.0f ? 0.1 * log((double)a.scale) + 1.0 : 1.0;
+    }
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
       if (s0 + c * kFeWaves < s_end) {  // wave-uniform
@@ -189,20 +237,117 @@ __global__ __launch_bounds__(kFinishThreads) void qk_finish_kernel(FrontArgs a) 
     x += p[0];
     y += p[half];
   }
-  const int pos = a.pos[b];
-  const double mscale = a.scale > 1.0f ? 0.1 * log((double)a.scale) + 1.0 : 1.0;
-  double sn, cs;
-  sincos((double)pos * yarn_theta(a, i), &sn, &cs);
-  const float c = (float)(mscale * cs), s = (float)(mscale * sn);
-  uint16_t* dst;
-  if (mat == 0) {
-    dst = a.q_r + ((size_t)b * a.H_r + h) * a.d_r;
-  } else {
-    if (pos < 0 || pos >= a.L_cap) return;  // nothing appended outside the cache
-    dst = a.k_r + (size_t)b * a.kr_stride_b + ((size_t)pos * a.H_r + h) * a.d_r;
+  store_pair(a, mat, b, h, i, x, y, a.theta[i], (float)a.theta[half]);
+}
+
+constexpr int kGvSlab = 512;  // hidden elements per wave slab: 64 lanes x 8
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// acc + lo(x) * lo(y) + hi(x) * hi(y) for two packed bf16 pairs.
+__device__ __forceinline__ float dot2_bf16(uint32_t x, uint32_t y, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, x),
+                                         __builtin_bit_cast(bf16x2, y), acc, false);
+}
+
+// TB: token rows held per lane (B <= TB; rows past B repeat the last one and
+// are never stored).  CH: slabs whose loads are issued together.
+template <int TB, int CH>
+__global__ __launch_bounds__(kFeThreads) void qk_gemv_kernel(FrontArgs a) {
+  __shared__ float red[kFeWaves * 4 * 4 * TB];  // [wave][row][feature][token]
+  __shared__ float tot[4 * TB];
+  __shared__ double theta[2];
+  __shared__ float mscale;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int half = a.d_r / 2;
+  const int tiles_per_head = a.d_r / 4;
+  const int per_mat = a.H_r * tiles_per_head;
+  const int mat = blockIdx.x / per_mat;  // 0: Q, 1: K
+  const int rem = blockIdx.x - mat * per_mat;
+  const int h = rem / tiles_per_head;
+  const int i0 = 2 * (rem - h * tiles_per_head);
+  // features i0, i0 + 1 and their rotary partners i0 + d_r/2, i0 + 1 + d_r/2
+  const uint16_t* wm = (mat ? a.w_k : a.w_q) + (size_t)(h * a.d_r + i0) * a.hidden;
+  const uint16_t* wr[4] = {wm, wm + a.hidden, wm + (size_t)half * a.hidden,
+                           wm + (size_t)(half + 1) * a.hidden};
+  const uint16_t* er[TB];
+#pragma unroll
+  for (int t = 0; t < TB; ++t) {
+    const int tok = clampi(a.tokens[min(t, a.B - 1)], 0, a.vocab - 1);
+    er[t] = a.emb + (size_t)tok * a.hidden;
   }
-  dst[i] = to_bf16(x * c - y * s);
-  dst[i + half] = to_bf16(x * s + y * c);
+
+  float acc[4][TB];
+#pragma unroll
+  for (int f = 0; f < 4; ++f)
+#pragma unroll
+    for (int t = 0; t < TB; ++t) acc[f][t] = 0.f;
+
+  const int n_slabs = (a.hidden + kGvSlab - 1) / kGvSlab;
+  for (int s0 = wave; s0 < n_slabs; s0 += kFeWaves * CH) {
+    // Loads of the chunk, all unconditional: past the end of the row a lane
+    // re-reads the row's last 8 elements and its products are dropped.
+    uint4 w[CH][4];
+    uint4 e[CH][TB];
+    int kk[CH];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      kk[c] = min(s0 + c * kFeWaves, n_slabs - 1) * kGvSlab + 8 * lane;
+      const int kc = min(kk[c], a.hidden - 8);
+#pragma unroll
+      for (int f = 0; f < 4; ++f) w[c][f] = ldg16(wr[f] + kc);
+#pragma unroll
+      for (int t = 0; t < TB; ++t) e[c][t] = ldg16(er[t] + kc);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // every load of the chunk is in flight first
+    if (s0 == wave && wave == 0 && lane < 2) {
+      theta[lane] = yarn_theta(a, i0 + lane);
+      if (lane == 0) mscale = a.scale > 1.0f ? (float)(0.1 * log((double)a.scale) + 1.0) : 1.0f;
+    }
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      if (s0 + c * kFeWaves < n_slabs && kk[c] < a.hidden) {
+        // v_dot2_f32_bf16: two bf16 products added to the fp32 sum
+#pragma unroll
+        for (int t = 0; t < TB; ++t)
+#pragma unroll
+          for (int f = 0; f < 4; ++f) {
+            acc[f][t] = dot2_bf16(w[c][f].x, e[c][t].x, acc[f][t]);
+            acc[f][t] = dot2_bf16(w[c][f].y, e[c][t].y, acc[f][t]);
+            acc[f][t] = dot2_bf16(w[c][f].z, e[c][t].z, acc[f][t]);
+            acc[f][t] = dot2_bf16(w[c][f].w, e[c][t].w, acc[f][t]);
+          }
+      }
+    }
+  }
+
+  // Reduce: 16-lane rows by DPP (all chains first, so that they interleave),
+  // then the 4 rows x 4 waves in LDS.
+#pragma unroll
+  for (int f = 0; f < 4; ++f)
+#pragma unroll
+    for (int t = 0; t < TB; ++t) acc[f][t] = row_sum<16>(acc[f][t]);
+  if ((lane & 15) == 0) {
+#pragma unroll
+    for (int f = 0; f < 4; ++f)
+#pragma unroll
+      for (int t = 0; t < TB; ++t) red[((wave * 4 + (lane >> 4)) * 4 + f) * TB + t] = acc[f][t];
+  }
+  __syncthreads();
+  if (threadIdx.x < 4 * TB) {
+    float s = 0.f;
+#pragma unroll
+    for (int r = 0; r < kFeWaves * 4; ++r) s += red[r * 4 * TB + threadIdx.x];
+    tot[threadIdx.x] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x < 2 * TB) {
+    const int p = threadIdx.x / TB, t = threadIdx.x - p * TB;
+    if (t < a.B)
+      store_pair(a, mat, t, h, i0 + p, tot[p * TB + t], tot[(p + 2) * TB + t], theta[p], mscale);
+  }
 }
 
 struct FrontPlan {
@@ -220,6 +365,23 @@ FrontPlan front_plan(const Dims& d, const FrontDims& f) {
   p.steps_per_split = (n_steps + ks - 1) / ks;
   p.ks = (n_steps + p.steps_per_split - 1) / p.steps_per_split;
   return p;
+}
+
+template <int TB>
+void launch_gemv(const FrontArgs& a, hipStream_t s) {
+  const int grid = 2 * a.H_r * (a.d_r / 4);
+  const int n_slabs = (a.hidden + kGvSlab - 1) / kGvSlab;
+  const int per_wave = (n_slabs + kFeWaves - 1) / kFeWaves;
+  if constexpr (TB <= 4) {
+    if (per_wave >= 4) {
+      hipLaunchKernelGGL((qk_gemv_kernel<TB, 4>), dim3(grid), dim3(kFeThreads), 0, s, a);
+      return;
+    }
+  }
+  if (per_wave >= 2)
+    hipLaunchKernelGGL((qk_gemv_kernel<TB, 2>), dim3(grid), dim3(kFeThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((qk_gemv_kernel<TB, 1>), dim3(grid), dim3(kFeThreads), 0, s, a);
 }
 
 template <int T>
@@ -240,8 +402,14 @@ void launch_partial(const FrontArgs& a, dim3 grid, hipStream_t s) {
 
 }  // namespace
 
+// Workspace: the frequency table and m, then the partial sums.
+static size_t front_table_bytes(const Dims& d) {
+  return align_up(sizeof(double) * (size_t)(d.d_r / 2 + 1));
+}
+
 size_t front_ws_bytes(const Dims& d) {
-  return align_up(sizeof(float) * (size_t)kFrontMaxSplit * d.B * 2 * d.H_r * d.d_r);
+  return front_table_bytes(d) +
+         align_up(sizeof(float) * (size_t)kFrontMaxSplit * d.B * 2 * d.H_r * d.d_r);
 }
 
 hipError_t launch_retrieval_qk(const Dims& d, const FrontDims& f, const int32_t* tokens,
@@ -257,7 +425,8 @@ hipError_t launch_retrieval_qk(const Dims& d, const FrontDims& f, const int32_t*
   a.w_k = w_k;
   a.q_r = q_r;
   a.k_r = k_r;
-  a.part = static_cast<float*>(ws);
+  a.theta = static_cast<double*>(ws);
+  a.part = reinterpret_cast<float*>(static_cast<char*>(ws) + front_table_bytes(d));
   a.kr_stride_b = d.kr_stride_b;
   a.B = d.B;
   a.vocab = f.vocab;
@@ -272,10 +441,16 @@ hipError_t launch_retrieval_qk(const Dims& d, const FrontDims& f, const int32_t*
   a.alpha = f.alpha;
   a.beta = f.beta;
   a.orig_ctx = f.orig_ctx;
+  if (d.B <= 16) {  // one kernel, whole hidden dimension per workgroup
+    if (d.B == 1) launch_gemv<1>(a, s);
+    else if (d.B == 2) launch_gemv<2>(a, s);
+    else if (d.B <= 4) launch_gemv<4>(a, s);
+    else if (d.B <= 8) launch_gemv<8>(a, s);
+    else launch_gemv<16>(a, s);
+    return hipGetLastError();
+  }
   const int n_tiles = 2 * d.H_r * (d.d_r / 16);
-  if (d.B <= 16) {
-    launch_partial<1>(a, dim3(n_tiles * p.ks, 1), s);
-  } else if (d.B <= 32) {
+  if (d.B <= 32) {
     launch_partial<2>(a, dim3(n_tiles * p.ks, 1), s);
   } else {
     launch_partial<4>(a, dim3(n_tiles * p.ks, (d.B + 63) / 64), s);
