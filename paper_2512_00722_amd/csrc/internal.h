@@ -85,8 +85,8 @@ struct FrontDims {
   int orig_ctx;
 };
 // The projection splits the hidden dimension over at most this many
-// workgroups per output tile; the workspace holds one fp32 partial result
-// [split][B][2 * H_r * d_r] per split.
+// workgroups per output tile; the workspace holds the rotary frequency table
+// and one fp32 partial result [split][B][2 * H_r * d_r] per split.
 constexpr int kFrontMaxSplit = 16;
 size_t front_ws_bytes(const Dims& d);
 
