@@ -20,7 +20,12 @@ What it computes (SpeContext, arXiv 2512.00722):
   group share one KV head;
 * elastic loading (Sec. 5.4): with S_last the set held on the device and
   S_now the new selection, only S_now - S_last is loaded, into the places freed
-  by S_last - S_now (equal in size because the budget is fixed).
+  by S_last - S_now (equal in size because the budget is fixed);
+* the retrieval head's front end (Sec. 4.3): the new token's embedding row,
+  the Q/K projection and the rotary embedding with YaRN scaling (Peng et al.)
+  that extends the distilled model's 2K context;
+* MLA (Sec. 4.3 "Support for MLA"): the cache holds a latent per token and
+  only the selected latents are raised to per-head keys and values.
 
 Everything is computed in float64 from the bf16-rounded inputs (bf16 embeds
 exactly in float64).  Readings of points the paper leaves open:
@@ -63,6 +68,7 @@ __all__ = [
     "yarn_frequencies",
     "rope_rotate",
     "retrieval_qk",
+    "mla_sparse_attention",
 ]
 
 
@@ -247,6 +253,52 @@ def dense_gqa_attention(q, K, V, L: int, scale: float | None = None):
 # Details": the head keeps the draft model's embedding and Q/K projection
 # weights and extends its context with YaRN)
 # ---------------------------------------------------------------------------
+
+def mla_sparse_attention(q_nope: np.ndarray, q_rope: np.ndarray, c: np.ndarray,
+                         k_rope: np.ndarray, w_uk: np.ndarray, w_uv: np.ndarray,
+                         idx: np.ndarray, scale: float | None = None):
+    """Decode attention of one sequence and one layer of an MLA model over
+    the selected tokens (Sec. 4.3, "Support for MLA").
+
+    The cache holds, per token, the latent c_t [d_c] and the rotary key
+    k_rope_t [d_rope] that all heads share.  Only the selected latents are
+    raised to per-head keys and values:
+        key of head h at token j   = [W_UK[h] c_j ; k_rope_j]     (d_nope + d_rope)
+        value of head h at token j = W_UV[h] c_j                  (d_v)
+    and head h attends over them as in Eq. 1, its query being
+    [q_nope[h] ; q_rope[h]] and the scale 1/sqrt(d_nope + d_rope).
+
+    q_nope [H, d_nope], q_rope [H, d_rope]; c [L_cap, d_c]; k_rope
+    [L_cap, d_rope]; w_uk [H, d_nope, d_c], w_uv [H, d_v, d_c] (each maps a
+    latent to one head's part, as a linear layer stores [out, in]).
+    Returns (out [H, d_v], lse [H]); with no selected token out is 0 and lse
+    is -inf.
+    """
+    q_nope = np.asarray(q_nope, dtype=np.float64)
+    q_rope = np.asarray(q_rope, dtype=np.float64)
+    H, d_nope = q_nope.shape
+    d_rope = q_rope.shape[1]
+    d_v = w_uv.shape[1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d_nope + d_rope)
+    idx = np.asarray(idx, dtype=np.int64)
+    out = np.zeros((H, d_v), dtype=np.float64)
+    lse = np.full((H,), -np.inf, dtype=np.float64)
+    if idx.size == 0:
+        return out, lse
+    cs = np.asarray(c[idx], dtype=np.float64)          # the selected latents only
+    krs = np.asarray(k_rope[idx], dtype=np.float64)
+    for h in range(H):
+        k_nope = cs @ np.asarray(w_uk[h], dtype=np.float64).T   # [k, d_nope]
+        v = cs @ np.asarray(w_uv[h], dtype=np.float64).T        # [k, d_v]
+        s = (k_nope @ q_nope[h] + krs @ q_rope[h]) * scale
+        m = s.max()
+        w = np.exp(s - m)
+        z = w.sum()
+        out[h] = (w / z) @ v
+        lse[h] = math.log(z) + m
+    return out, lse
+
 
 def yarn_frequencies(d_r: int, base: float, scale: float, orig_ctx: int,
                      alpha: float = 1.0, beta: float = 32.0):

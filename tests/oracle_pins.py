@@ -423,6 +423,117 @@ def pin_elastic_identities(o):
         assert loads3 == [] and new3.tolist() == new.tolist()
 
 
+# --------------------------------------------------------------- MLA (Sec. 4.3 "Support for MLA")
+
+def _mla_case(rng, H=3, d_c=12, d_nope=5, d_rope=3, d_v=7, L=20):
+    """Random MLA inputs with every dimension different, so that a
+    transposed or swapped weight fails on shapes."""
+    return dict(q_nope=rng.standard_normal((H, d_nope)), q_rope=rng.standard_normal((H, d_rope)),
+                c=rng.standard_normal((L, d_c)), k_rope=rng.standard_normal((L, d_rope)),
+                w_uk=rng.standard_normal((H, d_nope, d_c)) / math.sqrt(d_c),
+                w_uv=rng.standard_normal((H, d_v, d_c)) / math.sqrt(d_c))
+
+
+def pin_mla_worked_example(o):
+    """One head, d_c = 2, d_nope = d_rope = d_v = 1, three cached tokens of
+    which 0 and 2 are selected, by hand (W_UK = (1, 2), W_UV = (3, -1),
+    query (1, 1), scale 1/sqrt(2)):
+      token 0: c = (1, 0), k_rope = 0: key (1, 0), value 3, logit 1/sqrt(2);
+      token 2: c = (1, 1), k_rope = 1: key (3, 1), value 2, logit 4/sqrt(2);
+    the unselected token 1 (c = (0, 1), k_rope = 5) would change both."""
+    c = np.array([[1.0, 0.0], [0.0, 1.0], [1.0, 1.0]])
+    kr = np.array([[0.0], [5.0], [1.0]])
+    out, lse = o.mla_sparse_attention(np.array([[1.0]]), np.array([[1.0]]), c, kr,
+                                      np.array([[[1.0, 2.0]]]), np.array([[[3.0, -1.0]]]),
+                                      np.array([0, 2]))
+    e0, e2 = math.exp(1.0 / math.sqrt(2.0)), math.exp(4.0 / math.sqrt(2.0))
+    assert out.shape == (1, 1) and lse.shape == (1,)
+    assert abs(out[0, 0] - (3.0 * e0 + 2.0 * e2) / (e0 + e2)) < 1e-13
+    assert abs(lse[0] - math.log(e0 + e2)) < 1e-13
+
+
+def pin_mla_identity_projection_is_mqa(o):
+    """No rotary part and identity up-projections (d_c = d_nope = d_v): keys
+    and values are the latents themselves, i.e. multi-query attention over c."""
+    rng = np.random.default_rng(31)
+    H, d, L = 4, 16, 40
+    idx = np.sort(rng.choice(L, 11, replace=False))
+    q, c = rng.standard_normal((H, d)), rng.standard_normal((L, d))
+    eye = np.broadcast_to(np.eye(d), (H, d, d))
+    out, lse = o.mla_sparse_attention(q, np.zeros((H, 0)), c, np.zeros((L, 0)), eye, eye, idx)
+    want, wl = o.sparse_gqa_attention(q, c[:, None, :], c[:, None, :], idx)
+    np.testing.assert_allclose(out, want, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lse, wl, atol=1e-12, rtol=0)
+
+
+def pin_mla_dense_matches_sdpa(o):
+    """Every token selected: equal to torch's scaled_dot_product_attention
+    (fp64) on explicitly up-projected keys [W_UK c ; k_rope] and values W_UV c."""
+    rng = np.random.default_rng(32)
+    x = _mla_case(rng)
+    L = x["c"].shape[0]
+    out, lse = o.mla_sparse_attention(**x, idx=np.arange(L))
+    t = {k: torch.from_numpy(np.ascontiguousarray(v)) for k, v in x.items()}
+    K = torch.cat([torch.einsum("lc,hnc->hln", t["c"], t["w_uk"]),
+                   t["k_rope"].unsqueeze(0).expand(3, -1, -1)], dim=-1)      # [H, L, 8]
+    V = torch.einsum("lc,hvc->hlv", t["c"], t["w_uv"])                     # [H, L, 7]
+    Q = torch.cat([t["q_nope"], t["q_rope"]], dim=-1).unsqueeze(1)         # [H, 1, 8]
+    want = torch.nn.functional.scaled_dot_product_attention(Q, K, V, scale=1.0 / math.sqrt(8))
+    np.testing.assert_allclose(out, want[:, 0].numpy(), atol=1e-12, rtol=0)
+    s = (Q @ K.transpose(1, 2))[:, 0] / math.sqrt(8)
+    np.testing.assert_allclose(lse, torch.logsumexp(s, dim=-1).numpy(), atol=1e-12, rtol=0)
+
+
+def pin_mla_single_token(o):
+    """One selected token: the output is its value W_UV[h] c_j and the lse
+    its logit."""
+    rng = np.random.default_rng(33)
+    x = _mla_case(rng)
+    j = 13
+    out, lse = o.mla_sparse_attention(**x, idx=np.array([j]))
+    for h in range(3):
+        np.testing.assert_allclose(out[h], x["w_uv"][h] @ x["c"][j], atol=1e-12, rtol=0)
+        logit = (x["q_nope"][h] @ (x["w_uk"][h] @ x["c"][j]) + x["q_rope"][h] @ x["k_rope"][j])
+        assert abs(lse[h] - logit / math.sqrt(8)) < 1e-12
+
+
+def pin_mla_absorbed_form(o):
+    """Absorbing W_UK into the query and applying W_UV after the weighted sum
+    of the latents gives the same result:
+      q~_h = W_UK[h]^T q_nope[h],  s_hj = (q~_h . c_j + q_rope[h] . k_rope_j) / sqrt(d_nope + d_rope),
+      o_h = W_UV[h] sum_j softmax_j(s_h) c_j."""
+    rng = np.random.default_rng(34)
+    x = _mla_case(rng, L=30)
+    idx = np.array([2, 3, 7, 19, 28])
+    out, lse = o.mla_sparse_attention(**x, idx=idx)
+    for h in range(3):
+        qt = x["w_uk"][h].T @ x["q_nope"][h]                                  # [d_c]
+        s = (x["c"][idx] @ qt + x["k_rope"][idx] @ x["q_rope"][h]) / math.sqrt(8)
+        p = np.exp(s - s.max())
+        lat = (p / p.sum()) @ x["c"][idx]                                    # [d_c]
+        np.testing.assert_allclose(out[h], x["w_uv"][h] @ lat, atol=1e-12, rtol=0)
+        assert abs(lse[h] - (s.max() + math.log(p.sum()))) < 1e-12
+
+
+def pin_mla_unselected_rows_ignored(o):
+    """Latents and rotary keys of unselected tokens do not matter; the empty
+    selection gives 0 and -inf."""
+    rng = np.random.default_rng(35)
+    x = _mla_case(rng)
+    idx = np.array([1, 4, 9, 15])
+    out, lse = o.mla_sparse_attention(**x, idx=idx)
+    y = dict(x)
+    rest = np.setdiff1d(np.arange(20), idx)
+    y["c"] = x["c"].copy()
+    y["k_rope"] = x["k_rope"].copy()
+    y["c"][rest] = 100.0
+    y["k_rope"][rest] = -50.0
+    out2, lse2 = o.mla_sparse_attention(**y, idx=idx)
+    assert np.array_equal(out, out2) and np.array_equal(lse, lse2)
+    out3, lse3 = o.mla_sparse_attention(**x, idx=np.array([], dtype=np.int64))
+    assert np.all(out3 == 0) and np.all(np.isneginf(lse3)) and out3.shape == (3, 7)
+
+
 # --------------------------------------------------------------- helpers
 
 def pin_bf16_decode(o):

@@ -35,6 +35,17 @@ MUTANTS = {
     "rope_exponent_over_d": ("theta = base ** (-2.0 * i / d_r)", "theta = base ** (-1.0 * i / d_r)"),
     "rope_rotation_sign": ("return m * np.concatenate([x * c - y * s_, x * s_ + y * c], axis=-1)", "return m * np.concatenate([x * c + y * s_, -x * s_ + y * c], axis=-1)"),
     "qk_swapped": ("k = (np.asarray(w_k, dtype=np.float64) @ x).reshape(H_r, -1)", "k = (np.asarray(w_q, dtype=np.float64) @ x).reshape(H_r, -1)"),
+    "mla_uk_not_transposed": ("k_nope = cs @ np.asarray(w_uk[h], dtype=np.float64).T",
+                              "k_nope = cs @ np.asarray(w_uk[h], dtype=np.float64)"),
+    "mla_no_rope_term": ("s = (k_nope @ q_nope[h] + krs @ q_rope[h]) * scale",
+                         "s = (k_nope @ q_nope[h]) * scale"),
+    "mla_values_are_latents": ("v = cs @ np.asarray(w_uv[h], dtype=np.float64).T", "v = cs"),
+    "mla_uv_head0": ("v = cs @ np.asarray(w_uv[h], dtype=np.float64).T",
+                     "v = cs @ np.asarray(w_uv[0], dtype=np.float64).T"),
+    "mla_scale_over_latent": ("scale = 1.0 / math.sqrt(d_nope + d_rope)",
+                              "scale = 1.0 / math.sqrt(c.shape[1])"),
+    "mla_all_tokens": ("cs = np.asarray(c[idx], dtype=np.float64)",
+                       "cs = np.asarray(c[:len(idx)], dtype=np.float64)"),
     "sets_wrong_kv_head": ("o, l_ = sparse_gqa_attention(q[g * G:(g + 1) * G], K[:, g:g + 1], V[:, g:g + 1],",
                            "o, l_ = sparse_gqa_attention(q[g * G:(g + 1) * G], K[:, 0:1], V[:, g:g + 1],"),
 }
