@@ -261,6 +261,64 @@ SPEC_API spec_status spec_retrieval_qk(const spec_dims* dm, const spec_frontend*
                               const uint16_t* w_k, uint16_t* q_r, uint16_t* k_r,
                               void* ws, size_t ws_bytes, spec_stream stream);
 
+/* MLA problem dimensions (host struct).  The MLA models this serves
+ * (DeepSeek-V3/R1 and Kimi-K2 style) have d_c = 512, d_rope = 64,
+ * d_nope = d_v = 128; those values are the supported ones.                  */
+typedef struct spec_mla_dims {
+  int32_t B;         /* sequences in the batch                                */
+  int32_t L_cap;     /* token capacity of every cache row                     */
+  int32_t k_max;     /* row length of idx, <= L_cap, <= 32768                 */
+  int32_t n_layers;  /* layers attended with one selection                    */
+  int32_t H;         /* query heads (64 or 128)                               */
+  int32_t d_c;       /* latent width (512)                                    */
+  int32_t d_rope;    /* rotary key width, shared by the heads (64)            */
+  int32_t d_nope;    /* per-head query/key width without position (128)      */
+  int32_t d_v;       /* per-head value width (128)                            */
+  int32_t reserved;  /* must be 0                                             */
+  int64_t ckv_stride_layer; /* elements between layers of ckv; 0 = B*ckv_stride_b */
+  int64_t ckv_stride_b;     /* elements between sequences; 0 = L_cap*(d_c+d_rope) */
+  float scale;       /* softmax scale; 0 = 1/sqrt(d_nope + d_rope)            */
+  int32_t reserved2; /* must be 0                                             */
+} spec_mla_dims;
+
+/* Sparse decode attention of an MLA model over the selected tokens (Sec. 4.3,
+ * "Support for MLA": the cache holds a low-dimensional latent per token and
+ * only the selected latents are raised to the heads' dimension).  For every
+ * layer l, sequence b and head h, with j over idx[b, 0..counts[b]):
+ *     key_j   = [W_UK[l,h] c_j ; r_j],   value_j = W_UV[l,h] c_j,
+ *     s_j     = scale * dot(q[l,b,h,:], key_j),
+ *     out[l,b,h,:] = sum_j softmax_j(s) value_j,  lse[l,b,h] = log sum_j e^{s_j}
+ * where the cache row of token t is ckv[l,b,t,:] = [c_t (d_c) ; r_t (d_rope)]
+ * and q[l,b,h,:] = [q_nope (d_nope) ; q_rope (d_rope)].  The result is
+ * computed in the absorbed form (W_UK folded into the query, W_UV applied to
+ * the weighted sum of latents), equal in exact arithmetic: the per-head keys
+ * and values are never formed.  Layouts (bf16 unless noted):
+ *     q      [n_layers][B][H][d_nope + d_rope]
+ *     ckv    [n_layers][B][L_cap][d_c + d_rope]  (strides in dm; rows dense)
+ *     w_uk   [n_layers][H][d_nope][d_c],  w_uv [n_layers][H][d_v][d_c]
+ *            (each maps a latent to one head's part: a linear layer's [out][in])
+ *     idx    [B][k_max] int32 (indices outside [0, L_cap) are clamped),
+ *     counts [B] int32 (clamped into [0, k_max]),
+ *     out    [n_layers][B][H][d_v] fp32, lse [n_layers][B][H] fp32 (nullable).
+ * counts[b] = 0 gives out = 0 and lse = -inf.  fp32 accumulation; the
+ * absorbed query is rounded to bf16 for the matrix cores, the softmax weights
+ * and the latent output enter them as bf16 high + low pairs.
+ * SPEC_ERR_INVALID: null pointer, non-positive dimension, k_max > L_cap,
+ * misaligned pointer (16 bytes for tensors, 4 for idx/counts/lse), a stride
+ * below the block it steps over or not a multiple of 8, a negative or
+ * non-finite scale, non-zero reserved fields.  SPEC_ERR_UNSUPPORTED: other
+ * widths than the ones above, H not 64 or 128, k_max > 32768, B > 65535.
+ * SPEC_ERR_WORKSPACE: ws_bytes below spec_mla_workspace_size().             */
+SPEC_API spec_status spec_mla_sparse_decode_attn(const spec_mla_dims* dm, const uint16_t* q,
+                                        const uint16_t* ckv, const uint16_t* w_uk,
+                                        const uint16_t* w_uv, const int32_t* idx,
+                                        const int32_t* counts, float* out, float* lse,
+                                        void* ws, size_t ws_bytes, spec_stream stream);
+
+/* Workspace bytes of spec_mla_sparse_decode_attn (the absorbed queries and
+ * the partial results of split selections).                                 */
+SPEC_API spec_status spec_mla_workspace_size(const spec_mla_dims* dm, size_t* bytes);
+
 /* Workspace bytes needed by `op` for dimensions `dm` (0 for SPEC_OP_GATHER).
  * Returns the same validation status as the op itself.                      */
 SPEC_API spec_status spec_workspace_size(const spec_dims* dm, spec_op op,

@@ -23,7 +23,7 @@ import torch
 __all__ = [
     "SpecError", "load_library", "lib_path", "Dims", "workspace_size", "score", "topk",
     "gather", "sparse_decode_attn", "delta_gather", "ElasticState", "step", "Frontend",
-    "retrieval_qk",
+    "retrieval_qk", "MlaDims", "mla_workspace_size", "mla_sparse_decode_attn",
     "OP_SCORE", "OP_TOPK", "OP_GATHER", "OP_ATTN", "OP_DELTA", "OP_STEP", "OP_FRONTEND",
     "EXPORTED_SYMBOLS",
 ]
@@ -36,7 +36,8 @@ STATUS = {0: "SPEC_OK", 1: "SPEC_ERR_INVALID", 2: "SPEC_ERR_UNSUPPORTED",
           3: "SPEC_ERR_WORKSPACE", 4: "SPEC_ERR_HIP"}
 
 EXPORTED_SYMBOLS = ["spec_score", "spec_topk", "spec_gather", "spec_sparse_decode_attn",
-                    "spec_delta_gather", "spec_step", "spec_retrieval_qk", "spec_workspace_size",
+                    "spec_delta_gather", "spec_step", "spec_retrieval_qk",
+                    "spec_mla_sparse_decode_attn", "spec_mla_workspace_size", "spec_workspace_size",
                     "spec_status_string", "spec_last_hip_error", "spec_version"]
 
 
@@ -86,6 +87,22 @@ class Frontend(ctypes.Structure):
                 ("yarn_beta", ctypes.c_float), ("reserved", ctypes.c_int32)]
 
 
+class MlaDims(ctypes.Structure):
+    """Mirror of `spec_mla_dims`."""
+    _fields_ = [("B", ctypes.c_int32), ("L_cap", ctypes.c_int32), ("k_max", ctypes.c_int32),
+                ("n_layers", ctypes.c_int32), ("H", ctypes.c_int32), ("d_c", ctypes.c_int32),
+                ("d_rope", ctypes.c_int32), ("d_nope", ctypes.c_int32), ("d_v", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("ckv_stride_layer", ctypes.c_int64),
+                ("ckv_stride_b", ctypes.c_int64), ("scale", ctypes.c_float),
+                ("reserved2", ctypes.c_int32)]
+
+    @classmethod
+    def make(cls, B, L_cap, k_max, n_layers, H, d_c=512, d_rope=64, d_nope=128, d_v=128,
+             ckv_stride_layer=0, ckv_stride_b=0, scale=0.0):
+        return cls(B, L_cap, k_max, n_layers, H, d_c, d_rope, d_nope, d_v, 0, ckv_stride_layer,
+                   ckv_stride_b, scale, 0)
+
+
 _lib = None
 
 
@@ -103,6 +120,7 @@ def load_library(path: Optional[str] = None):
     D = ctypes.POINTER(Dims)
     E = ctypes.POINTER(Elastic)
     F = ctypes.POINTER(Frontend)
+    M = ctypes.POINTER(MlaDims)
     sig = {
         "spec_score": [D, P, P, P, P, P, S, P],
         "spec_topk": [D, P, P, P, P, P, P, S, P],
@@ -111,6 +129,8 @@ def load_library(path: Optional[str] = None):
         "spec_delta_gather": [D, P, P, P, P, E, P, S, P],
         "spec_step": [D, P, P, P, P, P, P, P, P, P, P, P, P, E, P, S, P],
         "spec_retrieval_qk": [D, F, P, P, P, P, P, P, P, P, S, P],
+        "spec_mla_sparse_decode_attn": [M, P, P, P, P, P, P, P, P, P, S, P],
+        "spec_mla_workspace_size": [M, ctypes.POINTER(S)],
         "spec_workspace_size": [D, I, ctypes.POINTER(S)],
     }
     for name, args in sig.items():
@@ -479,3 +499,63 @@ def retrieval_qk(tokens: torch.Tensor, pos: torch.Tensor, emb: torch.Tensor, w_q
                                  _p(emb), _p(w_q), _p(w_k), _p(q_r), _p(K_r), _p(ws), nws,
                                  _stream(K_r)), "spec_retrieval_qk")
     return q_r
+
+
+def mla_workspace_size(dims: MlaDims) -> int:
+    lib = load_library()
+    n = ctypes.c_size_t(0)
+    _check(lib.spec_mla_workspace_size(ctypes.byref(dims), ctypes.byref(n)),
+           "spec_mla_workspace_size")
+    return int(n.value)
+
+
+def mla_sparse_decode_attn(q: torch.Tensor, ckv: torch.Tensor, w_uk: torch.Tensor,
+                           w_uv: torch.Tensor, idx: torch.Tensor, counts: torch.Tensor,
+                           scale: float = 0.0, out: Optional[torch.Tensor] = None,
+                           lse: Optional[torch.Tensor] = None, with_lse: bool = True,
+                           ws: Optional[torch.Tensor] = None):
+    """Sparse decode attention of an MLA model over the selected tokens.
+    q [n_layers, B, H, d_nope + d_rope]; ckv [n_layers, B, L_cap, d_c + d_rope]
+    (latent, then rotary key; the last two dims packed); w_uk [n_layers, H,
+    d_nope, d_c]; w_uv [n_layers, H, d_v, d_c] (bf16); idx [B, k_max] and
+    counts [B] int32.  Returns (out fp32 [n_layers, B, H, d_v], lse fp32
+    [n_layers, B, H] or None)."""
+    lib = load_library()
+    _need(q, "q", torch.bfloat16, 4)
+    _need(ckv, "ckv", torch.bfloat16, 4)
+    _need(w_uk, "w_uk", torch.bfloat16, 4)
+    _need(w_uv, "w_uv", torch.bfloat16, 4)
+    _need(idx, "idx", torch.int32, 2)
+    n_layers, B, L_cap, dk = ckv.shape
+    H = q.shape[2]
+    d_nope = w_uk.shape[2]
+    d_c = w_uk.shape[3]
+    d_rope = dk - d_c
+    d_v = w_uv.shape[2]
+    if tuple(q.shape) != (n_layers, B, H, d_nope + d_rope) or not q.is_contiguous():
+        raise ValueError("q must be contiguous [n_layers, B, H, d_nope + d_rope]")
+    if tuple(w_uk.shape) != (n_layers, H, d_nope, d_c) or not w_uk.is_contiguous():
+        raise ValueError("w_uk must be contiguous [n_layers, H, d_nope, d_c]")
+    if tuple(w_uv.shape) != (n_layers, H, d_v, d_c) or not w_uv.is_contiguous():
+        raise ValueError("w_uv must be contiguous [n_layers, H, d_v, d_c]")
+    _inner_contig(ckv, "ckv", 2)
+    if idx.shape[0] != B or not idx.is_contiguous():
+        raise ValueError("idx must be contiguous [B, k_max]")
+    _i32(counts, "counts", B)
+    dims = MlaDims.make(B=B, L_cap=L_cap, k_max=idx.shape[1], n_layers=n_layers, H=H, d_c=d_c,
+                        d_rope=d_rope, d_nope=d_nope, d_v=d_v, ckv_stride_layer=ckv.stride(0),
+                        ckv_stride_b=ckv.stride(1), scale=scale)
+    need = mla_workspace_size(dims)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    elif ws.numel() * ws.element_size() < need:
+        raise ValueError(f"workspace too small: {need} bytes needed")
+    if out is None:
+        out = torch.empty((n_layers, B, H, d_v), dtype=torch.float32, device=q.device)
+    if lse is None and with_lse:
+        lse = torch.empty((n_layers, B, H), dtype=torch.float32, device=q.device)
+    _check(lib.spec_mla_sparse_decode_attn(ctypes.byref(dims), _p(q), _p(ckv), _p(w_uk),
+                                           _p(w_uv), _p(idx), _p(counts), _p(out), _p(lse),
+                                           _p(ws), need, _stream(q)),
+           "spec_mla_sparse_decode_attn")
+    return out, lse

@@ -90,6 +90,15 @@ struct FrontDims {
 constexpr int kFrontMaxSplit = 16;
 size_t front_ws_bytes(const Dims& d);
 
+// MLA sparse decode attention: d_c = 512, d_rope = 64, d_nope = d_v = 128
+// (validated), H in {64, 128}; the latent cache rows are d_c + d_rope wide.
+struct MlaDims {
+  int B, L_cap, k_max, n_layers, H;
+  int64_t stride_layer, stride_b;  // elements between layers / sequences of the cache
+  float scale;                     // resolved: 1/sqrt(d_nope + d_rope) by default
+};
+size_t mla_ws_bytes(const MlaDims& d);
+
 // ---- launchers (return the HIP launch status) --------------------------
 hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
                         const int32_t* seq_lens, float* scores, void* ws,
@@ -111,6 +120,9 @@ hipError_t launch_delta(const Dims& d, const int32_t* idx_now, const int32_t* co
                         const uint16_t* k_cache, const uint16_t* v_cache,
                         int32_t* slot_tok, uint16_t* kbuf, uint16_t* vbuf,
                         int32_t* n_changed, void* ws, hipStream_t s);
+hipError_t launch_mla(const MlaDims& d, const uint16_t* q, const uint16_t* ckv,
+                      const uint16_t* w_uk, const uint16_t* w_uv, const int32_t* idx,
+                      const int32_t* counts, float* out, float* lse, void* ws, hipStream_t s);
 hipError_t launch_retrieval_qk(const Dims& d, const FrontDims& f, const int32_t* tokens,
                                const int32_t* pos, const uint16_t* emb, const uint16_t* w_q,
                                const uint16_t* w_k, uint16_t* q_r, uint16_t* k_r, void* ws,

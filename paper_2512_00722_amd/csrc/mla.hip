@@ -1,0 +1,581 @@
+// Sparse decode attention of an MLA model (Sec. 4.3, "Support for MLA"): the
+// cache holds one latent row per token -- the latent c (d_c = 512) followed by
+// the rotary key shared by all heads (d_rope = 64) -- and only the selected
+// rows are raised to per-head keys [W_UK[h] c ; k_rope] and values W_UV[h] c.
+//
+// The kernels compute the same attention in the absorbed form, which never
+// materialises a per-head key or value:
+//   q~_h = W_UK[h]^T q_nope_h  (and q_rope_h appended), so that
+//   q_h . key_{h,j} = q~_h . [c_j ; k_rope_j];
+//   o_h = W_UV[h] (sum_j p_hj c_j), since the weights p_hj sum to one.
+// All H heads then read the same selected latent rows (multi-query
+// attention with 576-wide keys and 512-wide values).  Three kernels:
+//
+//  1. mla_absorb_kernel: one wavefront per (layer, head) streams W_UK[h]
+//     (d_nope rows of d_c) once for every sequence, forms q~ in fp32 and
+//     stores it as a bf16 high part and a bf16 low part (q~ - high), so that
+//     it reaches the matrix cores to ~2^-17; the rotary part is copied as is
+//     (already bf16) and the scale is applied to the fp32 logits.
+//  2. mla_attn_kernel: one workgroup per CU, four wavefronts; a work unit is
+//     (layer, sequence, split of the selection, group of 64 heads).  Per
+//     32-token chunk the workgroup copies the selected latent rows into LDS
+//     once (double buffered: the next chunk's rows are in flight during this
+//     chunk's math), and every wavefront -- 16 heads -- runs
+//       S^T = C Q~^T  on v_mfma_f32_16x16x32_bf16 (A = 16 latent rows from
+//                     LDS, B = q~ of 16 heads, resident in registers: two
+//                     MFMAs per k-step on the latent part, high and low),
+//       online softmax in log2 units per head,
+//       O^T += C^T P^T (A = latent columns read transposed from LDS with
+//                     ds_read_b64_tr_b16, B = P as a bf16 high + low pair).
+//     It leaves (max, sum, acc) per (unit, head) in the workspace.  A wave
+//     holds q~ of its heads (144 VGPRs) and their latent accumulator (256):
+//     a register file of 512 fits 16 heads, not 32, so 128 heads take two
+//     workgroups.  Their work units are numbered 8 apart, which puts them on
+//     the same XCD (workgroups are dealt to the 8 XCDs in turn) at the same
+//     time: the second reads the latent rows from that XCD's L2.
+//  3. mla_out_kernel: one workgroup per (layer, head) merges the splits of
+//     every sequence into the latent output o~ (log-sum-exp), splits it into
+//     bf16 high + low parts in LDS and applies W_UV[h] on the matrix cores
+//     (A = 16 rows of W_UV streamed from HBM, B = o~ of up to 16 sequences),
+//     writing out and lse.
+#include "device_common.h"
+#include "internal.h"
+
+namespace spec {
+namespace {
+
+constexpr int kDC = 512;             // latent width
+constexpr int kDR = 64;              // rotary key width
+constexpr int kDK = kDC + kDR;       // key width of the latent row
+constexpr int kDN = 128;             // per-head no-position query width
+constexpr int kDVo = 128;            // per-head value width
+constexpr int kMWaves = 4;           // wavefronts per workgroup
+constexpr int kMThreads = 64 * kMWaves;
+constexpr int kMChunk = 32;          // selected tokens per inner step
+constexpr int kCPitch = kDK + 80;    // LDS row pitch (elements): rows start 32 B apart mod 256 B
+constexpr int kQSteps = kDK / 32;    // k-steps of S^T = C Q~^T
+constexpr int kLSteps = kDC / 32;    // k-steps on the latent part (high + low)
+constexpr int kQT = 2 * kDC + kDR;   // absorbed query row: high, low, rotary
+constexpr int kVBlocks = kDC / 16;   // 16-dim blocks of O^T
+constexpr int kRowU4 = kDK / 8;      // 16-byte pieces per latent row
+constexpr int kChunkU4 = kMChunk * kRowU4 / kMThreads;  // per thread and chunk
+constexpr int kMMaxSplit = 2048;     // longest split (tokens per work unit)
+constexpr int kMMinSplit = 256;
+constexpr int kMMaxSplitCount = 16;  // splits per (layer, sequence); the merge holds 16 weights
+
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+struct MlaArgs {
+  const uint16_t* q;       // [n_layers][B][H][d_nope + d_rope]
+  const uint16_t* ckv;     // latent rows [n_layers][B][L_cap][576] (strides below)
+  const uint16_t* w_uk;    // [n_layers][H][d_nope][d_c]
+  const uint16_t* w_uv;    // [n_layers][H][d_v][d_c]
+  const int32_t* idx;      // [B][k_max]
+  const int32_t* counts;   // [B]
+  uint16_t* qt;            // workspace: [n_layers][B][H][2 d_c + d_rope] absorbed queries
+  float* part_acc;         // workspace: [n_layers * B][n_split][H][d_c]
+  float* part_ml;          // workspace: [n_layers * B][n_split][H][2]
+  float* out;              // [n_layers][B][H][d_v]
+  float* lse;              // [n_layers][B][H] or null
+  int64_t stride_layer, stride_b;  // elements of ckv
+  int B, H, k_max, L_cap, n_layers, n_split, split_tokens, n_units, n_hg, n_items;
+  float scale_log2;        // scale * log2(e)
+};
+
+__device__ __forceinline__ uint32_t f2bf_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+// 8 values -> bf16 high part and bf16 low part (value - high), packed.
+__device__ __forceinline__ void split8(const float* p, uint4& hi, uint4& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t h0 = f2bf_rne(p[2 * j]), h1 = f2bf_rne(p[2 * j + 1]);
+    const uint32_t l0 = f2bf_rne(p[2 * j] - __uint_as_float(h0 << 16));
+    const uint32_t l1 = f2bf_rne(p[2 * j + 1] - __uint_as_float(h1 << 16));
+    h[j] = h0 | (h1 << 16);
+    l[j] = l0 | (l1 << 16);
+  }
+  hi = make_uint4(h[0], h[1], h[2], h[3]);
+  lo = make_uint4(l[0], l[1], l[2], l[3]);
+}
+
+// max / sum over the four lanes {l, l^16, l^32, l^48} (one head's lanes).
+__device__ __forceinline__ float xg_max(float v) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float xg_sum(float v) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// Transposing LDS read: within each 16-lane group, lane i receives element
+// (i & 3) of the 8-byte chunks read by lanes (i >> 2) + 4j, j = 0..3.
+__device__ __forceinline__ bf16x4 lds_read_tr(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (__attribute__((address_space(3))) bf16x4*)(p));
+}
+
+// ---------------------------------------------------------------------------
+// 1. q~ = [W_UK[h]^T q_nope (high, low) ; q_rope]
+// ---------------------------------------------------------------------------
+// One wavefront per (layer, head); lane l owns latent dims 8l..8l+7 and
+// walks the d_nope rows of W_UK[h] (one 1 KiB row per load instruction),
+// for up to TB sequences at a time.
+template <int TB>
+__global__ __launch_bounds__(64) void mla_absorb_kernel(MlaArgs a) {
+  __shared__ float qs[TB][kDN];
+  const int lane = threadIdx.x;
+  const int layer = blockIdx.x / a.H;
+  const int h = blockIdx.x - layer * a.H;
+  const uint16_t* w = a.w_uk + ((size_t)layer * a.H + h) * kDN * kDC + 8 * lane;
+  for (int b0 = 0; b0 < a.B; b0 += TB) {
+    __syncthreads();
+    // this head's no-position queries of sequences b0 .. b0+TB-1
+    for (int e = lane; e < TB * kDN; e += 64) {
+      const int t = e / kDN, n = e - t * kDN;
+      const int b = min(b0 + t, a.B - 1);
+      const uint16_t v = a.q[(((size_t)layer * a.B + b) * a.H + h) * (kDN + kDR) + n];
+      qs[t][n] = __uint_as_float((uint32_t)v << 16);
+    }
+    __syncthreads();
+    float acc[TB][8];
+#pragma unroll
+    for (int t = 0; t < TB; ++t)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[t][j] = 0.f;
+    for (int n0 = 0; n0 < kDN; n0 += 16) {
+      uint4 wr[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) wr[i] = ldg16(w + (size_t)(n0 + i) * kDC);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float wf[8];
+        unpack8(wr[i], wf);
+#pragma unroll
+        for (int t = 0; t < TB; ++t) {
+          const float qv = qs[t][n0 + i];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) acc[t][j] = fmaf(qv, wf[j], acc[t][j]);
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < TB; ++t) {
+      const int b = b0 + t;
+      if (b >= a.B) break;
+      uint16_t* dst = a.qt + (((size_t)layer * a.B + b) * a.H + h) * kQT;
+      uint4 hi, lo;
+      split8(acc[t], hi, lo);
+      *reinterpret_cast<uint4*>(dst + 8 * lane) = hi;
+      *reinterpret_cast<uint4*>(dst + kDC + 8 * lane) = lo;
+      if (lane < kDR / 8) {  // the rotary part, unchanged
+        const uint16_t* src = a.q + (((size_t)layer * a.B + b) * a.H + h) * (kDN + kDR) + kDN;
+        *reinterpret_cast<uint4*>(dst + 2 * kDC + 8 * lane) = ldg16(src + 8 * lane);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 2. latent attention over the selected rows
+// ---------------------------------------------------------------------------
+// HT: 16-head tiles per wavefront.
+template <int HT>
+__global__ __launch_bounds__(kMThreads) __attribute__((amdgpu_waves_per_eu(1)))
+void mla_attn_kernel(MlaArgs a) {
+  __shared__ __align__(16) uint16_t cbuf[2][kMChunk * kCPitch];
+  __shared__ int rows[kMMaxSplit + 2 * kMChunk];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int r16 = lane & 15;  // MFMA column: a head of the tile; row: a token of a C tile
+  const int kg = lane >> 4;   // MFMA k-group
+
+  for (int item = blockIdx.x; item < a.n_items; item += gridDim.x) {
+    // items 8 n_hg q + 8 hg + r: unit 8q + r, head group hg
+    const int hg = (item >> 3) % a.n_hg;
+    const int unit = item / (8 * a.n_hg) * 8 + (item & 7);
+    if (unit >= a.n_units) continue;  // uniform per workgroup
+    const int split = unit % a.n_split;
+    const int lb = unit / a.n_split;  // layer * B + b
+    const int b = lb % a.B;
+    const int layer = lb / a.B;
+    const int count = clampi(a.counts[b], 0, a.k_max);
+    const int j0 = split * a.split_tokens;
+    const int n_tok = max(0, min(a.split_tokens, count - j0));
+    const int n_pad = (n_tok + kMChunk - 1) / kMChunk * kMChunk + kMChunk;
+
+    __syncthreads();  // the previous unit is done with rows and cbuf
+    for (int j = tid; j < n_pad; j += kMThreads)
+      rows[j] = j < n_tok ? clampi(a.idx[(size_t)b * a.k_max + j0 + j], 0, a.L_cap - 1) : 0;
+
+    // q~ of this wavefront's heads (B operand): head
+    // 64 hg + 16 (HT wave + ht) + r16, dims 32s + 8kg .. +8.
+    const int head0 = 64 * HT * hg + 16 * HT * wave;
+    uint4 qh[HT][kQSteps], ql[HT][kLSteps];  // high parts (then rotary), low parts
+#pragma unroll
+    for (int ht = 0; ht < HT; ++ht) {
+      const uint16_t* qp = a.qt + ((size_t)lb * a.H + head0 + 16 * ht + r16) * kQT + 8 * kg;
+#pragma unroll
+      for (int s = 0; s < kLSteps; ++s) {
+        qh[ht][s] = ldg16(qp + 32 * s);
+        ql[ht][s] = ldg16(qp + kDC + 32 * s);
+      }
+#pragma unroll
+      for (int s = kLSteps; s < kQSteps; ++s) qh[ht][s] = ldg16(qp + kDC + 32 * s);
+    }
+    __syncthreads();  // rows staged
+
+    const uint16_t* cb = a.ckv + (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b;
+    uint4 cr[kChunkU4];
+    auto load_chunk = [&](int c) {
+#pragma unroll
+      for (int r = 0; r < kChunkU4; ++r) {
+        const int e = tid + kMThreads * r;
+        const int row = e / kRowU4, col = e - (e / kRowU4) * kRowU4;
+        cr[r] = ldg16_stream(cb + (int64_t)rows[c + row] * kDK + 8 * col);
+      }
+    };
+    auto store_chunk = [&](int buf) {
+#pragma unroll
+      for (int r = 0; r < kChunkU4; ++r) {
+        const int e = tid + kMThreads * r;
+        const int row = e / kRowU4, col = e - (e / kRowU4) * kRowU4;
+        *reinterpret_cast<uint4*>(cbuf[buf] + row * kCPitch + 8 * col) = cr[r];
+      }
+    };
+
+    float m_run[HT], l_run[HT];
+    floatx4 acc[HT][kVBlocks];  // O^T[16db + 4kg + i][head r16 of tile ht]
+#pragma unroll
+    for (int ht = 0; ht < HT; ++ht) {
+      m_run[ht] = -INFINITY;
+      l_run[ht] = 0.f;
+#pragma unroll
+      for (int db = 0; db < kVBlocks; ++db) acc[ht][db] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    if (n_tok > 0) {
+      load_chunk(0);
+      store_chunk(0);
+      __syncthreads();
+    }
+    for (int c = 0; c < n_tok; c += kMChunk) {
+      const int buf = (c / kMChunk) & 1;
+      const bool more = c + kMChunk < n_tok;
+      if (more) load_chunk(c + kMChunk);  // in flight through this chunk's math
+      const uint16_t* C = cbuf[buf];
+
+      // S^T tiles: lane holds S[head r16][token 16t + 4kg + i].
+      floatx4 sacc[HT][2];
+#pragma unroll
+      for (int ht = 0; ht < HT; ++ht) {
+        sacc[ht][0] = floatx4{0.f, 0.f, 0.f, 0.f};
+        sacc[ht][1] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int s = 0; s < kQSteps; ++s) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const uint4 ca =
+              *reinterpret_cast<const uint4*>(C + (16 * t + r16) * kCPitch + 32 * s + 8 * kg);
+#pragma unroll
+          for (int ht = 0; ht < HT; ++ht) {
+            sacc[ht][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, ca), __builtin_bit_cast(bf16x8, qh[ht][s]),
+                sacc[ht][t], 0, 0, 0);
+            if (s < kLSteps)
+              sacc[ht][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(bf16x8, ca), __builtin_bit_cast(bf16x8, ql[ht][s]),
+                  sacc[ht][t], 0, 0, 0);
+          }
+        }
+      }
+
+      // Online softmax per head (log2 units).
+      uint4 phi[HT], plo[HT];
+#pragma unroll
+      for (int ht = 0; ht < HT; ++ht) {
+        float sv[8];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const bool valid = c + 16 * t + 4 * kg + i < n_tok;
+            sv[4 * t + i] = valid ? sacc[ht][t][i] * a.scale_log2 : -INFINITY;
+            mx = fmaxf(mx, sv[4 * t + i]);
+          }
+        mx = xg_max(mx);
+        const float mn = fmaxf(m_run[ht], mx);
+        const float alpha = exp2f(m_run[ht] - mn);
+        float ls = 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          sv[j] = exp2f(sv[j] - mn);
+          ls += sv[j];
+        }
+        l_run[ht] = l_run[ht] * alpha + ls;
+        m_run[ht] = mn;
+#pragma unroll
+        for (int db = 0; db < kVBlocks; ++db) acc[ht][db] *= alpha;
+        // k-slots 8kg..8kg+7 of the 32-token block are tokens 4kg..4kg+3 of
+        // the first tile and of the second: exactly the S^T entries held here.
+        split8(sv, phi[ht], plo[ht]);
+      }
+
+      // O^T += C^T P^T: the latent columns (dims 0..511 of the row) read
+      // transposed from LDS in the same token order as the P slots.
+      const uint16_t* r0 = C + (4 * kg + (r16 >> 2)) * kCPitch + 4 * (r16 & 3);
+      const uint16_t* r1 = r0 + 16 * kCPitch;
+#pragma unroll
+      for (int db = 0; db < kVBlocks; ++db) {
+        const bf16x4 va = lds_read_tr(r0 + 16 * db);
+        const bf16x4 vb = lds_read_tr(r1 + 16 * db);
+        const bf16x8 vA = __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+        for (int ht = 0; ht < HT; ++ht) {
+          acc[ht][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              vA, __builtin_bit_cast(bf16x8, phi[ht]), acc[ht][db], 0, 0, 0);
+          acc[ht][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              vA, __builtin_bit_cast(bf16x8, plo[ht]), acc[ht][db], 0, 0, 0);
+        }
+      }
+      if (more) store_chunk(buf ^ 1);  // the other buffer was released by the last barrier
+      __syncthreads();
+    }
+
+    // Partial results of this unit: (max, sum) per head and the unnormalised
+    // latent accumulator.
+#pragma unroll
+    for (int ht = 0; ht < HT; ++ht) {
+      const float l = xg_sum(l_run[ht]);
+      const int head = head0 + 16 * ht + r16;
+      const size_t prow = ((size_t)lb * a.n_split + split) * a.H + head;
+      float* dst = a.part_acc + prow * kDC + 4 * kg;
+#pragma unroll
+      for (int db = 0; db < kVBlocks; ++db)
+        *reinterpret_cast<float4*>(dst + 16 * db) =
+            make_float4(acc[ht][db][0], acc[ht][db][1], acc[ht][db][2], acc[ht][db][3]);
+      if (kg == 0) {
+        a.part_ml[prow * 2] = m_run[ht];
+        a.part_ml[prow * 2 + 1] = l;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 3. merge the splits, o = W_UV[h] o~, lse
+// ---------------------------------------------------------------------------
+constexpr int kOPitch = kDC + 8;  // LDS pitch of the o~ tiles (elements)
+
+__global__ __launch_bounds__(kMThreads) void mla_out_kernel(MlaArgs a) {
+  __shared__ __align__(16) uint16_t ohi[16 * kOPitch];
+  __shared__ __align__(16) uint16_t olo[16 * kOPitch];
+  __shared__ float wsp[16][17];  // per sequence: split weights, then the lse
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int r16 = lane & 15;
+  const int kg = lane >> 4;
+  const int layer = blockIdx.x / a.H;
+  const int h = blockIdx.x - layer * a.H;
+  const uint16_t* w = a.w_uv + ((size_t)layer * a.H + h) * kDVo * kDC;
+
+  for (int b0 = 0; b0 < a.B; b0 += 16) {
+    __syncthreads();
+    // split weights w_s = 2^(m_s - M) / sum_s' 2^(m_s' - M) l_s' per sequence
+    if (tid < 16) {
+      const int b = b0 + tid;
+      if (b < a.B) {
+        const size_t base = ((size_t)layer * a.B + b) * a.n_split;
+        float M = -INFINITY;
+        for (int s = 0; s < a.n_split; ++s) M = fmaxf(M, a.part_ml[((base + s) * a.H + h) * 2]);
+        float L = 0.f;
+        for (int s = 0; s < a.n_split; ++s) {
+          const size_t pr = ((base + s) * a.H + h) * 2;
+          L += M == -INFINITY ? 0.f : exp2f(a.part_ml[pr] - M) * a.part_ml[pr + 1];
+        }
+        const float inv = L > 0.f ? 1.f / L : 0.f;
+        for (int s = 0; s < a.n_split; ++s) {
+          const float ms = a.part_ml[((base + s) * a.H + h) * 2];
+          wsp[tid][s] = (L > 0.f && ms != -INFINITY) ? exp2f(ms - M) * inv : 0.f;
+        }
+        wsp[tid][16] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+      }
+    }
+    __syncthreads();
+    // o~ of sequences b0 .. b0+15 as bf16 high + low parts (zero past B)
+    for (int e = tid; e < 16 * (kDC / 8); e += kMThreads) {
+      const int t = e / (kDC / 8), c8 = e - t * (kDC / 8);
+      const int b = b0 + t;
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = 0.f;
+      if (b < a.B) {
+        const size_t base = ((size_t)layer * a.B + b) * a.n_split;
+        for (int s = 0; s < a.n_split; ++s) {
+          const float ws = wsp[t][s];
+          const float* src = a.part_acc + ((base + s) * a.H + h) * kDC + 8 * c8;
+          const float4 x0 = *reinterpret_cast<const float4*>(src);
+          const float4 x1 = *reinterpret_cast<const float4*>(src + 4);
+          v[0] += ws * x0.x; v[1] += ws * x0.y; v[2] += ws * x0.z; v[3] += ws * x0.w;
+          v[4] += ws * x1.x; v[5] += ws * x1.y; v[6] += ws * x1.z; v[7] += ws * x1.w;
+        }
+      }
+      uint4 hi, lo;
+      split8(v, hi, lo);
+      *reinterpret_cast<uint4*>(ohi + t * kOPitch + 8 * c8) = hi;
+      *reinterpret_cast<uint4*>(olo + t * kOPitch + 8 * c8) = lo;
+    }
+    __syncthreads();
+
+    // out^T[v][b] = W_UV[h][v][:] . o~[b][:]: wavefront w owns v-tiles 2w, 2w+1.
+    floatx4 acc[2];
+    uint4 wr[2][kDC / 32];
+#pragma unroll
+    for (int vt = 0; vt < 2; ++vt) {
+      const uint16_t* wp = w + (size_t)(32 * wave + 16 * vt + r16) * kDC + 8 * kg;
+#pragma unroll
+      for (int s = 0; s < kDC / 32; ++s) wr[vt][s] = ldg16_stream(wp + 32 * s);
+    }
+#pragma unroll
+    for (int vt = 0; vt < 2; ++vt) acc[vt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < kDC / 32; ++s) {
+      const uint4 bh = *reinterpret_cast<const uint4*>(ohi + r16 * kOPitch + 32 * s + 8 * kg);
+      const uint4 bl = *reinterpret_cast<const uint4*>(olo + r16 * kOPitch + 32 * s + 8 * kg);
+#pragma unroll
+      for (int vt = 0; vt < 2; ++vt) {
+        acc[vt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8, wr[vt][s]), __builtin_bit_cast(bf16x8, bh), acc[vt], 0, 0, 0);
+        acc[vt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            __builtin_bit_cast(bf16x8, wr[vt][s]), __builtin_bit_cast(bf16x8, bl), acc[vt], 0, 0, 0);
+      }
+    }
+    // lane (b = r16, kg) holds out[b][v = 32w + 16vt + 4kg + i]
+    const int b = b0 + r16;
+    if (b < a.B) {
+      float* dst = a.out + (((size_t)layer * a.B + b) * a.H + h) * kDVo + 32 * wave + 4 * kg;
+#pragma unroll
+      for (int vt = 0; vt < 2; ++vt)
+        *reinterpret_cast<float4*>(dst + 16 * vt) =
+            make_float4(acc[vt][0], acc[vt][1], acc[vt][2], acc[vt][3]);
+      if (a.lse && wave == 0 && kg == 0)
+        a.lse[((size_t)layer * a.B + b) * a.H + h] = wsp[r16][16];
+    }
+  }
+}
+
+// Splits of the selection: enough work units for 256 CUs (a fixed target,
+// so that the workspace size does not depend on the device), 256..2048
+// tokens per unit, at most 16 units per (layer, sequence).
+struct MlaPlan {
+  int n_split, split_tokens, n_units, n_hg, n_items;
+};
+
+MlaPlan mla_plan(const MlaDims& d) {
+  constexpr int kTargetUnits = 256;
+  const int groups = d.n_layers * d.B * (d.H / 64);
+  MlaPlan p;
+  const int want = groups >= kTargetUnits ? 1 : (kTargetUnits + groups - 1) / groups;
+  int split = (d.k_max + want - 1) / want;
+  const int at_most_16 = (d.k_max + kMMaxSplitCount - 1) / kMMaxSplitCount;
+  split = split < at_most_16 ? at_most_16 : split;
+  split = (split + kMChunk - 1) / kMChunk * kMChunk;
+  split = split < kMMinSplit ? kMMinSplit : split;
+  split = split > kMMaxSplit ? kMMaxSplit : split;
+  p.split_tokens = split;
+  p.n_split = (d.k_max + split - 1) / split;
+  p.n_hg = d.H / 64;
+  p.n_units = d.n_layers * d.B * p.n_split;
+  p.n_items = (p.n_units + 7) / 8 * 8 * p.n_hg;
+  return p;
+}
+
+size_t qt_bytes(const MlaDims& d) {
+  return align_up(sizeof(uint16_t) * (size_t)d.n_layers * d.B * d.H * kQT);
+}
+size_t part_acc_bytes(const MlaDims& d, int n_split) {
+  return align_up(sizeof(float) * (size_t)d.n_layers * d.B * n_split * d.H * kDC);
+}
+
+}  // namespace
+
+size_t mla_ws_bytes(const MlaDims& d) {
+  const int ns = mla_plan(d).n_split;
+  return qt_bytes(d) + part_acc_bytes(d, ns) +
+         align_up(sizeof(float) * (size_t)d.n_layers * d.B * ns * d.H * 2);
+}
+
+hipError_t launch_mla(const MlaDims& d, const uint16_t* q, const uint16_t* ckv,
+                      const uint16_t* w_uk, const uint16_t* w_uv, const int32_t* idx,
+                      const int32_t* counts, float* out, float* lse, void* ws, hipStream_t s) {
+  const MlaPlan p = mla_plan(d);
+  int n_cu = 256;
+  int dev = 0;
+  if (hipGetDevice(&dev) == hipSuccess) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        v > 0)
+      n_cu = v;
+  }
+  MlaArgs a;
+  a.q = q;
+  a.ckv = ckv;
+  a.w_uk = w_uk;
+  a.w_uv = w_uv;
+  a.idx = idx;
+  a.counts = counts;
+  char* base = static_cast<char*>(ws);
+  a.qt = reinterpret_cast<uint16_t*>(base);
+  base += qt_bytes(d);
+  a.part_acc = reinterpret_cast<float*>(base);
+  base += part_acc_bytes(d, p.n_split);
+  a.part_ml = reinterpret_cast<float*>(base);
+  a.out = out;
+  a.lse = lse;
+  a.stride_layer = d.stride_layer;
+  a.stride_b = d.stride_b;
+  a.B = d.B;
+  a.H = d.H;
+  a.k_max = d.k_max;
+  a.L_cap = d.L_cap;
+  a.n_layers = d.n_layers;
+  a.n_split = p.n_split;
+  a.split_tokens = p.split_tokens;
+  a.n_units = p.n_units;
+  a.n_hg = p.n_hg;
+  a.n_items = p.n_items;
+  a.scale_log2 = d.scale * kLog2e;
+
+  const int grid_lh = d.n_layers * d.H;
+  // a multiple of 16 keeps the two head groups of a unit on one XCD
+  const int grid = p.n_items < n_cu ? p.n_items : (n_cu / 16 > 0 ? n_cu / 16 * 16 : n_cu);
+  if (d.B == 1)
+    hipLaunchKernelGGL((mla_absorb_kernel<1>), dim3(grid_lh), dim3(64), 0, s, a);
+  else if (d.B <= 4)
+    hipLaunchKernelGGL((mla_absorb_kernel<4>), dim3(grid_lh), dim3(64), 0, s, a);
+  else
+    hipLaunchKernelGGL((mla_absorb_kernel<8>), dim3(grid_lh), dim3(64), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((mla_attn_kernel<1>), dim3(grid), dim3(kMThreads), 0, s, a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(mla_out_kernel, dim3(grid_lh), dim3(kMThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace spec

@@ -140,9 +140,65 @@ spec_status resolve_frontend(const spec_frontend* fe, spec::FrontDims* f) {
   return SPEC_OK;
 }
 
+spec_status resolve_mla(const spec_mla_dims* dm, spec::MlaDims* o) {
+  if (!dm || dm->reserved != 0 || dm->reserved2 != 0) return SPEC_ERR_INVALID;
+  if (dm->B <= 0 || dm->L_cap <= 0 || dm->k_max <= 0 || dm->n_layers <= 0 || dm->H <= 0 ||
+      dm->d_c <= 0 || dm->d_rope <= 0 || dm->d_nope <= 0 || dm->d_v <= 0)
+    return SPEC_ERR_INVALID;
+  if (dm->k_max > dm->L_cap) return SPEC_ERR_INVALID;
+  if (dm->ckv_stride_layer < 0 || dm->ckv_stride_b < 0) return SPEC_ERR_INVALID;
+  if (!isfinite(dm->scale) || dm->scale < 0.f) return SPEC_ERR_INVALID;
+  if (dm->d_c != 512 || dm->d_rope != 64 || dm->d_nope != 128 || dm->d_v != 128)
+    return SPEC_ERR_UNSUPPORTED;
+  if (dm->H != 64 && dm->H != 128) return SPEC_ERR_UNSUPPORTED;
+  if (dm->k_max > 32768 || dm->B > 65535) return SPEC_ERR_UNSUPPORTED;
+  if ((int64_t)dm->n_layers * dm->H > INT32_MAX || (int64_t)dm->n_layers * dm->B > 1 << 24)
+    return SPEC_ERR_UNSUPPORTED;
+  const int64_t row = (int64_t)dm->L_cap * (dm->d_c + dm->d_rope);
+  o->B = dm->B;
+  o->L_cap = dm->L_cap;
+  o->k_max = dm->k_max;
+  o->n_layers = dm->n_layers;
+  o->H = dm->H;
+  o->stride_b = dm->ckv_stride_b ? dm->ckv_stride_b : row;
+  o->stride_layer = dm->ckv_stride_layer ? dm->ckv_stride_layer : (int64_t)dm->B * o->stride_b;
+  if (o->stride_b < row || o->stride_b % 8) return SPEC_ERR_INVALID;
+  if (o->stride_layer < row || o->stride_layer % 8) return SPEC_ERR_INVALID;
+  o->scale = dm->scale > 0.f ? dm->scale : 1.0f / sqrtf((float)(dm->d_nope + dm->d_rope));
+  return SPEC_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+spec_status spec_mla_workspace_size(const spec_mla_dims* dm, size_t* bytes) {
+  if (!bytes) return SPEC_ERR_INVALID;
+  spec::MlaDims d;
+  const spec_status st = resolve_mla(dm, &d);
+  if (st != SPEC_OK) return st;
+  *bytes = spec::mla_ws_bytes(d);
+  return SPEC_OK;
+}
+
+spec_status spec_mla_sparse_decode_attn(const spec_mla_dims* dm, const uint16_t* q,
+                                        const uint16_t* ckv, const uint16_t* w_uk,
+                                        const uint16_t* w_uv, const int32_t* idx,
+                                        const int32_t* counts, float* out, float* lse, void* ws,
+                                        size_t ws_bytes, spec_stream stream) {
+  spec::MlaDims d;
+  spec_status st = resolve_mla(dm, &d);
+  if (st != SPEC_OK) return st;
+  if (!q || !ckv || !w_uk || !w_uv || !idx || !counts || !out) return SPEC_ERR_INVALID;
+  if (!aligned16(q) || !aligned16(ckv) || !aligned16(w_uk) || !aligned16(w_uv) ||
+      !aligned4(idx) || !aligned4(counts) || !aligned16(out) || (lse && !aligned4(lse)))
+    return SPEC_ERR_INVALID;
+  const size_t need = spec::mla_ws_bytes(d);
+  if (!ws || ws_bytes < need) return SPEC_ERR_WORKSPACE;
+  if (!aligned16(ws)) return SPEC_ERR_INVALID;
+  return hip_status(spec::launch_mla(d, q, ckv, w_uk, w_uv, idx, counts, out, lse, ws,
+                                     as_stream(stream)));
+}
 
 spec_status spec_workspace_size(const spec_dims* dm, spec_op op, size_t* bytes) {
   if (!bytes) return SPEC_ERR_INVALID;

@@ -207,6 +207,55 @@ def test_frontend_rejects_before_hip(lib):
     assert lib.spec_last_hip_error() == 0
 
 
+def good_mla(**kw):
+    base = dict(B=8, L_cap=32768, k_max=2048, n_layers=61, H=128)
+    base.update(kw)
+    return spec.MlaDims.make(**base)
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("B", 0, 1), ("k_max", 40000, 1), ("n_layers", -1, 1), ("reserved", 1, 1), ("reserved2", 2, 1),
+    ("scale", -1.0, 1), ("scale", float("nan"), 1), ("ckv_stride_b", 100, 1),
+    ("ckv_stride_b", 32768 * 576 + 4, 1),
+    ("d_c", 256, 2), ("d_rope", 32, 2), ("d_nope", 64, 2), ("d_v", 64, 2), ("H", 32, 2),
+    ("H", 96, 2), ("B", 70000, 2),
+])
+def test_mla_validation(lib, field, value, status):
+    d = good_mla()
+    if field == "k_max" and value > 32768:
+        d.L_cap = 65536   # k_max within L_cap, above the supported 32768
+        status = 2
+    setattr(d, field, value)
+    n = ctypes.c_size_t(0)
+    assert lib.spec_mla_workspace_size(ctypes.byref(d), ctypes.byref(n)) == status
+    assert lib.spec_mla_sparse_decode_attn(ctypes.byref(d), *(FAKE,) * 6, FAKE, None, FAKE,
+                                           1 << 40, None) == status
+    assert lib.spec_last_hip_error() == 0
+
+
+def test_mla_rejects_before_hip(lib):
+    d = good_mla()
+    n = ctypes.c_size_t(0)
+    assert lib.spec_mla_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
+    # absorbed queries of every (layer, sequence, head) and one split of partials
+    assert n.value >= 61 * 8 * 128 * (576 * 2 + 512 * 4)
+    byref = ctypes.byref
+    for i in range(7):              # q, ckv, w_uk, w_uv, idx, counts, out: null, then misaligned
+        args = [FAKE] * 7
+        args[i] = None
+        assert lib.spec_mla_sparse_decode_attn(byref(d), *args, None, FAKE, n.value, None) == 1
+        args[i] = ctypes.c_void_p(FAKE.value + (2 if i in (4, 5) else 8))
+        assert lib.spec_mla_sparse_decode_attn(byref(d), *args, None, FAKE, n.value, None) == 1
+    args = [FAKE] * 7
+    assert lib.spec_mla_sparse_decode_attn(byref(d), *args, None, None, n.value, None) == 3
+    assert lib.spec_mla_sparse_decode_attn(byref(d), *args, None, FAKE, n.value - 1, None) == 3
+    assert lib.spec_mla_sparse_decode_attn(byref(d), *args, ctypes.c_void_p(FAKE.value + 2),
+                                           FAKE, n.value, None) == 1     # misaligned lse
+    assert lib.spec_mla_workspace_size(None, byref(n)) == 1
+    assert lib.spec_mla_workspace_size(byref(d), None) == 1
+    assert lib.spec_last_hip_error() == 0
+
+
 def test_python_wrappers_refuse_cpu_tensors(lib):
     import torch
     q_r = torch.zeros((1, 8, 64), dtype=torch.bfloat16)

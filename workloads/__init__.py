@@ -32,7 +32,7 @@ import torch
 
 __all__ = ["Workload", "WORKLOADS", "BENCH_WORKLOAD", "tensor_seed",
            "generate", "elastic_sequence", "algorithmic_bytes", "small_workload",
-           "frontend_inputs", "frontend_bytes"]
+           "frontend_inputs", "frontend_bytes", "generate_mla", "mla_bytes", "mla_attn_bytes"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -65,6 +65,13 @@ class Workload:
     vocab: int = 128256
     rope_base: float = 500000.0
     orig_ctx: int = 2048
+    # MLA models (DeepSeek-V3 / Kimi-K2 shapes): H_q query heads attend over
+    # a latent cache of d_c + d_rope per token (H_kv and d are unused)
+    mla: bool = False
+    d_c: int = 512
+    d_rope: int = 64
+    d_nope: int = 128
+    d_v: int = 128
 
     @property
     def L_cap(self) -> int:
@@ -94,6 +101,9 @@ WORKLOADS = {
     "b1_l131072_k4096_g8": Workload(
         "b1_l131072_k4096_g8", B=1, L=131072, H_r=8, d_r=128, n_layers=32,
         H_q=64, H_kv=8, d=128, k=4096, n_clusters=3, cluster_len=512, hidden=8192),
+    "b8_l32768_k2048_mla": Workload(
+        "b8_l32768_k2048_mla", B=8, L=32768, H_r=8, d_r=64, n_layers=61,
+        H_q=128, H_kv=1, d=128, k=2048, heavy_frac=0.02, recent=256, mla=True),
     "b64_ragged_l2k_16k_elastic": Workload(
         "b64_ragged_l2k_16k_elastic", B=64, L=16384, H_r=8, d_r=64,
         n_layers=32, H_q=32, H_kv=8, d=128, k=2048, heavy_frac=0.02,
@@ -282,6 +292,56 @@ def frontend_bytes(w: Workload) -> int:
     embedding row per sequence, and q_r and the new K_r row written."""
     return (2 * w.H_r * w.d_r * w.hidden * 2 + w.B * w.hidden * 2
             + 2 * w.B * w.H_r * w.d_r * 2)
+
+
+def generate_mla(w: Workload, seed: int = 0, device="cpu", layers: Optional[range] = None):
+    """Inputs of an MLA decode step: the retrieval inputs of `generate`
+    (q_r, K_r, seq_lens, ks, heavy; same seeds) and, per layer, the queries
+    q_mla [n_layers, B, H, d_nope + d_rope] N(0,1), the latent cache ckv
+    [n_layers, B, L_cap, d_c + d_rope] N(0,1) (the latent after its RMS norm,
+    then the rotary key), and the up-projections w_uk [n_layers, H, d_nope,
+    d_c], w_uv [n_layers, H, d_v, d_c] N(0, 1/d_c); all bf16."""
+    device = torch.device(device)
+    x = generate(w, seed=seed, device=device, with_kv=False)
+    del x["q"]
+    rng_layers = layers if layers is not None else range(w.n_layers)
+    nl = len(rng_layers)
+    dk = w.d_c + w.d_rope
+    sd = 1.0 / float(np.sqrt(w.d_c))
+    q = torch.empty((nl, w.B, w.H_q, w.d_nope + w.d_rope), dtype=torch.bfloat16, device=device)
+    ckv = torch.empty((nl, w.B, w.L_cap, dk), dtype=torch.bfloat16, device=device)
+    w_uk = torch.empty((nl, w.H_q, w.d_nope, w.d_c), dtype=torch.bfloat16, device=device)
+    w_uv = torch.empty((nl, w.H_q, w.d_v, w.d_c), dtype=torch.bfloat16, device=device)
+    for i, layer in enumerate(rng_layers):
+        q[i] = torch.randn(q.shape[1:], generator=_gen(device, seed, f"mla.q.{layer}"),
+                           device=device, dtype=torch.float32).to(torch.bfloat16)
+        for b in range(w.B):
+            ckv[i, b] = torch.randn((w.L_cap, dk), generator=_gen(device, seed, f"mla.ckv.{layer}.{b}"),
+                                    device=device, dtype=torch.float32).to(torch.bfloat16)
+        w_uk[i] = (torch.randn(w_uk.shape[1:], generator=_gen(device, seed, f"mla.w_uk.{layer}"),
+                               device=device, dtype=torch.float32) * sd).to(torch.bfloat16)
+        w_uv[i] = (torch.randn(w_uv.shape[1:], generator=_gen(device, seed, f"mla.w_uv.{layer}"),
+                               device=device, dtype=torch.float32) * sd).to(torch.bfloat16)
+    x.update({"q_mla": q, "ckv": ckv, "w_uk": w_uk, "w_uv": w_uv})
+    return x
+
+
+def mla_attn_bytes(w: Workload, seq_lens, ks) -> int:
+    """Bytes an MLA sparse attention must move: every selected latent row of
+    every layer, the queries and up-projection weights of every layer, and
+    the fp32 outputs."""
+    kb = sum(min(int(k), int(L)) for k, L in zip(ks, seq_lens))
+    dk = w.d_c + w.d_rope
+    per_layer = (kb * dk * 2 + w.B * w.H_q * (w.d_nope + w.d_rope) * 2
+                 + w.H_q * (w.d_nope + w.d_v) * w.d_c * 2 + w.B * w.H_q * w.d_v * 4)
+    return w.n_layers * per_layer
+
+
+def mla_bytes(w: Workload, seq_lens, ks) -> int:
+    """Bytes of an MLA decode step: the retrieval head's K_r rows and q_r,
+    then the MLA sparse attention."""
+    kr = sum(int(L) for L in seq_lens) * w.H_r * w.d_r * 2 + w.B * w.H_r * w.d_r * 2
+    return kr + mla_attn_bytes(w, seq_lens, ks)
 
 
 def algorithmic_bytes(w: Workload, seq_lens, ks, delta_rows: int = 0) -> int:
