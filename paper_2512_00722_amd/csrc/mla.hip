@@ -18,8 +18,8 @@
 //     (already bf16) and the scale is applied to the fp32 logits.
 //  2. mla_attn_kernel: one workgroup per CU, four wavefronts; a work unit is
 //     (layer, sequence, split of the selection, group of 64 heads).  Per
-//     32-token chunk the workgroup copies the selected latent rows into LDS
-//     once (double buffered: the next chunk's rows are in flight during this
+//     32-token chunk the selected latent rows go from HBM straight into LDS
+//     (no registers; three stages, so two chunks stream in during this
 //     chunk's math), and every wavefront -- 16 heads -- runs
 //       S^T = C Q~^T  on v_mfma_f32_16x16x32_bf16 (A = 16 latent rows from
 //                     LDS, B = q~ of 16 heads, resident in registers: two
@@ -52,16 +52,14 @@ constexpr int kDVo = 128;            // per-head value width
 constexpr int kMWaves = 4;           // wavefronts per workgroup
 constexpr int kMThreads = 64 * kMWaves;
 constexpr int kMChunk = 32;          // selected tokens per inner step
-constexpr int kCPitch = kDK + 80;    // LDS row pitch (elements): rows start 32 B apart mod 256 B
 constexpr int kQSteps = kDK / 32;    // k-steps of S^T = C Q~^T
 constexpr int kLSteps = kDC / 32;    // k-steps on the latent part (high + low)
 constexpr int kQT = 2 * kDC + kDR;   // absorbed query row: high, low, rotary
 constexpr int kVBlocks = kDC / 16;   // 16-dim blocks of O^T
-constexpr int kRowU4 = kDK / 8;      // 16-byte pieces per latent row
-constexpr int kChunkU4 = kMChunk * kRowU4 / kMThreads;  // per thread and chunk
 constexpr int kMMaxSplit = 2048;     // longest split (tokens per work unit)
 constexpr int kMMinSplit = 256;
 constexpr int kMMaxSplitCount = 16;  // splits per (layer, sequence); the merge holds 16 weights
+constexpr float kLazy = 8.f;         // log2 headroom of the lazy softmax reference
 
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
@@ -126,9 +124,12 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const uint16_t* p) {
 // ---------------------------------------------------------------------------
 // 1. q~ = [W_UK[h]^T q_nope (high, low) ; q_rope]
 // ---------------------------------------------------------------------------
-// One wavefront per (layer, head); lane l owns latent dims 8l..8l+7 and
-// walks the d_nope rows of W_UK[h] (one 1 KiB row per load instruction),
-// for up to TB sequences at a time.
+// One wavefront per (layer, head): lane l owns latent dims 8l..8l+7 and walks
+// the d_nope rows of W_UK[h] in batches of 16 (one 1 KiB row per load
+// instruction); the first batch is requested before the queries are staged.
+// Up to TB sequences per pass.
+constexpr int kAbsBatch = 16;
+
 template <int TB>
 __global__ __launch_bounds__(64) void mla_absorb_kernel(MlaArgs a) {
   __shared__ float qs[TB][kDN];
@@ -137,13 +138,22 @@ __global__ __launch_bounds__(64) void mla_absorb_kernel(MlaArgs a) {
   const int h = blockIdx.x - layer * a.H;
   const uint16_t* w = a.w_uk + ((size_t)layer * a.H + h) * kDN * kDC + 8 * lane;
   for (int b0 = 0; b0 < a.B; b0 += TB) {
+    uint4 wa[kAbsBatch];
+    auto load = [&](uint4 (&wr)[kAbsBatch], int bt) {
+#pragma unroll
+      for (int i = 0; i < kAbsBatch; ++i)
+        wr[i] = ldg16_stream(w + (size_t)(bt * kAbsBatch + i) * kDC);
+    };
+    load(wa, 0);
     __syncthreads();
-    // this head's no-position queries of sequences b0 .. b0+TB-1
-    for (int e = lane; e < TB * kDN; e += 64) {
-      const int t = e / kDN, n = e - t * kDN;
+    // this head's no-position queries of sequences b0 .. b0+TB-1, 16 bytes a load
+    for (int e = lane; e < TB * (kDN / 8); e += 64) {
+      const int t = e / (kDN / 8), n8 = e - t * (kDN / 8);
       const int b = min(b0 + t, a.B - 1);
-      const uint16_t v = a.q[(((size_t)layer * a.B + b) * a.H + h) * (kDN + kDR) + n];
-      qs[t][n] = __uint_as_float((uint32_t)v << 16);
+      float f[8];
+      unpack8(ldg16(a.q + (((size_t)layer * a.B + b) * a.H + h) * (kDN + kDR) + 8 * n8), f);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) qs[t][8 * n8 + j] = f[j];
     }
     __syncthreads();
     float acc[TB][8];
@@ -151,17 +161,18 @@ __global__ __launch_bounds__(64) void mla_absorb_kernel(MlaArgs a) {
     for (int t = 0; t < TB; ++t)
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[t][j] = 0.f;
-    for (int n0 = 0; n0 < kDN; n0 += 16) {
-      uint4 wr[16];
+    // one batch of rows in flight at a time (the first requested before the
+    // queries were staged); several wavefronts per SIMD overlap the batches
+#pragma unroll 1
+    for (int bt = 0; bt < kDN / kAbsBatch; ++bt) {
+      if (bt > 0) load(wa, bt);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) wr[i] = ldg16(w + (size_t)(n0 + i) * kDC);
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
+      for (int i = 0; i < kAbsBatch; ++i) {
         float wf[8];
-        unpack8(wr[i], wf);
+        unpack8(wa[i], wf);
 #pragma unroll
         for (int t = 0; t < TB; ++t) {
-          const float qv = qs[t][n0 + i];
+          const float qv = qs[t][bt * kAbsBatch + i];
 #pragma unroll
           for (int j = 0; j < 8; ++j) acc[t][j] = fmaf(qv, wf[j], acc[t][j]);
         }
@@ -187,12 +198,35 @@ __global__ __launch_bounds__(64) void mla_absorb_kernel(MlaArgs a) {
 // ---------------------------------------------------------------------------
 // 2. latent attention over the selected rows
 // ---------------------------------------------------------------------------
+// LDS stage of 32 selected tokens, filled straight from HBM by
+// global_load_lds_dwordx4 (lane l of an instruction lands at base + 16 l):
+//  * latent region: one instruction per token (its 512 latent dims, 1 KiB),
+//    rows 1056 bytes apart (32 bytes apart modulo 256: the transposed reads
+//    of four rows and the row reads of sixteen spread over the banks);
+//  * rotary region: one instruction per 8 tokens (8 x 128 bytes, packed);
+//    16-byte piece p of token m sits in slot p ^ (m & 7) of its row.
+// Four stages rotate: chunk c is read while chunks c+1 .. c+3 stream in (one
+// CU keeps ~100 KiB in flight; with fewer it cannot stream fast enough).
+constexpr int kLPitch = kDC + 16;                   // latent row pitch (elements)
+constexpr int kStageLat = kMChunk * kLPitch;        // elements
+constexpr int kStage = kStageLat + kMChunk * kDR;   // elements
+constexpr int kStages = 4;
+constexpr int kAhead = kStages - 1;  // chunks requested ahead of the one being read
+constexpr int kLoadsPerChunk = kMChunk / kMWaves + 1;  // per wavefront: 8 rows + 1 rotary group
+static_assert(kMChunk == 8 * kMWaves, "one rotary group of 8 tokens per wavefront");
+
+// s_waitcnt immediates (gfx9 encoding: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8],
+// vmcnt[5:4] in bits [15:14]): wait for the vector-memory count only.
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
 // HT: 16-head tiles per wavefront.
 template <int HT>
 __global__ __launch_bounds__(kMThreads) __attribute__((amdgpu_waves_per_eu(1)))
 void mla_attn_kernel(MlaArgs a) {
-  __shared__ __align__(16) uint16_t cbuf[2][kMChunk * kCPitch];
-  __shared__ int rows[kMMaxSplit + 2 * kMChunk];
+  __shared__ __align__(16) uint16_t cbuf[kStages * kStage];
+  __shared__ int rows[kMMaxSplit + kStages * kMChunk];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -212,9 +246,11 @@ void mla_attn_kernel(MlaArgs a) {
     const int count = clampi(a.counts[b], 0, a.k_max);
     const int j0 = split * a.split_tokens;
     const int n_tok = max(0, min(a.split_tokens, count - j0));
-    const int n_pad = (n_tok + kMChunk - 1) / kMChunk * kMChunk + kMChunk;
+    // rows of the selection, then padding (row 0) for the chunks the
+    // pipeline requests past the end
+    const int n_pad = (n_tok + kMChunk - 1) / kMChunk * kMChunk + kAhead * kMChunk;
 
-    __syncthreads();  // the previous unit is done with rows and cbuf
+    __syncthreads();  // the previous unit is done with rows and every stage
     for (int j = tid; j < n_pad; j += kMThreads)
       rows[j] = j < n_tok ? clampi(a.idx[(size_t)b * a.k_max + j0 + j], 0, a.L_cap - 1) : 0;
 
@@ -236,22 +272,22 @@ void mla_attn_kernel(MlaArgs a) {
     __syncthreads();  // rows staged
 
     const uint16_t* cb = a.ckv + (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b;
-    uint4 cr[kChunkU4];
-    auto load_chunk = [&](int c) {
+    // This wavefront's share of chunk cc: latent rows 8 wave .. 8 wave + 7
+    // and the rotary group of the same rows.
+    auto issue = [&](int cc, int st) {
+      uint16_t* base = cbuf + st * kStage;
 #pragma unroll
-      for (int r = 0; r < kChunkU4; ++r) {
-        const int e = tid + kMThreads * r;
-        const int row = e / kRowU4, col = e - (e / kRowU4) * kRowU4;
-        cr[r] = ldg16_stream(cb + (int64_t)rows[c + row] * kDK + 8 * col);
+      for (int r = 0; r < kMChunk / kMWaves; ++r) {
+        const int row = (kMChunk / kMWaves) * wave + r;
+        const uint16_t* g = cb + (int64_t)rows[cc + row] * kDK + 8 * lane;
+        __builtin_amdgcn_global_load_lds((const void*)g, (lds_ptr_t)(base + row * kLPitch), 16, 0,
+                                         0);
       }
-    };
-    auto store_chunk = [&](int buf) {
-#pragma unroll
-      for (int r = 0; r < kChunkU4; ++r) {
-        const int e = tid + kMThreads * r;
-        const int row = e / kRowU4, col = e - (e / kRowU4) * kRowU4;
-        *reinterpret_cast<uint4*>(cbuf[buf] + row * kCPitch + 8 * col) = cr[r];
-      }
+      const int m = 8 * wave + (lane >> 3);
+      const int piece = (lane & 7) ^ (m & 7);
+      const uint16_t* g = cb + (int64_t)rows[cc + m] * kDK + kDC + 8 * piece;
+      __builtin_amdgcn_global_load_lds((const void*)g,
+                                       (lds_ptr_t)(base + kStageLat + 8 * kDR * wave), 16, 0, 0);
     };
 
     float m_run[HT], l_run[HT];
@@ -265,15 +301,19 @@ void mla_attn_kernel(MlaArgs a) {
     }
 
     if (n_tok > 0) {
-      load_chunk(0);
-      store_chunk(0);
-      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < kAhead; ++i) issue(i * kMChunk, i);
     }
     for (int c = 0; c < n_tok; c += kMChunk) {
-      const int buf = (c / kMChunk) & 1;
-      const bool more = c + kMChunk < n_tok;
-      if (more) load_chunk(c + kMChunk);  // in flight through this chunk's math
-      const uint16_t* C = cbuf[buf];
+      const int ci = c / kMChunk;
+      // this wavefront's loads of chunk c are done (those of the later
+      // chunks may not be), then every wavefront's: the stage is complete,
+      // and the stage of chunk c-1 is free for chunk c+kAhead
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm((kAhead - 1) * kLoadsPerChunk));
+      __syncthreads();
+      issue(c + kAhead * kMChunk, (ci + kAhead) % kStages);
+      const uint16_t* C = cbuf + (ci % kStages) * kStage;
+      const uint16_t* R = C + kStageLat;
 
       // S^T tiles: lane holds S[head r16][token 16t + 4kg + i].
       floatx4 sacc[HT][2];
@@ -282,77 +322,121 @@ void mla_attn_kernel(MlaArgs a) {
         sacc[ht][0] = floatx4{0.f, 0.f, 0.f, 0.f};
         sacc[ht][1] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
-#pragma unroll
-      for (int s = 0; s < kQSteps; ++s) {
+      // One k-step ahead: the A operands of step s+1 are read from LDS while
+      // the MFMAs of step s run (the scheduling barriers keep the compiler
+      // from hoisting every read, which would need ~150 more registers).
+      auto read_a = [&](int s, uint4 (&ca)[2]) {
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          const uint4 ca =
-              *reinterpret_cast<const uint4*>(C + (16 * t + r16) * kCPitch + 32 * s + 8 * kg);
+          const int m = 16 * t + r16;
+          ca[t] = s < kLSteps
+                      ? *reinterpret_cast<const uint4*>(C + m * kLPitch + 32 * s + 8 * kg)
+                      : *reinterpret_cast<const uint4*>(
+                            R + m * kDR + 8 * ((4 * (s - kLSteps) + kg) ^ (m & 7)));
+        }
+      };
+      constexpr int kQA = 3;  // A-operand buffers: reads run two k-steps ahead
+      uint4 ca[kQA][2];
+      read_a(0, ca[0]);
+      read_a(1, ca[1]);
+#pragma unroll
+      for (int s = 0; s < kQSteps; ++s) {
+        if (s + 2 < kQSteps) read_a(s + 2, ca[(s + 2) % kQA]);
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
 #pragma unroll
           for (int ht = 0; ht < HT; ++ht) {
             sacc[ht][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8, ca), __builtin_bit_cast(bf16x8, qh[ht][s]),
+                __builtin_bit_cast(bf16x8, ca[s % kQA][t]), __builtin_bit_cast(bf16x8, qh[ht][s]),
                 sacc[ht][t], 0, 0, 0);
             if (s < kLSteps)
               sacc[ht][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                  __builtin_bit_cast(bf16x8, ca), __builtin_bit_cast(bf16x8, ql[ht][s]),
-                  sacc[ht][t], 0, 0, 0);
+                  __builtin_bit_cast(bf16x8, ca[s % kQA][t]),
+                  __builtin_bit_cast(bf16x8, ql[ht][s]), sacc[ht][t], 0, 0, 0);
           }
         }
+        __builtin_amdgcn_sched_barrier(0);
       }
 
-      // Online softmax per head (log2 units).
-      uint4 phi[HT], plo[HT];
+      // Online softmax per head (log2 units) with a lazy reference: the
+      // weights are 2^(s - m_ref); m_ref moves (and the accumulators are
+      // rescaled) only when a chunk's maximum passes it by more than
+      // kLazy, so weights stay below 2^kLazy and the accumulators are not
+      // touched by the vector ALU on most chunks.
+      float sv[HT][8];
+      bool grow = false;
 #pragma unroll
       for (int ht = 0; ht < HT; ++ht) {
-        float sv[8];
         float mx = -INFINITY;
 #pragma unroll
         for (int t = 0; t < 2; ++t)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const bool valid = c + 16 * t + 4 * kg + i < n_tok;
-            sv[4 * t + i] = valid ? sacc[ht][t][i] * a.scale_log2 : -INFINITY;
-            mx = fmaxf(mx, sv[4 * t + i]);
+            sv[ht][4 * t + i] = valid ? sacc[ht][t][i] * a.scale_log2 : -INFINITY;
+            mx = fmaxf(mx, sv[ht][4 * t + i]);
           }
         mx = xg_max(mx);
-        const float mn = fmaxf(m_run[ht], mx);
-        const float alpha = exp2f(m_run[ht] - mn);
+        grow |= mx > m_run[ht] + kLazy;
+        sacc[ht][0][0] = mx;  // reuse: the chunk maximum of this lane's head
+      }
+      if (__builtin_amdgcn_ballot_w64(grow) != 0) {  // rare after the first chunk
+#pragma unroll
+        for (int ht = 0; ht < HT; ++ht) {
+          const float mx = sacc[ht][0][0];
+          if (mx > m_run[ht] + kLazy) {
+            const float alpha = exp2f(m_run[ht] - mx);  // 0 on the first chunk
+            l_run[ht] *= alpha;
+            m_run[ht] = mx;
+#pragma unroll
+            for (int db = 0; db < kVBlocks; ++db) acc[ht][db] *= alpha;
+          }
+        }
+      }
+      uint4 phi[HT], plo[HT];
+#pragma unroll
+      for (int ht = 0; ht < HT; ++ht) {
         float ls = 0.f;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          sv[j] = exp2f(sv[j] - mn);
-          ls += sv[j];
+          sv[ht][j] = exp2f(sv[ht][j] - m_run[ht]);
+          ls += sv[ht][j];
         }
-        l_run[ht] = l_run[ht] * alpha + ls;
-        m_run[ht] = mn;
-#pragma unroll
-        for (int db = 0; db < kVBlocks; ++db) acc[ht][db] *= alpha;
+        l_run[ht] += ls;
         // k-slots 8kg..8kg+7 of the 32-token block are tokens 4kg..4kg+3 of
         // the first tile and of the second: exactly the S^T entries held here.
-        split8(sv, phi[ht], plo[ht]);
+        split8(sv[ht], phi[ht], plo[ht]);
       }
 
-      // O^T += C^T P^T: the latent columns (dims 0..511 of the row) read
-      // transposed from LDS in the same token order as the P slots.
-      const uint16_t* r0 = C + (4 * kg + (r16 >> 2)) * kCPitch + 4 * (r16 & 3);
-      const uint16_t* r1 = r0 + 16 * kCPitch;
-#pragma unroll
-      for (int db = 0; db < kVBlocks; ++db) {
+      // O^T += C^T P^T: the latent columns read transposed from LDS in the
+      // same token order as the P slots.
+      const uint16_t* r0 = C + (4 * kg + (r16 >> 2)) * kLPitch + 4 * (r16 & 3);
+      const uint16_t* r1 = r0 + 16 * kLPitch;
+      constexpr int kVA = 4;  // reads run three dim blocks ahead
+      bf16x8 vA[kVA];
+      auto read_v = [&](int db) {
         const bf16x4 va = lds_read_tr(r0 + 16 * db);
         const bf16x4 vb = lds_read_tr(r1 + 16 * db);
-        const bf16x8 vA = __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7);
+        return __builtin_shufflevector(va, vb, 0, 1, 2, 3, 4, 5, 6, 7);
+      };
+#pragma unroll
+      for (int i = 0; i < kVA - 1; ++i) vA[i] = read_v(i);
+#pragma unroll
+      for (int db = 0; db < kVBlocks; ++db) {
+        if (db + kVA - 1 < kVBlocks) vA[(db + kVA - 1) % kVA] = read_v(db + kVA - 1);
 #pragma unroll
         for (int ht = 0; ht < HT; ++ht) {
           acc[ht][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              vA, __builtin_bit_cast(bf16x8, phi[ht]), acc[ht][db], 0, 0, 0);
+              vA[db % kVA], __builtin_bit_cast(bf16x8, phi[ht]), acc[ht][db], 0, 0, 0);
           acc[ht][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              vA, __builtin_bit_cast(bf16x8, plo[ht]), acc[ht][db], 0, 0, 0);
+              vA[db % kVA], __builtin_bit_cast(bf16x8, plo[ht]), acc[ht][db], 0, 0, 0);
         }
+        __builtin_amdgcn_sched_barrier(0);
       }
-      if (more) store_chunk(buf ^ 1);  // the other buffer was released by the last barrier
-      __syncthreads();
     }
+    // the padding chunks requested past the end land before the stages are
+    // reused
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
 
     // Partial results of this unit: (max, sum) per head and the unnormalised
     // latent accumulator.
@@ -393,6 +477,15 @@ __global__ __launch_bounds__(kMThreads) void mla_out_kernel(MlaArgs a) {
   const int h = blockIdx.x - layer * a.H;
   const uint16_t* w = a.w_uv + ((size_t)layer * a.H + h) * kDVo * kDC;
 
+  // this wavefront's rows of W_UV[h] (v-tiles 2w, 2w+1), requested first so
+  // that they stream in while the latent outputs are merged
+  uint4 wr[2][kDC / 32];
+#pragma unroll
+  for (int vt = 0; vt < 2; ++vt) {
+    const uint16_t* wp = w + (size_t)(32 * wave + 16 * vt + r16) * kDC + 8 * kg;
+#pragma unroll
+    for (int s = 0; s < kDC / 32; ++s) wr[vt][s] = ldg16_stream(wp + 32 * s);
+  }
   for (int b0 = 0; b0 < a.B; b0 += 16) {
     __syncthreads();
     // split weights w_s = 2^(m_s - M) / sum_s' 2^(m_s' - M) l_s' per sequence
@@ -443,13 +536,6 @@ __global__ __launch_bounds__(kMThreads) void mla_out_kernel(MlaArgs a) {
 
     // out^T[v][b] = W_UV[h][v][:] . o~[b][:]: wavefront w owns v-tiles 2w, 2w+1.
     floatx4 acc[2];
-    uint4 wr[2][kDC / 32];
-#pragma unroll
-    for (int vt = 0; vt < 2; ++vt) {
-      const uint16_t* wp = w + (size_t)(32 * wave + 16 * vt + r16) * kDC + 8 * kg;
-#pragma unroll
-      for (int s = 0; s < kDC / 32; ++s) wr[vt][s] = ldg16_stream(wp + 32 * s);
-    }
 #pragma unroll
     for (int vt = 0; vt < 2; ++vt) acc[vt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -563,12 +649,13 @@ hipError_t launch_mla(const MlaDims& d, const uint16_t* q, const uint16_t* ckv,
   const int grid_lh = d.n_layers * d.H;
   // a multiple of 16 keeps the two head groups of a unit on one XCD
   const int grid = p.n_items < n_cu ? p.n_items : (n_cu / 16 > 0 ? n_cu / 16 * 16 : n_cu);
+  const dim3 abs_block(64);
   if (d.B == 1)
-    hipLaunchKernelGGL((mla_absorb_kernel<1>), dim3(grid_lh), dim3(64), 0, s, a);
+    hipLaunchKernelGGL((mla_absorb_kernel<1>), dim3(grid_lh), abs_block, 0, s, a);
   else if (d.B <= 4)
-    hipLaunchKernelGGL((mla_absorb_kernel<4>), dim3(grid_lh), dim3(64), 0, s, a);
+    hipLaunchKernelGGL((mla_absorb_kernel<4>), dim3(grid_lh), abs_block, 0, s, a);
   else
-    hipLaunchKernelGGL((mla_absorb_kernel<8>), dim3(grid_lh), dim3(64), 0, s, a);
+    hipLaunchKernelGGL((mla_absorb_kernel<8>), dim3(grid_lh), abs_block, 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((mla_attn_kernel<1>), dim3(grid), dim3(kMThreads), 0, s, a);
