@@ -32,6 +32,8 @@ ATTN_SOURCES = ("attn.hip", "device_common.h", "internal.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
 FRONT_SOURCES = ("frontend.hip", "device_common.h", "internal.h")
 FRONT_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "frontend_traffic.json")
+MLA_SOURCES = ("mla.hip", "device_common.h", "internal.h")
+MLA_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "mla_traffic.json")
 
 
 def parse():
@@ -182,13 +184,23 @@ def main():
     name = args.workload or BENCH_WORKLOAD
     w = WORKLOADS[name]
     t_gen = time.perf_counter()
-    x = generate(w, seed=args.seed, device=dev, with_kv=not args.frontend)
+    if w.mla and not args.frontend:
+        from workloads import generate_mla
+        x = generate_mla(w, seed=args.seed, device=dev)
+    else:
+        x = generate(w, seed=args.seed, device=dev, with_kv=not args.frontend and not w.mla)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
     print(f"[bench] workload {name} generated in {t_gen:.1f}s", file=sys.stderr, flush=True)
 
     if args.frontend:
         print(json.dumps(run_frontend(args, spec, w, x)), flush=True)
+        return
+    if w.mla:
+        if args.head_level:
+            print("bench.py: the MLA workload keeps one token set per sequence", file=sys.stderr)
+            sys.exit(2)
+        print(json.dumps(run_mla(args, spec, w, x)), flush=True)
         return
     if w.steps > 1 and args.head_level:
         print("bench.py: elastic loading keeps one token set per sequence; --head-level does "
@@ -506,6 +518,142 @@ def run_frontend(args, spec, w, x):
     if args.copy_calibration:
         copy_calibration(dev)
     return line
+
+
+def run_mla(args, spec, w, x):
+    """A decode step of an MLA model: retrieval scores, top-k, then the MLA
+    sparse attention of every layer over the selected latent rows.  Timed
+    over --steps eager steps between two device synchronisations (HIP
+    events on the launch stream); the roofline is that of the MLA entry
+    point (absorption, latent attention, output projection) with its
+    algorithmic bytes: selected latent rows, queries, up-projection weights
+    and outputs of every layer."""
+    import numpy as np
+    import torch
+    from workloads import mla_attn_bytes, mla_bytes
+
+    dev = x["K_r"].device
+    dims_s = _dims_of_retrieval(spec, w, x)
+    scores = torch.empty((w.B, w.L_cap), dtype=torch.float32, device=dev)
+    idx = torch.empty((w.B, w.k), dtype=torch.int32, device=dev)
+    counts = torch.empty((w.B,), dtype=torch.int32, device=dev)
+    ws_s = torch.zeros(spec.workspace_size(dims_s, spec.OP_SCORE), dtype=torch.uint8, device=dev)
+    dims_t = spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, H_q=1, H_kv=1)
+    ws_t = torch.zeros(max(16, spec.workspace_size(dims_t, spec.OP_TOPK)), dtype=torch.uint8,
+                       device=dev)
+    dims_m = spec.MlaDims.make(B=w.B, L_cap=w.L_cap, k_max=w.k, n_layers=w.n_layers, H=w.H_q,
+                               ckv_stride_layer=x["ckv"].stride(0),
+                               ckv_stride_b=x["ckv"].stride(1))
+    ws_m = torch.zeros(spec.mla_workspace_size(dims_m), dtype=torch.uint8, device=dev)
+    out = torch.empty((w.n_layers, w.B, w.H_q, w.d_v), dtype=torch.float32, device=dev)
+
+    def mla():
+        spec.mla_sparse_decode_attn(x["q_mla"], x["ckv"], x["w_uk"], x["w_uv"], idx, counts,
+                                    out=out, with_lse=False, ws=ws_m)
+
+    def step():
+        spec.score(x["q_r"], x["K_r"], x["seq_lens"], out=scores, ws=ws_s)
+        spec.topk(scores, x["seq_lens"], x["ks"], w.k, idx=idx, counts=counts, ws=ws_t)
+        mla()
+
+    for _ in range(max(args.warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    print(f"[bench] {args.steps} MLA steps in {wall:.3f}s", file=sys.stderr, flush=True)
+
+    n_it = args.attn_iters
+    mla()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(n_it):
+        mla()
+    e1.record()
+    torch.cuda.synchronize()
+    mla_us = e0.elapsed_time(e1) * 1e3 / n_it
+    seq = x["seq_lens"].cpu().tolist()
+    ks = x["ks"].cpu().tolist()
+    m_bytes = mla_attn_bytes(w, seq, ks)
+    s_bytes = mla_bytes(w, seq, ks)
+    achieved = m_bytes / (mla_us * 1e-6) / 1e9
+    value = args.steps / wall
+    line = {
+        "metric": "decode steps/s of retrieve + top-k + MLA sparse attention (latent cache); "
+                  "achieved HBM GB/s vs peak",
+        "value": round(value, 3), "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "L": w.L, "H_r": w.H_r, "d_r": w.d_r,
+                   "n_layers": w.n_layers, "H": w.H_q, "d_c": w.d_c, "d_rope": w.d_rope,
+                   "d_nope": w.d_nope, "d_v": w.d_v, "k": w.k},
+        "roofline": {
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
+            "traffic": stored_traffic(w.name, MLA_TRAFFIC_FILE, MLA_SOURCES),
+            "kernel": "MLA sparse attention (mla_absorb_kernel + mla_attn_kernel + "
+                      "mla_out_kernel)",
+            "bytes_per_launch": m_bytes, "avg_launch_us": round(mla_us, 2),
+        },
+        "step_hbm_gbps": round(s_bytes * value / 1e9, 1),
+        "step_frac_of_peak": round(s_bytes * value / 1e9 / PEAK_HBM_GBPS, 4),
+        "step_algorithmic_bytes": s_bytes,
+        "step_ms_events": round(ev0.elapsed_time(ev1) / args.steps, 4),
+    }
+    if args.copy_calibration:
+        copy_calibration(dev)
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = mla_cpu_baseline(w, x, idx, counts)
+    return line
+
+
+def mla_cpu_baseline(w, x, idx, counts, budget_s=20.0):
+    """The fp64 oracle on a bounded sample of the MLA step: one sequence's
+    scoring + top-k and its MLA attention over as many (layer) units as fit
+    the budget, scaled to all sequences and layers."""
+    import numpy as np
+    import oracle
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+
+    def f64(t):
+        return t.float().cpu().numpy().astype(np.float64)
+
+    L = int(x["seq_lens"][0])
+    qr, kr = f64(x["q_r"][0]), f64(x["K_r"][0, :L])
+    t0 = time.perf_counter()
+    sel = oracle.topk_indices(oracle.retrieval_scores(qr, kr, L), int(x["ks"][0]))
+    t_score = time.perf_counter() - t0
+    t_attn, done = 0.0, 0
+    for layer in range(w.n_layers):
+        q = f64(x["q_mla"][layer, 0])
+        ckv = f64(x["ckv"][layer, 0])
+        wuk, wuv = f64(x["w_uk"][layer]), f64(x["w_uv"][layer])
+        t0 = time.perf_counter()
+        oracle.mla_sparse_attention(q[:, :w.d_nope], q[:, w.d_nope:], ckv[:, :w.d_c],
+                                    ckv[:, w.d_c:], wuk, wuv, sel)
+        t_attn += time.perf_counter() - t0
+        done += 1
+        if t_score + t_attn > budget_s:
+            break
+    per_step = w.B * (t_score + t_attn * w.n_layers / done)
+    return {"value": 1.0 / per_step, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"fp64 numpy oracle: scoring + top-k and MLA attention (per-head keys "
+                       f"and values raised from the selected latents) of sequence 0 for "
+                       f"{done} of {w.n_layers} layers, scaled to {w.n_layers} layers and "
+                       f"{w.B} sequences; {t_score + t_attn:.1f} s of CPU work")}
 
 
 def _dims_of_retrieval(spec, w, x):
