@@ -249,17 +249,29 @@ def main():
     n_sets = w.H_kv if args.head_level else 1
     sets = (n_sets,) if args.head_level else ()
     scores = torch.empty((w.B,) + sets + (w.L_cap,), dtype=torch.float32, device=dev)
-    # Each op is timed over n_it back-to-back launches between two events on
-    # the launch stream (no host synchronisation inside the window).
+    # Each op is timed over n_it back-to-back launches captured in a HIP
+    # graph and replayed between two events on the launch stream, so that the
+    # figure is the GPU's, not the Python launch path's (the standalone
+    # scoring call takes about as long to launch from Python as to run).
     def timed(fn):
-        fn()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(n_it):
+                fn()
+        graph.replay()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        for _ in range(n_it):
-            fn()
+        graph.replay()
         e1.record()
         torch.cuda.synchronize()
+        del graph
         return e0.elapsed_time(e1) * 1e3 / n_it
 
     dims_hl = _dims_of(spec, w, x, args.head_level)
