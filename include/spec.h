@@ -56,6 +56,15 @@
  *    below spec_workspace_size().  SPEC_ERR_HIP: a launch failed; the HIP
  *    error code is kept (per thread) for spec_last_hip_error().
  *  - Calls are reentrant; concurrent calls must not share a workspace.
+ *  - Debugging: with the environment variable SPEC_DEBUG=1 (read at every
+ *    call) each entry point first copies the device-resident lengths and
+ *    indices it is given to the host and returns SPEC_ERR_INVALID, with
+ *    nothing enqueued, for values the kernels would otherwise clamp:
+ *    seq_lens outside [0, L_max], negative ks, counts outside [0, k_max],
+ *    idx entries below counts outside [0, L_cap), token ids outside the
+ *    vocabulary; after the launch it synchronises the stream and reports an
+ *    asynchronous failure as SPEC_ERR_HIP.  The calls then synchronise and
+ *    cannot be captured in a graph.
  */
 #ifndef SPEC_H_
 #define SPEC_H_

@@ -3,7 +3,10 @@
 // stream.  The library holds no state except a per-thread last HIP error.
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
+
+#include <vector>
 
 #include "../../include/spec.h"
 #include "internal.h"
@@ -104,6 +107,70 @@ spec_status hip_status(hipError_t e) {
 
 hipStream_t as_stream(spec_stream s) { return reinterpret_cast<hipStream_t>(s); }
 
+// ---- SPEC_DEBUG=1 ---------------------------------------------------------
+// Read at every call.  Before a launch, the device-resident lengths and
+// indices are copied to the host (a synchronising copy on the caller's
+// stream) and values the kernels would clamp are reported as
+// SPEC_ERR_INVALID, with nothing enqueued; after the launch the stream is
+// synchronised and an asynchronous failure is reported as SPEC_ERR_HIP.
+// For debugging: the calls then synchronise and cannot be graph-captured.
+bool debug_on() {
+  const char* e = getenv("SPEC_DEBUG");
+  return e && e[0] == '1' && e[1] == 0;
+}
+
+template <class T>
+bool d2h(std::vector<T>& h, const T* p, size_t n, hipStream_t s) {
+  h.resize(n);
+  if (n == 0) return true;
+  if (hipMemcpyAsync(h.data(), p, n * sizeof(T), hipMemcpyDeviceToHost, s) != hipSuccess)
+    return false;
+  return hipStreamSynchronize(s) == hipSuccess;
+}
+
+// seq_lens[b] in [0, L_max]; ks[b] >= 0 (either pointer may be null).
+spec_status debug_lengths(const spec::Dims& d, const int32_t* seq_lens, const int32_t* ks,
+                          hipStream_t s) {
+  std::vector<int32_t> h;
+  if (seq_lens) {
+    if (!d2h(h, seq_lens, d.B, s)) return SPEC_ERR_HIP;
+    for (int32_t v : h)
+      if (v < 0 || v > d.L_max) return SPEC_ERR_INVALID;
+  }
+  if (ks) {
+    if (!d2h(h, ks, d.B, s)) return SPEC_ERR_HIP;
+    for (int32_t v : h)
+      if (v < 0) return SPEC_ERR_INVALID;
+  }
+  return SPEC_OK;
+}
+
+// counts[b] in [0, k_max]; with idx, idx[b][set][j] in [0, limit) for j < counts[b].
+spec_status debug_selection(int B, int k_max, int n_sets, const int32_t* idx,
+                            const int32_t* counts, int limit, hipStream_t s) {
+  std::vector<int32_t> c, ix;
+  if (!d2h(c, counts, (size_t)B, s)) return SPEC_ERR_HIP;
+  for (int32_t v : c)
+    if (v < 0 || v > k_max) return SPEC_ERR_INVALID;
+  if (!idx) return SPEC_OK;
+  if (!d2h(ix, idx, (size_t)B * n_sets * k_max, s)) return SPEC_ERR_HIP;
+  for (int b = 0; b < B; ++b)
+    for (int g = 0; g < n_sets; ++g)
+      for (int j = 0; j < c[b]; ++j) {
+        const int32_t v = ix[((size_t)b * n_sets + g) * k_max + j];
+        if (v < 0 || v >= limit) return SPEC_ERR_INVALID;
+      }
+  return SPEC_OK;
+}
+
+// After a launch: in debug mode wait for the stream and report its status.
+spec_status finish(spec_status st, hipStream_t s) {
+  if (st != SPEC_OK || !debug_on()) return st;
+  hipError_t e = hipStreamSynchronize(s);
+  if (e == hipSuccess) e = hipGetLastError();
+  return hip_status(e);
+}
+
 spec_status check_elastic(const spec::Dims& d, const spec_elastic* el) {
   if (!el || !el->slot_tok || !el->kbuf || !el->vbuf || !el->n_changed) return SPEC_ERR_INVALID;
   // the compact slot buffers hold one token per slot for every KV head
@@ -196,8 +263,12 @@ spec_status spec_mla_sparse_decode_attn(const spec_mla_dims* dm, const uint16_t*
   const size_t need = spec::mla_ws_bytes(d);
   if (!ws || ws_bytes < need) return SPEC_ERR_WORKSPACE;
   if (!aligned16(ws)) return SPEC_ERR_INVALID;
-  return hip_status(spec::launch_mla(d, q, ckv, w_uk, w_uv, idx, counts, out, lse, ws,
-                                     as_stream(stream)));
+  if (debug_on() && (st = debug_selection(d.B, d.k_max, 1, idx, counts, d.L_cap,
+                                          as_stream(stream))) != SPEC_OK)
+    return st;
+  return finish(hip_status(spec::launch_mla(d, q, ckv, w_uk, w_uv, idx, counts, out, lse, ws,
+                                            as_stream(stream))),
+                as_stream(stream));
 }
 
 spec_status spec_workspace_size(const spec_dims* dm, spec_op op, size_t* bytes) {
@@ -220,7 +291,11 @@ spec_status spec_score(const spec_dims* dm, const uint16_t* q_r, const uint16_t*
   if (!aligned16(q_r) || !aligned16(k_r) || !aligned4(seq_lens) || !aligned4(scores))
     return SPEC_ERR_INVALID;
   if ((st = check_ws(d, SPEC_OP_SCORE, ws, ws_bytes)) != SPEC_OK) return st;
-  return hip_status(spec::launch_score(d, q_r, k_r, seq_lens, scores, ws, as_stream(stream)));
+  if (debug_on() && (st = debug_lengths(d, seq_lens, nullptr, as_stream(stream))) != SPEC_OK)
+    return st;
+  return finish(
+      hip_status(spec::launch_score(d, q_r, k_r, seq_lens, scores, ws, as_stream(stream))),
+      as_stream(stream));
 }
 
 spec_status spec_topk(const spec_dims* dm, const float* scores, const int32_t* seq_lens,
@@ -234,8 +309,10 @@ spec_status spec_topk(const spec_dims* dm, const float* scores, const int32_t* s
       (counts && !aligned4(counts)))
     return SPEC_ERR_INVALID;
   if ((st = check_ws(d, SPEC_OP_TOPK, ws, ws_bytes)) != SPEC_OK) return st;
-  return hip_status(
-      spec::launch_topk(d, scores, seq_lens, ks, idx, counts, ws, as_stream(stream)));
+  if (debug_on() && (st = debug_lengths(d, seq_lens, ks, as_stream(stream))) != SPEC_OK) return st;
+  return finish(hip_status(spec::launch_topk(d, scores, seq_lens, ks, idx, counts, ws,
+                                             as_stream(stream))),
+                as_stream(stream));
 }
 
 spec_status spec_gather(const spec_dims* dm, const uint16_t* k_cache, const uint16_t* v_cache,
@@ -248,8 +325,12 @@ spec_status spec_gather(const spec_dims* dm, const uint16_t* k_cache, const uint
   if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(k_sel) || !aligned16(v_sel) ||
       !aligned4(idx) || !aligned4(counts))
     return SPEC_ERR_INVALID;
-  return hip_status(
-      spec::launch_gather(d, k_cache, v_cache, idx, counts, k_sel, v_sel, as_stream(stream)));
+  if (debug_on() && (st = debug_selection(d.B, d.k_max, d.n_sets, idx, counts, d.L_cap,
+                                          as_stream(stream))) != SPEC_OK)
+    return st;
+  return finish(hip_status(spec::launch_gather(d, k_cache, v_cache, idx, counts, k_sel, v_sel,
+                                               as_stream(stream))),
+                as_stream(stream));
 }
 
 spec_status spec_sparse_decode_attn(const spec_dims* dm, const uint16_t* q, const uint16_t* k,
@@ -264,8 +345,12 @@ spec_status spec_sparse_decode_attn(const spec_dims* dm, const uint16_t* q, cons
       !aligned16(out) || (idx && !aligned4(idx)) || (lse && !aligned4(lse)))
     return SPEC_ERR_INVALID;
   if ((st = check_ws(d, SPEC_OP_ATTN, ws, ws_bytes)) != SPEC_OK) return st;
-  return hip_status(
-      spec::launch_attn(d, q, k, v, idx, counts, out, lse, ws, as_stream(stream)));
+  if (debug_on() && (st = debug_selection(d.B, d.k_max, d.n_sets, idx, counts, d.L_cap,
+                                          as_stream(stream))) != SPEC_OK)
+    return st;
+  return finish(hip_status(spec::launch_attn(d, q, k, v, idx, counts, out, lse, ws,
+                                             as_stream(stream))),
+                as_stream(stream));
 }
 
 spec_status spec_delta_gather(const spec_dims* dm, const int32_t* idx_now,
@@ -280,9 +365,13 @@ spec_status spec_delta_gather(const spec_dims* dm, const int32_t* idx_now,
     return SPEC_ERR_INVALID;
   if ((st = check_elastic(d, el)) != SPEC_OK) return st;
   if ((st = check_ws(d, SPEC_OP_DELTA, ws, ws_bytes)) != SPEC_OK) return st;
-  return hip_status(spec::launch_delta(d, idx_now, counts, k_cache, v_cache, el->slot_tok,
-                                       el->kbuf, el->vbuf, el->n_changed, ws,
-                                       as_stream(stream)));
+  if (debug_on() && (st = debug_selection(d.B, d.k_max, 1, idx_now, counts, d.L_cap,
+                                          as_stream(stream))) != SPEC_OK)
+    return st;
+  return finish(hip_status(spec::launch_delta(d, idx_now, counts, k_cache, v_cache,
+                                              el->slot_tok, el->kbuf, el->vbuf, el->n_changed,
+                                              ws, as_stream(stream))),
+                as_stream(stream));
 }
 
 spec_status spec_step(const spec_dims* dm, const uint16_t* q_r, const uint16_t* k_r,
@@ -304,6 +393,7 @@ spec_status spec_step(const spec_dims* dm, const uint16_t* q_r, const uint16_t* 
     return SPEC_ERR_INVALID;
   if (el && (st = check_elastic(d, el)) != SPEC_OK) return st;
   if ((st = check_ws(d, SPEC_OP_STEP, ws, ws_bytes)) != SPEC_OK) return st;
+  if (debug_on() && (st = debug_lengths(d, seq_lens, ks, as_stream(stream))) != SPEC_OK) return st;
 
   char* p = static_cast<char*>(ws);
   float* scores = reinterpret_cast<float*>(p);
@@ -333,7 +423,7 @@ spec_status spec_step(const spec_dims* dm, const uint16_t* q_r, const uint16_t* 
   } else {
     e = spec::launch_attn(d, q, k_cache, v_cache, idx_out, counts_out, out, lse, ws_attn, s);
   }
-  return hip_status(e);
+  return finish(hip_status(e), s);
 }
 
 spec_status spec_retrieval_qk(const spec_dims* dm, const spec_frontend* fe,
@@ -350,8 +440,15 @@ spec_status spec_retrieval_qk(const spec_dims* dm, const spec_frontend* fe,
       !aligned16(w_k) || !aligned16(q_r) || !aligned16(k_r))
     return SPEC_ERR_INVALID;
   if ((st = check_ws(d, SPEC_OP_FRONTEND, ws, ws_bytes)) != SPEC_OK) return st;
-  return hip_status(spec::launch_retrieval_qk(d, f, tokens, pos, emb, w_q, w_k, q_r, k_r, ws,
-                                              as_stream(stream)));
+  if (debug_on()) {  // token ids the kernel would clamp into the table
+    std::vector<int32_t> h;
+    if (!d2h(h, tokens, (size_t)d.B, as_stream(stream))) return SPEC_ERR_HIP;
+    for (int32_t v : h)
+      if (v < 0 || v >= f.vocab) return SPEC_ERR_INVALID;
+  }
+  return finish(hip_status(spec::launch_retrieval_qk(d, f, tokens, pos, emb, w_q, w_k, q_r, k_r,
+                                                     ws, as_stream(stream))),
+                as_stream(stream));
 }
 
 const char* spec_status_string(spec_status s) {
