@@ -206,7 +206,14 @@ __global__ __launch_bounds__(64) void mla_absorb_kernel(MlaArgs a) {
 //  * rotary region: one instruction per 8 tokens (8 x 128 bytes, packed);
 //    16-byte piece p of token m sits in slot p ^ (m & 7) of its row.
 // Four stages rotate: chunk c is read while chunks c+1 .. c+3 stream in (one
-// CU keeps ~100 KiB in flight; with fewer it cannot stream fast enough).
+// CU keeps ~100 KiB in flight).  The global-to-LDS loads are issued from
+// inline assembly: the compiler, which cannot tell that the stage being read
+// is not the one being filled, would otherwise wait for every pending load
+// before each LDS read, serialising the ring.  The kernel does the waiting
+// itself: a chunk is handed over by an explicit vector-memory count wait
+// (loads retire in issue order) and a bare barrier, with compiler-only
+// memory barriers around it (a workgroup fence would also wait for every
+// pending load).  Nothing else in the kernel uses M0.
 constexpr int kLPitch = kDC + 16;                   // latent row pitch (elements)
 constexpr int kStageLat = kMChunk * kLPitch;        // elements
 constexpr int kStage = kStageLat + kMChunk * kDR;   // elements
@@ -219,7 +226,15 @@ static_assert(kMChunk == 8 * kMWaves, "one rotary group of 8 tokens per wavefron
 // vmcnt[5:4] in bits [15:14]): wait for the vector-memory count only.
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
+// Global-to-LDS copy of 16 bytes per lane: lane l's bytes land at LDS
+// address lds + 16 l (M0 holds the wave-uniform base).
+__device__ __forceinline__ void load_to_lds(const void* g, const void* lds) {
+  const uint32_t base = (uint32_t)(uintptr_t)lds;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(base)), "v"(g)
+               : "memory", "m0");
+}
 
 // HT: 16-head tiles per wavefront.
 template <int HT>
@@ -269,6 +284,10 @@ void mla_attn_kernel(MlaArgs a) {
 #pragma unroll
       for (int s = kLSteps; s < kQSteps; ++s) qh[ht][s] = ldg16(qp + kDC + 32 * s);
     }
+    // q~ in registers before the ring starts: the compiler, which does not
+    // count the global-to-LDS loads, would otherwise wait for q~ inside the
+    // chunk loop with counts that also drain the chunks in flight
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();  // rows staged
 
     const uint16_t* cb = a.ckv + (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b;
@@ -280,14 +299,12 @@ void mla_attn_kernel(MlaArgs a) {
       for (int r = 0; r < kMChunk / kMWaves; ++r) {
         const int row = (kMChunk / kMWaves) * wave + r;
         const uint16_t* g = cb + (int64_t)rows[cc + row] * kDK + 8 * lane;
-        __builtin_amdgcn_global_load_lds((const void*)g, (lds_ptr_t)(base + row * kLPitch), 16, 0,
-                                         0);
+        load_to_lds(g, base + row * kLPitch);
       }
       const int m = 8 * wave + (lane >> 3);
       const int piece = (lane & 7) ^ (m & 7);
       const uint16_t* g = cb + (int64_t)rows[cc + m] * kDK + kDC + 8 * piece;
-      __builtin_amdgcn_global_load_lds((const void*)g,
-                                       (lds_ptr_t)(base + kStageLat + 8 * kDR * wave), 16, 0, 0);
+      load_to_lds(g, base + kStageLat + 8 * kDR * wave);
     };
 
     float m_run[HT], l_run[HT];
@@ -310,7 +327,9 @@ void mla_attn_kernel(MlaArgs a) {
       // chunks may not be), then every wavefront's: the stage is complete,
       // and the stage of chunk c-1 is free for chunk c+kAhead
       __builtin_amdgcn_s_waitcnt(waitcnt_vm((kAhead - 1) * kLoadsPerChunk));
-      __syncthreads();
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
       issue(c + kAhead * kMChunk, (ci + kAhead) % kStages);
       const uint16_t* C = cbuf + (ci % kStages) * kStage;
       const uint16_t* R = C + kStageLat;
