@@ -482,10 +482,11 @@ void mla_attn_kernel(MlaArgs a) {
 // ---------------------------------------------------------------------------
 constexpr int kOPitch = kDC + 8;  // LDS pitch of the o~ tiles (elements)
 
-__global__ __launch_bounds__(kMThreads) void mla_out_kernel(MlaArgs a) {
+__global__ __launch_bounds__(kMThreads, 2) void mla_out_kernel(MlaArgs a) {
   __shared__ __align__(16) uint16_t ohi[16 * kOPitch];
   __shared__ __align__(16) uint16_t olo[16 * kOPitch];
   __shared__ float wsp[16][17];  // per sequence: split weights, then the lse
+  __shared__ float2 wml[kMMaxSplitCount][16];  // per split and sequence: (max, sum)
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -505,31 +506,52 @@ __global__ __launch_bounds__(kMThreads) void mla_out_kernel(MlaArgs a) {
 #pragma unroll
     for (int s = 0; s < kDC / 32; ++s) wr[vt][s] = ldg16_stream(wp + 32 * s);
   }
+  constexpr int kItems = 16 * (kDC / 8) / kMThreads;  // (sequence, 8 dims) items per thread
   for (int b0 = 0; b0 < a.B; b0 += 16) {
+    // Everything the merge reads is requested before the first wait: the
+    // first split's partials of this thread's items and one (sequence, split)
+    // pair of (max, sum) per thread.  (Loads retire in order, so a chain of
+    // dependent loads here would queue each link behind the W_UV rows.)
+    float4 x0[kItems][2];
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      const int e = tid + i * kMThreads;
+      const int t = e / (kDC / 8), c8 = e - t * (kDC / 8);
+      const int b = min(b0 + t, a.B - 1);
+      const float* src =
+          a.part_acc + (((size_t)layer * a.B + b) * a.n_split * a.H + h) * kDC + 8 * c8;
+      x0[i][0] = *reinterpret_cast<const float4*>(src);
+      x0[i][1] = *reinterpret_cast<const float4*>(src + 4);
+    }
+    static_assert(kMMaxSplitCount * 16 == kMThreads, "one (split, sequence) pair per thread");
+    const int ms_s = tid >> 4;
+    const int ms_b = min(b0 + (tid & 15), a.B - 1);
+    float2 ml = make_float2(-INFINITY, 0.f);
+    if (ms_s < a.n_split)
+      ml = *reinterpret_cast<const float2*>(
+          a.part_ml + ((((size_t)layer * a.B + ms_b) * a.n_split + ms_s) * a.H + h) * 2);
+    __syncthreads();  // the previous group's o~ tiles and weights are no longer read
+    wml[ms_s][tid & 15] = ml;
     __syncthreads();
     // split weights w_s = 2^(m_s - M) / sum_s' 2^(m_s' - M) l_s' per sequence
-    if (tid < 16) {
-      const int b = b0 + tid;
-      if (b < a.B) {
-        const size_t base = ((size_t)layer * a.B + b) * a.n_split;
-        float M = -INFINITY;
-        for (int s = 0; s < a.n_split; ++s) M = fmaxf(M, a.part_ml[((base + s) * a.H + h) * 2]);
-        float L = 0.f;
-        for (int s = 0; s < a.n_split; ++s) {
-          const size_t pr = ((base + s) * a.H + h) * 2;
-          L += M == -INFINITY ? 0.f : exp2f(a.part_ml[pr] - M) * a.part_ml[pr + 1];
-        }
-        const float inv = L > 0.f ? 1.f / L : 0.f;
-        for (int s = 0; s < a.n_split; ++s) {
-          const float ms = a.part_ml[((base + s) * a.H + h) * 2];
-          wsp[tid][s] = (L > 0.f && ms != -INFINITY) ? exp2f(ms - M) * inv : 0.f;
-        }
-        wsp[tid][16] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
+    if (tid < 16 && b0 + tid < a.B) {
+      float M = -INFINITY;
+      for (int s = 0; s < a.n_split; ++s) M = fmaxf(M, wml[s][tid].x);
+      float L = 0.f;
+      for (int s = 0; s < a.n_split; ++s)
+        L += M == -INFINITY ? 0.f : exp2f(wml[s][tid].x - M) * wml[s][tid].y;
+      const float inv = L > 0.f ? 1.f / L : 0.f;
+      for (int s = 0; s < a.n_split; ++s) {
+        const float ms = wml[s][tid].x;
+        wsp[tid][s] = (L > 0.f && ms != -INFINITY) ? exp2f(ms - M) * inv : 0.f;
       }
+      wsp[tid][16] = L > 0.f ? (M + log2f(L)) * kLn2 : -INFINITY;
     }
     __syncthreads();
     // o~ of sequences b0 .. b0+15 as bf16 high + low parts (zero past B)
-    for (int e = tid; e < 16 * (kDC / 8); e += kMThreads) {
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) {
+      const int e = tid + i * kMThreads;
       const int t = e / (kDC / 8), c8 = e - t * (kDC / 8);
       const int b = b0 + t;
       float v[8];
@@ -539,11 +561,14 @@ __global__ __launch_bounds__(kMThreads) void mla_out_kernel(MlaArgs a) {
         const size_t base = ((size_t)layer * a.B + b) * a.n_split;
         for (int s = 0; s < a.n_split; ++s) {
           const float ws = wsp[t][s];
-          const float* src = a.part_acc + ((base + s) * a.H + h) * kDC + 8 * c8;
-          const float4 x0 = *reinterpret_cast<const float4*>(src);
-          const float4 x1 = *reinterpret_cast<const float4*>(src + 4);
-          v[0] += ws * x0.x; v[1] += ws * x0.y; v[2] += ws * x0.z; v[3] += ws * x0.w;
-          v[4] += ws * x1.x; v[5] += ws * x1.y; v[6] += ws * x1.z; v[7] += ws * x1.w;
+          float4 y0 = x0[i][0], y1 = x0[i][1];
+          if (s > 0) {
+            const float* src = a.part_acc + ((base + s) * a.H + h) * kDC + 8 * c8;
+            y0 = *reinterpret_cast<const float4*>(src);
+            y1 = *reinterpret_cast<const float4*>(src + 4);
+          }
+          v[0] += ws * y0.x; v[1] += ws * y0.y; v[2] += ws * y0.z; v[3] += ws * y0.w;
+          v[4] += ws * y1.x; v[5] += ws * y1.y; v[6] += ws * y1.z; v[7] += ws * y1.w;
         }
       }
       uint4 hi, lo;
