@@ -310,8 +310,9 @@ typedef struct spec_mla_dims {
  *     counts [B] int32 (clamped into [0, k_max]),
  *     out    [n_layers][B][H][d_v] fp32, lse [n_layers][B][H] fp32 (nullable).
  * counts[b] = 0 gives out = 0 and lse = -inf.  fp32 accumulation; the
- * absorbed query is rounded to bf16 for the matrix cores, the softmax weights
- * and the latent output enter them as bf16 high + low pairs.
+ * absorbed query and the latent output enter the matrix cores as bf16 high +
+ * low pairs (~2^-16 relative), the softmax weights as a truncated pair
+ * (2^-14).
  * SPEC_ERR_INVALID: null pointer, non-positive dimension, k_max > L_cap,
  * misaligned pointer (16 bytes for tensors, 4 for idx/counts/lse), a stride
  * below the block it steps over or not a multiple of 8, a negative or

@@ -26,7 +26,8 @@
 //                     MFMAs per k-step on the latent part, high and low),
 //       online softmax in log2 units per head,
 //       O^T += C^T P^T (A = latent columns read transposed from LDS with
-//                     ds_read_b64_tr_b16, B = P as a bf16 high + low pair).
+//                     ds_read_b64_tr_b16, B = P as a bf16 high + low pair,
+//                     both truncated: 2^-14 relative).
 //     It leaves (max, sum, acc) per (unit, head) in the workspace.  A wave
 //     holds q~ of its heads (144 VGPRs) and their latent accumulator (256):
 //     a register file of 512 fits 16 heads, not 32, so 128 heads take two
@@ -95,6 +96,24 @@ __device__ __forceinline__ void split8(const float* p, uint4& hi, uint4& lo) {
     const uint32_t l1 = f2bf_rne(p[2 * j + 1] - __uint_as_float(h1 << 16));
     h[j] = h0 | (h1 << 16);
     l[j] = l0 | (l1 << 16);
+  }
+  hi = make_uint4(h[0], h[1], h[2], h[3]);
+  lo = make_uint4(l[0], l[1], l[2], l[3]);
+}
+
+// 8 values -> bf16 high part (truncated) and bf16 low part (the exact fp32
+// remainder, truncated), packed: the pair holds each value to 2^-14
+// relative, in six instructions per two values where the rounded split
+// takes about twenty.
+__device__ __forceinline__ void split8_trunc(const float* p, uint4& hi, uint4& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t u0 = __float_as_uint(p[2 * j]), u1 = __float_as_uint(p[2 * j + 1]);
+    const float r0 = p[2 * j] - __uint_as_float(u0 & 0xffff0000u);
+    const float r1 = p[2 * j + 1] - __uint_as_float(u1 & 0xffff0000u);
+    h[j] = __builtin_amdgcn_perm(u1, u0, 0x07060302u);  // high halves of u0 (low), u1 (high)
+    l[j] = __builtin_amdgcn_perm(__float_as_uint(r1), __float_as_uint(r0), 0x07060302u);
   }
   hi = make_uint4(h[0], h[1], h[2], h[3]);
   lo = make_uint4(l[0], l[1], l[2], l[3]);
@@ -424,7 +443,7 @@ void mla_attn_kernel(MlaArgs a) {
         l_run[ht] += ls;
         // k-slots 8kg..8kg+7 of the 32-token block are tokens 4kg..4kg+3 of
         // the first tile and of the second: exactly the S^T entries held here.
-        split8(sv[ht], phi[ht], plo[ht]);
+        split8_trunc(sv[ht], phi[ht], plo[ht]);
       }
 
       // O^T += C^T P^T: the latent columns read transposed from LDS in the

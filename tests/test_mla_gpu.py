@@ -5,8 +5,9 @@ form), softmax over the selection, all layers in one call.
 
 Tolerance: max |out - out64| <= 2e-3 and the same on lse, the bound of the
 other attention path.  The absorbed query is rounded to bf16 once for the
-matrix cores (the softmax weights and the latent output enter them as bf16
-high + low pairs, ~2^-16 relative); the test prints the measured error.
+matrix cores (the latent output enters them as a bf16 high + low pair,
+~2^-16 relative, the softmax weights as a truncated pair, 2^-14); the test
+prints the measured error.
 """
 import numpy as np
 import pytest
