@@ -38,13 +38,25 @@ FLAGS = [
 ]
 
 
+# Per-source additions.  mla.hip: MFMA results in VGPRs rather than AGPRs.
+# The MLA attention's latent accumulators are also rescaled by the vector
+# ALU, rarely; held in AGPRs, the compiler copies every one of them into
+# VGPRs on each chunk for that branch and spills the queries.  In VGPRs, the
+# queries (only ever MFMA operands) take the AGPRs instead.
+EXTRA_FLAGS = {"mla.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
+def flags_for(src: str) -> list:
+    return FLAGS + EXTRA_FLAGS.get(os.path.basename(src), [])
+
+
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", src, "-o", obj]
+    cmd = [HIPCC, *flags_for(src), "-x", "hip", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

@@ -29,9 +29,11 @@
 //                     ds_read_b64_tr_b16, B = P as a bf16 high + low pair,
 //                     both truncated: 2^-14 relative).
 //     It leaves (max, sum, acc) per (unit, head) in the workspace.  A wave
-//     holds q~ of its heads (144 VGPRs) and their latent accumulator (256):
-//     a register file of 512 fits 16 heads, not 32, so 128 heads take two
-//     workgroups.  Their work units are numbered 8 apart, which puts them on
+//     holds q~ of its heads (136 registers, in AGPRs: only ever an MFMA
+//     operand) and their latent accumulator (128, in VGPRs: this file is
+//     built with MFMA results in VGPRs, so that the rare rescale of the
+//     accumulators needs no copies): a register file of 512 fits 16 heads,
+//     not 32, so 128 heads take two workgroups.  Their work units are numbered 8 apart, which puts them on
 //     the same XCD (workgroups are dealt to the 8 XCDs in turn) at the same
 //     time: the second reads the latent rows from that XCD's L2.
 //  3. mla_out_kernel: one workgroup per (layer, head) merges the splits of
