@@ -147,34 +147,42 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const uint16_t* p) {
 // ---------------------------------------------------------------------------
 // One wavefront per (layer, head): lane l owns latent dims 8l..8l+7 and walks
 // the d_nope rows of W_UK[h] in batches of 16 (one 1 KiB row per load
-// instruction); the first batch is requested before the queries are staged.
-// Up to TB sequences per pass.
-constexpr int kAbsBatch = 16;
+// instruction), two batches in flight: the next batch is requested before
+// this one is used.  Rows n and n+1 are paired per latent dim with a byte
+// permute and meet the query pair (q[n], q[n+1]) -- the input's own 32-bit
+// words, staged in LDS -- in one v_dot2_f32_bf16 (exact products, fp32
+// sum): 64 dot products and 8 permutes per row pair for 8 sequences, where
+// unpacking and fp32 FMAs took twice as many instructions.  Up to TB
+// sequences per pass.
+constexpr int kAbsBatch = 8;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float dot2_bf16(uint32_t x, uint32_t y, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, x),
+                                         __builtin_bit_cast(bf16x2, y), acc, false);
+}
 
 template <int TB>
 __global__ __launch_bounds__(64) void mla_absorb_kernel(MlaArgs a) {
-  __shared__ float qs[TB][kDN];
+  __shared__ __align__(16) uint32_t qs2[TB][kDN / 2];  // (q[2p], q[2p+1]) as bf16 pairs
   const int lane = threadIdx.x;
   const int layer = blockIdx.x / a.H;
   const int h = blockIdx.x - layer * a.H;
   const uint16_t* w = a.w_uk + ((size_t)layer * a.H + h) * kDN * kDC + 8 * lane;
-  for (int b0 = 0; b0 < a.B; b0 += TB) {
-    uint4 wa[kAbsBatch];
-    auto load = [&](uint4 (&wr)[kAbsBatch], int bt) {
+  auto load = [&](uint4 (&wr)[kAbsBatch], int bt) {
 #pragma unroll
-      for (int i = 0; i < kAbsBatch; ++i)
-        wr[i] = ldg16_stream(w + (size_t)(bt * kAbsBatch + i) * kDC);
-    };
+    for (int i = 0; i < kAbsBatch; ++i) wr[i] = ldg16_stream(w + (size_t)(bt * kAbsBatch + i) * kDC);
+  };
+  for (int b0 = 0; b0 < a.B; b0 += TB) {
+    uint4 wa[kAbsBatch], wb[kAbsBatch];
     load(wa, 0);
-    __syncthreads();
-    // this head's no-position queries of sequences b0 .. b0+TB-1, 16 bytes a load
+    __syncthreads();  // the previous pass is done with qs2
+    // this head's no-position queries of sequences b0 .. b0+TB-1: four pairs a load
     for (int e = lane; e < TB * (kDN / 8); e += 64) {
       const int t = e / (kDN / 8), n8 = e - t * (kDN / 8);
       const int b = min(b0 + t, a.B - 1);
-      float f[8];
-      unpack8(ldg16(a.q + (((size_t)layer * a.B + b) * a.H + h) * (kDN + kDR) + 8 * n8), f);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) qs[t][8 * n8 + j] = f[j];
+      *reinterpret_cast<uint4*>(&qs2[t][4 * n8]) =
+          ldg16(a.q + (((size_t)layer * a.B + b) * a.H + h) * (kDN + kDR) + 8 * n8);
     }
     __syncthreads();
     float acc[TB][8];
@@ -182,22 +190,37 @@ __global__ __launch_bounds__(64) void mla_absorb_kernel(MlaArgs a) {
     for (int t = 0; t < TB; ++t)
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[t][j] = 0.f;
-    // one batch of rows in flight at a time (the first requested before the
-    // queries were staged); several wavefronts per SIMD overlap the batches
-#pragma unroll 1
-    for (int bt = 0; bt < kDN / kAbsBatch; ++bt) {
-      if (bt > 0) load(wa, bt);
+    auto use = [&](const uint4 (&wr)[kAbsBatch], int bt) {
 #pragma unroll
-      for (int i = 0; i < kAbsBatch; ++i) {
-        float wf[8];
-        unpack8(wa[i], wf);
+      for (int i = 0; i < kAbsBatch / 2; ++i) {
+        const uint32_t* x = reinterpret_cast<const uint32_t*>(&wr[2 * i]);      // row n
+        const uint32_t* y = reinterpret_cast<const uint32_t*>(&wr[2 * i + 1]);  // row n+1
+        uint32_t wp[8];  // (W[n][c], W[n+1][c]) for this lane's 8 latent dims
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          wp[2 * j] = __builtin_amdgcn_perm(y[j], x[j], 0x05040100u);
+          wp[2 * j + 1] = __builtin_amdgcn_perm(y[j], x[j], 0x07060302u);
+        }
 #pragma unroll
         for (int t = 0; t < TB; ++t) {
-          const float qv = qs[t][bt * kAbsBatch + i];
+          const uint32_t qp = qs2[t][bt * (kAbsBatch / 2) + i];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) acc[t][j] = fmaf(qv, wf[j], acc[t][j]);
+          for (int c = 0; c < 8; ++c) acc[t][c] = dot2_bf16(wp[c], qp, acc[t][c]);
         }
       }
+    };
+    // the scheduling barriers keep each refill after the last use of its
+    // buffer (hoisted, it would need a second copy of the buffer)
+#pragma unroll 1
+    for (int bt = 0; bt < kDN / kAbsBatch; bt += 2) {
+      load(wb, bt + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      use(wa, bt);
+      __builtin_amdgcn_sched_barrier(0);
+      if (bt + 2 < kDN / kAbsBatch) load(wa, bt + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      use(wb, bt + 1);
+      __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int t = 0; t < TB; ++t) {
