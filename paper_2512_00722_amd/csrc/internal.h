@@ -57,13 +57,16 @@ inline int32_t* score_ws_hist(const Dims& d, void* ws) {
                                     score_part_bytes(d));
 }
 
-// Per-tile lists of the selection (tokens per tile: kTopkTile): counts, the
-// tokens above the threshold bin, and the bin's candidates (key, token).
+// Per-tile lists of the selection (tokens per tile: kTopkTile): the
+// threshold bin of each row, per-tile counts, the tokens above the threshold
+// bin, and the bin's candidates (key, token).
 constexpr int kTopkTile = 2048;
 inline int topk_tiles(const Dims& d) { return (d.L_max + kTopkTile - 1) / kTopkTile; }
 inline size_t topk_lists_bytes(const Dims& d) {
-  const size_t n = (size_t)d.B * d.n_sets * topk_tiles(d);
-  return align_up(sizeof(int32_t) * 2 * n) + 3 * align_up(sizeof(int32_t) * n * kTopkTile);
+  const size_t rows = (size_t)d.B * d.n_sets;
+  const size_t n = rows * topk_tiles(d);
+  return align_up(sizeof(int32_t) * 4 * rows) + align_up(sizeof(int32_t) * 2 * n) +
+         3 * align_up(sizeof(int32_t) * n * kTopkTile);
 }
 inline size_t topk_ws_bytes(const Dims& d) { return topk_hist_bytes(d) + topk_lists_bytes(d); }
 

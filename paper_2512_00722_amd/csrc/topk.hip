@@ -9,15 +9,17 @@
 //
 // Two kernels follow the histogram:
 //  * topk_classify_kernel, one 256-thread workgroup per 2048-token tile,
-//    recomputes b1 from the histogram and appends, in token order, the tile's
-//    tokens of higher bins and its bin-b1 candidates (key, token) to per-tile
-//    lists (wave-ordered appends with ballots, coalesced loads);
-//  * topk_select_kernel, one 1024-thread workgroup per sequence, gathers the
-//    per-tile lists into LDS by prefix sums, resolves the remaining 20 key
-//    bits of T among the candidates only (two 10-bit LDS histogram passes),
-//    which also gives r, the number of keys equal to T to take (the
-//    lowest-index ones), compacts the selected candidates in order and
-//    merges the two ascending lists by binary search.
+//    recomputes b1 from the histogram (tile 0 also hands b1, c1, n1 on) and
+//    appends, in token order, the tile's tokens of higher bins and its
+//    bin-b1 candidates (key, token) to per-tile lists (wave-ordered appends
+//    with ballots, coalesced loads);
+//  * topk_select_kernel, one 1024-thread workgroup per sequence, loads b1
+//    with the per-tile counts, gathers the lists into LDS by prefix sums,
+//    resolves the remaining 20 key bits of T among the candidates only (two
+//    10-bit LDS histogram passes), which also gives r, the number of keys
+//    equal to T to take (the lowest-index ones), compacts the selected
+//    candidates in order and merges the two ascending lists by binary
+//    search.
 //  * When the lists would not fit (more than 8192 tokens above the bin or
 //    12288 candidates) the select kernel falls back to a general path: two
 //    more radix passes over the row (bits 19..8, 7..0) and an ordered
@@ -148,6 +150,7 @@ __device__ __forceinline__ void load_hist(const int32_t* g, int* sh) {
 
 // Per-tile lists written by the classify kernel (workspace).
 struct TileLists {
+  int32_t* sel;     // [B][4]: b1, c1, n1 of the histogram (classify's tile 0 writes them)
   int32_t* cnt;     // [B][n_tiles][2]: tokens above bin b1, candidates in b1
   int32_t* gt;      // [B][n_tiles][kTile]
   uint32_t* ckey;   // [B][n_tiles][kTile]
@@ -166,6 +169,29 @@ struct SelArgs {
   int L_max, k_max, n_sets;  // score rows: B * n_sets, sequence = row / n_sets
 };
 
+// Merge of two ascending lists of distinct values, a (n entries) and b (m),
+// into out[0 .. n+m): thread t writes outputs [t q, t q + q), q = ceil((n+m)
+// / threads).  Its starting split (i from a, d - i from b) is found by one
+// binary search along the diagonal d = t q; the q outputs follow in order.
+__device__ __forceinline__ void merge_path(const int* a, int n, const int* b, int m,
+                                           int32_t* out) {
+  const int total = n + m;
+  const int q = (total + kThreads - 1) / kThreads;
+  int d = threadIdx.x * q;
+  if (d >= total) return;
+  int lo = max(0, d - m), hi = min(d, n);
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (a[mid] < b[d - 1 - mid]) lo = mid + 1; else hi = mid;
+  }
+  int i = lo, j = d - lo;
+  const int end = min(d + q, total);
+  for (; d < end; ++d) {
+    if (j >= m || (i < n && a[i] < b[j])) out[d] = a[i++];
+    else out[d] = b[j++];
+  }
+}
+
 __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
   __shared__ int s_hist[kBins];
   __shared__ int s_gt[kGtCap];
@@ -182,6 +208,7 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
   const float* row = a.scores + (size_t)srow * a.L_max;
   int32_t* out = a.idx + (size_t)srow * a.k_max;
 
+  if (tid == 0) s_sel[0] = s_sel[1] = s_sel[2] = -1;
   if (tid == 0 && a.counts && srow == b * a.n_sets) a.counts[b] = k_b;
   for (int j = k_b + tid; j < a.k_max; j += kThreads) out[j] = -1;
   if (k_b == 0 || k_b == L_b) {  // nothing, or every token, is selected
@@ -189,29 +216,22 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
     return;
   }
 
-  // ---- the bin of the k-th key from the 12-bit histogram
-  const int32_t* gh = a.hist + (size_t)srow * kBins;
+  // ---- the bin b1 of the k-th key (the classify kernel found it in the
+  // 12-bit histogram), loaded with the per-tile list counts: one round trip
   const int n_tiles_b = (L_b + kTile - 1) / kTile;
-  // The per-tile list counts are loaded with the histogram (one round trip);
-  // they are only used on the fast path.
   const int32_t* tcnt = a.tl.cnt + (size_t)srow * a.tl.n_tiles * 2;
   const int tcl = min(tid, a.tl.n_tiles - 1);  // clamped: the load is unconditional
   int tg = tcnt[2 * tcl];
   int tc = tcnt[2 * tcl + 1];
   if (!(tid < n_tiles_b && n_tiles_b <= kMaxTiles)) tg = tc = 0;
-  load_hist<kThreads>(gh, s_hist);
-  if (tid == 0) s_sel[0] = s_sel[1] = s_sel[2] = -1;
-  __syncthreads();
-  find_bin<kThreads>(s_hist, kBins, k_b, s_scan, s_sel);
-  const int b1i = s_sel[0];
-  const int c1 = s_sel[1];  // keys in higher bins: all selected
-  const int n1 = s_sel[2];  // keys in bin b1
-  const int r1 = k_b - c1;  // keys still to take from bin b1 (1 <= r1 <= n1)
+  const int b1i = a.tl.sel[srow * 4];
+  const int c1 = a.tl.sel[srow * 4 + 1];  // keys in higher bins: all selected
+  const int n1 = a.tl.sel[srow * 4 + 2];  // keys in bin b1
+  const int r1 = k_b - c1;                // keys still to take from bin b1 (1 <= r1 <= n1)
   const uint32_t b1 = (uint32_t)b1i;
   // A histogram that does not describe this row (never produced by this
   // library) sends the sequence down the general path from scratch.
-  const bool hist_ok = b1i >= 0 && c1 >= 0 && c1 < k_b && r1 <= n1;
-  __syncthreads();
+  const bool hist_ok = b1i >= 0 && b1i < kBins && c1 >= 0 && c1 < k_b && r1 <= n1;
 
   if (hist_ok && c1 <= kGtCap && n1 <= kCandCap && n_tiles_b <= kMaxTiles) {
     // ---------------- fast path: gather the per-tile lists ----------------
@@ -222,13 +242,34 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
     int* s_off_c = s_hist + kMaxTiles;
     int* s_cnt_g = s_hist + 2 * kMaxTiles;
     int* s_cnt_c = s_hist + 3 * kMaxTiles;
-    int og, oc, sum_g, sum_c;
-    block_scan2<kThreads>(tg, tc, og, oc, sum_g, sum_c, s_scan);
-    if (tid < n_tiles_b) {
-      s_off_g[tid] = og;
-      s_off_c[tid] = oc;
-      s_cnt_g[tid] = tg;
-      s_cnt_c[tid] = tc;
+    if (n_tiles_b <= 64) {  // up to 128K tokens: one wavefront scans the counts
+      if (tid < 64) {
+        int ig = tg, ic = tc;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const int ng = __shfl_up(ig, off);
+          const int nc = __shfl_up(ic, off);
+          if (tid >= off) {
+            ig += ng;
+            ic += nc;
+          }
+        }
+        if (tid < n_tiles_b) {
+          s_off_g[tid] = ig - tg;
+          s_off_c[tid] = ic - tc;
+          s_cnt_g[tid] = tg;
+          s_cnt_c[tid] = tc;
+        }
+      }
+    } else {
+      int og, oc, sum_g, sum_c;
+      block_scan2<kThreads>(tg, tc, og, oc, sum_g, sum_c, s_scan);
+      if (tid < n_tiles_b) {
+        s_off_g[tid] = og;
+        s_off_c[tid] = oc;
+        s_cnt_g[tid] = tg;
+        s_cnt_c[tid] = tc;
+      }
     }
     __syncthreads();
     const int lane = tid & 63;
@@ -258,11 +299,21 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
         const int t = t0 + u * kWaves;
         if (t < n_tiles_b) {
           put(t, lane, gv[u], kv[u], iv[u]);
-          // tiles with more than 64 entries in a list (rare)
+          // tiles with more than 64 entries in a list (the heavy tokens
+          // crowd a few tiles): four rounds of loads in flight at a time
           const int n = max(s_cnt_g[t], s_cnt_c[t]);
-          for (int i = lane + 64; i < n; i += 64) {
-            const size_t q = (size_t)t * kTile + i;
-            put(t, i, tgt[q], tck[q], tci[q]);
+          for (int i0 = 64; i0 < n; i0 += 256) {
+            int gr[4], ir[4];
+            uint32_t kr[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const size_t q = (size_t)t * kTile + min(i0 + 64 * r + lane, kTile - 1);
+              gr[r] = tgt[q];
+              kr[r] = tck[q];
+              ir[r] = tci[q];
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) put(t, i0 + 64 * r + lane, gr[r], kr[r], ir[r]);
           }
         }
       }
@@ -323,24 +374,7 @@ __global__ __launch_bounds__(kThreads) void topk_select_kernel(SelArgs a) {
     __syncthreads();
 
     // ---- merge the two ascending lists (c1 + r1 = k_b entries)
-    for (int i = tid; i < c1; i += kThreads) {
-      const int v = s_gt[i];
-      int lo = 0, hi = r1;  // count of selected candidates below v
-      while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (s_selv[mid] < v) lo = mid + 1; else hi = mid;
-      }
-      out[i + lo] = v;
-    }
-    for (int j = tid; j < r1; j += kThreads) {
-      const int v = s_selv[j];
-      int lo = 0, hi = c1;
-      while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (s_gt[mid] < v) lo = mid + 1; else hi = mid;
-      }
-      out[j + lo] = v;
-    }
+    merge_path(s_gt, c1, s_selv, r1, out);
     return;
   }
 
@@ -450,6 +484,11 @@ __global__ __launch_bounds__(kClsThreads) void topk_classify_kernel(ClsArgs a) {
   __syncthreads();
   find_bin<kClsThreads>(s_hist, kBins, k_b, s_scan, s_sel);
   const int b1i = s_sel[0], c1 = s_sel[1], n1 = s_sel[2];
+  if (tile == 0 && tid == 0) {  // for the select kernel, valid or not
+    a.tl.sel[srow * 4] = b1i;
+    a.tl.sel[srow * 4 + 1] = c1;
+    a.tl.sel[srow * 4 + 2] = n1;
+  }
   // Same decision as the select kernel: it only reads the lists on its fast path.
   if (!(b1i >= 0 && c1 >= 0 && c1 < k_b && k_b - c1 <= n1) || c1 > kGtCap || n1 > kCandCap)
     return;
@@ -540,6 +579,8 @@ TileLists tile_lists(const Dims& d, void* lists) {
   const int n_tiles = topk_tiles(d);
   const size_t n = (size_t)d.B * d.n_sets * n_tiles;
   char* p = static_cast<char*>(lists);
+  tl.sel = reinterpret_cast<int32_t*>(p);
+  p += align_up(sizeof(int32_t) * 4 * (size_t)d.B * d.n_sets);
   tl.cnt = reinterpret_cast<int32_t*>(p);
   p += align_up(sizeof(int32_t) * 2 * n);
   tl.gt = reinterpret_cast<int32_t*>(p);
