@@ -337,18 +337,22 @@ void mla_attn_kernel(MlaArgs a) {
     const uint16_t* cb = a.ckv + (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b;
     // This wavefront's share of chunk cc: latent rows 8 wave .. 8 wave + 7
     // and the rotary group of the same rows.
+    // The row indices are read from LDS before the first load is issued:
+    // each load's memory clobber would otherwise keep the next index read
+    // behind it, one LDS round trip per row.
     auto issue = [&](int cc, int st) {
       uint16_t* base = cbuf + st * kStage;
+      constexpr int kRows = kMChunk / kMWaves;
+      int ri[kRows];
 #pragma unroll
-      for (int r = 0; r < kMChunk / kMWaves; ++r) {
-        const int row = (kMChunk / kMWaves) * wave + r;
-        const uint16_t* g = cb + (int64_t)rows[cc + row] * kDK + 8 * lane;
-        load_to_lds(g, base + row * kLPitch);
-      }
+      for (int r = 0; r < kRows; ++r) ri[r] = rows[cc + kRows * wave + r];
       const int m = 8 * wave + (lane >> 3);
+      const int rm = rows[cc + m];
+#pragma unroll
+      for (int r = 0; r < kRows; ++r)
+        load_to_lds(cb + (int64_t)ri[r] * kDK + 8 * lane, base + (kRows * wave + r) * kLPitch);
       const int piece = (lane & 7) ^ (m & 7);
-      const uint16_t* g = cb + (int64_t)rows[cc + m] * kDK + kDC + 8 * piece;
-      load_to_lds(g, base + kStageLat + 8 * kDR * wave);
+      load_to_lds(cb + (int64_t)rm * kDK + kDC + 8 * piece, base + kStageLat + 8 * kDR * wave);
     };
 
     float m_run[HT], l_run[HT];
