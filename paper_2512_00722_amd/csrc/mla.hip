@@ -389,9 +389,10 @@ void mla_attn_kernel(MlaArgs a) {
         sacc[ht][0] = floatx4{0.f, 0.f, 0.f, 0.f};
         sacc[ht][1] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
-      // One k-step ahead: the A operands of step s+1 are read from LDS while
-      // the MFMAs of step s run (the scheduling barriers keep the compiler
-      // from hoisting every read, which would need ~150 more registers).
+      // Reads run ahead: the A operands of steps s+1 .. s+3 are read from LDS
+      // while the MFMAs of step s run (the scheduling barriers keep the
+      // compiler from hoisting every read, which would need ~150 more
+      // registers).
       auto read_a = [&](int s, uint4 (&ca)[2]) {
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
@@ -402,13 +403,13 @@ void mla_attn_kernel(MlaArgs a) {
                             R + m * kDR + 8 * ((4 * (s - kLSteps) + kg) ^ (m & 7)));
         }
       };
-      constexpr int kQA = 3;  // A-operand buffers: reads run two k-steps ahead
+      constexpr int kQA = 4;  // A-operand buffers: reads run three k-steps ahead
       uint4 ca[kQA][2];
-      read_a(0, ca[0]);
-      read_a(1, ca[1]);
+#pragma unroll
+      for (int i = 0; i < kQA - 1; ++i) read_a(i, ca[i]);
 #pragma unroll
       for (int s = 0; s < kQSteps; ++s) {
-        if (s + 2 < kQSteps) read_a(s + 2, ca[(s + 2) % kQA]);
+        if (s + kQA - 1 < kQSteps) read_a(s + kQA - 1, ca[(s + kQA - 1) % kQA]);
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
 #pragma unroll
@@ -479,7 +480,7 @@ void mla_attn_kernel(MlaArgs a) {
       // same token order as the P slots.
       const uint16_t* r0 = C + (4 * kg + (r16 >> 2)) * kLPitch + 4 * (r16 & 3);
       const uint16_t* r1 = r0 + 16 * kLPitch;
-      constexpr int kVA = 4;  // reads run three dim blocks ahead
+      constexpr int kVA = 6;  // reads run five dim blocks ahead
       bf16x8 vA[kVA];
       auto read_v = [&](int db) {
         const bf16x4 va = lds_read_tr(r0 + 16 * db);
