@@ -467,7 +467,10 @@ void mla_attn_kernel(MlaArgs a) {
         float ls = 0.f;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          sv[ht][j] = exp2f(sv[ht][j] - m_run[ht]);
+          // v_exp_f32 itself: results below 2^-126 flush to zero, which a
+          // softmax weight can afford (exp2f adds a denormal-range fix-up,
+          // four more instructions per weight)
+          sv[ht][j] = __builtin_amdgcn_exp2f(sv[ht][j] - m_run[ht]);
           ls += sv[ht][j];
         }
         l_run[ht] += ls;
