@@ -12,14 +12,15 @@
 // attention with 576-wide keys and 512-wide values).  Three kernels:
 //
 //  1. mla_absorb_kernel: one wavefront per (layer, head) streams W_UK[h]
-//     (d_nope rows of d_c) once for every sequence, forms q~ in fp32 and
-//     stores it as a bf16 high part and a bf16 low part (q~ - high), so that
-//     it reaches the matrix cores to ~2^-17; the rotary part is copied as is
-//     (already bf16) and the scale is applied to the fp32 logits.
+//     (d_nope rows of d_c) once for every sequence, forms q~ with
+//     v_dot2_f32_bf16 (exact products, fp32 sums) and stores it as a bf16
+//     high part and a bf16 low part (q~ - high), so that it reaches the
+//     matrix cores to ~2^-17; the rotary part is copied as is (already bf16)
+//     and the scale is applied to the fp32 logits.
 //  2. mla_attn_kernel: one workgroup per CU, four wavefronts; a work unit is
 //     (layer, sequence, split of the selection, group of 64 heads).  Per
 //     32-token chunk the selected latent rows go from HBM straight into LDS
-//     (no registers; three stages, so two chunks stream in during this
+//     (no registers; four stages, so three chunks stream in during this
 //     chunk's math), and every wavefront -- 16 heads -- runs
 //       S^T = C Q~^T  on v_mfma_f32_16x16x32_bf16 (A = 16 latent rows from
 //                     LDS, B = q~ of 16 heads, resident in registers: two
@@ -33,9 +34,10 @@
 //     operand) and their latent accumulator (128, in VGPRs: this file is
 //     built with MFMA results in VGPRs, so that the rare rescale of the
 //     accumulators needs no copies): a register file of 512 fits 16 heads,
-//     not 32, so 128 heads take two workgroups.  Their work units are numbered 8 apart, which puts them on
-//     the same XCD (workgroups are dealt to the 8 XCDs in turn) at the same
-//     time: the second reads the latent rows from that XCD's L2.
+//     not 32, so 128 heads take two workgroups.  Their work units are
+//     numbered 8 apart, which puts them on the same XCD (workgroups are
+//     dealt to the 8 XCDs in turn) at the same time: the second reads the
+//     latent rows from that XCD's L2.
 //  3. mla_out_kernel: one workgroup per (layer, head) merges the splits of
 //     every sequence into the latent output o~ (log-sum-exp), splits it into
 //     bf16 high + low parts in LDS and applies W_UV[h] on the matrix cores
@@ -209,8 +211,9 @@ __global__ __launch_bounds__(64) void mla_absorb_kernel(MlaArgs a) {
         }
       }
     };
-    // the scheduling barriers keep each refill after the last use of its
-    // buffer (hoisted, it would need a second copy of the buffer)
+    // the scheduling barriers keep the order as written: a batch's loads are
+    // issued before the other batch is used, so that they are in flight
+    // during it, and a refill comes after the last use of its buffer
 #pragma unroll 1
     for (int bt = 0; bt < kDN / kAbsBatch; bt += 2) {
       load(wb, bt + 1);
@@ -271,7 +274,9 @@ static_assert(kMChunk == 8 * kMWaves, "one rotary group of 8 tokens per wavefron
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
 // Global-to-LDS copy of 16 bytes per lane: lane l's bytes land at LDS
-// address lds + 16 l (M0 holds the wave-uniform base).
+// address lds + 16 l (M0 holds the wave-uniform base).  The compiler reserves
+// M0 and warns about the clobber; no instruction it generates in this file
+// uses M0, which tests/test_isa_cpu.py checks on the generated assembly.
 __device__ __forceinline__ void load_to_lds(const void* g, const void* lds) {
   const uint32_t base = (uint32_t)(uintptr_t)lds;
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
