@@ -166,7 +166,7 @@ def cpu_baseline(w, x, res, budget_s=20.0):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+        print(f"bench.py: the library runs on one GPU; --gpus {args.gpus} is not supported "
               "(the decode step would shard by sequence with no exchange; that path is not built)",
               file=sys.stderr)
         sys.exit(2)
