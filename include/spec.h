@@ -49,8 +49,8 @@
  *    a misaligned pointer, a negative or non-finite scale, a stride not a
  *    multiple of 8 elements or smaller than the block it steps over, a
  *    non-zero `reserved`.  SPEC_ERR_UNSUPPORTED:
- *    d != 128, d_r not 64 or 128, H_r > 16, G = H_q/H_kv not in
- *    {1,2,4,8,16}, H_kv > 16, n_sets not 1 or H_kv, n_sets = H_kv with H_r
+ *    d != 128, d_r not 64 or 128, H_r > 16, G = H_q/H_kv not a power of
+ *    two up to 128, H_kv > 16, n_sets not 1 or H_kv, n_sets = H_kv with H_r
  *    not a multiple of H_kv or B*n_sets > 65535, B or n_layers > 65535, and
  *    for elastic loading L_cap > 245760 or n_sets != 1.  SPEC_ERR_WORKSPACE: ws_bytes
  *    below spec_workspace_size().  SPEC_ERR_HIP: a launch failed; the HIP

@@ -83,6 +83,8 @@ struct AttnArgs {
   int64_t stride_layer;   // elements between layers (indexed mode)
   int64_t stride_b;       // elements between sequences (indexed mode)
   int B, H_q, H_kv, G, k_max, L_cap, n_split, split_tokens, n_items;
+  int R;                  // column groups per KV head (1; G/16 for more than 16 query heads)
+                          // G above: query heads per column group (at most 16)
   int mode;               // kDirect or kGlobalPartials
   int n_sets;             // 1: idx [B][k_max]; H_kv: idx [B][H_kv][k_max], one set per KV head
   float scale_log2;       // scale * log2(e)
@@ -144,9 +146,13 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const uint16_t* p) {
 template <bool INDEXED>
 __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, const int lane,
                                              uint16_t* V, int* rows) {
+  // A group of more than 16 query heads is covered by R column groups of
+  // 16 (gv = g R .. g R + R - 1), each a unit of its own that reads KV head
+  // g; the query heads of column group gv are gv G .. gv G + G - 1.
   const int G = a.G;
-  const int g = item % a.H_kv;
-  const int rest = item / a.H_kv;
+  const int gv = item % (a.H_kv * a.R);
+  const int g = gv / a.R;
+  const int rest = item / (a.H_kv * a.R);
   const int split = rest % a.n_split;
   const int lb = rest / a.n_split;  // layer * B + b
   const int b = lb % a.B;
@@ -156,7 +162,7 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
   const int r16e = lane & 15;
   if (j0 >= count) {  // uniform per wavefront
     if (a.mode == kDirect && r16e < G) {  // no tokens: out = 0, lse = -inf
-      const size_t orow = (size_t)lb * a.H_q + (size_t)g * G + r16e;
+      const size_t orow = (size_t)lb * a.H_q + (size_t)gv * G + r16e;
       float* dst = a.out + orow * kD + 4 * (lane >> 4);
 #pragma unroll
       for (int db = 0; db < 8; ++db)
@@ -182,11 +188,11 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
 
   const int r16 = lane & 15;  // head of this lane (MFMA column); token of a K tile row
   const int kg = lane >> 4;   // MFMA k-group; also the token phase of V loads
-  // B operand of S^T = K Q^T: Q^T column r16 = query head g*G + r16 (zero if >= G),
+  // B operand of S^T = K Q^T: Q^T column r16 = query head gv*G + r16 (zero if >= G),
   // dims 32s + 8kg .. +8.  Loaded together with the row indices.
   bf16x8 qf[4];
   {
-    const uint16_t* qp = a.q + ((size_t)lb * a.H_q + g * G + (r16 < G ? r16 : 0)) * kD + 8 * kg;
+    const uint16_t* qp = a.q + ((size_t)lb * a.H_q + gv * G + (r16 < G ? r16 : 0)) * kD + 8 * kg;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       uint4 w = r16 < G ? ldg16(qp + 32 * s) : make_uint4(0, 0, 0, 0);
@@ -333,7 +339,7 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
   l_run = xgroup_sum(l_run);
   if (r16 < G) {
     if (a.mode == kDirect) {  // the whole selection: normalise and write the output
-      const size_t orow = (size_t)lb * a.H_q + (size_t)g * G + r16;
+      const size_t orow = (size_t)lb * a.H_q + (size_t)gv * G + r16;
       const float inv = 1.f / l_run;
       float* dst = a.out + orow * kD + 4 * kg;
 #pragma unroll
@@ -342,7 +348,7 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
             make_float4(acc[db][0] * inv, acc[db][1] * inv, acc[db][2] * inv, acc[db][3] * inv);
       if (a.lse && kg == 0) a.lse[orow] = (m_run + log2f(l_run)) * kLn2;
     } else {
-      const size_t prow = ((size_t)lb * a.n_split + split) * a.H_q + (size_t)g * G + r16;
+      const size_t prow = ((size_t)lb * a.n_split + split) * a.H_q + (size_t)gv * G + r16;
       float* dst = a.part_acc + prow * kD + 4 * kg;
 #pragma unroll
       for (int db = 0; db < 8; ++db)
@@ -451,8 +457,11 @@ struct AttnPlan {
 // Units are numbered KV head fastest, so that the wavefronts of a workgroup
 // read the same selected tokens' rows for neighbouring heads at the same time:
 // those pieces share DRAM pages.  A split is a whole number of chunks.
+// Column groups of at most 16 query heads per KV head.
+int attn_col_groups(const Dims& d) { return d.G > 16 ? d.G / 16 : 1; }
+
 AttnPlan attn_plan(const Dims& d) {
-  const int64_t base = (int64_t)d.n_layers * d.B * d.H_kv;
+  const int64_t base = (int64_t)d.n_layers * d.B * d.H_kv * attn_col_groups(d);
   auto round_chunk = [](int64_t t) { return (t + kChunk - 1) / kChunk * kChunk; };
   int64_t n_split = (kWaveSlots + base - 1) / base;
   int64_t split = round_chunk((d.k_max + n_split - 1) / n_split);
@@ -484,12 +493,13 @@ hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
                        ? reinterpret_cast<float*>(static_cast<char*>(ws) +
                                                   align_up(sizeof(float) * rows * d.d))
                        : nullptr;
-  const int64_t n_groups = (int64_t)d.n_layers * d.B * d.H_kv;
+  const int R = attn_col_groups(d);
+  const int64_t n_groups = (int64_t)d.n_layers * d.B * d.H_kv * R;
   const int64_t n_items = n_groups * pl.n_split;
   if (n_items > INT32_MAX / 2) return hipErrorInvalidValue;
   AttnArgs a{q, k, v, idx, counts, part_acc, part_ml, out, lse, d.kv_stride_layer, d.kv_stride_b,
-             d.B, d.H_q, d.H_kv, d.G, d.k_max, d.L_cap, pl.n_split, pl.split, (int)n_items,
-             pl.mode, d.n_sets, d.scale * kLog2e};
+             d.B, d.H_q, d.H_kv, d.G / R, d.k_max, d.L_cap, pl.n_split, pl.split, (int)n_items,
+             R, pl.mode, d.n_sets, d.scale * kLog2e};
   // One workgroup per CU, fewer only when there are fewer units than CUs:
   // with few units they are spread over all CUs (each CU's share of the
   // bandwidth is limited) rather than packed four to a CU.

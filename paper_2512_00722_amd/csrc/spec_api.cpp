@@ -24,7 +24,9 @@ constexpr int kMaxElasticLcap = 245760;  // two LDS bitmaps of L_cap bits <= 60 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
-bool is_pow2_group(int g) { return g == 1 || g == 2 || g == 4 || g == 8 || g == 16; }
+// Query heads per KV head: a power of two up to 128 (more than 16 run as
+// several 16-head column groups over the same KV head).
+bool is_pow2_group(int g) { return g >= 1 && g <= 128 && (g & (g - 1)) == 0; }
 
 spec_status resolve(const spec_dims* dm, spec::Dims* o) {
   if (!dm) return SPEC_ERR_INVALID;

@@ -81,6 +81,21 @@ def test_dims_validation(lib, field, value, status):
         assert st == status, (field, op, st)
 
 
+def test_large_query_groups(lib):
+    """More than 16 query heads per KV head (MQA-like) run as 16-head column
+    groups: powers of two up to 128 are accepted; the attention workspace
+    still holds one partial row per query head."""
+    for H_q, H_kv in [(32, 1), (64, 1), (128, 1), (64, 2), (128, 4)]:
+        d = good_dims(H_q=H_q, H_kv=H_kv)
+        for op in range(7):
+            assert ws_size(lib, d, op)[0] == 0, (H_q, H_kv, op)
+    assert ws_size(lib, good_dims(H_q=256, H_kv=1), spec.OP_ATTN)[0] == 2   # G = 256
+    assert ws_size(lib, good_dims(H_q=48, H_kv=1), spec.OP_ATTN)[0] == 2    # G = 48
+    # with fewer KV heads the groups split further: a workspace is still sized
+    _, n = ws_size(lib, good_dims(H_q=64, H_kv=1), spec.OP_ATTN)
+    assert n == 0 or n >= 2 * 2 * 64 * 128 * 4
+
+
 def test_head_level_sets(lib):
     # one set per KV head: valid when H_r is a multiple of H_kv
     d = good_dims(n_sets=8)

@@ -155,6 +155,11 @@ ATTN_CASES = [
     # selections longer than 4 x 2048: splits merged by the second kernel
     (1, 2, 12000, 8, 2, [9000, 8193], 9000),
     (1, 3, 9000, 8, 1, [8400, 0, 3], 8400),
+    # more than 16 query heads per KV head (MQA-like): 16-head column groups
+    # over the same KV head; split selections; an empty selection
+    (1, 2, 500, 32, 1, [300, 17], 300),
+    (2, 1, 9000, 64, 1, [8500], 8500),
+    (1, 2, 400, 64, 2, [200, 0], 256),
 ]
 
 
@@ -256,6 +261,8 @@ STEP_CASES = [
          cluster_len=64),
     dict(B=2, L=4000, H_r=8, d_r=64, n_layers=1, H_q=32, H_kv=8, k=512, heavy_frac=0.02,
          recent=256),
+    # one KV head for 32 query heads (MQA-like)
+    dict(B=2, L=2000, H_r=8, d_r=64, n_layers=2, H_q=32, H_kv=1, k=256, heavy_frac=0.02),
 ]
 
 
@@ -450,6 +457,7 @@ SET_ATTN_CASES = [
     (1, 3, 400, 16, 4, [1, 0, 17], 64),
     (4, 32, 160, 32, 8, [(37 * b) % 129 for b in range(32)], 128),   # one unit per group
     (1, 1, 12000, 8, 2, [9000], 9000),                               # split selections
+    (1, 2, 500, 64, 2, [300, 50], 300),                              # 32 query heads per set
 ]
 
 
