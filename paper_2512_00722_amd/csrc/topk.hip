@@ -162,7 +162,6 @@ struct SelArgs {
   const float* scores;  // [B][L_max]
   const int32_t* seq_lens;
   const int32_t* ks;
-  const int32_t* hist;  // [B][4096] of key bits 31..20 over t < L_b
   int32_t* idx;         // [B][k_max]
   int32_t* counts;      // [B] or null
   TileLists tl;
@@ -600,7 +599,7 @@ hipError_t launch_topk_select(const Dims& d, const float* scores, const int32_t*
   const TileLists tl = tile_lists(d, lists);
   ClsArgs c{scores, seq_lens, ks, hist, tl, d.L_max, d.k_max, d.n_sets};
   topk_classify_kernel<<<dim3(tl.n_tiles, d.B * d.n_sets), kClsThreads, 0, s>>>(c);
-  SelArgs a{scores, seq_lens, ks, hist, idx, counts, tl, d.L_max, d.k_max, d.n_sets};
+  SelArgs a{scores, seq_lens, ks, idx, counts, tl, d.L_max, d.k_max, d.n_sets};
   topk_select_kernel<<<d.B * d.n_sets, kThreads, 0, s>>>(a);
   return hipGetLastError();
 }
