@@ -3,9 +3,9 @@
 // and elastic loading (Sec. 5.4: keep S_last on the device, load only
 // S_now - S_last into the places freed by S_last - S_now).
 //
-// A token's K (or V) row of one layer is H_kv*d bf16 = 2 KiB contiguous in
-// the token-major cache, so every copy is whole rows moved with 16-byte
-// lanes: 128 lanes per row, fully coalesced on both sides.
+// A token's K (or V) row of one layer is H_kv*d bf16 contiguous in the
+// token-major cache (2 KiB at H_kv = 8), so every copy is whole rows moved
+// with 16-byte lanes (128 lanes per 2 KiB row), fully coalesced on both sides.
 #include "device_common.h"
 #include "internal.h"
 

@@ -5,7 +5,7 @@
 //  1. logits_kernel streams K_r once.  Each lane holds 8 bf16 of one
 //     (token, head) row slice in one 16-byte load; the d_r/8 lanes of a head
 //     reduce their partial dot products with cross-lane shuffles.  A
-//     workgroup covers 128 tokens; it writes the logits (log2 units, the
+//     workgroup covers 256 tokens; it writes the logits (log2 units, the
 //     scale and log2(e) folded into q_r) and its per-head (max, sum exp2).
 //  2. softmax_headsum_kernel merges the per-block pairs into each head's
 //     normaliser c_h = M_h + log2 Z_h and writes
