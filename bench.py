@@ -412,6 +412,8 @@ def run_elastic(args, spec, w, x, e, algorithmic_bytes):
     kb = sum(int(c) for c in counts.cpu().tolist())
     a_bytes = w.n_layers * (kb * w.H_kv * w.d * 2 * 2 + w.B * w.H_q * w.d * 2 + w.B * w.H_q * w.d * 4)
     achieved = a_bytes / (attn_us * 1e-6) / 1e9
+    if args.copy_calibration:
+        copy_calibration(dev)
     return {
         "metric": METRIC,
         "value": round(value, 3),
@@ -434,7 +436,7 @@ def run_elastic(args, spec, w, x, e, algorithmic_bytes):
             "peak": PEAK_HBM_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBPS, 4),
-            "traffic": None,
+            "traffic": stored_traffic(w.name),
             "kernel": "sparse GQA decode attention over the compact slot buffers",
             "bytes_per_launch": a_bytes,
             "avg_launch_us": round(attn_us, 2),
