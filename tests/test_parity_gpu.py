@@ -111,6 +111,8 @@ TOPK_CASES = [
     ("random", 2, 140000, 3000, [140000, 131072], [3000, 2999]),
     # a threshold bin too crowded for the candidate lists: the general path
     ("narrow", 1, 131072, 4096, [131072], [4096]),
+    # more tiles than the list gather takes (over 2M tokens): the general path
+    ("random", 1, 2_100_000, 8192, [2_100_000], [8192]),
     ("ties", 1, 150000, 4096, [150000], [4096]),
 ]
 
