@@ -1,0 +1,101 @@
+"""Seeded random shapes, HIP path vs the fp64 oracle.
+
+* Top-k: the same fp32 keys on both sides, so the index sets, the -1 padding
+  and the counts must match exactly.  Shapes mix short rows, rows spanning
+  several classify tiles and rows past 64 tiles; lengths and budgets are
+  ragged, zero or the whole row.
+* Sparse GQA attention (indexed: the gather fused into the loads): every
+  supported query-group size up to 64, one to three layers, ragged and empty
+  selections, budgets up to the whole cache; max-abs error within the
+  attention tolerance, lse included.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2512_00722_amd as spec
+from tests.gpu_helpers import TOL_ATTN, announce, f64, need_gpu
+from tests.test_parity_gpu import _topk_rows
+
+pytestmark = pytest.mark.gpu
+
+KINDS = ["random", "ties", "equal", "signed", "narrow"]
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return need_gpu()
+
+
+def _ragged(rng, n, hi, p_other=0.3):
+    """n values: mostly hi, some uniform in [0, hi]."""
+    return [int(rng.integers(0, hi + 1)) if rng.random() < p_other else hi for _ in range(n)]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_topk_random_shapes(dev, seed):
+    rng = np.random.default_rng(100 + seed)
+    for it in range(15):
+        kind = KINDS[(seed * 15 + it) % len(KINDS)]
+        B = int(rng.integers(1, 6))
+        L_max = int(rng.choice([rng.integers(1, 4096), rng.integers(4096, 70000),
+                                rng.integers(70000, 150001)]))
+        k_max = int(rng.integers(1, min(L_max, 12000) + 1))
+        lens = _ragged(rng, B, L_max)
+        ks = _ragged(rng, B, k_max)
+        announce(f"topk random seed={seed} it={it} kind={kind} B={B} L_max={L_max} k_max={k_max}")
+        g = torch.Generator().manual_seed(10_000 * seed + it)
+        sc = _topk_rows(kind, B, L_max, g).float()
+        idx, cnt = spec.topk(sc.to(dev), torch.tensor(lens, dtype=torch.int32).to(dev),
+                             torch.tensor(ks, dtype=torch.int32).to(dev), k_max)
+        idx, cnt = idx.cpu().numpy(), cnt.cpu().numpy()
+        scn = sc.numpy().astype(np.float64)
+        for b in range(B):
+            L = min(lens[b], L_max)
+            kb = max(0, min(ks[b], L, k_max))
+            want = oracle.topk_indices(scn[b, :L], kb)
+            assert cnt[b] == kb, (it, b)
+            assert idx[b, :kb].tolist() == want.tolist(), (it, b, kind, L, kb)
+            assert np.all(idx[b, kb:] == -1), (it, b)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_attention_random_shapes(dev, seed):
+    rng = np.random.default_rng(200 + seed)
+    for it in range(8):
+        n_layers = int(rng.integers(1, 4))
+        B = int(rng.integers(1, 5))
+        H_kv = int(rng.choice([1, 2, 4, 8]))
+        G = int(rng.choice([g for g in (1, 2, 4, 8, 16, 32, 64) if g * H_kv <= 128]))
+        H_q = H_kv * G
+        L_cap = int(rng.integers(64, 4001))
+        k_max = int(rng.integers(1, L_cap + 1))
+        counts = _ragged(rng, B, k_max, p_other=0.5)
+        announce(f"attn random seed={seed} it={it} layers={n_layers} B={B} H_q={H_q} "
+                 f"H_kv={H_kv} L_cap={L_cap} k_max={k_max} counts={counts}")
+        g = torch.Generator().manual_seed(20_000 * seed + it)
+        q = torch.randn((n_layers, B, H_q, 128), generator=g).to(torch.bfloat16)
+        K = torch.randn((n_layers, B, L_cap, H_kv, 128), generator=g).to(torch.bfloat16)
+        V = torch.randn((n_layers, B, L_cap, H_kv, 128), generator=g).to(torch.bfloat16)
+        idx = torch.full((B, k_max), -1, dtype=torch.int32)
+        for b in range(B):
+            sel = torch.randperm(L_cap, generator=g)[:counts[b]].sort().values
+            idx[b, :counts[b]] = sel.to(torch.int32)
+        cnt = torch.tensor(counts, dtype=torch.int32)
+        out, lse = spec.sparse_decode_attn(q.to(dev), K.to(dev), V.to(dev), cnt.to(dev),
+                                           idx=idx.to(dev), with_lse=True)
+        out, lse = out.cpu().numpy(), lse.cpu().numpy()
+        qn, Kn, Vn = f64(q), f64(K), f64(V)
+        for layer in range(n_layers):
+            for b in range(B):
+                sel = idx[b, :counts[b]].numpy()
+                want, want_lse = oracle.sparse_gqa_attention(qn[layer, b], Kn[layer, b],
+                                                             Vn[layer, b], sel)
+                if counts[b] == 0:
+                    assert np.all(out[layer, b] == 0.0)
+                    assert np.all(np.isneginf(lse[layer, b]))
+                    continue
+                err = np.abs(out[layer, b] - want).max()
+                assert err <= TOL_ATTN, (it, layer, b, err)
+                assert np.abs(lse[layer, b] - want_lse).max() <= TOL_ATTN, (it, layer, b)
