@@ -1,5 +1,7 @@
 """Seeded random shapes, HIP path vs the fp64 oracle.
 
+* Retrieval scores: any head count up to 16, d_r 64 or 128, ragged lengths
+  (zero and one included), L_max below L_cap; the internal score gate.
 * Top-k: the same fp32 keys on both sides, so the index sets, the -1 padding
   and the counts must match exactly.  Shapes mix short rows, rows spanning
   several classify tiles and rows past 64 tiles; lengths and budgets are
@@ -15,7 +17,7 @@ import torch
 
 import oracle
 import paper_2512_00722_amd as spec
-from tests.gpu_helpers import TOL_ATTN, announce, f64, need_gpu
+from tests.gpu_helpers import SCORE_ABS, SCORE_REL, TOL_ATTN, announce, f64, need_gpu
 from tests.test_parity_gpu import _topk_rows
 
 pytestmark = pytest.mark.gpu
@@ -99,3 +101,28 @@ def test_attention_random_shapes(dev, seed):
                 err = np.abs(out[layer, b] - want).max()
                 assert err <= TOL_ATTN, (it, layer, b, err)
                 assert np.abs(lse[layer, b] - want_lse).max() <= TOL_ATTN, (it, layer, b)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_score_random_shapes(dev, seed):
+    rng = np.random.default_rng(300 + seed)
+    for it in range(8):
+        B = int(rng.integers(1, 5))
+        H_r = int(rng.integers(1, 17))
+        d_r = int(rng.choice([64, 128]))
+        L_cap = int(rng.integers(1, 9000))
+        L_max = int(rng.integers(1, L_cap + 1))
+        lens = [int(rng.choice([0, 1, L_max, int(rng.integers(0, L_max + 1))])) for _ in range(B)]
+        announce(f"score random seed={seed} it={it} B={B} H_r={H_r} d_r={d_r} L_cap={L_cap} "
+                 f"L_max={L_max} lens={lens}")
+        g = torch.Generator().manual_seed(30_000 * seed + it)
+        q_r = torch.randn((B, H_r, d_r), generator=g).to(torch.bfloat16)
+        K_r = (torch.randn((B, L_cap, H_r, d_r), generator=g) * 1.5).to(torch.bfloat16)
+        got = spec.score(q_r.to(dev), K_r.to(dev), torch.tensor(lens, dtype=torch.int32).to(dev),
+                         L_max=L_max).cpu().numpy().astype(np.float64)
+        qn, Kn = f64(q_r), f64(K_r)
+        for b in range(B):
+            L = min(lens[b], L_max)
+            want = oracle.retrieval_scores(qn[b], Kn[b], L)
+            assert np.all(np.abs(got[b, :L] - want) <= SCORE_ABS + SCORE_REL * want), (it, b)
+            assert np.all(np.isneginf(got[b, L:L_max])), (it, b)
