@@ -6,6 +6,10 @@
   and the counts must match exactly.  Shapes mix short rows, rows spanning
   several classify tiles and rows past 64 tiles; lengths and budgets are
   ragged, zero or the whole row.
+* Elastic delta-gather: fixed or growing budgets per sequence, overlaps from
+  none to full between consecutive selections; the slot map equals the
+  oracle's pairing, every held row is a bit-exact copy, and the rows loaded
+  equal |S_now - S_last|.
 * Sparse GQA attention (indexed: the gather fused into the loads): every
   supported query-group size up to 64, one to three layers, ragged and empty
   selections, budgets up to the whole cache; max-abs error within the
@@ -126,3 +130,53 @@ def test_score_random_shapes(dev, seed):
             want = oracle.retrieval_scores(qn[b], Kn[b], L)
             assert np.all(np.abs(got[b, :L] - want) <= SCORE_ABS + SCORE_REL * want), (it, b)
             assert np.all(np.isneginf(got[b, L:L_max])), (it, b)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_elastic_random_shapes(dev, seed):
+    rng = np.random.default_rng(400 + seed)
+    n_layers = int(rng.integers(1, 3))
+    B = int(rng.integers(1, 5))
+    H_kv = int(rng.choice([1, 2, 4, 8]))
+    L_cap = int(rng.integers(50, 3001))
+    k_max = int(rng.integers(1, min(L_cap, 800) + 1))
+    announce(f"elastic random seed={seed} layers={n_layers} B={B} H_kv={H_kv} L_cap={L_cap} "
+             f"k_max={k_max}")
+    g = torch.Generator().manual_seed(40_000 + seed)
+    K = torch.randn((n_layers, B, L_cap, H_kv, 128), generator=g).to(torch.bfloat16)
+    V = torch.randn((n_layers, B, L_cap, H_kv, 128), generator=g).to(torch.bfloat16)
+    Kd, Vd = K.to(dev), V.to(dev)
+    st = spec.ElasticState(n_layers, B, k_max, H_kv, 128, dev)
+    budget = [int(rng.integers(0, k_max + 1)) for _ in range(B)]
+    slot_ref = [np.full(k_max, -1) for _ in range(B)]
+    prev = [np.zeros(0, dtype=np.int64) for _ in range(B)]
+    for it in range(6):
+        keep_p = float(rng.choice([0.0, 0.5, 0.8, 0.95, 1.0]))
+        now = []
+        for b in range(B):
+            if rng.random() < 0.3:  # the budget grows (never shrinks)
+                budget[b] = int(rng.integers(budget[b], k_max + 1))
+            keep = prev[b][rng.random(len(prev[b])) < keep_p][:budget[b]]
+            pool = np.setdiff1d(np.arange(L_cap), keep)  # may return dropped tokens
+            add = rng.choice(pool, budget[b] - len(keep), replace=False)
+            now.append(np.sort(np.concatenate([keep, add]).astype(np.int64)))
+        idx = torch.full((B, k_max), -1, dtype=torch.int32)
+        for b in range(B):
+            idx[b, :len(now[b])] = torch.tensor(now[b], dtype=torch.int32)
+        cnt = torch.tensor([len(x) for x in now], dtype=torch.int32)
+        spec.delta_gather(idx.to(dev), cnt.to(dev), Kd, Vd, st)
+        slots = st.slot_tok.cpu().numpy()
+        nch = st.n_changed.cpu().numpy()
+        kb, vb = st.kbuf.cpu(), st.vbuf.cpu()
+        for b in range(B):
+            ref, loads = oracle.elastic_update(slot_ref[b], now[b])
+            slot_ref[b] = ref
+            assert slots[b].tolist() == ref.tolist(), (it, b)
+            assert nch[b] == len(loads) == len(np.setdiff1d(now[b], prev[b])), (it, b)
+            held = [(sl, t) for sl, t in enumerate(ref.tolist()) if t >= 0]
+            if held:
+                ss = torch.tensor([sl for sl, _ in held])
+                tt = torch.tensor([t for _, t in held])
+                assert torch.equal(kb[:, b, ss].view(torch.int16), K[:, b, tt].view(torch.int16))
+                assert torch.equal(vb[:, b, ss].view(torch.int16), V[:, b, tt].view(torch.int16))
+        prev = now
