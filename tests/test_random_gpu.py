@@ -12,8 +12,9 @@
   below a kept token's slot: the documented full reload), every held row is
   a bit-exact copy, and the rows loaded equal what the pairing loads.
 * Sparse GQA attention (indexed: the gather fused into the loads): every
-  supported query-group size up to 64, one to three layers, ragged and empty
-  selections, budgets up to the whole cache; max-abs error within the
+  supported query-group size up to 64, one to three layers, one token set per
+  sequence or one per KV head, ragged and empty selections, budgets up to the
+  whole cache; max-abs error within the
   attention tolerance, lse included.
 """
 import numpy as np
@@ -67,7 +68,7 @@ def test_topk_random_shapes(dev, seed):
             assert np.all(idx[b, kb:] == -1), (it, b)
 
 
-@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("seed", range(4))
 def test_attention_random_shapes(dev, seed):
     rng = np.random.default_rng(200 + seed)
     for it in range(8):
@@ -79,16 +80,21 @@ def test_attention_random_shapes(dev, seed):
         L_cap = int(rng.integers(64, 4001))
         k_max = int(rng.integers(1, L_cap + 1))
         counts = _ragged(rng, B, k_max, p_other=0.5)
-        announce(f"attn random seed={seed} it={it} layers={n_layers} B={B} H_q={H_q} "
-                 f"H_kv={H_kv} L_cap={L_cap} k_max={k_max} counts={counts}")
         g = torch.Generator().manual_seed(20_000 * seed + it)
         q = torch.randn((n_layers, B, H_q, 128), generator=g).to(torch.bfloat16)
         K = torch.randn((n_layers, B, L_cap, H_kv, 128), generator=g).to(torch.bfloat16)
         V = torch.randn((n_layers, B, L_cap, H_kv, 128), generator=g).to(torch.bfloat16)
-        idx = torch.full((B, k_max), -1, dtype=torch.int32)
+        sets = rng.random() < 0.35  # one token set per KV head (head-level selection)
+        n_sets = H_kv if sets else 1
+        idx = torch.full((B, n_sets, k_max), -1, dtype=torch.int32)
         for b in range(B):
-            sel = torch.randperm(L_cap, generator=g)[:counts[b]].sort().values
-            idx[b, :counts[b]] = sel.to(torch.int32)
+            for s_ in range(n_sets):
+                sel = torch.randperm(L_cap, generator=g)[:counts[b]].sort().values
+                idx[b, s_, :counts[b]] = sel.to(torch.int32)
+        if not sets:
+            idx = idx[:, 0].contiguous()
+        announce(f"attn random seed={seed} it={it} layers={n_layers} B={B} H_q={H_q} "
+                 f"H_kv={H_kv} L_cap={L_cap} k_max={k_max} counts={counts} sets={sets}")
         cnt = torch.tensor(counts, dtype=torch.int32)
         out, lse = spec.sparse_decode_attn(q.to(dev), K.to(dev), V.to(dev), cnt.to(dev),
                                            idx=idx.to(dev), with_lse=True)
@@ -96,9 +102,13 @@ def test_attention_random_shapes(dev, seed):
         qn, Kn, Vn = f64(q), f64(K), f64(V)
         for layer in range(n_layers):
             for b in range(B):
-                sel = idx[b, :counts[b]].numpy()
-                want, want_lse = oracle.sparse_gqa_attention(qn[layer, b], Kn[layer, b],
-                                                             Vn[layer, b], sel)
+                if sets:
+                    want, want_lse = oracle.sparse_gqa_attention_sets(
+                        qn[layer, b], Kn[layer, b], Vn[layer, b],
+                        [idx[b, s_, :counts[b]].numpy() for s_ in range(H_kv)])
+                else:
+                    want, want_lse = oracle.sparse_gqa_attention(
+                        qn[layer, b], Kn[layer, b], Vn[layer, b], idx[b, :counts[b]].numpy())
                 if counts[b] == 0:
                     assert np.all(out[layer, b] == 0.0)
                     assert np.all(np.isneginf(lse[layer, b]))
