@@ -134,3 +134,37 @@ def test_mla_full_size_step(dev):
     print(f"max |out - oracle| = {worst:.2e}")
     del x
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_mla_random_shapes(dev, seed):
+    """Seeded random shapes: sequences, layers, 64 or 128 heads, ragged and
+    empty selections up to the whole cache; eight random heads of every
+    (layer, sequence) against the oracle."""
+    rng = np.random.default_rng(500 + seed)
+    for it in range(3):
+        B = int(rng.integers(1, 7))
+        n_layers = int(rng.integers(1, 3))
+        H = int(rng.choice([64, 128]))
+        L = int(rng.integers(16, 1500))
+        k_max = int(rng.integers(1, L + 1))
+        counts = [int(rng.integers(0, k_max + 1)) if rng.random() < 0.5 else k_max
+                  for _ in range(B)]
+        announce(f"mla random seed={seed} it={it} B={B} layers={n_layers} H={H} L={L} "
+                 f"k_max={k_max} counts={counts}")
+        w = small_workload(B=B, L=L, k=k_max, n_layers=n_layers, H_q=H, H_kv=1, mla=True)
+        x = generate_mla(w, seed=100 * seed + it, device=dev)
+        idx = _random_idx(rng, B, k_max, L, counts)
+        out, lse = spec.mla_sparse_decode_attn(
+            x["q_mla"], x["ckv"], x["w_uk"], x["w_uv"], torch.as_tensor(idx, device=dev),
+            torch.as_tensor(np.array(counts, dtype=np.int32), device=dev))
+        out, lse = out.cpu().numpy(), lse.cpu().numpy()
+        heads = np.sort(rng.choice(H, 8, replace=False))
+        for layer in range(n_layers):
+            for b in range(B):
+                if counts[b] == 0:
+                    assert np.all(out[layer, b] == 0) and np.all(np.isneginf(lse[layer, b]))
+                    continue
+                want, wl = _oracle(x, layer, b, idx[b, :counts[b]], heads=heads)
+                assert np.abs(out[layer, b][heads] - want).max() <= TOL_ATTN, (it, layer, b)
+                assert np.abs(lse[layer, b][heads] - wl).max() <= TOL_ATTN, (it, layer, b)
