@@ -21,8 +21,8 @@
 //    a bf16 low part (two MFMAs), which keeps it to ~2^-16 relative;
 //  * K and V of chunk c+1 are requested as soon as chunk c's registers are
 //    consumed and stay in flight through chunk c's softmax and MFMAs;
-//  * units are pipelined: when a wavefront starts a unit it also takes its
-//    next one and requests that unit's count, row indices and queries
+//  * when a wavefront has several units they are pipelined: when it starts a
+//    unit it also takes its next one and requests that unit's count, row indices and queries
 //    together (the indices unconditionally; the count only masks them), and
 //    stages its rows in the other half of a double-buffered row area.  The
 //    last chunk's refill then requests the next unit's first chunk, so a unit
@@ -149,8 +149,9 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const uint16_t* p) {
       (__attribute__((address_space(3))) bf16x4*)(p));
 }
 
-// Rows staged per unit: the selection split plus one chunk of padding (the
-// software pipeline reads one chunk past the end when no unit follows).
+// Rows staged per unit: up to kMaxSplit rows of the selection split plus one
+// chunk of padding (the software pipeline reads one chunk past the end when
+// no unit follows).
 constexpr int kRowsCap = kMaxSplit + kChunk;
 constexpr int kRowLoads = kMaxSplit / 64;  // index loads per lane for one unit
 
@@ -176,18 +177,246 @@ __device__ __forceinline__ Unit decode_unit(const AttnArgs& a, int item) {
   return u;
 }
 
+// One unit from a cold start (a wavefront with a single unit): count, then
+// indices staged in LDS, then the first chunk.
+template <bool INDEXED>
+__device__ __forceinline__ void process_item(const AttnArgs& a, const int item, const int lane,
+                                             uint16_t* V, int* rows) {
+  // A group of more than 16 query heads is covered by R column groups of
+  // 16 (gv = g R .. g R + R - 1), each a unit of its own that reads KV head
+  // g; the query heads of column group gv are gv G .. gv G + G - 1.
+  const int G = a.G;
+  const int gv = item % (a.H_kv * a.R);
+  const int g = gv / a.R;
+  const int rest = item / (a.H_kv * a.R);
+  const int split = rest % a.n_split;
+  const int lb = rest / a.n_split;  // layer * B + b
+  const int b = lb % a.B;
+  const int layer = lb / a.B;
+  const int count = __builtin_amdgcn_readfirstlane(clampi(a.counts[b], 0, a.k_max));
+  const int j0 = split * a.split_tokens;
+  const int r16e = lane & 15;
+  if (j0 >= count) {  // uniform per wavefront
+    if (a.mode == kDirect && r16e < G) {  // no tokens: out = 0, lse = -inf
+      const size_t orow = (size_t)lb * a.H_q + (size_t)gv * G + r16e;
+      float* dst = a.out + orow * kD + 4 * (lane >> 4);
+#pragma unroll
+      for (int db = 0; db < 8; ++db)
+        *reinterpret_cast<float4*>(dst + 16 * db) = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (a.lse && (lane >> 4) == 0) a.lse[orow] = -INFINITY;
+    }
+    return;
+  }
+  const int n_tok = min(a.split_tokens, count - j0);  // tokens of this work item
+
+  const int64_t rs = (int64_t)a.H_kv * kD;  // elements per token row
+  const uint16_t* kb;
+  const uint16_t* vb;
+  if (INDEXED) {
+    const int64_t off = (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b + g * kD;
+    kb = a.k + off;
+    vb = a.v + off;
+  } else {
+    const int64_t off = (int64_t)lb * a.k_max * rs + g * kD;
+    kb = a.k + off;
+    vb = a.v + off;
+  }
+
+  const int r16 = lane & 15;  // head of this lane (MFMA column); token of a K tile row
+  const int kg = lane >> 4;   // MFMA k-group; also the token phase of V loads
+  // B operand of S^T = K Q^T: Q^T column r16 = query head gv*G + r16 (zero if >= G),
+  // dims 32s + 8kg .. +8.  Loaded together with the row indices.
+  bf16x8 qf[4];
+  {
+    const uint16_t* qp = a.q + ((size_t)lb * a.H_q + gv * G + (r16 < G ? r16 : 0)) * kD + 8 * kg;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      uint4 w = r16 < G ? ldg16(qp + 32 * s) : make_uint4(0, 0, 0, 0);
+      qf[s] = __builtin_bit_cast(bf16x8, w);
+    }
+  }
+
+  // Stage the rows of this item's tokens in LDS (masked tokens read row 0),
+  // so that no chunk waits on an index load from memory.
+  wave_sync_lds();  // the previous item's reads of rows/V are done
+  {
+    // All index loads are issued before any is used (one round trip), and
+    // one chunk of padding follows the end: the software pipeline always
+    // prefetches the next chunk, and padding rows all read row 0 (cache hits).
+    const int32_t* idx_b =
+        INDEXED ? a.idx + ((size_t)b * a.n_sets + (a.n_sets > 1 ? g : 0)) * a.k_max + j0
+                : nullptr;
+    const int n_pad = (n_tok + kChunk - 1) / kChunk * kChunk + kChunk;
+    constexpr int kColdRowLoads = (kMaxSplit + kChunk + 63) / 64;
+    int rv[kColdRowLoads];
+#pragma unroll
+    for (int m = 0; m < kColdRowLoads; ++m) {
+      const int j = lane + 64 * m;
+      rv[m] = 0;
+      if (j < n_tok) rv[m] = INDEXED ? idx_b[j] : j0 + j;
+    }
+#pragma unroll
+    for (int m = 0; m < kColdRowLoads; ++m) {
+      const int j = lane + 64 * m;
+      if (j < n_pad) rows[j] = clampi(rv[m], 0, a.L_cap - 1);
+    }
+  }
+
+  wave_sync_lds();
+
+  // K rows in the MFMA A-operand layout: tile t, token 16t + r16, dims
+  // 32s + 8kg .. +8.  V rows: load r brings token 4r + kg, dims 8 r16 .. +8,
+  // i.e. four whole 256-byte rows per instruction.
+  auto load_k = [&](int c, uint4 (&kr)[kTiles][4]) {
+    const int* rc = rows + c;
+#pragma unroll
+    for (int t = 0; t < kTiles; ++t) {
+      const uint16_t* p = kb + (int64_t)rc[16 * t + r16] * rs + 8 * kg;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) kr[t][s] = ldkv(p + 32 * s);
+    }
+  };
+  auto load_v = [&](int c, uint4 (&vr)[kVRows]) {
+    const int* rc = rows + c;
+#pragma unroll
+    for (int r = 0; r < kVRows; ++r) vr[r] = ldkv(vb + (int64_t)rc[4 * r + kg] * rs + 8 * r16);
+  };
+
+  float m_run = -INFINITY, l_run = 0.f;  // head r16
+  floatx4 acc[8];                        // O^T[16db + 4kg + i][head r16]
+#pragma unroll
+  for (int db = 0; db < 8; ++db) acc[db] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  // Single register buffers, refilled as soon as they are consumed: V(c+1)
+  // is requested right after V(c) is staged in LDS, K(c+1) right after the
+  // Q.K^T MFMAs have read K(c); both stay in flight through the softmax and
+  // the P.V MFMAs of chunk c.  Loads retire in issue order, so each wait is
+  // a partial one.  The prefetch past the last chunk reads padding rows
+  // (row 0, cache hits).
+  uint4 kraw[kTiles][4], vraw[kVRows];
+  load_v(0, vraw);
+  __builtin_amdgcn_sched_barrier(0);
+  load_k(0, kraw);
+  __builtin_amdgcn_sched_barrier(0);
+  for (int c = 0; c < n_tok; c += kChunk) {
+#pragma unroll
+    for (int r = 0; r < kVRows; ++r)
+      *reinterpret_cast<uint4*>(V + (4 * r + kg) * kVPitch + 8 * r16) = vraw[r];
+    load_v(c + kChunk, vraw);
+    __builtin_amdgcn_sched_barrier(0);  // keep the refill here: issue order = retire order
+
+    // S^T tiles: lane holds S[head r16][token 16t + 4kg + i].
+    floatx4 sacc[kTiles];
+#pragma unroll
+    for (int t = 0; t < kTiles; ++t) {
+      sacc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kraw[t][s]),
+                                                          qf[s], sacc[t], 0, 0, 0);
+    }
+    load_k(c + kChunk, kraw);
+    __builtin_amdgcn_sched_barrier(0);
+
+    float sv[kTiles][4];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < kTiles; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool valid = c + 16 * t + 4 * kg + i < n_tok;
+        sv[t][i] = valid ? sacc[t][i] * a.scale_log2 : -INFINITY;
+        mx = fmaxf(mx, sv[t][i]);
+      }
+    mx = xgroup_max(mx);
+    const float mn = fmaxf(m_run, mx);
+    const float alpha = exp2f(m_run - mn);
+    float ls = 0.f;
+#pragma unroll
+    for (int t = 0; t < kTiles; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        sv[t][i] = exp2f(sv[t][i] - mn);
+        ls += sv[t][i];
+      }
+    l_run = l_run * alpha + ls;
+    m_run = mn;
+#pragma unroll
+    for (int db = 0; db < 8; ++db) acc[db] *= alpha;
+
+    // O^T += V^T P^T on the matrix cores.  The k-slots 8kg..8kg+7 of a
+    // 32-token block are tokens 4kg..4kg+3 of its first tile and of its
+    // second tile: exactly the S^T entries this lane holds.
+    wave_sync_lds();
+#pragma unroll
+    for (int kb2 = 0; kb2 < kChunk / 32; ++kb2) {
+      float pv[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        pv[i] = sv[2 * kb2][i];
+        pv[4 + i] = sv[2 * kb2 + 1][i];
+      }
+      bf16x8 phi, plo;
+      split_bf16x8(pv, phi, plo);
+      const uint16_t* r0 = V + (32 * kb2 + 4 * kg + (r16 >> 2)) * kVPitch + 4 * (r16 & 3);
+      const uint16_t* r1 = r0 + 16 * kVPitch;
+#pragma unroll
+      for (int db = 0; db < 8; ++db) {
+        const bf16x4 va = lds_read_tr(r0 + 16 * db);
+        const bf16x4 vb4 = lds_read_tr(r1 + 16 * db);
+        const bf16x8 vA = __builtin_shufflevector(va, vb4, 0, 1, 2, 3, 4, 5, 6, 7);
+        acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vA, phi, acc[db], 0, 0, 0);
+        acc[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vA, plo, acc[db], 0, 0, 0);
+      }
+    }
+    wave_sync_lds();  // the V tile is rewritten by the next chunk
+  }
+
+  l_run = xgroup_sum(l_run);
+  if (r16 < G) {
+    if (a.mode == kDirect) {  // the whole selection: normalise and write the output
+      const size_t orow = (size_t)lb * a.H_q + (size_t)gv * G + r16;
+      const float inv = 1.f / l_run;
+      float* dst = a.out + orow * kD + 4 * kg;
+#pragma unroll
+      for (int db = 0; db < 8; ++db)
+        *reinterpret_cast<float4*>(dst + 16 * db) =
+            make_float4(acc[db][0] * inv, acc[db][1] * inv, acc[db][2] * inv, acc[db][3] * inv);
+      if (a.lse && kg == 0) a.lse[orow] = (m_run + log2f(l_run)) * kLn2;
+    } else {
+      const size_t prow = ((size_t)lb * a.n_split + split) * a.H_q + (size_t)gv * G + r16;
+      float* dst = a.part_acc + prow * kD + 4 * kg;
+#pragma unroll
+      for (int db = 0; db < 8; ++db)
+        *reinterpret_cast<float4*>(dst + 16 * db) =
+            make_float4(acc[db][0], acc[db][1], acc[db][2], acc[db][3]);
+      if (kg == 0) {
+        a.part_ml[prow * 2] = m_run;
+        a.part_ml[prow * 2 + 1] = l_run;
+      }
+    }
+  }
+}
+
+
 // Dynamic LDS requested on top of the static arrays so that one workgroup
 // takes more than half of a CU's 160 KiB: exactly one per CU.
 constexpr size_t kLdsPerCU = 160 * 1024;
-constexpr size_t kStaticLds =
-    sizeof(uint16_t) * kWaves * kChunk * kVPitch + sizeof(int) * kWaves * 2 * kRowsCap + 16;
-constexpr size_t kLdsReserve = kLdsPerCU / 2 + 1024 > kStaticLds ? kLdsPerCU / 2 + 1024 - kStaticLds : 0;
+constexpr size_t static_lds(bool pipe) {
+  return sizeof(uint16_t) * kWaves * kChunk * kVPitch + sizeof(int) * kWaves * (pipe ? 2 : 1) * kRowsCap + 16;
+}
+constexpr size_t lds_reserve(bool pipe) {
+  return kLdsPerCU / 2 + 1024 > static_lds(pipe) ? kLdsPerCU / 2 + 1024 - static_lds(pipe) : 0;
+}
 
-template <bool INDEXED>
+// PIPE: some wavefront has more than one unit, and units are pipelined
+// across their boundaries; otherwise each unit starts cold (the pipeline's
+// bookkeeping made one-unit launches ~1.5 us slower).
+template <bool INDEXED, bool PIPE>
 __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(SPEC_ATTN_WPE)))
 void attn_split_kernel(AttnArgs a) {
   __shared__ __align__(16) uint16_t vlds[kWaves][kChunk * kVPitch];
-  __shared__ int rows_lds[kWaves][2][kRowsCap];
+  __shared__ int rows_lds[kWaves][PIPE ? 2 : 1][kRowsCap];
   __shared__ int next_unit;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -209,6 +438,13 @@ void attn_split_kernel(AttnArgs a) {
     return unit < u1 ? unit : -1;  // uniform per wave
   };
 
+  if constexpr (!PIPE) {
+    for (;;) {
+      const int item = take();
+      if (item < 0) return;  // uniform per wave: every wave ends here
+      process_item<INDEXED>(a, item, lane, vlds[wave], rows_lds[wave][0]);
+    }
+  } else {
   uint16_t* V = vlds[wave];
   const int r16 = lane & 15;  // head of this lane (MFMA column); token of a K tile row
   const int kg = lane >> 4;   // MFMA k-group; also the token phase of V loads
@@ -221,7 +457,7 @@ void attn_split_kernel(AttnArgs a) {
   };
 
   // The loads that start a unit, all independent of each other: its count,
-  // its row indices (unconditionally, clamped into the index row: the count
+  // its row indices (all of a split's, clamped into the index row: the count
   // only masks them later) and its queries.  B operand of S^T = K Q^T: Q^T
   // column r16 = query head gv G + r16 (zero if >= G), dims 32s + 8kg .. +8.
   int cnt_raw;
@@ -231,10 +467,12 @@ void attn_split_kernel(AttnArgs a) {
     cnt_raw = a.counts[u.b];
     const int32_t* idx_b =
         INDEXED ? a.idx + ((size_t)u.b * a.n_sets + (a.n_sets > 1 ? u.g : 0)) * a.k_max : nullptr;
+    // loads past the split re-read its last index (one cache line)
+    const int jmax = min(u.j0 + a.split_tokens, a.k_max) - 1;
 #pragma unroll
     for (int m = 0; m < kRowLoads; ++m) {
       const int j = u.j0 + lane + 64 * m;
-      rv[m] = INDEXED ? idx_b[min(j, a.k_max - 1)] : j;
+      rv[m] = INDEXED ? idx_b[min(j, jmax)] : j;
     }
     const uint16_t* qp =
         a.q + ((size_t)u.lb * a.H_q + u.gv * a.G + (r16 < a.G ? r16 : 0)) * kD + 8 * kg;
@@ -449,6 +687,7 @@ void attn_split_kernel(AttnArgs a) {
     }
     buf ^= 1;
   }
+  }
 }
 
 struct CombineArgs {
@@ -541,6 +780,8 @@ hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
                        const uint16_t* v, const int32_t* idx, const int32_t* counts,
                        float* out, float* lse, void* ws, hipStream_t s) {
   const AttnPlan pl = attn_plan(d);
+  // the row staging area holds one split plus a chunk of padding
+  if (pl.split > kMaxSplit || pl.split % kChunk != 0) return hipErrorInvalidValue;
   const size_t rows = (size_t)d.n_layers * d.B * pl.n_split * d.H_q;
   float* part_acc = static_cast<float*>(ws);
   float* part_ml = pl.mode == kGlobalPartials
@@ -563,10 +804,15 @@ hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
       n_cu <= 0)
     n_cu = 256;
   const dim3 grid((unsigned)(n_items < n_cu ? n_items : n_cu));
-  if (idx)
-    attn_split_kernel<true><<<grid, kWaves * 64, kLdsReserve, s>>>(a);
+  const bool pipe = n_items > (int64_t)grid.x * kWaves;  // some wavefront takes several units
+  if (idx && pipe)
+    attn_split_kernel<true, true><<<grid, kWaves * 64, lds_reserve(true), s>>>(a);
+  else if (idx)
+    attn_split_kernel<true, false><<<grid, kWaves * 64, lds_reserve(false), s>>>(a);
+  else if (pipe)
+    attn_split_kernel<false, true><<<grid, kWaves * 64, lds_reserve(true), s>>>(a);
   else
-    attn_split_kernel<false><<<grid, kWaves * 64, kLdsReserve, s>>>(a);
+    attn_split_kernel<false, false><<<grid, kWaves * 64, lds_reserve(false), s>>>(a);
   if (pl.mode != kGlobalPartials) return hipGetLastError();
   CombineArgs c{part_acc, part_ml, counts, out, lse, d.B, d.H_q, d.k_max, pl.n_split, pl.split};
   const dim3 g2(d.n_layers * d.B, (d.H_q + 7) / 8);
