@@ -27,6 +27,9 @@
 //    stages its rows in the other half of a double-buffered row area.  The
 //    last chunk's refill then requests the next unit's first chunk, so a unit
 //    boundary costs no round trip.
+// The workgroups own contiguous ranges of a permuted unit order (groups of a
+// (layer, sequence, split) spread over the whole range), so that ragged
+// selections even out across workgroups.
 // A unit that covers a whole selection normalises and writes out/lse itself;
 // split selections leave (max, sum, acc) partials that a second kernel merges
 // with a log-sum-exp combine.
@@ -92,6 +95,8 @@ struct AttnArgs {
   int R;                  // column groups per KV head (1; G/16 for more than 16 query heads)
                           // G above: query heads per column group (at most 16)
   int mode;               // kDirect or kGlobalPartials
+  int n_groups, perm;     // work order: group g (G_u = H_kv R consecutive units) runs as group
+                          // (g perm) mod n_groups, perm coprime to n_groups
   int n_sets;             // 1: idx [B][k_max]; H_kv: idx [B][H_kv][k_max], one set per KV head
   float scale_log2;       // scale * log2(e)
 };
@@ -435,7 +440,10 @@ void attn_split_kernel(AttnArgs a) {
     int t = 0;
     if (lane == 0) t = atomicAdd(&next_unit, 1);
     const int unit = __builtin_amdgcn_readfirstlane(t);
-    return unit < u1 ? unit : -1;  // uniform per wave
+    if (unit >= u1) return -1;  // uniform per wave
+    const int gu = a.H_kv * a.R;  // units per group (all column groups of one (layer, sequence, split))
+    const int grp = unit / gu;
+    return (int)(((int64_t)grp * a.perm) % a.n_groups) * gu + (unit - grp * gu);
   };
 
   if constexpr (!PIPE) {
@@ -792,9 +800,19 @@ hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
   const int64_t n_groups = (int64_t)d.n_layers * d.B * d.H_kv * R;
   const int64_t n_items = n_groups * pl.n_split;
   if (n_items > INT32_MAX / 2) return hipErrorInvalidValue;
+  // Work order: the ranges of consecutive units the workgroups own are spread
+  // over all (layer, sequence, split) groups by a multiplicative permutation,
+  // so that ragged selections even out across workgroups.
+  const int n_order = (int)(n_items / (d.H_kv * R));  // (layer, sequence, split) groups
+  int perm = 1;
+  if (n_order > 2) {
+    perm = (int)(0.618 * n_order);
+    auto gcd = [](int x, int y) { while (y) { const int t = x % y; x = y; y = t; } return x; };
+    while (gcd(perm, n_order) != 1) ++perm;
+  }
   AttnArgs a{q, k, v, idx, counts, part_acc, part_ml, out, lse, d.kv_stride_layer, d.kv_stride_b,
              d.B, d.H_q, d.H_kv, d.G / R, d.k_max, d.L_cap, pl.n_split, pl.split, (int)n_items,
-             R, pl.mode, d.n_sets, d.scale * kLog2e};
+             R, pl.mode, n_order, perm, d.n_sets, d.scale * kLog2e};
   // One workgroup per CU, fewer only when there are fewer units than CUs:
   // with few units they are spread over all CUs (each CU's share of the
   // bandwidth is limited) rather than packed four to a CU.
