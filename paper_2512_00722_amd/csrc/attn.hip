@@ -428,9 +428,10 @@ void attn_split_kernel(AttnArgs a) {
   // One workgroup per CU, one wavefront per SIMD.  Two wavefronts on a SIMD
   // do not progress at equal rates (the older one wins instruction issue), and
   // they add no bandwidth over one wavefront with its loads in flight, so the
-  // CU runs one per SIMD.  The workgroup owns a contiguous range of work
-  // units; its wavefronts take them on demand from an LDS counter, which also
-  // evens out units of unequal length (ragged selections).
+  // CU runs one per SIMD.  The workgroup owns a contiguous range of the
+  // permuted unit order; its wavefronts take them on demand from an LDS
+  // counter, which evens out units of unequal length within the workgroup
+  // (the permutation evens them out across workgroups).
   const int per_block = (a.n_items + gridDim.x - 1) / gridDim.x;
   const int u0 = blockIdx.x * per_block;
   const int u1 = min(u0 + per_block, a.n_items);
