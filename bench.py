@@ -318,7 +318,11 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBPS, 4),
             "traffic": traffic,
-            "kernel": "sparse GQA decode attention (attn_split_kernel + attn_combine_kernel)",
+            # the partials workspace exists only when selections are split (then a
+            # second kernel merges them)
+            "kernel": "sparse GQA decode attention (attn_split_kernel"
+                      + (" + attn_combine_kernel)" if spec.workspace_size(dims_a, spec.OP_ATTN) > 0
+                         else ")"),
             "bytes_per_launch": a_bytes,
             "avg_launch_us": round(op_us["attn"], 2),
         },
