@@ -221,6 +221,79 @@ def pin_full_budget_is_dense(o):
         np.testing.assert_allclose(out, _sdpa_dense(q, K, V, L), rtol=1e-10, atol=1e-12)
 
 
+def pin_dense_attention_matches_sdpa(o):
+    """Dense decode attention over the first L rows of a longer cache equals
+    torch's SDPA (fp64, CPU) on those rows, for the default and an explicit
+    scale; lse equals torch's logsumexp of the scaled logits."""
+    rng = np.random.default_rng(23)
+    for H_q, H_kv, L, L_cap, scale in [(4, 1, 6, 9, None), (8, 2, 13, 20, 0.3),
+                                        (6, 6, 1, 4, None), (16, 4, 31, 31, 0.05)]:
+        d = 32
+        q = rng.standard_normal((H_q, d))
+        K = rng.standard_normal((L_cap, H_kv, d))
+        V = rng.standard_normal((L_cap, H_kv, d))
+        out, lse = o.dense_gqa_attention(q, K, V, L, scale)
+        np.testing.assert_allclose(out, _sdpa_dense(q, K, V, L, scale), rtol=1e-10, atol=1e-12)
+        sc = scale if scale is not None else 1.0 / math.sqrt(d)
+        G = H_q // H_kv
+        kt = torch.as_tensor(K[:L], dtype=torch.float64)
+        for h in range(H_q):
+            lg = (kt[:, h // G, :] @ torch.as_tensor(q[h], dtype=torch.float64)) * sc
+            assert abs(lse[h] - float(torch.logsumexp(lg, 0))) < 1e-12
+
+
+def _decode_step_case(rng):
+    """A tiny batched, multi-layer, ragged decode step whose two scales
+    differ from each other and from their defaults."""
+    B, L_cap, n_layers, H_r, d_r, H_q, H_kv, d = 3, 14, 3, 2, 64, 4, 2, 16
+    return dict(
+        q_r=rng.standard_normal((B, H_r, d_r)), K_r=rng.standard_normal((B, L_cap, H_r, d_r)) * 2,
+        seq_lens=np.array([5, 9, 12]), ks=np.array([3, 20, 7]),
+        q=rng.standard_normal((n_layers, B, H_q, d)) * 2,
+        K_layers=rng.standard_normal((n_layers, B, L_cap, H_kv, d)),
+        V_layers=rng.standard_normal((n_layers, B, L_cap, H_kv, d)),
+        scale_r=0.37, scale=0.21)
+
+
+def pin_decode_step_composition(o):
+    """The batched decode step against an independent composition in torch
+    (fp64, CPU): per-head softmax of the retrieval logits at scale_r summed
+    over heads; the k_b largest (ties to the lower index) by a plain sort;
+    then, for every layer and sequence, SDPA at `scale` with a boolean mask
+    that keeps only the selected tokens (KV heads repeated G times)."""
+    c = _decode_step_case(np.random.default_rng(29))
+    idxs, scores, out, lse = o.decode_step(c["q_r"], c["K_r"], c["seq_lens"], c["ks"], c["q"],
+                                           c["K_layers"], c["V_layers"], c["scale_r"],
+                                           c["scale"])
+    n_layers, B, H_q, d = c["q"].shape
+    H_kv = c["K_layers"].shape[3]
+    G = H_q // H_kv
+    for b in range(B):
+        L = int(c["seq_lens"][b])
+        kr = torch.as_tensor(c["K_r"][b, :L], dtype=torch.float64)      # [L, H_r, d_r]
+        qr = torch.as_tensor(c["q_r"][b], dtype=torch.float64)          # [H_r, d_r]
+        lg = torch.einsum("thi,hi->ht", kr, qr) * c["scale_r"]
+        want_s = torch.softmax(lg, dim=1).sum(0).numpy()
+        np.testing.assert_allclose(scores[b], want_s, rtol=1e-12, atol=1e-14)
+        kb = min(int(c["ks"][b]), L)
+        want_idx = sorted(sorted(range(L), key=lambda t: (-want_s[t], t))[:kb])
+        assert idxs[b].tolist() == want_idx, (b, idxs[b], want_idx)
+        mask = torch.zeros((1, 1, 1, L), dtype=torch.bool)
+        mask[..., want_idx] = True
+        for layer in range(n_layers):
+            qt = torch.as_tensor(c["q"][layer, b], dtype=torch.float64).reshape(1, H_q, 1, d)
+            kt = torch.as_tensor(c["K_layers"][layer, b, :L], dtype=torch.float64).permute(1, 0, 2)
+            vt = torch.as_tensor(c["V_layers"][layer, b, :L], dtype=torch.float64).permute(1, 0, 2)
+            kt = kt.repeat_interleave(G, dim=0).unsqueeze(0).contiguous()
+            vt = vt.repeat_interleave(G, dim=0).unsqueeze(0).contiguous()
+            want_o = torch.nn.functional.scaled_dot_product_attention(
+                qt, kt, vt, attn_mask=mask, scale=c["scale"]).reshape(H_q, d).numpy()
+            np.testing.assert_allclose(out[layer, b], want_o, rtol=1e-10, atol=1e-12)
+            lg2 = (kt[0] @ qt[0].transpose(1, 2)).squeeze(-1) * c["scale"]   # [H_q, L]
+            want_l = torch.logsumexp(lg2[:, want_idx], dim=1).numpy()
+            np.testing.assert_allclose(lse[layer, b], want_l, rtol=0, atol=1e-12)
+
+
 def pin_attention_special_cases(o):
     rng = np.random.default_rng(18)
     H_q, H_kv, d, L = 8, 2, 128, 20

@@ -46,6 +46,22 @@ MUTANTS = {
                               "scale = 1.0 / math.sqrt(c.shape[1])"),
     "mla_all_tokens": ("cs = np.asarray(c[idx], dtype=np.float64)",
                        "cs = np.asarray(c[:len(idx)], dtype=np.float64)"),
+    "dense_one_row_too_many": ("return sparse_gqa_attention(q, K, V, np.arange(L), scale)",
+                               "return sparse_gqa_attention(q, K, V, np.arange(L + 1), scale)"),
+    "dense_default_scale_only": ("return sparse_gqa_attention(q, K, V, np.arange(L), scale)",
+                                 "return sparse_gqa_attention(q, K, V, np.arange(L))"),
+    "decode_retrieval_at_llm_scale": ("s = retrieval_scores(q_r[b], K_r[b], L, scale_r)",
+                                      "s = retrieval_scores(q_r[b], K_r[b], L, scale)"),
+    "decode_attention_at_retrieval_scale": ("V_layers[layer][b], idx, scale)",
+                                            "V_layers[layer][b], idx, scale_r)"),
+    "decode_query_of_layer0": ("o, l_ = sparse_gqa_attention(q[layer][b], K_layers[layer][b],",
+                               "o, l_ = sparse_gqa_attention(q[0][b], K_layers[layer][b],"),
+    "decode_kv_of_sequence0": ("o, l_ = sparse_gqa_attention(q[layer][b], K_layers[layer][b],",
+                               "o, l_ = sparse_gqa_attention(q[layer][b], K_layers[layer][0],"),
+    "decode_budget_of_sequence0": ("idx = topk_indices(s, int(ks[b]))",
+                                   "idx = topk_indices(s, int(ks[0]))"),
+    "decode_values_of_layer0": ("V_layers[layer][b], idx, scale)",
+                                "V_layers[0][b], idx, scale)"),
     "sets_wrong_kv_head": ("o, l_ = sparse_gqa_attention(q[g * G:(g + 1) * G], K[:, g:g + 1], V[:, g:g + 1],",
                            "o, l_ = sparse_gqa_attention(q[g * G:(g + 1) * G], K[:, 0:1], V[:, g:g + 1],"),
 }
