@@ -79,6 +79,42 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+SANITIZED_LIB = os.path.join(BUILD_DIR, "libspecctx_hostsan.so")
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    """A host-sanitizer variant for the CPU ABI tests: the C-ABI host code
+    (spec_api.cpp: validation, workspace carve-up, dispatch) compiled by g++
+    with AddressSanitizer and UndefinedBehaviorSanitizer, linked with the
+    kernel objects of the last build().  No device code is instrumented.
+    Loading it needs the ASan runtime preloaded (LD_PRELOAD)."""
+    objs = [os.path.join(BUILD_DIR, os.path.basename(s) + ".o") for s in sources()
+            if not s.endswith("spec_api.cpp")]
+    if not all(os.path.exists(o) for o in objs):
+        build(verbose)
+    san_obj = os.path.join(BUILD_DIR, "spec_api.hostsan.o")
+    gxx = os.environ.get("CXX", "g++")
+    rocm = os.path.dirname(os.path.dirname(HIPCC))
+    cmd = [gxx, "-std=c++17", "-O1", "-g", "-fPIC", "-fno-omit-frame-pointer",
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+           "-D__HIP_PLATFORM_AMD__", f"-I{os.path.join(rocm, 'include')}",
+           f"-I{os.path.join(ROOT, 'include')}", "-c", os.path.join(CSRC, "spec_api.cpp"),
+           "-o", san_obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized compile failed:\n{' '.join(cmd)}\n{r.stderr}")
+    tmp = SANITIZED_LIB + ".tmp"
+    cmd = [gxx, "-shared", "-fPIC", "-fsanitize=address,undefined", "-o", tmp, san_obj, *objs,
+           f"-L{os.path.join(rocm, 'lib')}", "-lamdhip64", f"-Wl,-rpath,{os.path.join(rocm, 'lib')}"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized link failed:\n{' '.join(cmd)}\n{r.stderr}")
+    os.replace(tmp, SANITIZED_LIB)
+    if verbose:
+        print(f"built {SANITIZED_LIB} (host ASan + UBSan on the C-ABI layer)")
+    return SANITIZED_LIB
+
+
 def clean():
     shutil.rmtree(BUILD_DIR, ignore_errors=True)
     if os.path.exists(LIB):

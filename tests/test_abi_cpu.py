@@ -14,6 +14,11 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 @pytest.fixture(scope="module")
 def lib():
+    # SPEC_TEST_LIB names another build of the same library (the host
+    # sanitizer variant, run by test_host_sanitizers in a child process)
+    other = os.environ.get("SPEC_TEST_LIB")
+    if other:
+        return spec.load_library(other)
     if not os.path.exists(spec.lib_path):
         pytest.fail("libspecctx.so is not built (run __graft_entry__.build())")
     return spec.load_library()
@@ -279,3 +284,34 @@ def test_python_wrappers_refuse_cpu_tensors(lib):
         spec.score(q_r, K_r, torch.zeros(1, dtype=torch.int32))
     with pytest.raises(TypeError):
         spec.score(q_r.float(), K_r, torch.zeros(1, dtype=torch.int32))
+
+
+def test_host_sanitizers():
+    """Every ABI test above, again in a child process against the host
+    sanitizer build (spec_api.cpp under AddressSanitizer and
+    UndefinedBehaviorSanitizer): any out-of-bounds access, use of freed
+    memory or undefined behaviour in the host-side validation and
+    workspace carve-up aborts the child."""
+    import subprocess
+    import sys
+
+    from paper_2512_00722_amd import build as b
+
+    if os.environ.get("SPEC_TEST_LIB"):
+        pytest.skip("already the sanitized child")
+    path = b.build_sanitized()
+    nm = subprocess.run(["nm", "-D", path], capture_output=True, text=True).stdout
+    assert "__asan_report_load" in nm and "__ubsan_handle" in nm   # really instrumented
+    asan = subprocess.run(["gcc", "-print-file-name=libasan.so"], capture_output=True,
+                          text=True).stdout.strip()
+    env = dict(os.environ, SPEC_TEST_LIB=path, LD_PRELOAD=asan,
+               ASAN_OPTIONS="detect_leaks=0:abort_on_error=1",
+               UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_abi_cpu.py"),
+                        "-k", "not host_sanitizers"],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    out = r.stdout + r.stderr
+    assert r.returncode == 0, out[-4000:]
+    assert "AddressSanitizer" not in out and "runtime error" not in out, out[-4000:]
+    assert " passed" in out, out[-2000:]
