@@ -56,6 +56,9 @@ def parse():
                     help="time only the retrieval head's front end for the new token "
                          "(embedding row, Q/K projection, YaRN rotary embedding, K_r append): "
                          "--steps calls, replayed from HIP graphs of 20 calls")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="time only the benchmark workload (by default the other four "
+                         "decode-step workloads follow it, under \"configs\")")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run three 1 GiB device-to-device copies (known HBM bytes) so "
                          "that PMC byte counters can be scaled")
@@ -98,6 +101,34 @@ def stored_traffic(workload, path=TRAFFIC_FILE, sources=ATTN_SOURCES):
         return None
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def host_blas():
+    """(threads, description) of the BLAS numpy runs the oracle's products on."""
+    import numpy as np
+    np.ones((64, 64)) @ np.ones((64, 64))   # the BLAS is loaded on first use
+    try:
+        from threadpoolctl import threadpool_info
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if info:
+            i = info[0]
+            return (int(i.get("num_threads", 1)),
+                    f"{i.get('internal_api')} {i.get('version')} ({i.get('threading_layer')}, "
+                    f"{i.get('architecture')})")
+    except Exception:
+        pass
+    return len(os.sched_getaffinity(0)), "unknown"
+
+
 def cpu_baseline(w, x, res, budget_s=20.0):
     """Time the fp64 oracle on a bounded sample of the same step on the host
     cores: every sequence's scoring + top-k, and attention for as many
@@ -108,11 +139,7 @@ def cpu_baseline(w, x, res, budget_s=20.0):
 
     import oracle
 
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = len(os.sched_getaffinity(0))
+    threads, blas = host_blas()
 
     def f64(t):
         return t.float().cpu().numpy().astype(np.float64)
@@ -155,6 +182,8 @@ def cpu_baseline(w, x, res, budget_s=20.0):
         "value": 1.0 / per_step,
         "unit": "steps/s",
         "cores": int(threads),
+        "cpu_model": cpu_model(),
+        "blas": blas,
         "kind": "oracle",
         "sample": (f"fp64 numpy oracle on the same workload, median of {len(per_steps)} "
                    f"step(s): scoring + top-k for all {w.B} sequences, attention for "
@@ -212,6 +241,24 @@ def main():
         print(json.dumps(line), flush=True)
         return
 
+    line = run_fixed(args, spec, w, x, name)
+    if args.workload is None and not args.headline_only:
+        # the other decode-step workloads, each generated, measured and freed in turn
+        del x
+        torch.cuda.empty_cache()
+        line["configs"] = other_configs(args, spec, WORKLOADS, dev)
+    print(json.dumps(line), flush=True)
+
+
+def run_fixed(args, spec, w, x, name):
+    """The fused step on a fixed-length workload: exactly args.steps steps
+    timed between two device synchronisations (the headline), per-step HIP
+    events over as many steps again (median, p10, p90), per-op times from
+    graph replays, the attention kernel against the HBM roofline."""
+    import torch
+    from workloads import algorithmic_bytes
+
+    dev = x["q"].device
     call = dict(q_r=x["q_r"], K_r=x["K_r"], seq_lens=x["seq_lens"], ks=x["ks"], q=x["q"],
                 K=x["K"], V=x["V"], k_max=w.k, head_level=args.head_level)
     outputs = {}
@@ -237,6 +284,8 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
     ev_ms_per_step = ev0.elapsed_time(ev1) / args.steps
     print(f"[bench] {args.steps} steps in {wall:.3f}s", file=sys.stderr, flush=True)
+    per_step = per_step_events(lambda: spec.step(**call, outputs=outputs, ws=ws),
+                               max(args.steps, 50))
 
     # ---- per-op times (same inputs, same stream), HIP events
     counts = outputs["counts"].cpu().tolist()
@@ -330,6 +379,7 @@ def main():
         "step_frac_of_peak": round(step_bytes * value / 1e9 / PEAK_HBM_GBPS, 4),
         "step_algorithmic_bytes": step_bytes,
         "step_ms_events": round(ev_ms_per_step, 4),
+        "step_us": per_step,
         "op_us": {k: round(v, 2) for k, v in op_us.items()},
     }
     if args.variants:
@@ -339,7 +389,70 @@ def main():
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(w, x, res)
-    print(json.dumps(line), flush=True)
+    return line
+
+
+def _spread(t):
+    t = sorted(t)
+    q = lambda f: t[min(len(t) - 1, int(f * len(t)))]
+    return {"n": len(t), "median": round(statistics.median(t), 2), "p10": round(q(0.1), 2),
+            "p90": round(q(0.9), 2), "mean": round(statistics.mean(t), 2)}
+
+
+def per_step_events(fn, n):
+    """Median, p10, p90 and mean of n single steps, each between two HIP
+    events on the launch stream (eager launches, as in the timed loop)."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(n)]
+    for e0, e1 in evs:
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    return _spread([e0.elapsed_time(e1) * 1e3 for e0, e1 in evs])
+
+
+def other_configs(args, spec, workloads, dev):
+    """The other decode-step workloads of the benchmark, one after another
+    (each generated on the GPU, measured, then freed): steps/s, per-step
+    spread, the step's algorithmic bytes against peak, and the attention
+    kernel against the roofline with its stored PMC traffic."""
+    import copy
+
+    import torch
+    from workloads import BENCH_WORKLOAD, algorithmic_bytes, elastic_sequence, generate
+
+    res = {}
+    for name in ("b1_l4096_k512_1layer", "b32_l16384_k1024_hr16", "b1_l131072_k4096_g8",
+                 "b64_ragged_l2k_16k_elastic"):
+        if name == BENCH_WORKLOAD:
+            continue
+        w = workloads[name]
+        a = copy.copy(args)
+        a.no_cpu_baseline, a.variants, a.copy_calibration = True, False, False
+        t0 = time.perf_counter()
+        x = generate(w, seed=args.seed, device=dev)
+        torch.cuda.synchronize()
+        print(f"[bench] config {name} generated in {time.perf_counter() - t0:.1f}s",
+              file=sys.stderr, flush=True)
+        if w.steps > 1:
+            a.steps, a.warmup = 3 * w.steps, w.steps     # three 16-step passes
+            ln = run_elastic(a, spec, w, x, elastic_sequence(w, x, seed=args.seed, device=dev),
+                             algorithmic_bytes)
+        else:
+            ln = run_fixed(a, spec, w, x, name)
+        keep = ("value", "ms_per_step", "step_us", "step_frac_of_peak", "step_hbm_gbps",
+                "step_algorithmic_bytes", "op_us", "first_step_us", "later_steps_us_mean")
+        r = {k: ln[k] for k in keep if k in ln}
+        r["steps"] = a.steps
+        r["roofline"] = {k: ln["roofline"][k] for k in ("achieved", "frac", "traffic",
+                                                         "bytes_per_launch", "avg_launch_us",
+                                                         "kernel")}
+        res[name] = r
+        del x, ln
+        torch.cuda.empty_cache()
+    return res
 
 
 def run_elastic(args, spec, w, x, e, algorithmic_bytes):
@@ -450,6 +563,7 @@ def run_elastic(args, spec, w, x, e, algorithmic_bytes):
         "step_algorithmic_bytes": round(timed_bytes / args.steps),
         "rows_loaded_per_step": deltas,
         "selected_rows": k_total,
+        "step_us": _spread(step_us),
         "first_step_us": round(step_us[0], 1),
         "later_steps_us_mean": round(statistics.mean(step_us[1:]), 1) if S > 1 else None,
     }
@@ -640,11 +754,7 @@ def mla_cpu_baseline(w, x, idx, counts, budget_s=20.0):
     import numpy as np
     import oracle
 
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = len(os.sched_getaffinity(0))
+    threads, blas = host_blas()
 
     def f64(t):
         return t.float().cpu().numpy().astype(np.float64)
@@ -667,7 +777,8 @@ def mla_cpu_baseline(w, x, idx, counts, budget_s=20.0):
         if t_score + t_attn > budget_s:
             break
     per_step = w.B * (t_score + t_attn * w.n_layers / done)
-    return {"value": 1.0 / per_step, "unit": "steps/s", "cores": int(threads), "kind": "oracle",
+    return {"value": 1.0 / per_step, "unit": "steps/s", "cores": int(threads),
+            "cpu_model": cpu_model(), "blas": blas, "kind": "oracle",
             "sample": (f"fp64 numpy oracle: scoring + top-k and MLA attention (per-head keys "
                        f"and values raised from the selected latents) of sequence 0 for "
                        f"{done} of {w.n_layers} layers, scaled to {w.n_layers} layers and "

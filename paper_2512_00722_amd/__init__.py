@@ -387,7 +387,8 @@ class ElasticState:
 
 
 def delta_gather(idx_now: torch.Tensor, counts: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
-                 state: ElasticState, L_max: Optional[int] = None):
+                 state: ElasticState, L_max: Optional[int] = None,
+                 ws: Optional[torch.Tensor] = None):
     """Elastic loading: copy only S_now - S_last rows into freed slots."""
     lib = load_library()
     _check_cache(K, V)
@@ -400,7 +401,7 @@ def delta_gather(idx_now: torch.Tensor, counts: torch.Tensor, K: torch.Tensor, V
     dims = Dims.make(B=B, L_cap=L_cap, L_max=L_cap if L_max is None else L_max, k_max=k_max,
                      n_layers=n_layers, H_q=H_kv, H_kv=H_kv, d=d,
                      kv_stride_layer=K.stride(0), kv_stride_b=K.stride(1))
-    ws, nws = _workspace(dims, OP_DELTA, K.device, None)
+    ws, nws = _workspace(dims, OP_DELTA, K.device, ws)
     el = state.c_struct()
     _check(lib.spec_delta_gather(ctypes.byref(dims), _p(idx_now.contiguous()), _p(counts),
                                  _p(K), _p(V), ctypes.byref(el), _p(ws), nws, _stream(K)),

@@ -33,6 +33,9 @@
 // A unit that covers a whole selection normalises and writes out/lse itself;
 // split selections leave (max, sum, acc) partials that a second kernel merges
 // with a log-sum-exp combine.
+#include <stdlib.h>
+#include <string.h>
+
 #include "device_common.h"
 #include "internal.h"
 
@@ -776,6 +779,18 @@ AttnPlan attn_plan(const Dims& d) {
 
 }  // namespace
 
+int device_cu_count() {
+  static const int n = [] {
+    int dev = 0, n_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n_cu <= 0)
+      n_cu = 256;
+    return n_cu;
+  }();
+  return n;
+}
+
 int attn_split_tokens(const Dims& d) { return attn_plan(d).split; }
 
 size_t attn_ws_bytes(const Dims& d) {
@@ -817,13 +832,14 @@ hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
   // One workgroup per CU, fewer only when there are fewer units than CUs:
   // with few units they are spread over all CUs (each CU's share of the
   // bandwidth is limited) rather than packed four to a CU.
-  int dev = 0, n_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      n_cu <= 0)
-    n_cu = 256;
+  const int n_cu = device_cu_count();
   const dim3 grid((unsigned)(n_items < n_cu ? n_items : n_cu));
-  const bool pipe = n_items > (int64_t)grid.x * kWaves;  // some wavefront takes several units
+  // SPEC_ATTN_SCHEDULE=cold runs every unit from a cold start even where a
+  // wavefront takes several (the tests compare both schedules bit for bit).
+  const char* sched = getenv("SPEC_ATTN_SCHEDULE");
+  const bool force_cold = sched && strcmp(sched, "cold") == 0;
+  // some wavefront takes several units: pipeline them
+  const bool pipe = !force_cold && n_items > (int64_t)grid.x * kWaves;
   if (idx && pipe)
     attn_split_kernel<true, true><<<grid, kWaves * 64, lds_reserve(true), s>>>(a);
   else if (idx)

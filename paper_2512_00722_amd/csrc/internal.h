@@ -102,6 +102,11 @@ struct MlaDims {
 };
 size_t mla_ws_bytes(const MlaDims& d);
 
+// Compute units of the device the process first launches on, queried once
+// and cached (kernels size their grids with it; every grid size is correct,
+// so the launch path makes no device query).
+int device_cu_count();
+
 // ---- launchers (return the HIP launch status) --------------------------
 hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
                         const int32_t* seq_lens, float* scores, void* ws,

@@ -710,14 +710,7 @@ hipError_t launch_mla(const MlaDims& d, const uint16_t* q, const uint16_t* ckv,
                       const uint16_t* w_uk, const uint16_t* w_uv, const int32_t* idx,
                       const int32_t* counts, float* out, float* lse, void* ws, hipStream_t s) {
   const MlaPlan p = mla_plan(d);
-  int n_cu = 256;
-  int dev = 0;
-  if (hipGetDevice(&dev) == hipSuccess) {
-    int v = 0;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        v > 0)
-      n_cu = v;
-  }
+  const int n_cu = device_cu_count();
   MlaArgs a;
   a.q = q;
   a.ckv = ckv;

@@ -1,0 +1,210 @@
+"""Guard bands around every output and workspace buffer of every entry
+point.  Each buffer the library may write is the interior of a larger
+allocation whose two 4 KiB bands (and the interior, before the call) hold a
+fixed byte pattern; after the call the bands must still hold it bit for bit.
+The library clamps device-resident lengths and indices instead of
+validating them, so these cases include ragged, empty, out-of-range and
+split selections.  The outputs themselves are checked against the oracle
+elsewhere; here a few are spot-checked so that a call that did nothing would
+not pass."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2512_00722_amd as spec
+from tests.gpu_helpers import TOL_ATTN, announce, f64, need_gpu
+from workloads import frontend_inputs, generate, generate_mla, small_workload
+
+pytestmark = pytest.mark.gpu
+
+GUARD = 4096
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return need_gpu()
+
+
+class Guarded:
+    """Tensors carved from the interiors of pattern-filled allocations."""
+
+    def __init__(self, dev):
+        self.dev = dev
+        self.bufs = []
+
+    def __call__(self, shape, dtype, name):
+        n = int(np.prod(shape)) * torch.empty((), dtype=dtype).element_size()
+        n_al = (n + 255) // 256 * 256
+        total = GUARD + n_al + GUARD
+        pat = (torch.arange(total, dtype=torch.int64) * 37 + 11) % 251
+        buf = pat.to(torch.uint8).to(self.dev)
+        self.bufs.append((name, buf, pat.to(torch.uint8), n))
+        return buf[GUARD:GUARD + n].view(dtype).view(shape)
+
+    def ws(self, nbytes, name="ws"):
+        return self(((max(nbytes, 16) + 15) // 16 * 16,), torch.uint8, name)
+
+    def check(self, where):
+        torch.cuda.synchronize()
+        for name, buf, pat, n in self.bufs:
+            host = buf.cpu()
+            lo = torch.equal(host[:GUARD], pat[:GUARD])
+            hi = torch.equal(host[GUARD + n:], pat[GUARD + n:])
+            assert lo and hi, f"{where}: {name} written outside its bounds (low {lo}, high {hi})"
+
+
+def _dims(w, x, head_level=False):
+    return spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, H_r=w.H_r, d_r=w.d_r,
+                          n_layers=w.n_layers, H_q=w.H_q, H_kv=w.H_kv, d=w.d,
+                          kr_stride_b=x["K_r"].stride(0), kv_stride_layer=x["K"].stride(0),
+                          kv_stride_b=x["K"].stride(1), n_sets=w.H_kv if head_level else 1)
+
+
+# (B, L, H_r, d_r, n_layers, H_q, H_kv, k, ragged_min): one unit per group,
+# split selections merged by the second kernel, ragged lengths
+CASES = [
+    dict(B=3, L=3000, H_r=8, d_r=64, n_layers=2, H_q=32, H_kv=8, k=700, ragged_min=600,
+         heavy_frac=0.02),
+    dict(B=1, L=20000, H_r=8, d_r=128, n_layers=1, H_q=64, H_kv=8, k=9000, heavy_frac=0.01),
+    dict(B=40, L=700, H_r=16, d_r=64, n_layers=1, H_q=32, H_kv=8, k=128, ragged_min=1,
+         heavy_frac=0.05),
+]
+
+
+@pytest.mark.parametrize("kw", CASES, ids=[str(i) for i in range(len(CASES))])
+@pytest.mark.parametrize("head_level", [False, True], ids=["sets1", "setsHkv"])
+def test_guard_bands_retrieval_and_attention(dev, kw, head_level):
+    announce(f"guard bands {kw} head_level={head_level}")
+    w = small_workload(**kw)
+    x = generate(w, seed=3, device=dev)
+    # out-of-range device lengths and budgets, clamped by the kernels
+    x["seq_lens"][0] = w.L_cap + 1000
+    x["ks"][-1] = 10 ** 6
+    if w.B > 2:
+        x["seq_lens"][1] = 0
+    g = Guarded(dev)
+    n_sets = w.H_kv if head_level else 1
+    sets = (n_sets,) if head_level else ()
+    dims = _dims(w, x, head_level)
+
+    # spec_score
+    scores = g((w.B,) + sets + (w.L_cap,), torch.float32, "scores")
+    ws_s = g.ws(spec.workspace_size(dims, spec.OP_SCORE), "score ws")
+    spec.score(x["q_r"], x["K_r"], x["seq_lens"], out=scores, ws=ws_s, n_sets=n_sets)
+    g.check("spec_score")
+
+    # spec_topk
+    idx = g((w.B,) + sets + (w.k,), torch.int32, "idx")
+    counts = g((w.B,), torch.int32, "counts")
+    ws_t = g.ws(spec.workspace_size(dims, spec.OP_TOPK), "topk ws")
+    spec.topk(scores, x["seq_lens"], x["ks"], w.k, idx=idx, counts=counts, ws=ws_t)
+    g.check("spec_topk")
+    lens = np.minimum(x["seq_lens"].cpu().numpy(), w.L_cap)
+    kb = np.minimum(x["ks"].cpu().numpy(), np.minimum(lens, w.k))
+    assert counts.cpu().numpy().tolist() == kb.tolist()
+
+    # spec_gather
+    ksel = g((w.n_layers, w.B, w.k, w.H_kv, w.d), torch.bfloat16, "K_sel")
+    vsel = g((w.n_layers, w.B, w.k, w.H_kv, w.d), torch.bfloat16, "V_sel")
+    spec.gather(x["K"], x["V"], idx, counts, out=(ksel, vsel))
+    g.check("spec_gather")
+
+    # spec_sparse_decode_attn, indexed and compact
+    out = g((w.n_layers, w.B, w.H_q, w.d), torch.float32, "out")
+    lse = g((w.n_layers, w.B, w.H_q), torch.float32, "lse")
+    dims_a = spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, n_layers=w.n_layers,
+                            H_q=w.H_q, H_kv=w.H_kv, d=w.d, kv_stride_layer=x["K"].stride(0),
+                            kv_stride_b=x["K"].stride(1), n_sets=n_sets)
+    ws_a = g.ws(spec.workspace_size(dims_a, spec.OP_ATTN), "attn ws")
+    spec.sparse_decode_attn(x["q"], x["K"], x["V"], counts, idx=idx, out=out, lse=lse, ws=ws_a)
+    g.check("spec_sparse_decode_attn indexed")
+    out_i = out.clone()
+    if not head_level:
+        out_c = g((w.n_layers, w.B, w.H_q, w.d), torch.float32, "out compact")
+        lse_c = g((w.n_layers, w.B, w.H_q), torch.float32, "lse compact")
+        dims_c = spec.Dims.make(B=w.B, L_cap=w.k, L_max=w.k, k_max=w.k, n_layers=w.n_layers,
+                                H_q=w.H_q, H_kv=w.H_kv, d=w.d)
+        ws_c = g.ws(spec.workspace_size(dims_c, spec.OP_ATTN), "attn ws compact")
+        spec.sparse_decode_attn(x["q"], ksel, vsel, counts, out=out_c, lse=lse_c, ws=ws_c)
+        g.check("spec_sparse_decode_attn compact")
+        assert torch.equal(out_c, out_i)
+
+    # spec_step (and, with one set per sequence, spec_step with elastic loading)
+    o = {"idx": g((w.B,) + sets + (w.k,), torch.int32, "step idx"),
+         "counts": g((w.B,), torch.int32, "step counts"),
+         "out": g((w.n_layers, w.B, w.H_q, w.d), torch.float32, "step out"),
+         "lse": g((w.n_layers, w.B, w.H_q), torch.float32, "step lse"),
+         "scores": g((w.B,) + sets + (w.L_cap,), torch.float32, "step scores")}
+    ws_st = g.ws(spec.workspace_size(dims, spec.OP_STEP), "step ws")
+    spec.step(x["q_r"], x["K_r"], x["seq_lens"], x["ks"], x["q"], x["K"], x["V"], k_max=w.k,
+              outputs=o, ws=ws_st, head_level=head_level)
+    g.check("spec_step")
+    assert torch.equal(o["idx"], idx) and torch.equal(o["out"], out_i)
+    if not head_level:
+        st = spec.ElasticState(w.n_layers, w.B, w.k, w.H_kv, w.d, dev)
+        st.slot_tok = g((w.B, w.k), torch.int32, "slot_tok")
+        st.slot_tok.fill_(-1)
+        st.kbuf = g((w.n_layers, w.B, w.k, w.H_kv, w.d), torch.bfloat16, "kbuf")
+        st.vbuf = g((w.n_layers, w.B, w.k, w.H_kv, w.d), torch.bfloat16, "vbuf")
+        st.n_changed = g((w.B,), torch.int32, "n_changed")
+        for rep in range(2):   # a full load, then an update with nothing changed
+            spec.step(x["q_r"], x["K_r"], x["seq_lens"], x["ks"], x["q"], x["K"], x["V"],
+                      k_max=w.k, outputs=o, ws=ws_st, elastic=st)
+            g.check(f"spec_step elastic {rep}")
+        assert int(st.n_changed.sum()) == 0
+        ws_d = g.ws(spec.workspace_size(dims, spec.OP_DELTA), "delta ws")
+        st.slot_tok.fill_(-1)
+        spec.delta_gather(idx, counts, x["K"], x["V"], st, ws=ws_d)
+        g.check("spec_delta_gather")
+        assert int(st.n_changed.sum()) == int(kb.sum())
+        # the attention of the full step: spot-check one (layer, sequence)
+        b = w.B - 1
+        sel = idx[b, :kb[b]].cpu().numpy()
+        want, _ = oracle.sparse_gqa_attention(f64(x["q"][0, b]), f64(x["K"][0, b]),
+                                              f64(x["V"][0, b]), sel)
+        assert np.abs(out_i[0, b].cpu().numpy() - want).max() <= TOL_ATTN
+
+
+def test_guard_bands_frontend(dev):
+    for B in (3, 24):   # the one-kernel projection and the split partial-sum one
+        announce(f"guard bands front end B={B}")
+        w = small_workload(B=B, L=900, H_r=8, d_r=64, hidden=1024, vocab=500)
+        x = generate(w, seed=4, device=dev, with_kv=False)
+        fe = frontend_inputs(w, x["seq_lens"], seed=4, device=dev)
+        g = Guarded(dev)
+        K_r = g(tuple(x["K_r"].shape), torch.bfloat16, "K_r")
+        K_r.copy_(x["K_r"])
+        q_r = g((w.B, w.H_r, w.d_r), torch.bfloat16, "q_r")
+        dims = spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=1, H_r=w.H_r,
+                              d_r=w.d_r, n_layers=1, H_q=1, H_kv=1, d=128,
+                              kr_stride_b=K_r.stride(0))
+        ws = g.ws(spec.workspace_size(dims, spec.OP_FRONTEND), "frontend ws")
+        spec.retrieval_qk(fe["tokens"], fe["pos"], fe["emb"], fe["w_q"], fe["w_k"], K_r,
+                          rope_base=w.rope_base, yarn_scale=w.yarn_scale,
+                          yarn_orig_ctx=w.orig_ctx, q_r=q_r, ws=ws)
+        g.check("spec_retrieval_qk")
+        assert torch.isfinite(q_r.float()).all() and q_r.float().abs().sum() > 0
+
+
+def test_guard_bands_mla(dev):
+    announce("guard bands MLA")
+    w = small_workload(B=3, L=2500, k=2100, n_layers=2, H_q=128, H_kv=1, mla=True)
+    x = generate_mla(w, seed=5, device=dev)
+    rng = np.random.default_rng(5)
+    counts = np.array([2100, 0, 37], dtype=np.int32)
+    idx = np.full((w.B, w.k), -1, dtype=np.int32)
+    for b in range(w.B):
+        idx[b, :counts[b]] = np.sort(rng.choice(w.L, counts[b], replace=False))
+    g = Guarded(dev)
+    out = g((w.n_layers, w.B, w.H_q, w.d_v), torch.float32, "mla out")
+    lse = g((w.n_layers, w.B, w.H_q), torch.float32, "mla lse")
+    dims = spec.MlaDims.make(B=w.B, L_cap=w.L_cap, k_max=w.k, n_layers=w.n_layers, H=w.H_q,
+                             ckv_stride_layer=x["ckv"].stride(0), ckv_stride_b=x["ckv"].stride(1))
+    ws = g.ws(spec.mla_workspace_size(dims), "mla ws")
+    spec.mla_sparse_decode_attn(x["q_mla"], x["ckv"], x["w_uk"], x["w_uv"],
+                                torch.as_tensor(idx, device=dev), torch.as_tensor(counts, device=dev),
+                                out=out, lse=lse, ws=ws)
+    g.check("spec_mla_sparse_decode_attn")
+    assert torch.all(out[:, 1] == 0) and torch.all(torch.isneginf(lse[:, 1]))
+    assert torch.isfinite(out).all()

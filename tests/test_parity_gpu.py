@@ -162,7 +162,14 @@ ATTN_CASES = [
     (1, 2, 500, 32, 1, [300, 17], 300),
     (2, 1, 9000, 64, 1, [8500], 8500),
     (1, 2, 400, 64, 2, [200, 0], 256),
+    # more work units than resident wavefronts (> 1024): units pipelined
+    # across their boundaries, one per (layer, sequence, KV head) group with
+    # empty selections breaking the chain; and split selections (partials)
+    # whose empty splits restart the pipeline cold
+    (5, 32, 160, 32, 8, [(37 * b) % 129 for b in range(32)], 128),
+    (1, 3, 20000, 8, 8, [16384, 0, 9001], 16384),
 ]
+PIPE_CASES = ATTN_CASES[-2:]
 
 
 def _attn_inputs(case, g):
@@ -206,6 +213,39 @@ def test_attention_indexed(dev, case):
                                        idx=idx.to(dev))
     worst = _check_attn(out.cpu().numpy(), lse.cpu().numpy(), q, K, V, idx, counts, case)
     print(f"max abs err {worst:.3e}")
+
+
+@pytest.mark.parametrize("case", PIPE_CASES, ids=[str(c[:5]) for c in PIPE_CASES])
+def test_pipelined_units_equal_cold_units(dev, case, monkeypatch):
+    """The pipelined schedule (a wavefront's next unit fetched and staged
+    while the current one streams) gives the same bits as every unit
+    starting cold, in indexed and compact mode."""
+    announce(f"attn pipelined vs cold {case}")
+    g = torch.Generator().manual_seed(7 + sum(case[:5]))
+    q, K, V, idx, counts = _attn_inputs(case, g)
+    qd, Kd, Vd, idxd, cd = q.to(dev), K.to(dev), V.to(dev), idx.to(dev), counts.to(dev)
+    ks, vs = spec.gather(Kd, Vd, idxd, cd)
+    runs = {}
+    for sched in ("auto", "cold"):
+        if sched == "cold":
+            monkeypatch.setenv("SPEC_ATTN_SCHEDULE", "cold")
+        else:
+            monkeypatch.delenv("SPEC_ATTN_SCHEDULE", raising=False)
+        runs[sched] = (spec.sparse_decode_attn(qd, Kd, Vd, cd, idx=idxd),
+                       spec.sparse_decode_attn(qd, ks, vs, cd))
+    monkeypatch.delenv("SPEC_ATTN_SCHEDULE", raising=False)
+    for mode in (0, 1):
+        (o_a, l_a), (o_c, l_c) = runs["auto"][mode], runs["cold"][mode]
+        assert torch.equal(o_a, o_c) and torch.equal(l_a, l_c), mode
+    _check_attn(runs["auto"][0][0].cpu().numpy(), runs["auto"][0][1].cpu().numpy(), q, K, V, idx,
+                counts, case)
+    n_layers = case[0]
+    if n_layers > 1:   # one layer per call: fewer units, every one cold; same plan per group
+        for layer in range(n_layers):
+            o_l, l_l = spec.sparse_decode_attn(qd[layer:layer + 1], Kd[layer:layer + 1],
+                                               Vd[layer:layer + 1], cd, idx=idxd)
+            assert torch.equal(o_l[0], runs["auto"][0][0][layer]), layer
+            assert torch.equal(l_l[0], runs["auto"][0][1][layer]), layer
 
 
 @pytest.mark.parametrize("case", ATTN_CASES[:4], ids=[str(c) for c in ATTN_CASES[:4]])

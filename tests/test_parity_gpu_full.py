@@ -1,7 +1,10 @@
 """Full-size decode-step workloads through the fused step (the launch
-configuration the benchmark times), checked against the fp64 oracle on
-sampled sequences and layers, and by properties that hold at any size on all
-sequences."""
+configuration the benchmark times).  Every sequence's fp32 scores are
+checked against the fp64 oracle and its index set is accepted against the
+oracle's; every (layer, sequence) output is checked against an fp32
+reference over the selected rows (outputs are NaN-filled before the call, so
+an unwritten row fails); every layer of one sequence is checked against the
+fp64 oracle."""
 import numpy as np
 import pytest
 import torch
@@ -26,13 +29,79 @@ def _sample_layers(n):
     return sorted({0, n // 2, n - 1})
 
 
+def _poisoned_outputs(w, dev, head_level=False):
+    """Step outputs pre-filled with values no call may leave behind."""
+    sets = (w.H_kv,) if head_level else ()
+    return {"idx": torch.full((w.B,) + sets + (w.k,), -7, dtype=torch.int32, device=dev),
+            "counts": torch.full((w.B,), -7, dtype=torch.int32, device=dev),
+            "out": torch.full((w.n_layers, w.B, w.H_q, w.d), float("nan"), device=dev),
+            "lse": torch.full((w.n_layers, w.B, w.H_q), float("nan"), device=dev),
+            "scores": torch.full((w.B,) + sets + (w.L_cap,), float("nan"), device=dev)}
+
+
+def _attn_ref_fp32(q_l, K_l, V_l, idx, counts, scale):
+    """fp32 decode attention of one layer for every sequence over its selected
+    rows (torch on the GPU, operands made contiguous): q_l [B, H_q, d],
+    K_l/V_l [B, L_cap, H_kv, d], idx [B, k_max] (rows j < counts[b])."""
+    B, H_q, d = q_l.shape
+    H_kv = K_l.shape[2]
+    G = H_q // H_kv
+    k_max = idx.shape[1]
+    ar = torch.arange(B, device=idx.device)[:, None]
+    rows = idx.long().clamp(min=0)
+    Ks = K_l[ar, rows].float().permute(0, 2, 3, 1).contiguous()   # [B, H_kv, d, k]
+    Vs = V_l[ar, rows].float().permute(0, 2, 1, 3).contiguous()   # [B, H_kv, k, d]
+    qg = q_l.float().view(B, H_kv, G, d).contiguous()
+    S = torch.matmul(qg, Ks) * scale                              # [B, H_kv, G, k]
+    valid = torch.arange(k_max, device=idx.device)[None, :] < counts.long()[:, None]
+    S = S.masked_fill(~valid[:, None, None, :], float("-inf"))
+    lse = torch.logsumexp(S, dim=-1)
+    P = torch.softmax(S, dim=-1).nan_to_num(0.0)                  # empty rows: 0
+    O = torch.matmul(P, Vs)
+    return O.reshape(B, H_q, d), lse.reshape(B, H_q)
+
+
+def _check_every_output(r, q, K, V, idx, counts, n_layers, what):
+    """Every (layer, sequence, head) output against the fp32 reference; an
+    empty selection must give out = 0 and lse = -inf."""
+    torch.backends.cuda.matmul.allow_tf32 = False
+    scale = 1.0 / np.sqrt(q.shape[-1])
+    empty = counts == 0
+    worst = 0.0
+    for layer in range(n_layers):
+        want, wl = _attn_ref_fp32(q[layer], K[layer], V[layer], idx, counts, scale)
+        got, gl = r["out"][layer], r["lse"][layer]
+        assert torch.isfinite(got).all(), (what, layer, "unwritten or non-finite output")
+        err = (got - want).abs().max().item()
+        worst = max(worst, err)
+        assert err <= TOL_ATTN, (what, layer, err)
+        assert torch.all(torch.isneginf(gl[empty])) and torch.all(got[empty] == 0)
+        ne = ~empty
+        assert torch.isfinite(gl[ne]).all()
+        assert (gl[ne] - wl[ne]).abs().max().item() <= TOL_ATTN if ne.any() else True
+    return worst
+
+
+def _check_all_layers_oracle(r, x, q, b, idx_b, n_layers, what):
+    """Every layer of sequence b against the fp64 oracle."""
+    kb = len(idx_b)
+    sel_t = torch.as_tensor(idx_b, device=x["K"].device, dtype=torch.long)
+    for layer in range(n_layers):
+        Ks = f64(x["K"][layer, b, sel_t])
+        Vs = f64(x["V"][layer, b, sel_t])
+        want, wl = oracle.sparse_gqa_attention(f64(q[layer, b]), Ks, Vs, np.arange(kb))
+        got = r["out"][layer, b].cpu().numpy()
+        assert np.abs(got - want).max() <= TOL_ATTN, (what, layer, np.abs(got - want).max())
+        assert np.abs(r["lse"][layer, b].cpu().numpy() - wl).max() <= TOL_ATTN, (what, layer)
+
+
 @pytest.mark.parametrize("name", FIXED)
 def test_full_size_step(dev, name):
     w = WORKLOADS[name]
     announce(f"full-size step {name}")
     x = generate(w, seed=0, device=dev)
     r = spec.step(x["q_r"], x["K_r"], x["seq_lens"], x["ks"], x["q"], x["K"], x["V"], k_max=w.k,
-                  with_scores=True, with_lse=True)
+                  outputs=_poisoned_outputs(w, dev))
     torch.cuda.synchronize()
     idx = r["idx"].cpu().numpy()
     cnt = r["counts"].cpu().numpy()
@@ -40,64 +109,76 @@ def test_full_size_step(dev, name):
     lens = x["seq_lens"].cpu().numpy()
     ks = x["ks"].cpu().numpy()
 
-    # properties on every sequence
+    # every sequence: properties, fp64 scores, the accepted set, planted tokens
     for b in range(w.B):
         L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
         assert cnt[b] == kb
         sel = idx[b, :kb]
         assert np.all(np.diff(sel) > 0) and sel[0] >= 0 and sel[-1] < L
         assert np.all(idx[b, kb:] == -1)
+        assert np.all(np.isneginf(sc[b, L:]))
         assert abs(sc[b, :L].sum() - w.H_r) < 1e-3 * w.H_r       # softmax rows sum to 1
         assert sel.tolist() == oracle.topk_indices(sc[b, :L], kb).tolist()  # exact on fp32 keys
-    assert np.all(np.isfinite(r["out"].cpu().numpy()))
-
-    # element-wise parity on sampled sequences and layers
-    for b in sorted({0, w.B - 1}):
-        L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
         s64 = oracle.retrieval_scores(f64(x["q_r"][b]), f64(x["K_r"][b, :L]), L)
         err = np.abs(sc[b, :L] - s64)
-        assert np.all(err <= SCORE_ABS + SCORE_REL * s64), err.max()
-        ok, info = oracle.accept_index_set(s64, kb, idx[b, :kb])
-        assert ok, info
-        print(f"b={b}: tie-band population {info['band_pop']}, set difference {info['sym_diff']}")
+        assert np.all(err <= SCORE_ABS + SCORE_REL * s64), (b, err.max())
+        ok, info = oracle.accept_index_set(s64, kb, sel)
+        assert ok, (b, info)
+        if b in (0, w.B - 1):
+            print(f"b={b}: tie-band population {info['band_pop']}, "
+                  f"set difference {info['sym_diff']}")
         heavy = x["heavy"][b]
         if len(heavy):
-            recall = np.isin(heavy, idx[b, :kb]).mean()
-            print(f"b={b}: planted-token recall {recall:.4f}")
-            assert recall >= 0.99
-        sel_t = torch.as_tensor(idx[b, :kb], device=dev, dtype=torch.long)
+            recall = np.isin(heavy, sel).mean()
+            assert recall >= 0.99, (b, recall)
+
+    # every (layer, sequence): the fp32 reference over the selected rows
+    worst = _check_every_output(r, x["q"], x["K"], x["V"], r["idx"], r["counts"], w.n_layers,
+                                name)
+    print(f"every output vs the fp32 reference: max abs err {worst:.2e}")
+    # every layer of the last sequence, and sampled layers of the first: fp64 oracle
+    b = w.B - 1
+    _check_all_layers_oracle(r, x, x["q"], b, idx[b, :cnt[b]], w.n_layers, name)
+    if w.B > 1:
+        sel_t = torch.as_tensor(idx[0, :cnt[0]], device=dev, dtype=torch.long)
         for layer in _sample_layers(w.n_layers):
-            Ks = f64(x["K"][layer, b, sel_t])
-            Vs = f64(x["V"][layer, b, sel_t])
-            want, wl = oracle.sparse_gqa_attention(f64(x["q"][layer, b]), Ks, Vs, np.arange(kb))
-            got = r["out"][layer, b].cpu().numpy()
-            assert np.abs(got - want).max() <= TOL_ATTN, (layer, np.abs(got - want).max())
-            assert np.abs(r["lse"][layer, b].cpu().numpy() - wl).max() <= TOL_ATTN
+            want, wl = oracle.sparse_gqa_attention(f64(x["q"][layer, 0]),
+                                                   f64(x["K"][layer, 0, sel_t]),
+                                                   f64(x["V"][layer, 0, sel_t]),
+                                                   np.arange(int(cnt[0])))
+            assert np.abs(r["out"][layer, 0].cpu().numpy() - want).max() <= TOL_ATTN
     del x, r
     torch.cuda.empty_cache()
 
 
 def test_full_size_elastic_sequence(dev):
     """The ragged 64-sequence workload over its 16 appended-token steps with
-    elastic loading.  Every sequence, every step: the slot buffer holds
-    exactly the selected set, and the rows loaded equal |S_now - S_last|.
-    Sampled sequences: scores vs fp64, index-set acceptance, the slot->token
-    map equals the oracle's elastic update of the previous map, held K/V rows
-    are bit-exact copies, and attention matches the oracle on sampled layers."""
+    elastic loading.  Every sequence, every step: fp32 scores vs fp64, the
+    index set accepted against the oracle's and exact on its own fp32 keys,
+    the slot->token map equal to the oracle's elastic update of the previous
+    map, the rows loaded equal to |S_now - S_last|, the held K/V rows
+    bit-exact copies of the cache rows (every layer at the first and last
+    steps, the first and last layers in between), and every (layer,
+    sequence) output against the fp32 reference over the cache rows at the
+    selected indices.  Every layer of one sequence against the fp64 oracle
+    at the first and last steps."""
     w = WORKLOADS["b64_ragged_l2k_16k_elastic"]
     announce(f"full-size elastic sequence {w.name}")
     x = generate(w, seed=0, device=dev)
     e = elastic_sequence(w, x, seed=0, device=dev)
     st = spec.ElasticState(w.n_layers, w.B, w.k, w.H_kv, w.d, dev)
     ks = x["ks"].cpu().numpy()
-    sample = sorted({0, w.B // 2, w.B - 1})
-    slot_ref = {b: np.full(w.k, -1, dtype=np.int64) for b in sample}
+    L_last = e["seq_lens"][w.steps - 1].cpu().numpy()
+    kr64 = [f64(x["K_r"][b, :int(L_last[b])]) for b in range(w.B)]   # the cache only grows
+    slot_ref = [np.full(w.k, -1, dtype=np.int64) for _ in range(w.B)]
     prev = [np.zeros(0, dtype=np.int64) for _ in range(w.B)]
     overlap = []
+    ar = torch.arange(w.B, device=dev)[:, None]
     for s in range(w.steps):
         lens_t = e["seq_lens"][s]
         r = spec.step(q_r=e["q_r"][s], K_r=x["K_r"], seq_lens=lens_t, ks=x["ks"], q=e["q"][s],
-                      K=x["K"], V=x["V"], k_max=w.k, elastic=st, with_scores=True, with_lse=True)
+                      K=x["K"], V=x["V"], k_max=w.k, elastic=st,
+                      outputs=_poisoned_outputs(w, dev))
         torch.cuda.synchronize()
         lens = lens_t.cpu().numpy()
         idx = r["idx"].cpu().numpy()
@@ -105,60 +186,56 @@ def test_full_size_elastic_sequence(dev):
         sc = r["scores"].cpu().numpy().astype(np.float64)
         slots = st.slot_tok.cpu().numpy()
         nch = st.n_changed.cpu().numpy()
+        qr64 = f64(e["q_r"][s])
         for b in range(w.B):
             L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
             sel = idx[b, :kb].astype(np.int64)
             assert cnt[b] == kb
+            assert np.all(idx[b, kb:] == -1)
             assert sel.tolist() == oracle.topk_indices(sc[b, :L], kb).tolist(), (s, b)
-            assert sorted(slots[b, :kb].tolist()) == sel.tolist(), (s, b)
-            assert np.all(slots[b, kb:] == -1)
-            assert nch[b] == len(np.setdiff1d(sel, prev[b])), (s, b)
+            s64 = oracle.retrieval_scores(qr64[b], kr64[b], L)
+            err = np.abs(sc[b, :L] - s64)
+            assert np.all(err <= SCORE_ABS + SCORE_REL * s64), (s, b, err.max())
+            ok, info = oracle.accept_index_set(s64, kb, sel)
+            assert ok, (s, b, info)
+            slot_ref[b], loads = oracle.elastic_update(slot_ref[b], sel)
+            assert slots[b].tolist() == slot_ref[b].tolist(), (s, b)
+            assert len(loads) == nch[b] == len(np.setdiff1d(sel, prev[b])), (s, b)
             if s > 0:
                 overlap.append(len(np.intersect1d(sel, prev[b])) / kb)
             prev[b] = sel
-        for b in sample:
-            L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
-            s64 = oracle.retrieval_scores(f64(e["q_r"][s, b]), f64(x["K_r"][b, :L]), L)
-            err = np.abs(sc[b, :L] - s64)
-            assert np.all(err <= SCORE_ABS + SCORE_REL * s64), (s, b, err.max())
-            ok, info = oracle.accept_index_set(s64, kb, idx[b, :kb])
-            assert ok, (s, b, info)
-            slot_ref[b], loads = oracle.elastic_update(slot_ref[b], idx[b, :kb])
-            assert slots[b].tolist() == slot_ref[b].tolist(), (s, b)
-            assert len(loads) == nch[b]
-            held = torch.as_tensor(np.nonzero(slot_ref[b] >= 0)[0], device=dev)
-            toks = torch.as_tensor(slot_ref[b][slot_ref[b] >= 0], device=dev)
-            for layer in (0, w.n_layers - 1):
-                assert torch.equal(st.kbuf[layer, b, held].view(torch.int16),
-                                   x["K"][layer, b, toks].view(torch.int16)), (s, b, layer)
-                assert torch.equal(st.vbuf[layer, b, held].view(torch.int16),
-                                   x["V"][layer, b, toks].view(torch.int16)), (s, b, layer)
-            if s in (0, w.steps - 1):
-                sel_t = torch.as_tensor(idx[b, :kb], device=dev, dtype=torch.long)
-                for layer in _sample_layers(w.n_layers):
-                    Ks = f64(x["K"][layer, b, sel_t])
-                    Vs = f64(x["V"][layer, b, sel_t])
-                    want, wl = oracle.sparse_gqa_attention(f64(e["q"][s, layer, b]), Ks, Vs,
-                                                           np.arange(kb))
-                    got = r["out"][layer, b].cpu().numpy()
-                    assert np.abs(got - want).max() <= TOL_ATTN, (s, b, layer)
-                    assert np.abs(r["lse"][layer, b].cpu().numpy() - wl).max() <= TOL_ATTN
+        # held rows: slot j of sequence b holds the cache row of token slot_tok[b, j]
+        held = st.slot_tok >= 0
+        toks = st.slot_tok.long().clamp(min=0)
+        layers = range(w.n_layers) if s in (0, w.steps - 1) else (0, w.n_layers - 1)
+        for layer in layers:
+            for buf, cache in ((st.kbuf, x["K"]), (st.vbuf, x["V"])):
+                want = cache[layer][ar, toks].view(torch.int16)
+                assert torch.equal(buf[layer].view(torch.int16)[held], want[held]), (s, layer)
+        _check_every_output(r, e["q"][s], x["K"], x["V"], r["idx"], r["counts"], w.n_layers,
+                            f"elastic step {s}")
+        if s in (0, w.steps - 1):
+            b = w.B // 2
+            _check_all_layers_oracle(r, x, e["q"][s], b, idx[b, :cnt[b]], w.n_layers,
+                                     f"elastic step {s}")
     print(f"adjacent-step overlap: min {min(overlap):.3f} mean {np.mean(overlap):.3f}")
     assert np.mean(overlap) > 0.7
-    del x, e, st, r
+    del x, e, st, r, kr64
     torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("name", ["b8_l32768_k2048_32layers", "b32_l16384_k1024_hr16"])
 def test_full_size_step_head_level(dev, name):
     """One token set per KV head at full size: every row's selection is the
-    exact top-k of its fp32 scores; sampled sequences match the fp64 oracle
-    (scores, accepted sets, attention over each head's own set)."""
+    exact top-k of its fp32 scores, its scores match the fp64 oracle and its
+    set is accepted against the oracle's; sampled sequences' attention over
+    each head's own set matches the fp64 oracle, and no output is left
+    unwritten."""
     w = WORKLOADS[name]
     announce(f"full-size head-level step {name}")
     x = generate(w, seed=0, device=dev)
     r = spec.step(x["q_r"], x["K_r"], x["seq_lens"], x["ks"], x["q"], x["K"], x["V"], k_max=w.k,
-                  with_scores=True, with_lse=True, head_level=True)
+                  outputs=_poisoned_outputs(w, dev, head_level=True), head_level=True)
     torch.cuda.synchronize()
     idx = r["idx"].cpu().numpy()
     cnt = r["counts"].cpu().numpy()
@@ -168,17 +245,17 @@ def test_full_size_step_head_level(dev, name):
     for b in range(w.B):
         L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
         assert cnt[b] == kb
+        s64 = oracle.head_level_scores(f64(x["q_r"][b]), f64(x["K_r"][b, :L]), L, w.H_kv)
         for h in range(w.H_kv):
             assert idx[b, h, :kb].tolist() == oracle.topk_indices(sc[b, h, :L], kb).tolist()
             assert np.all(idx[b, h, kb:] == -1)
-    for b in sorted({0, w.B - 1}):
-        L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
-        s64 = oracle.head_level_scores(f64(x["q_r"][b]), f64(x["K_r"][b, :L]), L, w.H_kv)
-        for h in range(w.H_kv):
             err = np.abs(sc[b, h, :L] - s64[h])
             assert np.all(err <= SCORE_ABS + SCORE_REL * s64[h]), (b, h, err.max())
             ok, info = oracle.accept_index_set(s64[h], kb, idx[b, h, :kb])
             assert ok, (b, h, info)
+    assert torch.isfinite(r["out"]).all() and torch.isfinite(r["lse"]).all()
+    for b in sorted({0, w.B - 1}):
+        L, kb = int(lens[b]), min(int(ks[b]), int(lens[b]))
         rows = sorted(set(np.concatenate([idx[b, h, :kb] for h in range(w.H_kv)]).tolist()))
         rows_t = torch.as_tensor(rows, device=dev, dtype=torch.long)
         pos = {t: i for i, t in enumerate(rows)}
