@@ -53,7 +53,8 @@
  *    two up to 128, H_kv > 16, n_sets not 1 or H_kv, n_sets = H_kv with H_r
  *    not a multiple of H_kv or B*n_sets > 65535, B or n_layers > 65535, and
  *    for elastic loading L_cap > 245760 or n_sets != 1.  SPEC_ERR_WORKSPACE: ws_bytes
- *    below spec_workspace_size().  SPEC_ERR_HIP: a launch failed; the HIP
+ *    below spec_workspace_size() (SPEC_ERR_TOO_LARGE: above the static scratch
+ *    of spec_step_noalloc).  SPEC_ERR_HIP: a launch failed; the HIP
  *    error code is kept (per thread) for spec_last_hip_error().
  *  - Calls are reentrant; concurrent calls must not share a workspace.
  *  - Debugging: with the environment variable SPEC_DEBUG=1 (read at every
@@ -83,7 +84,9 @@ typedef enum spec_status {
   SPEC_ERR_INVALID = 1,
   SPEC_ERR_UNSUPPORTED = 2,
   SPEC_ERR_WORKSPACE = 3,
-  SPEC_ERR_HIP = 4
+  SPEC_ERR_HIP = 4,
+  SPEC_ERR_TOO_LARGE = 5  /* spec_step_noalloc: the step needs more workspace
+                             than its static scratch holds                   */
 } spec_status;
 
 typedef enum spec_op {
@@ -224,6 +227,31 @@ SPEC_API spec_status spec_step(const spec_dims* dm, const uint16_t* q_r,
                       int32_t* idx_out, int32_t* counts_out, float* out,
                       float* lse, float* scores_out, const spec_elastic* el,
                       void* ws, size_t ws_bytes, spec_stream stream);
+
+/* The fused decode step of spec_step without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops that forbid allocation).  Arguments, outputs and errors are
+ * those of spec_step.  The workspace is a static device array of
+ * spec_step_noalloc_max_bytes() bytes (64 MiB) that every GPU the library
+ * runs on holds from the first call until the process ends; the call itself
+ * allocates nothing.  A step whose spec_workspace_size(SPEC_OP_STEP)
+ * exceeds it returns SPEC_ERR_TOO_LARGE before any HIP call (the five
+ * benchmark workloads need 0.3-53 MB with one set per sequence).  All calls
+ * on one GPU share that GPU's array, which keeps the last call's contents
+ * (no part of it needs to start zeroed): calls that overlap on one GPU
+ * (concurrent streams or threads) race and must be serialised by the
+ * caller.  The first call on a GPU looks the array's device address up
+ * (hipGetSymbolAddress), so make it once outside any graph capture.      */
+SPEC_API spec_status spec_step_noalloc(const spec_dims* dm, const uint16_t* q_r,
+                              const uint16_t* k_r, const int32_t* seq_lens,
+                              const int32_t* ks, const uint16_t* q,
+                              const uint16_t* k_cache, const uint16_t* v_cache,
+                              int32_t* idx_out, int32_t* counts_out, float* out,
+                              float* lse, float* scores_out, const spec_elastic* el,
+                              spec_stream stream);
+
+/* Size in bytes of spec_step_noalloc's static scratch (per GPU).            */
+SPEC_API size_t spec_step_noalloc_max_bytes(void);
 
 /* Retrieval-head front end parameters (host struct).                        */
 typedef struct spec_frontend {

@@ -22,7 +22,8 @@ import torch
 
 __all__ = [
     "SpecError", "load_library", "lib_path", "Dims", "workspace_size", "score", "topk",
-    "gather", "sparse_decode_attn", "delta_gather", "ElasticState", "step", "Frontend",
+    "gather", "sparse_decode_attn", "delta_gather", "ElasticState", "step", "step_noalloc",
+    "step_noalloc_max_bytes", "Frontend",
     "retrieval_qk", "MlaDims", "mla_workspace_size", "mla_sparse_decode_attn",
     "OP_SCORE", "OP_TOPK", "OP_GATHER", "OP_ATTN", "OP_DELTA", "OP_STEP", "OP_FRONTEND",
     "EXPORTED_SYMBOLS",
@@ -33,10 +34,11 @@ lib_path = os.path.join(_PKG, "libspecctx.so")
 
 OP_SCORE, OP_TOPK, OP_GATHER, OP_ATTN, OP_DELTA, OP_STEP, OP_FRONTEND = range(7)
 STATUS = {0: "SPEC_OK", 1: "SPEC_ERR_INVALID", 2: "SPEC_ERR_UNSUPPORTED",
-          3: "SPEC_ERR_WORKSPACE", 4: "SPEC_ERR_HIP"}
+          3: "SPEC_ERR_WORKSPACE", 4: "SPEC_ERR_HIP", 5: "SPEC_ERR_TOO_LARGE"}
 
 EXPORTED_SYMBOLS = ["spec_score", "spec_topk", "spec_gather", "spec_sparse_decode_attn",
-                    "spec_delta_gather", "spec_step", "spec_retrieval_qk",
+                    "spec_delta_gather", "spec_step", "spec_step_noalloc",
+                    "spec_step_noalloc_max_bytes", "spec_retrieval_qk",
                     "spec_mla_sparse_decode_attn", "spec_mla_workspace_size", "spec_workspace_size",
                     "spec_status_string", "spec_last_hip_error", "spec_version"]
 
@@ -128,6 +130,7 @@ def load_library(path: Optional[str] = None):
         "spec_sparse_decode_attn": [D, P, P, P, P, P, P, P, P, S, P],
         "spec_delta_gather": [D, P, P, P, P, E, P, S, P],
         "spec_step": [D, P, P, P, P, P, P, P, P, P, P, P, P, E, P, S, P],
+        "spec_step_noalloc": [D, P, P, P, P, P, P, P, P, P, P, P, P, E, P],
         "spec_retrieval_qk": [D, F, P, P, P, P, P, P, P, P, S, P],
         "spec_mla_sparse_decode_attn": [M, P, P, P, P, P, P, P, P, P, S, P],
         "spec_mla_workspace_size": [M, ctypes.POINTER(S)],
@@ -143,6 +146,8 @@ def load_library(path: Optional[str] = None):
     lib.spec_last_hip_error.restype = ctypes.c_int
     lib.spec_version.argtypes = []
     lib.spec_version.restype = ctypes.c_char_p
+    lib.spec_step_noalloc_max_bytes.argtypes = []
+    lib.spec_step_noalloc_max_bytes.restype = ctypes.c_size_t
     if path is None:
         _lib = lib
     return lib
@@ -409,15 +414,9 @@ def delta_gather(idx_now: torch.Tensor, counts: torch.Tensor, K: torch.Tensor, V
     return state
 
 
-def step(q_r, K_r, seq_lens, ks, q, K, V, k_max: int, L_max: Optional[int] = None,
-         scale_r: float = 0.0, scale: float = 0.0, elastic: Optional[ElasticState] = None,
-         with_scores: bool = False, with_lse: bool = False, ws: Optional[torch.Tensor] = None,
-         outputs: Optional[dict] = None, head_level: bool = False):
-    """One fused decode step (score -> top-k -> [elastic load] -> attention).
-    Returns a dict with idx, counts, out and optionally lse and scores.
-    head_level selects one token set per KV head (idx [B, H_kv, k_max],
-    scores [B, H_kv, L_max]) instead of one per sequence."""
-    lib = load_library()
+def _step_args(q_r, K_r, seq_lens, ks, q, K, V, k_max, L_max, scale_r, scale, with_scores,
+               with_lse, outputs, head_level):
+    """Checks and dims of a fused step; the outputs dict (allocated if absent)."""
     _need(q_r, "q_r", torch.bfloat16, 3)
     _need(K_r, "K_r", torch.bfloat16, 4)
     _need(q, "q", torch.bfloat16, 4)
@@ -438,7 +437,6 @@ def step(q_r, K_r, seq_lens, ks, q, K, V, k_max: int, L_max: Optional[int] = Non
                      kr_stride_b=K_r.stride(0), kv_stride_layer=K.stride(0),
                      kv_stride_b=K.stride(1), scale_r=scale_r, scale=scale,
                      n_sets=H_kv if head_level else 1)
-    ws, nws = _workspace(dims, OP_STEP, q.device, ws)
     dev = q.device
     sets = (H_kv,) if head_level else ()
     o = outputs if outputs is not None else {}
@@ -452,6 +450,21 @@ def step(q_r, K_r, seq_lens, ks, q, K, V, k_max: int, L_max: Optional[int] = Non
                        if with_scores else None)
     elif tuple(o["idx"].shape) != (B,) + sets + (int(k_max),):
         raise ValueError("outputs do not match the selection layout")
+    return dims, o
+
+
+def step(q_r, K_r, seq_lens, ks, q, K, V, k_max: int, L_max: Optional[int] = None,
+         scale_r: float = 0.0, scale: float = 0.0, elastic: Optional[ElasticState] = None,
+         with_scores: bool = False, with_lse: bool = False, ws: Optional[torch.Tensor] = None,
+         outputs: Optional[dict] = None, head_level: bool = False):
+    """One fused decode step (score -> top-k -> [elastic load] -> attention).
+    Returns a dict with idx, counts, out and optionally lse and scores.
+    head_level selects one token set per KV head (idx [B, H_kv, k_max],
+    scores [B, H_kv, L_max]) instead of one per sequence."""
+    lib = load_library()
+    dims, o = _step_args(q_r, K_r, seq_lens, ks, q, K, V, k_max, L_max, scale_r, scale,
+                         with_scores, with_lse, outputs, head_level)
+    ws, nws = _workspace(dims, OP_STEP, q.device, ws)
     el = elastic.c_struct() if elastic is not None else None
     _check(lib.spec_step(ctypes.byref(dims), _p(q_r), _p(K_r), _p(seq_lens), _p(ks), _p(q),
                          _p(K), _p(V), _p(o["idx"]), _p(o["counts"]), _p(o["out"]),
@@ -459,6 +472,32 @@ def step(q_r, K_r, seq_lens, ks, q, K, V, k_max: int, L_max: Optional[int] = Non
                          ctypes.byref(el) if el is not None else None, _p(ws), nws,
                          _stream(q)), "spec_step")
     return o
+
+
+def step_noalloc(q_r, K_r, seq_lens, ks, q, K, V, k_max: int, L_max: Optional[int] = None,
+                 scale_r: float = 0.0, scale: float = 0.0,
+                 elastic: Optional[ElasticState] = None, with_scores: bool = False,
+                 with_lse: bool = False, outputs: Optional[dict] = None,
+                 head_level: bool = False):
+    """spec_step_noalloc: the fused step on the library's static per-GPU
+    scratch instead of a caller workspace (the library allocates nothing;
+    pass `outputs` to allocate nothing here either).  Calls that overlap on
+    one GPU race on that scratch."""
+    lib = load_library()
+    dims, o = _step_args(q_r, K_r, seq_lens, ks, q, K, V, k_max, L_max, scale_r, scale,
+                         with_scores, with_lse, outputs, head_level)
+    el = elastic.c_struct() if elastic is not None else None
+    _check(lib.spec_step_noalloc(ctypes.byref(dims), _p(q_r), _p(K_r), _p(seq_lens), _p(ks),
+                                 _p(q), _p(K), _p(V), _p(o["idx"]), _p(o["counts"]),
+                                 _p(o["out"]), _p(o.get("lse")), _p(o.get("scores")),
+                                 ctypes.byref(el) if el is not None else None, _stream(q)),
+           "spec_step_noalloc")
+    return o
+
+
+def step_noalloc_max_bytes() -> int:
+    """Bytes of spec_step_noalloc's static scratch (per GPU)."""
+    return int(load_library().spec_step_noalloc_max_bytes())
 
 
 def retrieval_qk(tokens: torch.Tensor, pos: torch.Tensor, emb: torch.Tensor, w_q: torch.Tensor,

@@ -102,6 +102,12 @@ struct MlaDims {
 };
 size_t mla_ws_bytes(const MlaDims& d);
 
+// The allocation-free decode step keeps its workspace in a static device
+// array of this size (one per GPU, held until the process ends);
+// static_scratch() gives its device address on the current GPU.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+hipError_t static_scratch(void** out);
+
 // Compute units of the device the process first launches on, queried once
 // and cached (kernels size their grids with it; every grid size is correct,
 // so the launch path makes no device query).

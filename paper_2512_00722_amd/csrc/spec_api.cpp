@@ -237,6 +237,66 @@ spec_status resolve_mla(const spec_mla_dims* dm, spec::MlaDims* o) {
   return SPEC_OK;
 }
 
+
+// Host checks shared by the two step entry points (before any HIP call).
+spec_status check_step(const spec_dims* dm, spec::Dims* d, const uint16_t* q_r,
+                       const uint16_t* k_r, const int32_t* seq_lens, const int32_t* ks,
+                       const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                       const int32_t* idx_out, const int32_t* counts_out, const float* out,
+                       const float* lse, const float* scores_out, const spec_elastic* el) {
+  spec_status st = resolve(dm, d);
+  if (st != SPEC_OK) return st;
+  if (!q_r || !k_r || !seq_lens || !ks || !q || !k_cache || !v_cache || !idx_out ||
+      !counts_out || !out)
+    return SPEC_ERR_INVALID;
+  if (!aligned16(q_r) || !aligned16(k_r) || !aligned4(seq_lens) || !aligned4(ks) ||
+      !aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned4(idx_out) ||
+      !aligned4(counts_out) || !aligned16(out) || (lse && !aligned4(lse)) ||
+      (scores_out && !aligned4(scores_out)))
+    return SPEC_ERR_INVALID;
+  if (el && (st = check_elastic(*d, el)) != SPEC_OK) return st;
+  return SPEC_OK;
+}
+
+// The step's launches on workspace `ws` (spec_workspace_size(SPEC_OP_STEP)
+// bytes, carved as below).  Every region is written before it is read
+// within the call (the histogram is cleared by the first kernel), so the
+// workspace need not start zeroed.
+spec_status run_step(const spec::Dims& d, const uint16_t* q_r, const uint16_t* k_r,
+                     const int32_t* seq_lens, const int32_t* ks, const uint16_t* q,
+                     const uint16_t* k_cache, const uint16_t* v_cache, int32_t* idx_out,
+                     int32_t* counts_out, float* out, float* lse, float* scores_out,
+                     const spec_elastic* el, void* ws, hipStream_t s) {
+  char* p = static_cast<char*>(ws);
+  float* scores = reinterpret_cast<float*>(p);
+  p += spec::align_up(sizeof(float) * (size_t)d.B * d.n_sets * d.L_max);
+  if (scores_out) scores = scores_out;
+  void* ws_score = p;
+  p += spec::score_ws_bytes(d);
+  void* ws_topk = p;
+  p += spec::topk_ws_bytes(d);
+  void* ws_attn = p;
+  p += spec::attn_ws_bytes(d);
+  void* ws_delta = p;
+
+  hipError_t e = spec::launch_score(d, q_r, k_r, seq_lens, scores, ws_score, s);
+  if (e != hipSuccess) return hip_status(e);
+  // The score kernels already built the selection histogram.
+  e = spec::launch_topk_select(d, scores, seq_lens, ks, spec::score_ws_hist(d, ws_score),
+                               static_cast<char*>(ws_topk) + spec::topk_hist_bytes(d), idx_out,
+                               counts_out, s);
+  if (e != hipSuccess) return hip_status(e);
+  if (el) {
+    e = spec::launch_delta(d, idx_out, counts_out, k_cache, v_cache, el->slot_tok, el->kbuf,
+                           el->vbuf, el->n_changed, ws_delta, s);
+    if (e != hipSuccess) return hip_status(e);
+    e = spec::launch_attn(d, q, el->kbuf, el->vbuf, nullptr, counts_out, out, lse, ws_attn, s);
+  } else {
+    e = spec::launch_attn(d, q, k_cache, v_cache, idx_out, counts_out, out, lse, ws_attn, s);
+  }
+  return finish(hip_status(e), s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -383,50 +443,34 @@ spec_status spec_step(const spec_dims* dm, const uint16_t* q_r, const uint16_t* 
                       const spec_elastic* el, void* ws, size_t ws_bytes,
                       spec_stream stream) {
   spec::Dims d;
-  spec_status st = resolve(dm, &d);
+  spec_status st = check_step(dm, &d, q_r, k_r, seq_lens, ks, q, k_cache, v_cache, idx_out,
+                              counts_out, out, lse, scores_out, el);
   if (st != SPEC_OK) return st;
-  if (!q_r || !k_r || !seq_lens || !ks || !q || !k_cache || !v_cache || !idx_out ||
-      !counts_out || !out)
-    return SPEC_ERR_INVALID;
-  if (!aligned16(q_r) || !aligned16(k_r) || !aligned4(seq_lens) || !aligned4(ks) ||
-      !aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned4(idx_out) ||
-      !aligned4(counts_out) || !aligned16(out) || (lse && !aligned4(lse)) ||
-      (scores_out && !aligned4(scores_out)))
-    return SPEC_ERR_INVALID;
-  if (el && (st = check_elastic(d, el)) != SPEC_OK) return st;
   if ((st = check_ws(d, SPEC_OP_STEP, ws, ws_bytes)) != SPEC_OK) return st;
   if (debug_on() && (st = debug_lengths(d, seq_lens, ks, as_stream(stream))) != SPEC_OK) return st;
-
-  char* p = static_cast<char*>(ws);
-  float* scores = reinterpret_cast<float*>(p);
-  p += spec::align_up(sizeof(float) * (size_t)d.B * d.n_sets * d.L_max);
-  if (scores_out) scores = scores_out;
-  void* ws_score = p;
-  p += spec::score_ws_bytes(d);
-  void* ws_topk = p;
-  p += spec::topk_ws_bytes(d);
-  void* ws_attn = p;
-  p += spec::attn_ws_bytes(d);
-  void* ws_delta = p;
-
-  const hipStream_t s = as_stream(stream);
-  hipError_t e = spec::launch_score(d, q_r, k_r, seq_lens, scores, ws_score, s);
-  if (e != hipSuccess) return hip_status(e);
-  // The score kernels already built the selection histogram.
-  e = spec::launch_topk_select(d, scores, seq_lens, ks, spec::score_ws_hist(d, ws_score),
-                               static_cast<char*>(ws_topk) + spec::topk_hist_bytes(d), idx_out,
-                               counts_out, s);
-  if (e != hipSuccess) return hip_status(e);
-  if (el) {
-    e = spec::launch_delta(d, idx_out, counts_out, k_cache, v_cache, el->slot_tok, el->kbuf,
-                           el->vbuf, el->n_changed, ws_delta, s);
-    if (e != hipSuccess) return hip_status(e);
-    e = spec::launch_attn(d, q, el->kbuf, el->vbuf, nullptr, counts_out, out, lse, ws_attn, s);
-  } else {
-    e = spec::launch_attn(d, q, k_cache, v_cache, idx_out, counts_out, out, lse, ws_attn, s);
-  }
-  return finish(hip_status(e), s);
+  return run_step(d, q_r, k_r, seq_lens, ks, q, k_cache, v_cache, idx_out, counts_out, out, lse,
+                  scores_out, el, ws, as_stream(stream));
 }
+
+spec_status spec_step_noalloc(const spec_dims* dm, const uint16_t* q_r, const uint16_t* k_r,
+                              const int32_t* seq_lens, const int32_t* ks, const uint16_t* q,
+                              const uint16_t* k_cache, const uint16_t* v_cache,
+                              int32_t* idx_out, int32_t* counts_out, float* out, float* lse,
+                              float* scores_out, const spec_elastic* el, spec_stream stream) {
+  spec::Dims d;
+  spec_status st = check_step(dm, &d, q_r, k_r, seq_lens, ks, q, k_cache, v_cache, idx_out,
+                              counts_out, out, lse, scores_out, el);
+  if (st != SPEC_OK) return st;
+  if (ws_bytes_for(d, SPEC_OP_STEP) > spec::kStaticScratchBytes) return SPEC_ERR_TOO_LARGE;
+  if (debug_on() && (st = debug_lengths(d, seq_lens, ks, as_stream(stream))) != SPEC_OK) return st;
+  void* ws = nullptr;  // the device address of this GPU's static scratch
+  const hipError_t e = spec::static_scratch(&ws);
+  if (e != hipSuccess) return hip_status(e);
+  return run_step(d, q_r, k_r, seq_lens, ks, q, k_cache, v_cache, idx_out, counts_out, out, lse,
+                  scores_out, el, ws, as_stream(stream));
+}
+
+size_t spec_step_noalloc_max_bytes(void) { return spec::kStaticScratchBytes; }
 
 spec_status spec_retrieval_qk(const spec_dims* dm, const spec_frontend* fe,
                               const int32_t* tokens, const int32_t* pos, const uint16_t* emb,
@@ -460,6 +504,8 @@ const char* spec_status_string(spec_status s) {
     case SPEC_ERR_UNSUPPORTED: return "unsupported dimensions";
     case SPEC_ERR_WORKSPACE: return "workspace missing or too small";
     case SPEC_ERR_HIP: return "HIP launch failed";
+    case SPEC_ERR_TOO_LARGE:
+      return "the step needs more workspace than the allocation-free entry point's static scratch";
   }
   return "unknown status";
 }

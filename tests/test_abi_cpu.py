@@ -315,3 +315,28 @@ def test_host_sanitizers():
     assert r.returncode == 0, out[-4000:]
     assert "AddressSanitizer" not in out and "runtime error" not in out, out[-4000:]
     assert " passed" in out, out[-2000:]
+
+
+def test_step_noalloc_rejects_before_hip(lib):
+    """The allocation-free step validates as spec_step does and rejects a
+    step whose workspace exceeds its static scratch, all before any HIP
+    call (fake pointers are never touched)."""
+    assert lib.spec_step_noalloc_max_bytes() == 64 << 20
+    assert lib.spec_status_string(5) and lib.spec_status_string(5) != b"unknown status"
+    byref = ctypes.byref
+    args = lambda: [FAKE] * 10 + [None, None, None]   # q_r .. out; lse, scores, elastic
+    d = good_dims()
+    a = args()
+    a[0] = None
+    assert lib.spec_step_noalloc(byref(d), *a, None) == 1                 # null q_r
+    a = args()
+    a[5] = FAKE_ODD
+    assert lib.spec_step_noalloc(byref(d), *a, None) == 1                 # misaligned K
+    assert lib.spec_step_noalloc(byref(good_dims(d=96)), *args(), None) == 2
+    # a step that needs more than 64 MiB of workspace (logits and lists of
+    # 64 sequences of 128K tokens)
+    big = good_dims(B=64, L_cap=131072, L_max=131072, k_max=2048)
+    _, need = ws_size(lib, big, spec.OP_STEP)
+    assert need > 64 << 20
+    assert lib.spec_step_noalloc(byref(big), *args(), None) == 5
+    assert lib.spec_last_hip_error() == 0
