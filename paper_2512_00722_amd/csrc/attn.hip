@@ -65,6 +65,12 @@ constexpr int kMaxSplit = 2048;           // longest split (tokens per work item
 #endif
 
 constexpr int kMinSplitTokens = SPEC_ATTN_MIN_SPLIT;
+#ifndef SPEC_ATTN_SLOT_UNITS
+#define SPEC_ATTN_SLOT_UNITS 1
+#endif
+// Work units per resident wavefront the selections are split into when there
+// are fewer (layer, sequence, KV head) groups than wavefronts.
+constexpr int kSlotUnits = SPEC_ATTN_SLOT_UNITS;
 
 // K/V rows are read once per launch: stream them past the caches.
 __device__ __forceinline__ uint4 ldkv(const uint16_t* p) {
@@ -712,7 +718,10 @@ struct CombineArgs {
 };
 
 // One workgroup per (layer*B + b, group of 8 heads); thread = (head, 4 dims).
+// The splits' (max, sum) pairs and accumulator slices are requested eight at
+// a time, all before any is used (one round trip for up to eight splits).
 __global__ __launch_bounds__(256) void attn_combine_kernel(CombineArgs a) {
+  constexpr int kBatch = 8;
   const int lb = blockIdx.x;
   const int h = blockIdx.y * 8 + (threadIdx.x >> 5);
   const int d4 = threadIdx.x & 31;
@@ -727,19 +736,40 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(CombineArgs a) {
     return;
   }
   const size_t base = (size_t)lb * a.n_split * a.H_q + h;  // row of split 0
-  float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, a.part_ml[(base + (size_t)s * a.H_q) * 2]);
-  float L = 0.f;
+  const float2* ml2 = reinterpret_cast<const float2*>(a.part_ml);
+  float M = -INFINITY, L = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s = 0; s < ns; ++s) {
-    const size_t row = base + (size_t)s * a.H_q;
-    const float w = exp2f(a.part_ml[row * 2] - M);
-    L += a.part_ml[row * 2 + 1] * w;
-    const float4 p = reinterpret_cast<const float4*>(a.part_acc + row * kD)[d4];
-    acc.x += p.x * w;
-    acc.y += p.y * w;
-    acc.z += p.z * w;
-    acc.w += p.w * w;
+  for (int s0 = 0; s0 < ns; s0 += kBatch) {
+    float2 ml[kBatch];
+    float4 pa[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {  // clamped: every load is issued
+      const size_t row = base + (size_t)min(s0 + u, ns - 1) * a.H_q;
+      ml[u] = ml2[row];
+      pa[u] = reinterpret_cast<const float4*>(a.part_acc + row * kD)[d4];
+    }
+    float Mb = M;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      if (s0 + u < ns) Mb = fmaxf(Mb, ml[u].x);
+    const float r = exp2f(M - Mb);  // earlier batches onto the new maximum (0 at the first)
+    L *= r;
+    acc.x *= r;
+    acc.y *= r;
+    acc.z *= r;
+    acc.w *= r;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      if (s0 + u < ns) {
+        const float w = exp2f(ml[u].x - Mb);
+        L += ml[u].y * w;
+        acc.x += pa[u].x * w;
+        acc.y += pa[u].y * w;
+        acc.z += pa[u].z * w;
+        acc.w += pa[u].w * w;
+      }
+    }
+    M = Mb;
   }
   const float inv = 1.f / L;
   *o = make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
@@ -768,7 +798,7 @@ int attn_col_groups(const Dims& d) { return d.G > 16 ? d.G / 16 : 1; }
 AttnPlan attn_plan(const Dims& d) {
   const int64_t base = (int64_t)d.n_layers * d.B * d.H_kv * attn_col_groups(d);
   auto round_chunk = [](int64_t t) { return (t + kChunk - 1) / kChunk * kChunk; };
-  int64_t n_split = (kWaveSlots + base - 1) / base;
+  int64_t n_split = (kWaveSlots * kSlotUnits + base - 1) / base;
   int64_t split = round_chunk((d.k_max + n_split - 1) / n_split);
   if (split < kMinSplitTokens) split = kMinSplitTokens;
   if (split > kMaxSplit) split = kMaxSplit;

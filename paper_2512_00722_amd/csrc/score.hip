@@ -20,10 +20,11 @@ namespace {
 
 constexpr int T1 = kScoreTokensPerBlock;
 constexpr int T2 = kSoftTokensPerBlock;
-#ifndef SPEC_LOGITS_UNROLL
-#define SPEC_LOGITS_UNROLL 8
-#endif
-constexpr int kUnroll = SPEC_LOGITS_UNROLL;  // rows in flight per lane
+// Rows in flight per lane: 4 where the grid covers the CUs several times
+// over (more would only lengthen the queues), 8 for small grids, whose few
+// workgroups must each keep more bytes in flight.
+constexpr int kUnrollWide = 4;
+constexpr int kUnrollNarrow = 8;
 
 struct LogitsArgs {
   const uint16_t* q_r;
@@ -37,7 +38,7 @@ struct LogitsArgs {
   float qscale;   // scale_r * log2(e)
 };
 
-template <int LPH>  // lanes per head = d_r / 8
+template <int LPH, int kUnroll>  // lanes per head = d_r / 8; rows in flight per lane
 __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
   constexpr int d_r = LPH * 8;
   const int b = blockIdx.y;
@@ -134,6 +135,10 @@ struct SoftArgs {
 // A score row is a sequence (n_sets = 1: the heads' weights summed) or one
 // KV head of a sequence (n_sets = H_kv: the maximum over the H_r / n_sets
 // heads of its group).
+// Every load is issued before the sequence length arrives (they are all
+// independent of it): the thread's logits, clamped into the row, and every
+// per-block pair of its head, later masked to the sequence's blocks.  One
+// memory round trip precedes the arithmetic.
 __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
   __shared__ float c_h[16];
   __shared__ float2 wred[4];
@@ -146,27 +151,16 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
   const int tid = threadIdx.x;
   const int t0 = blockIdx.x * T2;
   const int t1 = min(t0 + T2, a.L_max);
-  const int L_b = clampi(a.seq_lens[b], 0, a.L_max);
+  const int L_raw = a.seq_lens[b];
   float* out = a.scores + (size_t)row * a.L_max;
-  if (t0 >= L_b) {
-    for (int t = t0 + tid; t < t1; t += 256) out[t] = -INFINITY;
-    return;
-  }
   for (int i = tid; i < kTopkBins; i += 256) sh_hist[i] = 0;
 
-  // Each head's normaliser c_h = M_h + log2 Z_h from the per-block pairs
-  // (head-major, so a head's pairs are contiguous): 256/P lanes per head (P =
-  // the row's head count rounded up to a power of two), 16 pairs in flight
-  // per lane, then a butterfly over the head's lanes of the wave and, for
-  // heads wider than a wave, a combine of the per-wave results.
-  const int nb = (L_b + T1 - 1) / T1;
+  // This thread's logits (4 tokens x the row's heads, at most 16), head-major
+  // rows: one float4 holds this thread's 4 tokens of a head.
   const int H_r = a.H_r;
-  // This thread's logits (4 tokens x the row's heads, at most 16) are loaded
-  // before the normalisers are merged: the two loads are independent.
-  // Logits are head-major: one float4 holds this thread's 4 tokens of a head.
   const int tb = t0 + 4 * tid;
   float lv[4][16];
-  const bool vec = (a.L_max & 3) == 0 && tb + 3 < L_b;
+  const bool vec = (a.L_max & 3) == 0 && tb + 3 < a.L_max;
 #pragma unroll
   for (int h = 0; h < 16; ++h) {
     if (h < per) {
@@ -177,9 +171,9 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
         lv[1][h] = v.y;
         lv[2][h] = v.z;
         lv[3][h] = v.w;
-      } else {  // row tail: clamp into [0, L_b) (L_b >= 1 here); unused values
+      } else {  // row tail: clamped into the row; values past the length are unused
 #pragma unroll
-        for (int e = 0; e < 4; ++e) lv[e][h] = l[min(tb + e, L_b - 1)];
+        for (int e = 0; e < 4; ++e) lv[e][h] = l[min(tb + e, a.L_max - 1)];
       }
     } else {
 #pragma unroll
@@ -190,11 +184,31 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
   const int LPH = 256 / P;
   const int hh = tid / LPH;
   const int j = tid - hh * LPH;
+  // Each head's normaliser c_h = M_h + log2 Z_h from the per-block pairs
+  // (head-major, so a head's pairs are contiguous): 256/P lanes per head, 16
+  // pairs in flight per lane, then a butterfly over the head's lanes of the
+  // wave and, for heads wider than a wave, a combine of the per-wave results.
+  // Pairs of blocks past the sequence (never written by this call) are
+  // loaded with the rest and masked once the length is known.
+  float2 pv[16];
+  const float2* pp =
+      reinterpret_cast<const float2*>(a.part) + ((size_t)b * H_r + h0 + min(hh, per - 1)) * a.n_blk;
+#pragma unroll
+  for (int u = 0; u < 16; ++u) pv[u] = pp[min(j + LPH * u, a.n_blk - 1)];
+
+  const int L_b = clampi(L_raw, 0, a.L_max);
+  if (t0 >= L_b) {  // uniform: the block lies past the sequence
+    for (int t = t0 + tid; t < t1; t += 256) out[t] = -INFINITY;
+    return;
+  }
+  const int nb = (L_b + T1 - 1) / T1;
   float m = -INFINITY, s = 0.f;
   if (hh < per) {
-    const float2* p =
-        reinterpret_cast<const float2*>(a.part) + ((size_t)b * H_r + h0 + hh) * a.n_blk;
-    for (int i0 = j; i0 < nb; i0 += LPH * 16) {
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (j + LPH * u < nb) ms_combine(m, s, pv[u].x, pv[u].y);
+    const float2* p = pp;
+    for (int i0 = j + LPH * 16; i0 < nb; i0 += LPH * 16) {  // long rows: more pairs per lane
       float2 v[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
@@ -260,10 +274,14 @@ hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
   LogitsArgs la{q_r, k_r, seq_lens, logits, part, hist, d.kr_stride_b,
                 d.L_max, d.H_r, n_blk, d.n_sets, d.scale_r * kLog2e};
   const dim3 g1(n_blk, d.B);
-  if (d.d_r == 64)
-    logits_kernel<8><<<g1, 256, 0, s>>>(la);
-  else
-    logits_kernel<16><<<g1, 256, 0, s>>>(la);
+  const bool wide = (int64_t)n_blk * d.B >= 2 * (int64_t)device_cu_count();
+  if (d.d_r == 64) {
+    if (wide) logits_kernel<8, kUnrollWide><<<g1, 256, 0, s>>>(la);
+    else logits_kernel<8, kUnrollNarrow><<<g1, 256, 0, s>>>(la);
+  } else {
+    if (wide) logits_kernel<16, kUnrollWide><<<g1, 256, 0, s>>>(la);
+    else logits_kernel<16, kUnrollNarrow><<<g1, 256, 0, s>>>(la);
+  }
   SoftArgs sa{logits, part, seq_lens, scores, hist, d.L_max, d.H_r, n_blk, d.n_sets};
   const dim3 g2((d.L_max + T2 - 1) / T2, d.B * d.n_sets);
   softmax_headsum_kernel<<<g2, 256, 0, s>>>(sa);

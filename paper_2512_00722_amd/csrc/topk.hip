@@ -463,22 +463,29 @@ __global__ __launch_bounds__(kClsThreads) void topk_classify_kernel(ClsArgs a) {
   const int b = srow / a.n_sets;
   const int tile = blockIdx.x;
   const int tid = threadIdx.x;
-  const int L_b = clampi(a.seq_lens[b], 0, a.L_max);
-  const int k_b = clampi(a.ks[b], 0, min(L_b, a.k_max));
   const int t0 = tile * kTile;
-  if (k_b == 0 || k_b == L_b || t0 >= L_b) return;  // uniform: nothing to classify
 
-  // The tile's keys and the histogram are independent: both loads are in
-  // flight before either is used.
+  // The lengths, the tile's scores and the histogram are independent: all
+  // are requested before any is used (the scores clamped into the row, and
+  // masked to the sequence once its length has arrived).
+  const int L_raw = a.seq_lens[b];
+  const int k_raw = a.ks[b];
   const float* row = a.scores + (size_t)srow * a.L_max;
   const int lane = tid & 63;
   const int wv = tid >> 6;
-  const int w0 = min(t0 + wv * (kTile / kClsWaves), L_b);
+  const int w0 = t0 + wv * (kTile / kClsWaves);
+  float sv[kClsPerLane];
+#pragma unroll
+  for (int j = 0; j < kClsPerLane; ++j) sv[j] = row[min(w0 + 64 * j + lane, a.L_max - 1)];
+  load_hist<kClsThreads>(a.hist + (size_t)srow * kBins, s_hist);
+  const int L_b = clampi(L_raw, 0, a.L_max);
+  const int k_b = clampi(k_raw, 0, min(L_b, a.k_max));
+  if (k_b == 0 || k_b == L_b || t0 >= L_b) return;  // uniform: nothing to classify
   const int w1 = min(w0 + kTile / kClsWaves, L_b);
   uint32_t kk[kClsPerLane];
 #pragma unroll
-  for (int j = 0; j < kClsPerLane; ++j) kk[j] = key_at(row, w0 + 64 * j + lane, w1, a.L_max);
-  load_hist<kClsThreads>(a.hist + (size_t)srow * kBins, s_hist);
+  for (int j = 0; j < kClsPerLane; ++j)  // a mask, not a select (see key_at)
+    kk[j] = order_key(sv[j]) & (0u - (uint32_t)(w0 + 64 * j + lane < w1));
   if (tid == 0) s_sel[0] = s_sel[1] = s_sel[2] = -1;
   __syncthreads();
   find_bin<kClsThreads>(s_hist, kBins, k_b, s_scan, s_sel);
