@@ -96,7 +96,8 @@ typedef enum spec_op {
   SPEC_OP_ATTN = 3,
   SPEC_OP_DELTA = 4,
   SPEC_OP_STEP = 5,
-  SPEC_OP_FRONTEND = 6
+  SPEC_OP_FRONTEND = 6,
+  SPEC_OP_OFFLOAD = 7     /* spec_step_offload */
 } spec_op;
 
 /* A hipStream_t handle; NULL selects the null stream. */
@@ -227,6 +228,64 @@ SPEC_API spec_status spec_step(const spec_dims* dm, const uint16_t* q_r,
                       int32_t* idx_out, int32_t* counts_out, float* out,
                       float* lse, float* scores_out, const spec_elastic* el,
                       void* ws, size_t ws_bytes, spec_stream stream);
+
+/* KV of offloaded layers held in host memory (host struct).  k and v are
+ * host pointers into pinned memory allocated with hipHostMalloc (the GPU
+ * reads it directly over the host link); layout as the device cache:
+ * [n_off][B][L_cap][H_kv][d] bf16 with the strides below.                   */
+typedef struct spec_host_kv {
+  const uint16_t* k;
+  const uint16_t* v;
+  int64_t stride_layer;  /* elements between layers; 0 = B * stride_b        */
+  int64_t stride_b;      /* elements between sequences; 0 = L_cap * H_kv * d */
+} spec_host_kv;
+
+/* Elastic loading from host memory with an asynchronous per-layer dataflow
+ * (Sec. 5.1: the selection is known before the LLM runs, so the loads of
+ * every layer are issued at once on their own stream and overlap the
+ * computation; Sec. 5.4: only S_now - S_last is loaded, into the slots freed
+ * by S_last - S_now).  dm->n_layers = the offloaded layers (those of `host`
+ * and of el->kbuf/vbuf).  On `stream`: the slot plan of spec_delta_gather
+ * (same pairing, same full reload when the budget shrinks, n_changed), then
+ * layer_ready[n_layers] is recorded (the fork point).  On `copy_stream`,
+ * after waiting for that event, for each layer l in order: the K and V rows
+ * of the new tokens copied from `host` into their slots of layer l, then
+ * layer_ready[l] recorded.  A consumer of layer l waits for layer_ready[l]
+ * only.  layer_ready: n_layers + 1 caller-created hipEvent_t handles; it may
+ * be NULL only when copy_stream is NULL, in which case every copy runs on
+ * `stream` after the plan.  The host pointers must be pinned host memory
+ * (SPEC_ERR_INVALID otherwise, before anything is enqueued).  Needs
+ * workspace spec_workspace_size(SPEC_OP_DELTA).                            */
+SPEC_API spec_status spec_offload_load(const spec_dims* dm, const int32_t* idx_now,
+                              const int32_t* counts, const spec_host_kv* host,
+                              const spec_elastic* el, void* ws, size_t ws_bytes,
+                              spec_stream stream, spec_stream copy_stream,
+                              void* const* layer_ready);
+
+/* One decode step with part of the KV offloaded to host memory (Sec. 5.1,
+ * 5.4; the offloaded layers are the last ones, as the paper's adaptive
+ * memory management offloads them first).  Layers [0, n_dev_layers) are in
+ * the device caches k_cache/v_cache (layout and strides of dm, as for
+ * spec_step); layers [n_dev_layers, dm->n_layers) are in `host`, and el's
+ * slot buffers hold their selected rows ([n_off][B][k_max][H_kv][d], n_off =
+ * n_layers - n_dev_layers; start from slot_tok = -1 for a full load).  On
+ * `stream`: spec_score, spec_topk, the slot plan, then the attention of the
+ * device layers (one launch, indexed over the caches) while the host loads
+ * run on `copy_stream` (spec_offload_load with layer_ready[0..n_off]), then,
+ * for each offloaded layer, a wait for its layer_ready event and its
+ * attention over its slots.  Outputs as spec_step (idx, counts, out for all
+ * layers, lse and scores nullable).  One token set per sequence (n_sets = 1).
+ * copy_stream NULL runs everything on `stream`.  0 <= n_dev_layers <
+ * n_layers.  Needs workspace spec_workspace_size(SPEC_OP_OFFLOAD).         */
+SPEC_API spec_status spec_step_offload(const spec_dims* dm, const uint16_t* q_r,
+                              const uint16_t* k_r, const int32_t* seq_lens,
+                              const int32_t* ks, const uint16_t* q,
+                              const uint16_t* k_cache, const uint16_t* v_cache,
+                              int32_t n_dev_layers, const spec_host_kv* host,
+                              int32_t* idx_out, int32_t* counts_out, float* out,
+                              float* lse, float* scores_out, const spec_elastic* el,
+                              void* ws, size_t ws_bytes, spec_stream stream,
+                              spec_stream copy_stream, void* const* layer_ready);
 
 /* The fused decode step of spec_step without a workspace argument, for
  * callers that cannot allocate device memory (code under HIP graph capture,

@@ -26,19 +26,21 @@ __all__ = [
     "step_noalloc_max_bytes", "Frontend",
     "retrieval_qk", "MlaDims", "mla_workspace_size", "mla_sparse_decode_attn",
     "OP_SCORE", "OP_TOPK", "OP_GATHER", "OP_ATTN", "OP_DELTA", "OP_STEP", "OP_FRONTEND",
+    "OP_OFFLOAD", "HostKv", "OffloadEvents", "offload_load", "step_offload",
     "EXPORTED_SYMBOLS",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 lib_path = os.path.join(_PKG, "libspecctx.so")
 
-OP_SCORE, OP_TOPK, OP_GATHER, OP_ATTN, OP_DELTA, OP_STEP, OP_FRONTEND = range(7)
+OP_SCORE, OP_TOPK, OP_GATHER, OP_ATTN, OP_DELTA, OP_STEP, OP_FRONTEND, OP_OFFLOAD = range(8)
 STATUS = {0: "SPEC_OK", 1: "SPEC_ERR_INVALID", 2: "SPEC_ERR_UNSUPPORTED",
           3: "SPEC_ERR_WORKSPACE", 4: "SPEC_ERR_HIP", 5: "SPEC_ERR_TOO_LARGE"}
 
 EXPORTED_SYMBOLS = ["spec_score", "spec_topk", "spec_gather", "spec_sparse_decode_attn",
                     "spec_delta_gather", "spec_step", "spec_step_noalloc",
-                    "spec_step_noalloc_max_bytes", "spec_retrieval_qk",
+                    "spec_step_noalloc_max_bytes", "spec_offload_load", "spec_step_offload",
+                    "spec_retrieval_qk",
                     "spec_mla_sparse_decode_attn", "spec_mla_workspace_size", "spec_workspace_size",
                     "spec_status_string", "spec_last_hip_error", "spec_version"]
 
@@ -79,6 +81,12 @@ class Elastic(ctypes.Structure):
     """Mirror of `spec_elastic`."""
     _fields_ = [("slot_tok", ctypes.c_void_p), ("kbuf", ctypes.c_void_p),
                 ("vbuf", ctypes.c_void_p), ("n_changed", ctypes.c_void_p)]
+
+
+class HostKv(ctypes.Structure):
+    """Mirror of `spec_host_kv`."""
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("stride_layer", ctypes.c_int64), ("stride_b", ctypes.c_int64)]
 
 
 class Frontend(ctypes.Structure):
@@ -131,6 +139,9 @@ def load_library(path: Optional[str] = None):
         "spec_delta_gather": [D, P, P, P, P, E, P, S, P],
         "spec_step": [D, P, P, P, P, P, P, P, P, P, P, P, P, E, P, S, P],
         "spec_step_noalloc": [D, P, P, P, P, P, P, P, P, P, P, P, P, E, P],
+        "spec_offload_load": [D, P, P, ctypes.POINTER(HostKv), E, P, S, P, P, P],
+        "spec_step_offload": [D, P, P, P, P, P, P, P, ctypes.c_int32, ctypes.POINTER(HostKv),
+                              P, P, P, P, P, E, P, S, P, P, P],
         "spec_retrieval_qk": [D, F, P, P, P, P, P, P, P, P, S, P],
         "spec_mla_sparse_decode_attn": [M, P, P, P, P, P, P, P, P, P, S, P],
         "spec_mla_workspace_size": [M, ctypes.POINTER(S)],
@@ -492,6 +503,132 @@ def step_noalloc(q_r, K_r, seq_lens, ks, q, K, V, k_max: int, L_max: Optional[in
                                  _p(o["out"]), _p(o.get("lse")), _p(o.get("scores")),
                                  ctypes.byref(el) if el is not None else None, _stream(q)),
            "spec_step_noalloc")
+    return o
+
+
+class OffloadEvents:
+    """The n_layers + 1 HIP events of the host-offload dataflow (caller-owned,
+    as the C ABI wants them): event l marks layer l's rows loaded, the last
+    one the fork after the slot plan."""
+
+    def __init__(self, n: int, device):
+        self.events = [torch.cuda.Event() for _ in range(n + 1)]
+        with torch.cuda.device(device):
+            for e in self.events:        # torch creates its events on first record
+                e.record()
+        self._arr = (ctypes.c_void_p * (n + 1))(*[e.cuda_event for e in self.events])
+
+    def c_array(self):
+        return self._arr
+
+
+def _host_kv(Kh: torch.Tensor, Vh: torch.Tensor) -> HostKv:
+    for t, nm in ((Kh, "K_host"), (Vh, "V_host")):
+        _need_host = t.dtype == torch.bfloat16 and t.dim() == 5 and t.device.type == "cpu"
+        if not _need_host or not t.is_pinned():
+            raise ValueError(f"{nm} must be a pinned host bf16 tensor [n_off, B, L_cap, H_kv, d]")
+    if Kh.shape != Vh.shape or Kh.stride() != Vh.stride():
+        raise ValueError("K_host and V_host must have the same shape and strides")
+    _inner_contig(Kh, "K_host", 3)
+    return HostKv(Kh.data_ptr(), Vh.data_ptr(), Kh.stride(0), Kh.stride(1))
+
+
+def offload_load(idx_now: torch.Tensor, counts: torch.Tensor, K_host: torch.Tensor,
+                 V_host: torch.Tensor, state: ElasticState, copy_stream=None,
+                 events: Optional[OffloadEvents] = None, L_max: Optional[int] = None,
+                 ws: Optional[torch.Tensor] = None):
+    """spec_offload_load: elastic loading of the offloaded layers from pinned
+    host memory.  The slot plan runs on the current stream; with copy_stream
+    (a torch.cuda.Stream) the per-layer host->device copies run there and
+    events.events[l] marks layer l loaded.  Returns the events (or None)."""
+    lib = load_library()
+    n_off, B, L_cap, H_kv, d = K_host.shape
+    _need(idx_now, "idx_now", torch.int32, 2)
+    k_max = idx_now.shape[1]
+    _i32(counts, "counts", B)
+    if tuple(state.kbuf.shape) != (n_off, B, k_max, H_kv, d):
+        raise ValueError("elastic state shape does not match")
+    dims = Dims.make(B=B, L_cap=L_cap, L_max=L_cap if L_max is None else L_max, k_max=k_max,
+                     n_layers=n_off, H_q=H_kv, H_kv=H_kv, d=d)
+    ws, nws = _workspace(dims, OP_DELTA, idx_now.device, ws)
+    host = _host_kv(K_host, V_host)
+    if copy_stream is not None and events is None:
+        events = OffloadEvents(n_off, idx_now.device)
+    el = state.c_struct()
+    _check(lib.spec_offload_load(ctypes.byref(dims), _p(idx_now.contiguous()), _p(counts),
+                                 ctypes.byref(host), ctypes.byref(el), _p(ws), nws,
+                                 _stream(idx_now),
+                                 ctypes.c_void_p(copy_stream.cuda_stream) if copy_stream else None,
+                                 events.c_array() if events is not None else None),
+           "spec_offload_load")
+    return events
+
+
+def step_offload(q_r, K_r, seq_lens, ks, q, K, V, K_host, V_host, k_max: int,
+                 state: ElasticState, copy_stream=None, events: Optional[OffloadEvents] = None,
+                 L_max: Optional[int] = None, with_scores: bool = False, with_lse: bool = False,
+                 ws: Optional[torch.Tensor] = None, outputs: Optional[dict] = None):
+    """spec_step_offload: one decode step whose last n_off layers live in
+    pinned host memory (K_host/V_host [n_off, B, L_cap, H_kv, d]) and whose
+    first n_dev layers are the device caches K/V ([n_dev, ...]; with n_dev =
+    0 pass None for both).  q is [n_dev + n_off, B, H_q, d].  The offloaded
+    layers' rows are loaded elastically into `state` (slot buffers [n_off,
+    B, k_max, H_kv, d]) on copy_stream (a torch.cuda.Stream, or None: all on
+    the current stream), each layer's attention waiting for its own rows.
+    Returns the outputs dict as step(), plus "events"."""
+    lib = load_library()
+    _need(q_r, "q_r", torch.bfloat16, 3)
+    _need(K_r, "K_r", torch.bfloat16, 4)
+    _need(q, "q", torch.bfloat16, 4)
+    _inner_contig(K_r, "K_r", 3)
+    n_off, B, L_cap, H_kv, d = K_host.shape
+    host = _host_kv(K_host, V_host)
+    n_dev = 0
+    if K is not None:
+        _check_cache(K, V)
+        n_dev = K.shape[0]
+        if tuple(K.shape[1:]) != (B, L_cap, H_kv, d):
+            raise ValueError("device and host caches must have the same [B, L_cap, H_kv, d]")
+    n_layers = n_dev + n_off
+    _, L_cap_r, H_r, d_r = K_r.shape
+    if K_r.shape[0] != B or tuple(q_r.shape) != (B, H_r, d_r) or not q_r.is_contiguous():
+        raise ValueError("q_r / K_r shapes do not match")
+    if tuple(q.shape[:2]) != (n_layers, B) or q.shape[3] != d or not q.is_contiguous():
+        raise ValueError("q must be contiguous [n_dev + n_off, B, H_q, d]")
+    _i32(seq_lens, "seq_lens", B)
+    _i32(ks, "ks", B)
+    if tuple(state.kbuf.shape) != (n_off, B, int(k_max), H_kv, d):
+        raise ValueError("elastic state shape does not match")
+    L = min(L_cap_r, L_cap)
+    L_max = L if L_max is None else int(L_max)
+    dims = Dims.make(B=B, L_cap=L, L_max=L_max, k_max=int(k_max), H_r=H_r, d_r=d_r,
+                     n_layers=n_layers, H_q=q.shape[2], H_kv=H_kv, d=d,
+                     kr_stride_b=K_r.stride(0),
+                     kv_stride_layer=K.stride(0) if n_dev else 0,
+                     kv_stride_b=K.stride(1) if n_dev else 0)
+    ws, nws = _workspace(dims, OP_OFFLOAD, q.device, ws)
+    dev = q.device
+    o = outputs if outputs is not None else {}
+    if "idx" not in o:
+        o["idx"] = torch.empty((B, int(k_max)), dtype=torch.int32, device=dev)
+        o["counts"] = torch.empty((B,), dtype=torch.int32, device=dev)
+        o["out"] = torch.empty((n_layers, B, q.shape[2], d), dtype=torch.float32, device=dev)
+        o["lse"] = (torch.empty((n_layers, B, q.shape[2]), dtype=torch.float32, device=dev)
+                    if with_lse else None)
+        o["scores"] = (torch.empty((B, L_max), dtype=torch.float32, device=dev)
+                       if with_scores else None)
+    if copy_stream is not None and events is None:
+        events = OffloadEvents(n_off, dev)
+    el = state.c_struct()
+    _check(lib.spec_step_offload(ctypes.byref(dims), _p(q_r), _p(K_r), _p(seq_lens), _p(ks),
+                                 _p(q), _p(K) if n_dev else None, _p(V) if n_dev else None,
+                                 n_dev, ctypes.byref(host), _p(o["idx"]), _p(o["counts"]),
+                                 _p(o["out"]), _p(o.get("lse")), _p(o.get("scores")),
+                                 ctypes.byref(el), _p(ws), nws, _stream(q),
+                                 ctypes.c_void_p(copy_stream.cuda_stream) if copy_stream else None,
+                                 events.c_array() if events is not None else None),
+           "spec_step_offload")
+    o["events"] = events
     return o
 
 

@@ -286,18 +286,33 @@ size_t elastic_plan_lds_bytes(const Dims& d) {
   return sizeof(uint32_t) * 2 * (size_t)((d.L_cap + 31) / 32);
 }
 
+hipError_t launch_delta_plan(const Dims& d, const int32_t* idx_now, const int32_t* counts,
+                             int32_t* slot_tok, int32_t* n_changed, void* ws, hipStream_t s) {
+  PlanArgs p{idx_now, counts, slot_tok, n_changed, static_cast<int32_t*>(ws), d.k_max, d.L_cap};
+  elastic_plan_kernel<<<d.B, kPlanThreads, elastic_plan_lds_bytes(d), s>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_delta_copy(const Dims& d, const uint16_t* k_src, const uint16_t* v_src,
+                             int64_t src_stride_layer, int64_t src_stride_b, int n_layers,
+                             const int32_t* n_changed, uint16_t* kbuf, uint16_t* vbuf,
+                             const void* ws, hipStream_t s) {
+  CopyArgs c{k_src, v_src, static_cast<const int32_t*>(ws), n_changed, kbuf, vbuf,
+             src_stride_layer, src_stride_b, (int64_t)d.H_kv * d.d, d.B, d.k_max, d.L_cap,
+             n_layers};
+  const dim3 grid((d.k_max + kRowsPerBlock - 1) / kRowsPerBlock, d.B);
+  elastic_copy_kernel<<<grid, 256, 0, s>>>(c);
+  return hipGetLastError();
+}
+
 hipError_t launch_delta(const Dims& d, const int32_t* idx_now, const int32_t* counts,
                         const uint16_t* k_cache, const uint16_t* v_cache,
                         int32_t* slot_tok, uint16_t* kbuf, uint16_t* vbuf,
                         int32_t* n_changed, void* ws, hipStream_t s) {
-  int32_t* loads = static_cast<int32_t*>(ws);
-  PlanArgs p{idx_now, counts, slot_tok, n_changed, loads, d.k_max, d.L_cap};
-  elastic_plan_kernel<<<d.B, kPlanThreads, elastic_plan_lds_bytes(d), s>>>(p);
-  CopyArgs c{k_cache, v_cache, loads, n_changed, kbuf, vbuf, d.kv_stride_layer, d.kv_stride_b,
-             (int64_t)d.H_kv * d.d, d.B, d.k_max, d.L_cap, d.n_layers};
-  const dim3 grid((d.k_max + kRowsPerBlock - 1) / kRowsPerBlock, d.B);
-  elastic_copy_kernel<<<grid, 256, 0, s>>>(c);
-  return hipGetLastError();
+  hipError_t e = launch_delta_plan(d, idx_now, counts, slot_tok, n_changed, ws, s);
+  if (e != hipSuccess) return e;
+  return launch_delta_copy(d, k_cache, v_cache, d.kv_stride_layer, d.kv_stride_b, d.n_layers,
+                           n_changed, kbuf, vbuf, ws, s);
 }
 
 }  // namespace spec

@@ -134,6 +134,16 @@ hipError_t launch_delta(const Dims& d, const int32_t* idx_now, const int32_t* co
                         const uint16_t* k_cache, const uint16_t* v_cache,
                         int32_t* slot_tok, uint16_t* kbuf, uint16_t* vbuf,
                         int32_t* n_changed, void* ws, hipStream_t s);
+// Elastic loading in two parts: the slot plan (the (slot, token) list in
+// ws), then the copy of the listed rows of n_layers layers from a source
+// cache (device memory, or pinned host memory through its device address)
+// into the slot buffers.
+hipError_t launch_delta_plan(const Dims& d, const int32_t* idx_now, const int32_t* counts,
+                             int32_t* slot_tok, int32_t* n_changed, void* ws, hipStream_t s);
+hipError_t launch_delta_copy(const Dims& d, const uint16_t* k_src, const uint16_t* v_src,
+                             int64_t src_stride_layer, int64_t src_stride_b, int n_layers,
+                             const int32_t* n_changed, uint16_t* kbuf, uint16_t* vbuf,
+                             const void* ws, hipStream_t s);
 hipError_t launch_mla(const MlaDims& d, const uint16_t* q, const uint16_t* ckv,
                       const uint16_t* w_uk, const uint16_t* w_uv, const int32_t* idx,
                       const int32_t* counts, float* out, float* lse, void* ws, hipStream_t s);

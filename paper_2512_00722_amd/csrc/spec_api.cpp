@@ -77,6 +77,20 @@ spec_status resolve(const spec_dims* dm, spec::Dims* o) {
   return SPEC_OK;
 }
 
+// Attention workspace large enough for a launch over any number of layers
+// up to d.n_layers (the offloaded step attends its device layers in one
+// launch and each offloaded layer in one of its own).
+size_t attn_ws_any_layers(const spec::Dims& d) {
+  size_t m = 0;
+  spec::Dims e = d;
+  for (int n = 1; n <= d.n_layers; ++n) {
+    e.n_layers = n;
+    const size_t b = spec::attn_ws_bytes(e);
+    if (b > m) m = b;
+  }
+  return m;
+}
+
 size_t ws_bytes_for(const spec::Dims& d, spec_op op) {
   switch (op) {
     case SPEC_OP_SCORE: return spec::score_ws_bytes(d);
@@ -89,6 +103,10 @@ size_t ws_bytes_for(const spec::Dims& d, spec_op op) {
       return spec::align_up(sizeof(float) * (size_t)d.B * d.n_sets * d.L_max) +
              spec::score_ws_bytes(d) +
              spec::topk_ws_bytes(d) + spec::attn_ws_bytes(d) + spec::delta_ws_bytes(d);
+    case SPEC_OP_OFFLOAD:
+      return spec::align_up(sizeof(float) * (size_t)d.B * d.n_sets * d.L_max) +
+             spec::score_ws_bytes(d) + spec::topk_ws_bytes(d) + attn_ws_any_layers(d) +
+             spec::delta_ws_bytes(d);
   }
   return 0;
 }
@@ -181,6 +199,66 @@ spec_status check_elastic(const spec::Dims& d, const spec_elastic* el) {
       !aligned16(el->vbuf))
     return SPEC_ERR_INVALID;
   if (d.L_cap > kMaxElasticLcap) return SPEC_ERR_UNSUPPORTED;
+  return SPEC_OK;
+}
+
+// Offloaded KV in pinned host memory: both pointers must be host memory the
+// GPU can read (hipHostMalloc); the kernels use their device addresses.
+// Strides default as for the device cache and are checked the same way.
+struct HostKv {
+  const uint16_t* k;
+  const uint16_t* v;
+  int64_t stride_layer, stride_b;
+};
+
+spec_status resolve_host_kv(const spec::Dims& d, const spec_host_kv* h, HostKv* o) {
+  if (!h || !h->k || !h->v) return SPEC_ERR_INVALID;
+  if (!aligned16(h->k) || !aligned16(h->v)) return SPEC_ERR_INVALID;
+  if (h->stride_layer < 0 || h->stride_b < 0) return SPEC_ERR_INVALID;
+  const int64_t row = (int64_t)d.L_cap * d.H_kv * d.d;
+  o->stride_b = h->stride_b ? h->stride_b : row;
+  o->stride_layer = h->stride_layer ? h->stride_layer : (int64_t)d.B * o->stride_b;
+  if (o->stride_b < row || o->stride_b % 8 || o->stride_layer < row || o->stride_layer % 8)
+    return SPEC_ERR_INVALID;
+  const void* src[2] = {h->k, h->v};
+  const uint16_t* dev[2] = {nullptr, nullptr};
+  for (int i = 0; i < 2; ++i) {
+    hipPointerAttribute_t at;
+    if (hipPointerGetAttributes(&at, src[i]) != hipSuccess) {
+      (void)hipGetLastError();  // an unknown (pageable) pointer: clear the error it leaves
+      return SPEC_ERR_INVALID;
+    }
+    if (at.type != hipMemoryTypeHost || !at.devicePointer) return SPEC_ERR_INVALID;
+    dev[i] = static_cast<const uint16_t*>(at.devicePointer);
+  }
+  o->k = dev[0];
+  o->v = dev[1];
+  return SPEC_OK;
+}
+
+// The host-to-device loads of n_off offloaded layers after the slot plan
+// (already enqueued on s): with a copy stream, forked at ready[n_off] and
+// each layer's rows followed by ready[l] on it; else on s.
+spec_status enqueue_host_loads(const spec::Dims& d_off, const HostKv& hk, const spec_elastic* el,
+                               const void* ws_delta, int n_off, hipStream_t s, hipStream_t cs,
+                               void* const* ready) {
+  const hipStream_t q = cs ? cs : s;
+  hipError_t e;
+  if (cs) {
+    hipEvent_t fork = static_cast<hipEvent_t>(ready[n_off]);
+    if ((e = hipEventRecord(fork, s)) != hipSuccess) return hip_status(e);
+    if ((e = hipStreamWaitEvent(cs, fork, 0)) != hipSuccess) return hip_status(e);
+  }
+  const int64_t slot_layer = (int64_t)d_off.B * d_off.k_max * d_off.H_kv * d_off.d;
+  for (int l = 0; l < n_off; ++l) {
+    e = spec::launch_delta_copy(d_off, hk.k + (int64_t)l * hk.stride_layer,
+                                hk.v + (int64_t)l * hk.stride_layer, hk.stride_layer, hk.stride_b,
+                                1, el->n_changed, el->kbuf + l * slot_layer,
+                                el->vbuf + l * slot_layer, ws_delta, q);
+    if (e != hipSuccess) return hip_status(e);
+    if (ready && (e = hipEventRecord(static_cast<hipEvent_t>(ready[l]), q)) != hipSuccess)
+      return hip_status(e);
+  }
   return SPEC_OK;
 }
 
@@ -335,7 +413,7 @@ spec_status spec_mla_sparse_decode_attn(const spec_mla_dims* dm, const uint16_t*
 
 spec_status spec_workspace_size(const spec_dims* dm, spec_op op, size_t* bytes) {
   if (!bytes) return SPEC_ERR_INVALID;
-  if ((int)op < SPEC_OP_SCORE || (int)op > SPEC_OP_FRONTEND) return SPEC_ERR_INVALID;
+  if ((int)op < SPEC_OP_SCORE || (int)op > SPEC_OP_OFFLOAD) return SPEC_ERR_INVALID;
   spec::Dims d;
   const spec_status st = resolve(dm, &d);
   if (st != SPEC_OK) return st;
@@ -471,6 +549,107 @@ spec_status spec_step_noalloc(const spec_dims* dm, const uint16_t* q_r, const ui
 }
 
 size_t spec_step_noalloc_max_bytes(void) { return spec::kStaticScratchBytes; }
+
+spec_status spec_offload_load(const spec_dims* dm, const int32_t* idx_now, const int32_t* counts,
+                              const spec_host_kv* host, const spec_elastic* el, void* ws,
+                              size_t ws_bytes, spec_stream stream, spec_stream copy_stream,
+                              void* const* layer_ready) {
+  spec::Dims d;
+  spec_status st = resolve(dm, &d);
+  if (st != SPEC_OK) return st;
+  if (!idx_now || !counts) return SPEC_ERR_INVALID;
+  if (!aligned4(idx_now) || !aligned4(counts)) return SPEC_ERR_INVALID;
+  if (copy_stream && !layer_ready) return SPEC_ERR_INVALID;
+  if ((st = check_elastic(d, el)) != SPEC_OK) return st;
+  if ((st = check_ws(d, SPEC_OP_DELTA, ws, ws_bytes)) != SPEC_OK) return st;
+  HostKv hk;
+  if ((st = resolve_host_kv(d, host, &hk)) != SPEC_OK) return st;
+  const hipStream_t s = as_stream(stream);
+  if (debug_on() && (st = debug_selection(d.B, d.k_max, 1, idx_now, counts, d.L_cap, s)) != SPEC_OK)
+    return st;
+  hipError_t e = spec::launch_delta_plan(d, idx_now, counts, el->slot_tok, el->n_changed, ws, s);
+  if (e != hipSuccess) return hip_status(e);
+  st = enqueue_host_loads(d, hk, el, ws, d.n_layers, s, as_stream(copy_stream), layer_ready);
+  if (st == SPEC_OK && debug_on() && copy_stream) st = finish(st, as_stream(copy_stream));
+  return finish(st, s);
+}
+
+spec_status spec_step_offload(const spec_dims* dm, const uint16_t* q_r, const uint16_t* k_r,
+                              const int32_t* seq_lens, const int32_t* ks, const uint16_t* q,
+                              const uint16_t* k_cache, const uint16_t* v_cache,
+                              int32_t n_dev_layers, const spec_host_kv* host, int32_t* idx_out,
+                              int32_t* counts_out, float* out, float* lse, float* scores_out,
+                              const spec_elastic* el, void* ws, size_t ws_bytes,
+                              spec_stream stream, spec_stream copy_stream,
+                              void* const* layer_ready) {
+  spec::Dims d;
+  spec_status st = resolve(dm, &d);
+  if (st != SPEC_OK) return st;
+  if (n_dev_layers < 0 || n_dev_layers >= d.n_layers) return SPEC_ERR_INVALID;
+  if (!el) return SPEC_ERR_INVALID;
+  // The device caches are needed only for device layers; the checks of
+  // spec_step apply with stand-ins when there are none.
+  const uint16_t* kc = n_dev_layers > 0 ? k_cache : q;
+  const uint16_t* vc = n_dev_layers > 0 ? v_cache : q;
+  if ((st = check_step(dm, &d, q_r, k_r, seq_lens, ks, q, kc, vc, idx_out, counts_out, out, lse,
+                       scores_out, el)) != SPEC_OK)
+    return st;
+  if (copy_stream && !layer_ready) return SPEC_ERR_INVALID;
+  if ((st = check_ws(d, SPEC_OP_OFFLOAD, ws, ws_bytes)) != SPEC_OK) return st;
+  const int n_off = d.n_layers - n_dev_layers;
+  spec::Dims d_off = d;   // the offloaded layers: the slot buffers and the host copy
+  d_off.n_layers = n_off;
+  HostKv hk;
+  if ((st = resolve_host_kv(d_off, host, &hk)) != SPEC_OK) return st;
+  const hipStream_t s = as_stream(stream);
+  const hipStream_t cs = as_stream(copy_stream);
+  if (debug_on() && (st = debug_lengths(d, seq_lens, ks, s)) != SPEC_OK) return st;
+
+  char* p = static_cast<char*>(ws);
+  float* scores = reinterpret_cast<float*>(p);
+  p += spec::align_up(sizeof(float) * (size_t)d.B * d.n_sets * d.L_max);
+  if (scores_out) scores = scores_out;
+  void* ws_score = p;
+  p += spec::score_ws_bytes(d);
+  void* ws_topk = p;
+  p += spec::topk_ws_bytes(d);
+  void* ws_attn = p;
+  p += attn_ws_any_layers(d);
+  void* ws_delta = p;
+
+  hipError_t e = spec::launch_score(d, q_r, k_r, seq_lens, scores, ws_score, s);
+  if (e != hipSuccess) return hip_status(e);
+  e = spec::launch_topk_select(d, scores, seq_lens, ks, spec::score_ws_hist(d, ws_score),
+                               static_cast<char*>(ws_topk) + spec::topk_hist_bytes(d), idx_out,
+                               counts_out, s);
+  if (e != hipSuccess) return hip_status(e);
+  e = spec::launch_delta_plan(d_off, idx_out, counts_out, el->slot_tok, el->n_changed, ws_delta,
+                              s);
+  if (e != hipSuccess) return hip_status(e);
+  if ((st = enqueue_host_loads(d_off, hk, el, ws_delta, n_off, s, cs, layer_ready)) != SPEC_OK)
+    return st;
+  const size_t q_layer = (size_t)d.B * d.H_q * d.d;  // elements of q / out per layer
+  if (n_dev_layers > 0) {  // the device layers, while the host rows are in flight
+    spec::Dims d_dev = d;
+    d_dev.n_layers = n_dev_layers;
+    e = spec::launch_attn(d_dev, q, k_cache, v_cache, idx_out, counts_out, out, lse, ws_attn, s);
+    if (e != hipSuccess) return hip_status(e);
+  }
+  spec::Dims d_one = d_off;  // one offloaded layer over its compact slots
+  d_one.n_layers = 1;
+  const int64_t slot_layer = (int64_t)d.B * d.k_max * d.H_kv * d.d;
+  for (int l = 0; l < n_off; ++l) {
+    if (cs && (e = hipStreamWaitEvent(s, static_cast<hipEvent_t>(layer_ready[l]), 0)) !=
+                  hipSuccess)
+      return hip_status(e);
+    const size_t lo = (size_t)(n_dev_layers + l);
+    e = spec::launch_attn(d_one, q + lo * q_layer, el->kbuf + l * slot_layer,
+                          el->vbuf + l * slot_layer, nullptr, counts_out, out + lo * q_layer,
+                          lse ? lse + lo * d.B * d.H_q : nullptr, ws_attn, s);
+    if (e != hipSuccess) return hip_status(e);
+  }
+  return finish(SPEC_OK, s);
+}
 
 spec_status spec_retrieval_qk(const spec_dims* dm, const spec_frontend* fe,
                               const int32_t* tokens, const int32_t* pos, const uint16_t* emb,

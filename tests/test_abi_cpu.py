@@ -340,3 +340,44 @@ def test_step_noalloc_rejects_before_hip(lib):
     assert need > 64 << 20
     assert lib.spec_step_noalloc(byref(big), *args(), None) == 5
     assert lib.spec_last_hip_error() == 0
+
+
+def test_offload_rejects_before_launch(lib):
+    """The host-offload entry points validate everything before any launch:
+    a host pointer that is not pinned host memory (here a fake address the
+    runtime does not know) is rejected, as are a copy stream without events,
+    device-layer counts out of range, head-level sets and small workspaces."""
+    byref = ctypes.byref
+    d = good_dims(n_layers=4)
+    st_off, n_off = ws_size(lib, d, spec.OP_OFFLOAD)
+    st_step, n_step = ws_size(lib, d, spec.OP_STEP)
+    assert st_off == 0 and n_off >= n_step - ws_size(lib, d, spec.OP_ATTN)[1]
+    host = spec.HostKv(FAKE.value, FAKE.value, 0, 0)
+    el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value)
+    _, nd = ws_size(lib, d, spec.OP_DELTA)
+    ev = (ctypes.c_void_p * 5)()
+    # spec_offload_load
+    assert lib.spec_offload_load(byref(d), FAKE, FAKE, byref(host), byref(el), FAKE, nd, None,
+                                 None, None) == 1          # not pinned host memory
+    assert lib.spec_offload_load(byref(d), FAKE, FAKE, byref(host), byref(el), FAKE, nd, None,
+                                 FAKE, None) == 1          # copy stream without events
+    assert lib.spec_offload_load(byref(d), FAKE, FAKE, None, byref(el), FAKE, nd, None, None,
+                                 None) == 1
+    assert lib.spec_offload_load(byref(d), FAKE, FAKE, byref(host), byref(el), None, 0, None,
+                                 None, None) == 3
+    assert lib.spec_offload_load(byref(good_dims(n_sets=8)), FAKE, FAKE, byref(host), byref(el),
+                                 FAKE, 1 << 40, None, None, None) == 2
+    # spec_step_offload
+    args = lambda n_dev: [FAKE] * 7 + [n_dev, byref(host)] + [FAKE] * 3 + [None, None]
+    for n_dev in (-1, 4, 5):
+        assert lib.spec_step_offload(byref(d), *args(n_dev), byref(el), FAKE, n_off, None, None,
+                                     None) == 1, n_dev
+    assert lib.spec_step_offload(byref(d), *args(2), None, FAKE, n_off, None, None, None) == 1
+    assert lib.spec_step_offload(byref(d), *args(2), byref(el), FAKE, n_off, None, FAKE,
+                                 None) == 1              # copy stream without events
+    assert lib.spec_step_offload(byref(d), *args(2), byref(el), FAKE, 64, None, None, None) == 3
+    assert lib.spec_step_offload(byref(d), *args(2), byref(el), FAKE, n_off, None, None,
+                                 None) == 1              # fake host memory
+    assert lib.spec_step_offload(byref(good_dims(n_layers=4, d=96)), *args(2), byref(el), FAKE,
+                                 n_off, None, None, None) == 2
+    assert lib.spec_last_hip_error() == 0
