@@ -56,6 +56,10 @@ def parse():
                     help="time only the retrieval head's front end for the new token "
                          "(embedding row, Q/K projection, YaRN rotary embedding, K_r append): "
                          "--steps calls, replayed from HIP graphs of 20 calls")
+    ap.add_argument("--offload", type=int, default=0, metavar="N",
+                    help="ragged elastic workload only: keep the last N layers' KV in pinned "
+                         "host memory (spec_step_offload: elastic loads over the host link on a "
+                         "second stream, one event per layer)")
     ap.add_argument("--headline-only", action="store_true",
                     help="time only the benchmark workload (by default the other four "
                          "decode-step workloads follow it, under \"configs\")")
@@ -235,6 +239,14 @@ def main():
         print("bench.py: elastic loading keeps one token set per sequence; --head-level does "
               "not apply to this workload", file=sys.stderr)
         sys.exit(2)
+    if args.offload:
+        if w.steps <= 1:
+            print("bench.py: --offload applies to the ragged elastic workload", file=sys.stderr)
+            sys.exit(2)
+        line = run_offload(args, spec, w, x, elastic_sequence(w, x, seed=args.seed, device=dev),
+                           args.offload)
+        print(json.dumps(line), flush=True)
+        return
     if w.steps > 1:
         line = run_elastic(args, spec, w, x, elastic_sequence(w, x, seed=args.seed, device=dev),
                            algorithmic_bytes)
@@ -450,6 +462,13 @@ def other_configs(args, spec, workloads, dev):
                                                          "bytes_per_launch", "avg_launch_us",
                                                          "kernel")}
         res[name] = r
+        if w.steps > 1:   # the same workload with its last 4 layers' KV in host memory
+            a.offload = 4
+            ln = run_offload(a, spec, w, x, elastic_sequence(w, x, seed=args.seed, device=dev), 4)
+            res[name + "_offload4"] = {k: ln[k] for k in ("value", "ms_per_step", "step_us",
+                                                          "first_step_us", "host_link",
+                                                          "host_bytes_per_step")}
+            res[name + "_offload4"]["steps"] = a.steps
         del x, ln
         torch.cuda.empty_cache()
     return res
@@ -566,6 +585,148 @@ def run_elastic(args, spec, w, x, e, algorithmic_bytes):
         "step_us": _spread(step_us),
         "first_step_us": round(step_us[0], 1),
         "later_steps_us_mean": round(statistics.mean(step_us[1:]), 1) if S > 1 else None,
+    }
+
+
+PCIE5_X16_GBPS = 64.0  # MI355X host link, PCIe 5.0 x16, one direction (published)
+
+
+def host_link_gbps(dev, nbytes=1 << 30):
+    """Host-to-device bandwidth of a plain copy from pinned memory (the
+    reference the elastic loads are compared with): median of 3 copies."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    dst = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    ts = []
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src, non_blocking=True)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e-3)
+    del src, dst
+    return nbytes / statistics.median(ts[1:]) / 1e9
+
+
+def run_offload(args, spec, w, x, e, n_off):
+    """The ragged elastic workload with the KV of its last n_off layers in
+    pinned host memory (spec_step_offload): per step the retrieval and top-k,
+    the elastic plan, the host-to-device loads of S_now - S_last for each
+    offloaded layer on a second stream, the attention of the device layers
+    meanwhile, then each offloaded layer's attention after its own rows.  The
+    16-step sequence runs cyclically; each pass starts from an empty slot
+    state (a full load).  Reports steps/s, the bytes each step moved over the
+    host link against a full reload of the same selection, and the loads'
+    host-link bandwidth (measured alone) against a plain pinned copy."""
+    import torch
+
+    dev = x["K"].device
+    S = w.steps
+    n_dev = w.n_layers - n_off
+    t0 = time.perf_counter()
+    host_k = torch.empty((n_off,) + tuple(x["K"].shape[1:]), dtype=torch.bfloat16,
+                         pin_memory=True)
+    host_v = torch.empty_like(host_k, pin_memory=True)
+    host_k.copy_(x["K"][n_dev:])
+    host_v.copy_(x["V"][n_dev:])
+    print(f"[bench] {n_off} layers ({2 * host_k.numel() * 2 / 1e9:.1f} GB) in pinned host memory "
+          f"in {time.perf_counter() - t0:.1f}s", file=sys.stderr, flush=True)
+    K_dev, V_dev = (x["K"][:n_dev], x["V"][:n_dev]) if n_dev else (None, None)
+    st = spec.ElasticState(n_off, w.B, w.k, w.H_kv, w.d, dev)
+    copy = torch.cuda.Stream()
+    events = spec.OffloadEvents(n_off, dev)
+    outputs = {}
+    dims = spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, H_r=w.H_r, d_r=w.d_r,
+                          n_layers=w.n_layers, H_q=w.H_q, H_kv=w.H_kv, d=w.d,
+                          kr_stride_b=x["K_r"].stride(0), kv_stride_layer=x["K"].stride(0),
+                          kv_stride_b=x["K"].stride(1))
+    ws = torch.zeros(spec.workspace_size(dims, spec.OP_OFFLOAD), dtype=torch.uint8, device=dev)
+
+    def one(i):
+        s = i % S
+        if s == 0:
+            st.reset()
+        spec.step_offload(e["q_r"][s], x["K_r"], e["seq_lens"][s], x["ks"], e["q"][s], K_dev,
+                          V_dev, host_k, host_v, w.k, st, copy_stream=copy, events=events,
+                          ws=ws, outputs=outputs)
+
+    for i in range(args.warmup):
+        one(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        one(i)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    value = args.steps / wall
+    print(f"[bench] {args.steps} offloaded steps in {wall:.3f}s", file=sys.stderr, flush=True)
+
+    # One more pass with per-step events and the rows each step loaded.
+    row_bytes = 2 * w.H_kv * w.d * 2          # K and V of one token in one layer
+    step_us, rows = [], []
+    for s in range(S):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        one(s)
+        e1.record()
+        torch.cuda.synchronize()
+        step_us.append(e0.elapsed_time(e1) * 1e3)
+        rows.append(int(st.n_changed.sum()))
+    k_total = int(outputs["counts"].sum())
+    host_bytes = [r * n_off * row_bytes for r in rows]
+    full_bytes = k_total * n_off * row_bytes
+
+    # The loads alone (plan + host copies, one stream) on the same selections:
+    # the host-link bandwidth they reach, later steps of a pass.
+    idx_seq = []
+    for s in range(S):
+        r = spec.step(e["q_r"][s], x["K_r"], e["seq_lens"][s], x["ks"], e["q"][s], x["K"],
+                      x["V"], k_max=w.k)
+        idx_seq.append((r["idx"].clone(), r["counts"].clone()))
+    st2 = spec.ElasticState(n_off, w.B, w.k, w.H_kv, w.d, dev)
+    load_us = []
+    for s in range(S):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        spec.offload_load(idx_seq[s][0], idx_seq[s][1], host_k, host_v, st2)
+        e1.record()
+        torch.cuda.synchronize()
+        load_us.append(e0.elapsed_time(e1) * 1e3)
+    link = host_link_gbps(dev)
+    later = range(1, S)
+    load_gbps = statistics.median(host_bytes[s] / (load_us[s] * 1e-6) / 1e9 for s in later)
+    full_gbps = host_bytes[0] / (load_us[0] * 1e-6) / 1e9
+    med_bytes = statistics.median(host_bytes[s] for s in later)
+    del host_k, host_v
+    return {
+        "metric": "decode steps/s of retrieve+top-k+sparse attn with the last layers' KV in "
+                  "host memory (elastic loading over the host link)",
+        "value": round(value, 3), "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "L0": [w.ragged_min, w.L], "n_layers": w.n_layers,
+                   "layers_in_host_memory": n_off, "H_q": w.H_q, "H_kv": w.H_kv, "d": w.d,
+                   "k": w.k, "steps_per_pass": S},
+        "step_us": _spread(step_us[1:]),
+        "first_step_us": round(step_us[0], 1),
+        "host_link": {
+            "bound": "host_link",
+            "elastic_load_gbps": round(load_gbps, 1),
+            "full_load_gbps": round(full_gbps, 1),
+            "plain_copy_gbps": round(link, 1),
+            "frac_of_plain_copy": round(load_gbps / link, 3),
+            "peak_gbps": PCIE5_X16_GBPS,
+            "load_us_median": round(statistics.median(load_us[s] for s in later), 1),
+        },
+        "host_bytes_per_step": {
+            "elastic_median": int(med_bytes),
+            "full_reload": int(full_bytes),
+            "reduction": round(1.0 - med_bytes / full_bytes, 4),
+            "rows_loaded_per_step": rows,
+            "selected_rows": k_total,
+        },
     }
 
 
