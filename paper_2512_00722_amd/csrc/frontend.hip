@@ -27,8 +27,8 @@
 // rotated in the workgroup.  Every weight byte is read once; the embedding
 // rows come from L2.
 //
-// More sequences: two kernels, since a narrow tile per workgroup would make
-// every workgroup re-read all embedding rows.
+// More than 64 sequences: two kernels, since a narrow tile per workgroup
+// would make every workgroup re-read all embedding rows.
 //
 //  1. qk_partial_kernel (matrix cores, v_mfma_f32_16x16x32_bf16, tokens on
 //     the M side): a workgroup owns 16 output features of Q or K -- the
@@ -238,6 +238,109 @@ __global__ __launch_bounds__(kFinishThreads) void qk_finish_kernel(FrontArgs a) 
     y += p[half];
   }
   store_pair(a, mat, b, h, i, x, y, a.theta[i], (float)a.theta[half]);
+}
+
+// 17 to 64 sequences, one kernel (qk_full_kernel): a workgroup owns the 16
+// features of qk_partial_kernel's tile (dimensions i0..i0+7 of one head and
+// their rotary partners) for 16 tokens over the WHOLE hidden dimension; its
+// waves take the 128-element steps in turn (the loads of up to CH steps
+// issued before the first MFMA), their tiles are summed in LDS in wave order
+// (deterministic), and the pairs are rotated and stored in the epilogue: no
+// partial sums leave the workgroup.  The token blocks of one feature tile
+// are n_tiles = 2 H_r d_r / 16 workgroups apart, a multiple of the 8 XCDs,
+// so they run on one XCD and its L2 serves the tile's weight rows to all of
+// them after the first read.
+constexpr int kFullWaves = 8;
+template <int T, int kFullWaves, int CH>
+__global__ __launch_bounds__(64 * kFullWaves) void qk_full_kernel(FrontArgs a) {
+  constexpr int kFullThreads = 64 * kFullWaves;
+  __shared__ float red[kFullWaves * T * 256];
+  __shared__ double theta[8];
+  __shared__ float mscale;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int tiles_per_head = a.d_r / 16;
+  const int per_mat = a.H_r * tiles_per_head;
+  const int tile = blockIdx.x;
+  const int mat = tile / per_mat;  // 0: Q, 1: K
+  const int rem = tile - mat * per_mat;
+  const int h = rem / tiles_per_head;
+  const int i0 = 8 * (rem - h * tiles_per_head);
+  const int b0 = blockIdx.y * 16 * T;
+  const int n_steps = a.hidden / kFeStep;
+
+  const int n = lane & 15;
+  const int g = lane >> 4;
+  const int fbase = h * a.d_r + i0 + (n & 7) + (n >> 3) * (a.d_r / 2);
+  const uint16_t* wrow = (mat ? a.w_k : a.w_q) + (size_t)fbase * a.hidden + 8 * g;
+  const uint16_t* erow[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int b = min(b0 + 16 * t + n, a.B - 1);  // rows past B compute a copy, never stored
+    const int tok = clampi(a.tokens[b], 0, a.vocab - 1);
+    erow[t] = a.emb + (size_t)tok * a.hidden + 8 * g;
+  }
+  if (wave == 0 && lane < 8) {  // frequencies of this tile's pairs, while the loads fly
+    theta[lane] = yarn_theta(a, i0 + lane);
+    if (lane == 0) mscale = a.scale > 1.0f ? (float)(0.1 * log((double)a.scale) + 1.0) : 1.0f;
+  }
+
+  floatx4 acc[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int s0 = wave; s0 < n_steps; s0 += kFullWaves * CH) {
+    // the loads of CH steps, all issued before the first MFMA (steps past the
+    // row re-read its last step and are not accumulated)
+    uint4 w[CH][4];
+    uint4 e[CH][T][4];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const size_t off = (size_t)min(s0 + c * kFullWaves, n_steps - 1) * kFeStep;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w[c][j] = ldg16(wrow + off + 32 * j);
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) e[c][t][j] = ldg16(erow[t] + off + 32 * j);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // no MFMA (and its wait) moves above a load
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      if (s0 + c * kFullWaves < n_steps) {  // wave-uniform
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, e[c][t][j]), __builtin_bit_cast(bf16x8, w[c][j]),
+                acc[t], 0, 0, 0);
+      }
+    }
+  }
+
+  // lane (n, g) holds D[4g + i][n]: token 16t + 4g + i, feature n of the tile
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[((wave * T + t) * 4 + i) * 64 + lane] = acc[t][i];
+  __syncthreads();
+  // one thread per (token, pair): the pair's two features summed over the waves
+  for (int e = threadIdx.x; e < 16 * T * 8; e += kFullThreads) {
+    const int p = e & 7;
+    const int tok = e >> 3;  // 0 .. 16T - 1
+    const int t = tok >> 4, r = tok & 15;
+    const int i = r & 3, gg = r >> 2;
+    const int lx = gg * 16 + p, ly = gg * 16 + 8 + p;  // lanes holding features p and p + half
+    float x = 0.f, y = 0.f;
+#pragma unroll
+    for (int w = 0; w < kFullWaves; ++w) {
+      x += red[((w * T + t) * 4 + i) * 64 + lx];
+      y += red[((w * T + t) * 4 + i) * 64 + ly];
+    }
+    const int b = b0 + tok;
+    if (b < a.B) store_pair(a, mat, b, h, i0 + p, x, y, theta[p], mscale);
+  }
 }
 
 constexpr int kGvSlab = 512;  // hidden elements per wave slab: 64 lanes x 8
@@ -450,11 +553,18 @@ hipError_t launch_retrieval_qk(const Dims& d, const FrontDims& f, const int32_t*
     return hipGetLastError();
   }
   const int n_tiles = 2 * d.H_r * (d.d_r / 16);
-  if (d.B <= 32) {
-    launch_partial<2>(a, dim3(n_tiles * p.ks, 1), s);
-  } else {
-    launch_partial<4>(a, dim3(n_tiles * p.ks, (d.B + 63) / 64), s);
+  if (d.B <= 64) {  // one kernel: 16 tokens and 16 features per workgroup, whole rows
+    const dim3 grid(n_tiles, (d.B + 15) / 16);
+    const int per_wave = (f.hidden / kFeStep + kFullWaves - 1) / kFullWaves;
+    if (per_wave >= 4)
+      hipLaunchKernelGGL((qk_full_kernel<1, kFullWaves, 4>), grid, dim3(64 * kFullWaves), 0, s, a);
+    else if (per_wave >= 2)
+      hipLaunchKernelGGL((qk_full_kernel<1, kFullWaves, 2>), grid, dim3(64 * kFullWaves), 0, s, a);
+    else
+      hipLaunchKernelGGL((qk_full_kernel<1, kFullWaves, 1>), grid, dim3(64 * kFullWaves), 0, s, a);
+    return hipGetLastError();
   }
+  launch_partial<4>(a, dim3(n_tiles * p.ks, (d.B + 63) / 64), s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int total = d.B * d.H_r * d.d_r;  // B * 2 * H_r * d_r/2 pairs
