@@ -787,7 +787,8 @@ def run_frontend(args, spec, w, x):
     us = e0.elapsed_time(e1) * 1e3 / calls
     fb = frontend_bytes(w)
     achieved = fb / (us * 1e-6) / 1e9
-    kernels = ("qk_gemv_kernel" if w.B <= 16 else "qk_partial_kernel + qk_finish_kernel")
+    kernels = ("qk_gemv_kernel" if w.B <= 16 else
+               "qk_full_kernel" if w.B <= 64 else "qk_partial_kernel + qk_finish_kernel")
     line = {
         "metric": "retrieval head front-end calls/s (embedding, Q/K projection, YaRN RoPE, "
                   "K_r append)",
