@@ -54,3 +54,33 @@ def test_debug_mode_rejects_and_matches(dev, monkeypatch):
     spec.gather(x["K"], x["V"], idx2, cnt)
     torch.cuda.synchronize()
     monkeypatch.delenv("SPEC_DEBUG")
+
+
+def test_debug_mode_offload(dev, monkeypatch):
+    """SPEC_DEBUG=1 on the host-offload entry points: a count above k_max is
+    rejected before anything is enqueued; valid calls match the plain ones."""
+    announce("SPEC_DEBUG offload")
+    w = small_workload(B=2, L=600, H_r=4, d_r=64, n_layers=2, H_q=8, H_kv=2, k=64)
+    x = generate(w, seed=2, device=dev)
+    host_k = torch.empty(x["K"][1:].shape, dtype=torch.bfloat16, pin_memory=True)
+    host_v = torch.empty_like(host_k, pin_memory=True)
+    host_k.copy_(x["K"][1:])
+    host_v.copy_(x["V"][1:])
+    st = spec.ElasticState(1, w.B, w.k, w.H_kv, w.d, dev)
+    ref = spec.step_offload(x["q_r"], x["K_r"], x["seq_lens"], x["ks"], x["q"], x["K"][:1],
+                            x["V"][:1], host_k, host_v, w.k, st)
+    torch.cuda.synchronize()
+    ref_out = ref["out"].clone()
+    monkeypatch.setenv("SPEC_DEBUG", "1")
+    st.reset()
+    got = spec.step_offload(x["q_r"], x["K_r"], x["seq_lens"], x["ks"], x["q"], x["K"][:1],
+                            x["V"][:1], host_k, host_v, w.k, st, copy_stream=torch.cuda.Stream())
+    assert torch.equal(got["out"], ref_out)
+    bad = torch.tensor([64, 65], dtype=torch.int32, device=dev)
+    before = st.slot_tok.clone()
+    with pytest.raises(spec.SpecError) as e:
+        spec.offload_load(ref["idx"], bad, host_k, host_v, st)
+    assert e.value.status == 1
+    torch.cuda.synchronize()
+    assert torch.equal(st.slot_tok, before)          # nothing was enqueued
+    monkeypatch.delenv("SPEC_DEBUG")

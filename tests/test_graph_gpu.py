@@ -49,3 +49,64 @@ def test_step_graph_replays_match_eager():
         torch.cuda.synchronize()
         for k, v in ref.items():
             assert torch.equal(outputs[k], v), (rep, k)
+
+
+def test_step_offload_graph_replays_match_eager():
+    """The step with host-offloaded layers captured in a graph: the copy
+    stream joins the capture through the caller's events (fork after the
+    slot plan, one join per offloaded layer).  Each replay, from an empty
+    slot state set eagerly, matches the eager step bit for bit."""
+    dev = need_gpu()
+    announce("graph replay of the offloaded step")
+    w = small_workload(B=3, L=2500, H_r=8, d_r=64, n_layers=3, H_q=32, H_kv=8, k=300,
+                       heavy_frac=0.02, ragged_min=1000)
+    x = generate(w, seed=12, device=dev)
+    n_dev = 1
+    host_k = torch.empty(x["K"][n_dev:].shape, dtype=torch.bfloat16, pin_memory=True)
+    host_v = torch.empty_like(host_k, pin_memory=True)
+    host_k.copy_(x["K"][n_dev:])
+    host_v.copy_(x["V"][n_dev:])
+    n_off = w.n_layers - n_dev
+    args = (x["q_r"], x["K_r"], x["seq_lens"], x["ks"], x["q"], x["K"][:n_dev], x["V"][:n_dev],
+            host_k, host_v, w.k)
+    copy = torch.cuda.Stream()
+    events = spec.OffloadEvents(n_off, dev)
+    st = spec.ElasticState(n_off, w.B, w.k, w.H_kv, w.d, dev)
+    dims = spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, H_r=w.H_r, d_r=w.d_r,
+                          n_layers=w.n_layers, H_q=w.H_q, H_kv=w.H_kv, d=w.d,
+                          kr_stride_b=x["K_r"].stride(0), kv_stride_layer=x["K"].stride(0),
+                          kv_stride_b=x["K"].stride(1))
+    ws = torch.zeros(spec.workspace_size(dims, spec.OP_OFFLOAD), dtype=torch.uint8, device=dev)
+    eager = spec.step_offload(*args, st, copy_stream=copy, events=events, with_scores=True,
+                              with_lse=True, ws=ws)
+    torch.cuda.synchronize()
+    ref = {k: v.clone() for k, v in eager.items() if isinstance(v, torch.Tensor)}
+    ref_slots = st.slot_tok.clone()
+    ref_nch = st.n_changed.clone()
+
+    outputs = {}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        st.reset()
+        spec.step_offload(*args, st, copy_stream=copy, events=events, with_scores=True,
+                          with_lse=True, ws=ws, outputs=outputs)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        spec.step_offload(*args, st, copy_stream=copy, events=events, with_scores=True,
+                          with_lse=True, ws=ws, outputs=outputs)
+    for rep in range(4):
+        for v in outputs.values():
+            if isinstance(v, torch.Tensor):
+                v.fill_(7)                      # stale values must be overwritten
+        st.reset()                              # each replay is a full load
+        st.kbuf.fill_(0)
+        spec.score(x["q_r"], x["K_r"], x["seq_lens"])   # eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k, v in ref.items():
+            assert torch.equal(outputs[k], v), (rep, k)
+        assert torch.equal(st.slot_tok, ref_slots) and torch.equal(st.n_changed, ref_nch), rep
