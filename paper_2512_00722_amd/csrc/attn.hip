@@ -788,19 +788,31 @@ struct AttnPlan {
 // split and each unit writes its output (kDirect).  With fewer groups the
 // selections are split until there is about one unit per slot, but not below
 // kMinSplitTokens (each unit pays a start-up latency and a partial-result
-// store) nor above kMaxSplit (the index staging area) (kGlobalPartials).
+// store; kMinSplitSmall for launches too small to fill the CUs) nor above
+// kMaxSplit (the index staging area) (kGlobalPartials).
 // Units are numbered KV head fastest, so that the wavefronts of a workgroup
 // read the same selected tokens' rows for neighbouring heads at the same time:
 // those pieces share DRAM pages.  A split is a whole number of chunks.
 // Column groups of at most 16 query heads per KV head.
 int attn_col_groups(const Dims& d) { return d.G > 16 ? d.G / 16 : 1; }
 
+// A launch whose units of kMinSplitTokens would not reach one per four CUs
+// (a single short layer) is latency-bound: its units may go down to
+// kMinSplitSmall tokens, so that more CUs take part.  Launches above that
+// keep the larger units, whose start-up cost is then the larger one.
+constexpr int kMinSplitSmall = 64;
+constexpr int64_t kSmallLaunchUnits = 64;
+
 AttnPlan attn_plan(const Dims& d) {
   const int64_t base = (int64_t)d.n_layers * d.B * d.H_kv * attn_col_groups(d);
   auto round_chunk = [](int64_t t) { return (t + kChunk - 1) / kChunk * kChunk; };
+  const int64_t min_split =
+      base * ((d.k_max + kMinSplitTokens - 1) / kMinSplitTokens) < kSmallLaunchUnits
+          ? kMinSplitSmall
+          : kMinSplitTokens;
   int64_t n_split = (kWaveSlots * kSlotUnits + base - 1) / base;
   int64_t split = round_chunk((d.k_max + n_split - 1) / n_split);
-  if (split < kMinSplitTokens) split = kMinSplitTokens;
+  if (split < min_split) split = min_split;
   if (split > kMaxSplit) split = kMaxSplit;
   n_split = (d.k_max + split - 1) / split;
   if (n_split == 1) return {kDirect, 1, (int)round_chunk(d.k_max)};

@@ -22,16 +22,26 @@ struct Dims {
 constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-// Retrieval scoring: tokens per workgroup of the logits kernel.
-#ifndef SPEC_SCORE_TPB
-#define SPEC_SCORE_TPB 256
-#endif
-constexpr int kScoreTokensPerBlock = SPEC_SCORE_TPB;
+// Retrieval scoring: tokens per workgroup of the logits kernel, 256, halved
+// (down to 64) while the grid would have fewer workgroups than the chip has
+// CUs: a short single sequence is latency-bound, and more, smaller blocks
+// keep more bytes in flight.
+constexpr int kScoreTokensPerBlock = 256;
+constexpr int kScoreTokensPerBlockMin = 64;
+constexpr int64_t kScoreMinBlocks = 256;
 // Softmax/head-sum kernel: tokens per workgroup.
 constexpr int kSoftTokensPerBlock = 1024;
 
+inline int score_tokens_per_block(const Dims& d) {
+  int tpb = kScoreTokensPerBlock;
+  while (tpb > kScoreTokensPerBlockMin &&
+         (int64_t)d.B * ((d.L_max + tpb - 1) / tpb) < kScoreMinBlocks)
+    tpb /= 2;
+  return tpb;
+}
 inline int score_blocks(const Dims& d) {
-  return (d.L_max + kScoreTokensPerBlock - 1) / kScoreTokensPerBlock;
+  const int tpb = score_tokens_per_block(d);
+  return (d.L_max + tpb - 1) / tpb;
 }
 // Top-k: 4096-bin histogram of the top 12 bits of the score keys per score
 // row (B * n_sets rows).

@@ -5,8 +5,9 @@
 //  1. logits_kernel streams K_r once.  Each lane holds 8 bf16 of one
 //     (token, head) row slice in one 16-byte load; the d_r/8 lanes of a head
 //     reduce their partial dot products with cross-lane shuffles.  A
-//     workgroup covers 256 tokens; it writes the logits (log2 units, the
-//     scale and log2(e) folded into q_r) and its per-head (max, sum exp2).
+//     workgroup covers 256 tokens (64 or 128 when the grid would not cover
+//     the CUs); it writes the logits (log2 units, the scale and log2(e)
+//     folded into q_r) and its per-head (max, sum exp2).
 //  2. softmax_headsum_kernel merges the per-block pairs into each head's
 //     normaliser c_h = M_h + log2 Z_h and writes
 //     score[t] = sum_h exp2(l[h,t] - c_h), -inf beyond the sequence length.
@@ -18,7 +19,6 @@
 namespace spec {
 namespace {
 
-constexpr int T1 = kScoreTokensPerBlock;
 constexpr int T2 = kSoftTokensPerBlock;
 // Rows in flight per lane: 4 where the grid covers the CUs several times
 // over (more would only lengthen the queues), 8 for small grids, whose few
@@ -38,7 +38,9 @@ struct LogitsArgs {
   float qscale;   // scale_r * log2(e)
 };
 
-template <int LPH, int kUnroll>  // lanes per head = d_r / 8; rows in flight per lane
+// LPH: lanes per head = d_r / 8; kUnroll: rows in flight per lane; T1:
+// tokens per workgroup.
+template <int LPH, int kUnroll, int T1>
 __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
   constexpr int d_r = LPH * 8;
   const int b = blockIdx.y;
@@ -129,6 +131,7 @@ struct SoftArgs {
   float* scores;   // [B][n_sets][L_max]
   int32_t* hist;   // [B][n_sets][4096]: histogram of key bits 31..20 of the scores
   int L_max, H_r, n_blk, n_sets;
+  int tpb;         // tokens per block of the logits kernel
 };
 
 // One workgroup per (T2 tokens, score row); thread = 4 consecutive tokens.
@@ -201,7 +204,7 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
     for (int t = t0 + tid; t < t1; t += 256) out[t] = -INFINITY;
     return;
   }
-  const int nb = (L_b + T1 - 1) / T1;
+  const int nb = (L_b + a.tpb - 1) / a.tpb;
   float m = -INFINITY, s = 0.f;
   if (hh < per) {
 #pragma unroll
@@ -262,6 +265,18 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
     if (sh_hist[i]) atomicAdd(&gh[i], sh_hist[i]);
 }
 
+template <int LPH>
+void launch_logits(dim3 g, int tpb, bool wide, const LogitsArgs& a, hipStream_t s) {
+  if (tpb == 256) {
+    if (wide) logits_kernel<LPH, kUnrollWide, 256><<<g, 256, 0, s>>>(a);
+    else logits_kernel<LPH, kUnrollNarrow, 256><<<g, 256, 0, s>>>(a);
+  } else if (tpb == 128) {
+    logits_kernel<LPH, kUnrollNarrow, 128><<<g, 256, 0, s>>>(a);
+  } else {
+    logits_kernel<LPH, kUnrollNarrow, 64><<<g, 256, 0, s>>>(a);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
@@ -273,16 +288,14 @@ hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
   int32_t* hist = score_ws_hist(d, ws);
   LogitsArgs la{q_r, k_r, seq_lens, logits, part, hist, d.kr_stride_b,
                 d.L_max, d.H_r, n_blk, d.n_sets, d.scale_r * kLog2e};
+  const int tpb = score_tokens_per_block(d);
   const dim3 g1(n_blk, d.B);
   const bool wide = (int64_t)n_blk * d.B >= 2 * (int64_t)device_cu_count();
-  if (d.d_r == 64) {
-    if (wide) logits_kernel<8, kUnrollWide><<<g1, 256, 0, s>>>(la);
-    else logits_kernel<8, kUnrollNarrow><<<g1, 256, 0, s>>>(la);
-  } else {
-    if (wide) logits_kernel<16, kUnrollWide><<<g1, 256, 0, s>>>(la);
-    else logits_kernel<16, kUnrollNarrow><<<g1, 256, 0, s>>>(la);
-  }
-  SoftArgs sa{logits, part, seq_lens, scores, hist, d.L_max, d.H_r, n_blk, d.n_sets};
+  if (d.d_r == 64)
+    launch_logits<8>(g1, tpb, wide, la, s);
+  else
+    launch_logits<16>(g1, tpb, wide, la, s);
+  SoftArgs sa{logits, part, seq_lens, scores, hist, d.L_max, d.H_r, n_blk, d.n_sets, tpb};
   const dim3 g2((d.L_max + T2 - 1) / T2, d.B * d.n_sets);
   softmax_headsum_kernel<<<g2, 256, 0, s>>>(sa);
   return hipGetLastError();

@@ -37,6 +37,10 @@ SCORE_CASES = [
     (1, 600, 600, 5, 128, [600]),
     # more per-block softmax pairs per head than one pass of the merge holds
     (1, 70000, 70000, 16, 64, [70000]),
+    # logits blocks of 128 tokens (one sequence, fewer than 256 blocks of 256)
+    (1, 40000, 40000, 8, 64, [39999]),
+    # blocks of 64 tokens, more pairs per head than one merge pass holds
+    (1, 30000, 30000, 16, 64, [29999]),
 ]
 
 
