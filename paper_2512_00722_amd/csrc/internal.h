@@ -61,11 +61,28 @@ inline size_t score_part_bytes(const Dims& d) {
 inline size_t score_ws_bytes(const Dims& d) {
   return score_logits_bytes(d) + score_part_bytes(d) + topk_hist_bytes(d);
 }
-// The histogram region inside a score workspace.
+// The regions of a score workspace: logits, per-block pairs, histogram.
+inline float* score_ws_logits(void* ws) { return static_cast<float*>(ws); }
+inline float* score_ws_part(const Dims& d, void* ws) {
+  return reinterpret_cast<float*>(static_cast<char*>(ws) + score_logits_bytes(d));
+}
 inline int32_t* score_ws_hist(const Dims& d, void* ws) {
   return reinterpret_cast<int32_t*>(static_cast<char*>(ws) + score_logits_bytes(d) +
                                     score_part_bytes(d));
 }
+
+// Short score rows are normalised, summed and selected by one workgroup each,
+// their keys held in LDS (one launch in place of the softmax and the two
+// tiled selection kernels): rows of at most kRowSelectMaxL tokens whose
+// logits (heads per row x tokens) number at most kRowSelectMaxLogits.  One
+// workgroup streams only a few tens of GB/s, so longer rows are faster on
+// the tiled path, which spreads a row over many workgroups.
+constexpr int kRowSelectMaxL = 8192;
+constexpr int64_t kRowSelectMaxLogits = 32768;
+// heads_per_row: H_r / n_sets for the fused step, 1 for a standalone
+// selection.  SPEC_TOPK_PATH=tiles in the environment forces the tiled
+// kernels (tests compare both paths).
+bool row_select_fits(const Dims& d, int heads_per_row);
 
 // Per-tile lists of the selection (tokens per tile: kTopkTile): the
 // threshold bin of each row, per-tile counts, the tokens above the threshold
@@ -127,6 +144,24 @@ int device_cu_count();
 hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
                         const int32_t* seq_lens, float* scores, void* ws,
                         hipStream_t s);
+// The logits kernel alone (logits and per-block pairs into the score
+// workspace); zero_hist: also clear the selection histogram there.
+hipError_t launch_logits(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
+                         const int32_t* seq_lens, void* ws, bool zero_hist, hipStream_t s);
+// One workgroup per score row (requires row_select_fits): from the logits
+// and pairs of the score workspace `ws_score` (scores written to `scores`
+// when not null), or, with ws_score null, from the scores in `scores`.
+hipError_t launch_row_select(const Dims& d, void* ws_score, float* scores,
+                             const int32_t* seq_lens, const int32_t* ks, int32_t* idx,
+                             int32_t* counts, hipStream_t s);
+// Scores and selection of the fused step: the row kernel where it fits,
+// else the score kernels and the tiled selection.  scores_keep: where the
+// caller wants the scores (may be null); scores_ws: a [B][n_sets][L_max]
+// fp32 buffer for the tiled path.
+hipError_t launch_score_select(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
+                               const int32_t* seq_lens, const int32_t* ks, float* scores_keep,
+                               float* scores_ws, int32_t* idx, int32_t* counts, void* ws_score,
+                               void* ws_topk, hipStream_t s);
 hipError_t launch_topk(const Dims& d, const float* scores, const int32_t* seq_lens,
                        const int32_t* ks, int32_t* idx, int32_t* counts, void* ws,
                        hipStream_t s);

@@ -15,6 +15,7 @@
 // formed, hence the logits round trip (1/(d_r/2) of the K_r bytes).
 #include "device_common.h"
 #include "internal.h"
+#include "score_norm.h"
 
 namespace spec {
 namespace {
@@ -32,7 +33,7 @@ struct LogitsArgs {
   const int32_t* seq_lens;
   float* logits;  // [B][H_r][L_max], log2 units
   float* part;    // [B][H_r][n_blk][2]: block max, block sum of exp2(l - max)
-  int32_t* hist;  // [B][n_sets][4096] top-k histograms, zeroed here for the next kernel
+  int32_t* hist;  // [B][n_sets][4096] top-k histograms, zeroed here for the next kernel (or null)
   int64_t kr_stride_b;
   int L_max, H_r, n_blk, n_sets;
   float qscale;   // scale_r * log2(e)
@@ -46,7 +47,7 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
   const int b = blockIdx.y;
   const int blk = blockIdx.x;
   const int L_b = clampi(a.seq_lens[b], 0, a.L_max);
-  if (blk == 0) {
+  if (blk == 0 && a.hist) {
     int32_t* h = a.hist + (size_t)b * a.n_sets * kTopkBins;
     for (int i = threadIdx.x; i < a.n_sets * kTopkBins; i += 256) h[i] = 0;
   }
@@ -183,64 +184,15 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
       for (int e = 0; e < 4; ++e) lv[e][h] = 0.f;
     }
   }
-  const int P = per <= 1 ? 1 : per <= 2 ? 2 : per <= 4 ? 4 : per <= 8 ? 8 : 16;
-  const int LPH = 256 / P;
-  const int hh = tid / LPH;
-  const int j = tid - hh * LPH;
-  // Each head's normaliser c_h = M_h + log2 Z_h from the per-block pairs
-  // (head-major, so a head's pairs are contiguous): 256/P lanes per head, 16
-  // pairs in flight per lane, then a butterfly over the head's lanes of the
-  // wave and, for heads wider than a wave, a combine of the per-wave results.
-  // Pairs of blocks past the sequence (never written by this call) are
-  // loaded with the rest and masked once the length is known.
-  float2 pv[16];
-  const float2* pp =
-      reinterpret_cast<const float2*>(a.part) + ((size_t)b * H_r + h0 + min(hh, per - 1)) * a.n_blk;
-#pragma unroll
-  for (int u = 0; u < 16; ++u) pv[u] = pp[min(j + LPH * u, a.n_blk - 1)];
+  HeadNorm nrm;
+  head_norm_load(nrm, a.part, b, H_r, h0, per, a.n_blk);
 
   const int L_b = clampi(L_raw, 0, a.L_max);
   if (t0 >= L_b) {  // uniform: the block lies past the sequence
     for (int t = t0 + tid; t < t1; t += 256) out[t] = -INFINITY;
     return;
   }
-  const int nb = (L_b + a.tpb - 1) / a.tpb;
-  float m = -INFINITY, s = 0.f;
-  if (hh < per) {
-#pragma unroll
-    for (int u = 0; u < 16; ++u)
-      if (j + LPH * u < nb) ms_combine(m, s, pv[u].x, pv[u].y);
-    const float2* p = pp;
-    for (int i0 = j + LPH * 16; i0 < nb; i0 += LPH * 16) {  // long rows: more pairs per lane
-      float2 v[16];
-#pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const int i = i0 + LPH * u;
-        v[u] = i < nb ? p[i] : make_float2(-INFINITY, 0.f);
-      }
-#pragma unroll
-      for (int u = 0; u < 16; ++u) ms_combine(m, s, v[u].x, v[u].y);
-    }
-  }
-  const int width = LPH < 64 ? LPH : 64;
-  for (int off = 1; off < width; off <<= 1) {
-    const float m2 = __shfl_xor(m, off);
-    const float s2 = __shfl_xor(s, off);
-    ms_combine(m, s, m2, s2);
-  }
-  if (LPH <= 64) {
-    if (j == 0 && hh < per) c_h[hh] = m + log2f(s);
-  } else {
-    if ((tid & 63) == 0) wred[tid >> 6] = make_float2(m, s);
-    __syncthreads();
-    if (tid < per) {
-      const int wpw = LPH / 64;  // waves per head
-      float mm = -INFINITY, ss = 0.f;
-      for (int w = tid * wpw; w < (tid + 1) * wpw; ++w) ms_combine(mm, ss, wred[w].x, wred[w].y);
-      c_h[tid] = mm + log2f(ss);
-    }
-  }
-  __syncthreads();
+  head_norm_finish(nrm, (L_b + a.tpb - 1) / a.tpb, c_h, wred);
 
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -266,7 +218,7 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
 }
 
 template <int LPH>
-void launch_logits(dim3 g, int tpb, bool wide, const LogitsArgs& a, hipStream_t s) {
+void logits_dispatch(dim3 g, int tpb, bool wide, const LogitsArgs& a, hipStream_t s) {
   if (tpb == 256) {
     if (wide) logits_kernel<LPH, kUnrollWide, 256><<<g, 256, 0, s>>>(a);
     else logits_kernel<LPH, kUnrollNarrow, 256><<<g, 256, 0, s>>>(a);
@@ -279,23 +231,29 @@ void launch_logits(dim3 g, int tpb, bool wide, const LogitsArgs& a, hipStream_t 
 
 }  // namespace
 
-hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
-                        const int32_t* seq_lens, float* scores, void* ws,
-                        hipStream_t s) {
+hipError_t launch_logits(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
+                         const int32_t* seq_lens, void* ws, bool zero_hist, hipStream_t s) {
   const int n_blk = score_blocks(d);
-  float* logits = static_cast<float*>(ws);
-  float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + score_logits_bytes(d));
-  int32_t* hist = score_ws_hist(d, ws);
-  LogitsArgs la{q_r, k_r, seq_lens, logits, part, hist, d.kr_stride_b,
+  LogitsArgs la{q_r, k_r, seq_lens, score_ws_logits(ws), score_ws_part(d, ws),
+                zero_hist ? score_ws_hist(d, ws) : nullptr, d.kr_stride_b,
                 d.L_max, d.H_r, n_blk, d.n_sets, d.scale_r * kLog2e};
   const int tpb = score_tokens_per_block(d);
   const dim3 g1(n_blk, d.B);
   const bool wide = (int64_t)n_blk * d.B >= 2 * (int64_t)device_cu_count();
   if (d.d_r == 64)
-    launch_logits<8>(g1, tpb, wide, la, s);
+    logits_dispatch<8>(g1, tpb, wide, la, s);
   else
-    launch_logits<16>(g1, tpb, wide, la, s);
-  SoftArgs sa{logits, part, seq_lens, scores, hist, d.L_max, d.H_r, n_blk, d.n_sets, tpb};
+    logits_dispatch<16>(g1, tpb, wide, la, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_score(const Dims& d, const uint16_t* q_r, const uint16_t* k_r,
+                        const int32_t* seq_lens, float* scores, void* ws,
+                        hipStream_t s) {
+  hipError_t e = launch_logits(d, q_r, k_r, seq_lens, ws, true, s);
+  if (e != hipSuccess) return e;
+  SoftArgs sa{score_ws_logits(ws), score_ws_part(d, ws), seq_lens, scores, score_ws_hist(d, ws),
+              d.L_max, d.H_r, score_blocks(d), d.n_sets, score_tokens_per_block(d)};
   const dim3 g2((d.L_max + T2 - 1) / T2, d.B * d.n_sets);
   softmax_headsum_kernel<<<g2, 256, 0, s>>>(sa);
   return hipGetLastError();

@@ -348,7 +348,6 @@ spec_status run_step(const spec::Dims& d, const uint16_t* q_r, const uint16_t* k
   char* p = static_cast<char*>(ws);
   float* scores = reinterpret_cast<float*>(p);
   p += spec::align_up(sizeof(float) * (size_t)d.B * d.n_sets * d.L_max);
-  if (scores_out) scores = scores_out;
   void* ws_score = p;
   p += spec::score_ws_bytes(d);
   void* ws_topk = p;
@@ -357,12 +356,8 @@ spec_status run_step(const spec::Dims& d, const uint16_t* q_r, const uint16_t* k
   p += spec::attn_ws_bytes(d);
   void* ws_delta = p;
 
-  hipError_t e = spec::launch_score(d, q_r, k_r, seq_lens, scores, ws_score, s);
-  if (e != hipSuccess) return hip_status(e);
-  // The score kernels already built the selection histogram.
-  e = spec::launch_topk_select(d, scores, seq_lens, ks, spec::score_ws_hist(d, ws_score),
-                               static_cast<char*>(ws_topk) + spec::topk_hist_bytes(d), idx_out,
-                               counts_out, s);
+  hipError_t e = spec::launch_score_select(d, q_r, k_r, seq_lens, ks, scores_out, scores,
+                                           idx_out, counts_out, ws_score, ws_topk, s);
   if (e != hipSuccess) return hip_status(e);
   if (el) {
     e = spec::launch_delta(d, idx_out, counts_out, k_cache, v_cache, el->slot_tok, el->kbuf,
@@ -608,7 +603,6 @@ spec_status spec_step_offload(const spec_dims* dm, const uint16_t* q_r, const ui
   char* p = static_cast<char*>(ws);
   float* scores = reinterpret_cast<float*>(p);
   p += spec::align_up(sizeof(float) * (size_t)d.B * d.n_sets * d.L_max);
-  if (scores_out) scores = scores_out;
   void* ws_score = p;
   p += spec::score_ws_bytes(d);
   void* ws_topk = p;
@@ -617,11 +611,8 @@ spec_status spec_step_offload(const spec_dims* dm, const uint16_t* q_r, const ui
   p += attn_ws_any_layers(d);
   void* ws_delta = p;
 
-  hipError_t e = spec::launch_score(d, q_r, k_r, seq_lens, scores, ws_score, s);
-  if (e != hipSuccess) return hip_status(e);
-  e = spec::launch_topk_select(d, scores, seq_lens, ks, spec::score_ws_hist(d, ws_score),
-                               static_cast<char*>(ws_topk) + spec::topk_hist_bytes(d), idx_out,
-                               counts_out, s);
+  hipError_t e = spec::launch_score_select(d, q_r, k_r, seq_lens, ks, scores_out, scores,
+                                           idx_out, counts_out, ws_score, ws_topk, s);
   if (e != hipSuccess) return hip_status(e);
   e = spec::launch_delta_plan(d_off, idx_out, counts_out, el->slot_tok, el->n_changed, ws_delta,
                               s);

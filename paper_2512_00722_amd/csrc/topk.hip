@@ -27,6 +27,7 @@
 // Both paths write the indices ascending, so no sort is needed.
 #include "device_common.h"
 #include "internal.h"
+#include "select_common.h"
 
 namespace spec {
 namespace {
@@ -38,93 +39,6 @@ constexpr int kGtCap = 8192;
 constexpr int kCandCap = 12288;
 constexpr int kTile = kTopkTile;  // tokens per classify workgroup
 constexpr int kMaxTiles = 1024;   // fast path: at most one tile per select thread
-
-// Exclusive scan of two ints over a workgroup of NT threads; returns the
-// totals too.  Must be called by all threads.
-template <int NT>
-__device__ __forceinline__ void block_scan2(int a, int b, int& ea, int& eb, int& ta, int& tb,
-                                            int* sh /* [2*NT/64] */) {
-  constexpr int NW = NT / 64;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  int ia = a, ib = b;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int na = __shfl_up(ia, off);
-    const int nb = __shfl_up(ib, off);
-    if (lane >= off) {
-      ia += na;
-      ib += nb;
-    }
-  }
-  if (lane == 63) {
-    sh[wave] = ia;
-    sh[NW + wave] = ib;
-  }
-  __syncthreads();
-  if (wave == 0) {
-    int wa = lane < NW ? sh[lane] : 0;
-    int wb = lane < NW ? sh[NW + lane] : 0;
-#pragma unroll
-    for (int off = 1; off < NW; off <<= 1) {
-      const int na = __shfl_up(wa, off);
-      const int nb = __shfl_up(wb, off);
-      if (lane >= off) {
-        wa += na;
-        wb += nb;
-      }
-    }
-    if (lane < NW) {
-      sh[lane] = wa;  // inclusive prefix over waves
-      sh[NW + lane] = wb;
-    }
-  }
-  __syncthreads();
-  const int pa = wave > 0 ? sh[wave - 1] : 0;
-  const int pb = wave > 0 ? sh[NW + wave - 1] : 0;
-  ea = pa + ia - a;
-  eb = pb + ib - b;
-  ta = sh[NW - 1];
-  tb = sh[2 * NW - 1];
-  __syncthreads();  // sh is reused by the next call
-}
-
-// Among `nbins` descending bins held by the workgroup (thread i owns bins
-// nbins-1-i*bpt .. with bpt = max(1, nbins/NT)), find the bin where the
-// running count from the top first reaches `need`.  Writes the bin and the
-// count of keys in higher bins to sel[0], sel[1] and the bin's count to
-// sel[2].  All threads must call; the result is valid after the call.
-template <int NT>
-__device__ __forceinline__ void find_bin(const int* hist, int nbins, int need, int* sh,
-                                         int* sel) {
-  constexpr int kMaxBpt = kBins / NT;
-  const int tid = threadIdx.x;
-  const int bpt = nbins >= NT ? nbins / NT : 1;
-  const bool owns = tid * bpt < nbins;
-  int cnt[kMaxBpt];
-  int local = 0;
-#pragma unroll
-  for (int e = 0; e < kMaxBpt; ++e) {
-    cnt[e] = (owns && e < bpt) ? hist[nbins - 1 - (tid * bpt + e)] : 0;
-    local += cnt[e];
-  }
-  int before, d0, t0, t1;
-  block_scan2<NT>(local, 0, before, d0, t0, t1, sh);
-  if (owns) {
-#pragma unroll
-    for (int e = 0; e < kMaxBpt; ++e) {
-      if (e < bpt) {
-        if (before < need && need <= before + cnt[e]) {
-          sel[0] = nbins - 1 - (tid * bpt + e);
-          sel[1] = before;
-          sel[2] = cnt[e];
-        }
-        before += cnt[e];
-      }
-    }
-  }
-  __syncthreads();
-}
 
 // Key of row[t] for t < L, else 0 (below every real key).  The load is
 // unconditional, from an index clamped into [0, row_len): a conditional load
@@ -614,6 +528,9 @@ hipError_t launch_topk_select(const Dims& d, const float* scores, const int32_t*
 hipError_t launch_topk(const Dims& d, const float* scores, const int32_t* seq_lens,
                        const int32_t* ks, int32_t* idx, int32_t* counts, void* ws,
                        hipStream_t s) {
+  if (row_select_fits(d, 1))  // short rows: one workgroup per row, keys in LDS
+    return launch_row_select(d, nullptr, const_cast<float*>(scores), seq_lens, ks, idx, counts,
+                             s);
   int32_t* hist = static_cast<int32_t*>(ws);
   const int n = d.B * d.n_sets * kBins;
   zero_kernel<<<(n + 255) / 256, 256, 0, s>>>(hist, n);

@@ -74,8 +74,13 @@ CASES = [
 
 @pytest.mark.parametrize("kw", CASES, ids=[str(i) for i in range(len(CASES))])
 @pytest.mark.parametrize("head_level", [False, True], ids=["sets1", "setsHkv"])
-def test_guard_bands_retrieval_and_attention(dev, kw, head_level):
-    announce(f"guard bands {kw} head_level={head_level}")
+@pytest.mark.parametrize("path", ["auto", "tiles"])
+def test_guard_bands_retrieval_and_attention(dev, kw, head_level, path, monkeypatch):
+    """path "tiles" forces the tiled selection where short rows would take
+    the one-workgroup-per-row kernel."""
+    if path == "tiles":
+        monkeypatch.setenv("SPEC_TOPK_PATH", "tiles")
+    announce(f"guard bands {kw} head_level={head_level} path={path}")
     w = small_workload(**kw)
     x = generate(w, seed=3, device=dev)
     # out-of-range device lengths and budgets, clamped by the kernels

@@ -122,11 +122,16 @@ TOPK_CASES = [
 
 
 @pytest.mark.parametrize("case", TOPK_CASES, ids=[f"{c[0]}-{c[2]}-{c[3]}" for c in TOPK_CASES])
-def test_topk_exact(dev, case):
+@pytest.mark.parametrize("path", ["auto", "tiles"])
+def test_topk_exact(dev, case, path, monkeypatch):
     """Same fp32 keys on both sides: the index sets must match bit-exactly,
-    including the -1 padding and the counts."""
+    including the -1 padding and the counts.  Rows of up to 8192 tokens take
+    the one-workgroup-per-row kernel unless path "tiles" forces the tiled
+    kernels."""
     kind, B, L_max, k_max, lens, ks = case
-    announce(f"topk {case[:4]}")
+    if path == "tiles":
+        monkeypatch.setenv("SPEC_TOPK_PATH", "tiles")
+    announce(f"topk {case[:4]} path={path}")
     g = torch.Generator().manual_seed(B * L_max + k_max)
     sc = _topk_rows(kind, B, L_max, g).float()
     seq = torch.tensor(lens, dtype=torch.int32)
@@ -342,6 +347,44 @@ def test_step_vs_oracle(dev, kw):
         for layer in range(w.n_layers):
             want, _ = oracle.sparse_gqa_attention(qn[layer, b], Kn[layer, b], Vn[layer, b], got)
             assert np.abs(out[layer, b] - want).max() <= TOL_ATTN
+
+
+ROW_CASES = STEP_CASES + [
+    # the longest rows the row kernel takes: 8 heads x 4096 tokens, and
+    # (head-level sets, one head per row) 8192 tokens; many short rows
+    dict(B=2, L=4096, H_r=8, d_r=64, n_layers=1, H_q=32, H_kv=8, k=1000, heavy_frac=0.02,
+         ragged_min=4000),
+    dict(B=2, L=8192, H_r=8, d_r=64, n_layers=1, H_q=32, H_kv=8, k=2000, heavy_frac=0.02,
+         ragged_min=8000),
+    dict(B=50, L=300, H_r=8, d_r=64, n_layers=1, H_q=32, H_kv=8, k=64, ragged_min=1,
+         heavy_frac=0.05),
+]
+
+
+@pytest.mark.parametrize("kw", ROW_CASES, ids=[str(i) for i in range(len(ROW_CASES))])
+@pytest.mark.parametrize("head_level", [False, True], ids=["sets1", "setsHkv"])
+def test_row_select_equals_tiles(dev, kw, head_level, monkeypatch):
+    """Short rows: the one-workgroup-per-row kernel (normalisers merged in
+    the softmax kernel's order, the same sum over heads) gives the tiled
+    path's scores, selections and attention bit for bit, with and without
+    the scores kept."""
+    announce(f"row vs tiles {kw} head_level={head_level}")
+    w = small_workload(**kw)
+    x = generate(w, seed=kw["B"] * 7 + kw["L"], device=dev)
+    args = [x[n] for n in ("q_r", "K_r", "seq_lens", "ks", "q", "K", "V")]
+    runs = {}
+    for path in ("auto", "tiles"):
+        if path == "tiles":
+            monkeypatch.setenv("SPEC_TOPK_PATH", "tiles")
+        runs[path] = spec.step(*args, k_max=w.k, with_scores=True, with_lse=True,
+                               head_level=head_level)
+        runs[path + "-noscores"] = spec.step(*args, k_max=w.k, with_lse=True,
+                                             head_level=head_level)
+    monkeypatch.delenv("SPEC_TOPK_PATH", raising=False)
+    for key in ("scores", "idx", "counts", "out", "lse"):
+        assert torch.equal(runs["auto"][key], runs["tiles"][key]), key
+    for key in ("idx", "counts", "out", "lse"):
+        assert torch.equal(runs["auto-noscores"][key], runs["auto"][key]), key
 
 
 def test_step_deterministic(dev):
