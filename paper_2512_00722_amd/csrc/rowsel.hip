@@ -60,7 +60,7 @@ __global__ __launch_bounds__(kThreads) void row_select_kernel(RowArgs a) {
   const int per = kFromLogits ? a.H_r / a.n_sets : 0;  // heads of this row
   const int h0 = (srow - b * a.n_sets) * per;
   HeadNorm nrm;
-  if (kFromLogits) head_norm_load(nrm, a.part, b, a.H_r, h0, per, a.n_blk);
+  if (kFromLogits) head_norm_load<true>(nrm, a.part, b, a.H_r, h0, per, a.n_blk);
   for (int i = tid; i < kTopkBins; i += kThreads) s_hist[i] = 0;
   if (tid == 0) s_sel[0] = s_sel[1] = s_sel[2] = -1;
   const int L_b = clampi(L_raw, 0, a.L_max);

@@ -185,7 +185,7 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
     }
   }
   HeadNorm nrm;
-  head_norm_load(nrm, a.part, b, H_r, h0, per, a.n_blk);
+  head_norm_load<false>(nrm, a.part, b, H_r, h0, per, a.n_blk);
 
   const int L_b = clampi(L_raw, 0, a.L_max);
   if (t0 >= L_b) {  // uniform: the block lies past the sequence

@@ -22,7 +22,9 @@ struct HeadNorm {
 
 // Issues the pair loads; they depend on nothing but the row.  Pairs of
 // blocks past the sequence (not written by this call) are loaded with the
-// rest, clamped into the row, and masked by head_norm_finish.
+// rest, clamped into the row, and masked by head_norm_finish.  kWide: the
+// workgroup has more than 256 threads (the others load nothing).
+template <bool kWide>
 __device__ __forceinline__ void head_norm_load(HeadNorm& n, const float* part, int b, int H_r,
                                                int h0, int per, int n_blk) {
   const int P = per <= 1 ? 1 : per <= 2 ? 2 : per <= 4 ? 4 : per <= 8 ? 8 : 16;
@@ -32,10 +34,13 @@ __device__ __forceinline__ void head_norm_load(HeadNorm& n, const float* part, i
   n.j = (int)threadIdx.x - n.hh * n.lph;
   n.pp = reinterpret_cast<const float2*>(part) +
          ((size_t)b * H_r + h0 + min(n.hh, per - 1)) * n_blk;
+  if (kWide && threadIdx.x >= 256) {
 #pragma unroll
-  for (int u = 0; u < 16; ++u)
-    n.pv[u] = threadIdx.x < 256 ? n.pp[min(n.j + n.lph * u, n_blk - 1)]
-                                : make_float2(-INFINITY, 0.f);
+    for (int u = 0; u < 16; ++u) n.pv[u] = make_float2(-INFINITY, 0.f);
+    return;
+  }
+#pragma unroll
+  for (int u = 0; u < 16; ++u) n.pv[u] = n.pp[min(n.j + n.lph * u, n_blk - 1)];
 }
 
 // Merges the pairs of the sequence's nb blocks into c_h[0 .. per) (LDS).
