@@ -525,17 +525,29 @@ def run_elastic(args, spec, w, x, e, algorithmic_bytes):
     timed_bytes = sum(step_bytes[i % S] for i in range(args.steps))
     k_total = sum(min(k, int(L)) for k, L in zip(ks, e["seq_lens"][0].cpu().tolist()))
 
-    # Attention over the compact slot buffers (the dominant kernel), timed
-    # back to back between HIP events on the launch stream.
+    # The dominant kernel, timed back to back between HIP events on the
+    # launch stream: the step's attention over the slots.  On a steady
+    # update (a fifth of the rows new) the step copies the new rows first
+    # and the attention only reads the slots, which the compact attention
+    # over the slot buffers reproduces.  With SPEC_ELASTIC_PATH=fused the
+    # attention loads every update's rows itself: then the kernel timed is
+    # that attention with the last update's slot sources (rerunning it
+    # rewrites the same rows).
     counts = outputs["counts"]
     attn_out = torch.empty_like(outputs["out"])
     q_last = e["q"][S - 1]
+    copy_path = os.environ.get("SPEC_ELASTIC_PATH") != "fused"
     dims_a = spec.Dims.make(B=w.B, L_cap=w.k, L_max=w.k, k_max=w.k, n_layers=w.n_layers,
                             H_q=w.H_q, H_kv=w.H_kv, d=w.d)
-    ws_attn = torch.zeros(max(16, spec.workspace_size(dims_a, spec.OP_ATTN)), dtype=torch.uint8,
-                          device=dev)
-    fn = lambda: spec.sparse_decode_attn(q_last, st.kbuf, st.vbuf, counts, idx=None,
-                                         out=attn_out, with_lse=False, ws=ws_attn)
+    ws_attn = torch.zeros(max(16, spec.workspace_size(dims_a, spec.OP_ATTN),
+                              spec.workspace_size(_dims_of(spec, w, x), spec.OP_ATTN)),
+                          dtype=torch.uint8, device=dev)
+    if copy_path:
+        fn = lambda: spec.sparse_decode_attn(q_last, st.kbuf, st.vbuf, counts, idx=None,
+                                             out=attn_out, with_lse=False, ws=ws_attn)
+    else:
+        fn = lambda: spec.sparse_decode_attn_elastic(q_last, x["K"], x["V"], st, counts,
+                                                     out=attn_out, with_lse=False, ws=ws_attn)
     fn()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -547,6 +559,8 @@ def run_elastic(args, spec, w, x, e, algorithmic_bytes):
     attn_us = e0.elapsed_time(e1) * 1e3 / args.attn_iters
     kb = sum(int(c) for c in counts.cpu().tolist())
     a_bytes = w.n_layers * (kb * w.H_kv * w.d * 2 * 2 + w.B * w.H_q * w.d * 2 + w.B * w.H_q * w.d * 4)
+    if not copy_path:  # plus the rows written into their slots
+        a_bytes += w.n_layers * int(st.n_changed.sum()) * w.H_kv * w.d * 2 * 2
     achieved = a_bytes / (attn_us * 1e-6) / 1e9
     if args.copy_calibration:
         copy_calibration(dev)
@@ -573,7 +587,9 @@ def run_elastic(args, spec, w, x, e, algorithmic_bytes):
             "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBPS, 4),
             "traffic": stored_traffic(w.name),
-            "kernel": "sparse GQA decode attention over the compact slot buffers",
+            "kernel": ("sparse GQA decode attention over the slot buffers (attn_split_kernel)"
+                       if copy_path else "sparse GQA decode attention over the slots, loading "
+                       "the update's rows (attn_split_kernel)"),
             "bytes_per_launch": a_bytes,
             "avg_launch_us": round(attn_us, 2),
         },

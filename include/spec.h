@@ -128,12 +128,15 @@ typedef struct spec_dims {
 /* Device-resident elastic-loading state (host struct of device pointers).
  *   slot_tok  [B][k_max] int32: token held by each slot, -1 = empty (S_last);
  *   kbuf,vbuf [n_layers][B][k_max][H_kv][d] bf16: the rows held by the slots;
- *   n_changed [B] int32 (output): rows loaded by the last update.           */
+ *   n_changed [B] int32 (output): rows loaded by the last update;
+ *   slot_src  [B][k_max] int32 (output): per slot, the token the last update
+ *             loaded into it, or -1 (kept or left empty).                   */
 typedef struct spec_elastic {
   int32_t* slot_tok;
   uint16_t* kbuf;
   uint16_t* vbuf;
   int32_t* n_changed;
+  int32_t* slot_src;
 } spec_elastic;
 
 /* Retrieval scoring (Sec. 4.3 "Implementation Details"; Eq. 1 per head;
@@ -195,6 +198,22 @@ SPEC_API spec_status spec_sparse_decode_attn(const spec_dims* dm, const uint16_t
                                     float* out, float* lse, void* ws,
                                     size_t ws_bytes, spec_stream stream);
 
+/* Sparse decode attention over the slots of an elastic state whose last
+ * update has not been copied yet (Sec. 5.4's loads fused into Eq. 1's
+ * reads).  As compact-mode spec_sparse_decode_attn over slots
+ * [0, counts[b]) of el->kbuf/vbuf, except that a slot with
+ * el->slot_src[b,s] = t >= 0 is read from the caches at token t (clamped into
+ * [0, L_cap)), and that row, K and V of every layer, is written into the slot
+ * on the way, bit for bit.  After the call the slot buffers hold what the
+ * update's copy would have written; calling it again with the same slot_src
+ * rewrites the same rows (same outputs).  el->slot_tok and el->n_changed are
+ * not used.  Needs workspace spec_workspace_size(SPEC_OP_ATTN).             */
+SPEC_API spec_status spec_sparse_decode_attn_elastic(const spec_dims* dm,
+                                    const uint16_t* q, const uint16_t* k_cache,
+                                    const uint16_t* v_cache, const spec_elastic* el,
+                                    const int32_t* counts, float* out, float* lse,
+                                    void* ws, size_t ws_bytes, spec_stream stream);
+
 /* Elastic loading on the device (Sec. 5.4).  S_now = idx_now[b, 0..c) with
  * c = min(counts[b], k_max): distinct tokens in ascending order, as spec_topk
  * writes them.  S_last = the tokens held in el->slot_tok[b, 0..k_max).  Slots
@@ -205,18 +224,20 @@ SPEC_API spec_status spec_sparse_decode_attn(const spec_dims* dm, const uint16_t
  * (the paper's |S_last| = |S_now|) slots [0, c) hold exactly S_now afterwards
  * and the rest are -1; if c shrank so that a kept token sits at a slot >= c,
  * the sequence is reloaded in full to restore that layout.
- * el->n_changed[b] = number of rows loaded.  Start from slot_tok = -1
- * everywhere for a full load.  Needs workspace
- * spec_workspace_size(SPEC_OP_DELTA).                                       */
+ * el->n_changed[b] = number of rows loaded; el->slot_src[b,s] = the token
+ * loaded into slot s, or -1.  Start from slot_tok = -1 everywhere for a full
+ * load.  Needs workspace spec_workspace_size(SPEC_OP_DELTA).               */
 SPEC_API spec_status spec_delta_gather(const spec_dims* dm, const int32_t* idx_now,
                               const int32_t* counts, const uint16_t* k_cache,
                               const uint16_t* v_cache, const spec_elastic* el,
                               void* ws, size_t ws_bytes, spec_stream stream);
 
-/* One fused decode step: spec_score -> spec_topk -> [spec_delta_gather when
- * el != NULL] -> spec_sparse_decode_attn (indexed over the caches, or compact
- * over el->kbuf/vbuf when el != NULL), all enqueued on `stream` with no host
- * synchronisation.  idx_out [B][n_sets][k_max] and counts_out [B] receive
+/* One fused decode step: spec_score -> spec_topk -> spec_sparse_decode_attn
+ * indexed over the caches; or, when el != NULL, spec_score -> spec_topk ->
+ * the elastic update's slot plan -> spec_sparse_decode_attn_elastic (the
+ * update's rows are read from the caches once, by the attention, which also
+ * writes them into their slots: the state afterwards is spec_delta_gather's).
+ * All enqueued on `stream` with no host synchronisation.  idx_out [B][n_sets][k_max] and counts_out [B] receive
  * the selection; out/lse as for spec_sparse_decode_attn (lse nullable);
  * scores_out [B][n_sets][L_max] (nullable) receives the retrieval scores.
  * Elastic loading needs n_sets = 1.  Needs workspace

@@ -38,7 +38,7 @@ STATUS = {0: "SPEC_OK", 1: "SPEC_ERR_INVALID", 2: "SPEC_ERR_UNSUPPORTED",
           3: "SPEC_ERR_WORKSPACE", 4: "SPEC_ERR_HIP", 5: "SPEC_ERR_TOO_LARGE"}
 
 EXPORTED_SYMBOLS = ["spec_score", "spec_topk", "spec_gather", "spec_sparse_decode_attn",
-                    "spec_delta_gather", "spec_step", "spec_step_noalloc",
+                    "spec_sparse_decode_attn_elastic", "spec_delta_gather", "spec_step", "spec_step_noalloc",
                     "spec_step_noalloc_max_bytes", "spec_offload_load", "spec_step_offload",
                     "spec_retrieval_qk",
                     "spec_mla_sparse_decode_attn", "spec_mla_workspace_size", "spec_workspace_size",
@@ -80,7 +80,8 @@ class Dims(ctypes.Structure):
 class Elastic(ctypes.Structure):
     """Mirror of `spec_elastic`."""
     _fields_ = [("slot_tok", ctypes.c_void_p), ("kbuf", ctypes.c_void_p),
-                ("vbuf", ctypes.c_void_p), ("n_changed", ctypes.c_void_p)]
+                ("vbuf", ctypes.c_void_p), ("n_changed", ctypes.c_void_p),
+                ("slot_src", ctypes.c_void_p)]
 
 
 class HostKv(ctypes.Structure):
@@ -136,6 +137,7 @@ def load_library(path: Optional[str] = None):
         "spec_topk": [D, P, P, P, P, P, P, S, P],
         "spec_gather": [D, P, P, P, P, P, P, P],
         "spec_sparse_decode_attn": [D, P, P, P, P, P, P, P, P, S, P],
+        "spec_sparse_decode_attn_elastic": [D, P, P, P, E, P, P, P, P, S, P],
         "spec_delta_gather": [D, P, P, P, P, E, P, S, P],
         "spec_step": [D, P, P, P, P, P, P, P, P, P, P, P, P, E, P, S, P],
         "spec_step_noalloc": [D, P, P, P, P, P, P, P, P, P, P, P, P, E, P],
@@ -393,13 +395,48 @@ class ElasticState:
         self.kbuf = torch.zeros((n_layers, B, k_max, H_kv, d), dtype=torch.bfloat16, device=device)
         self.vbuf = torch.zeros_like(self.kbuf)
         self.n_changed = torch.zeros((B,), dtype=torch.int32, device=device)
+        # per slot, the token the last update loaded into it (-1: kept or empty)
+        self.slot_src = torch.full((B, k_max), -1, dtype=torch.int32, device=device)
 
     def reset(self):
         self.slot_tok.fill_(-1)
 
     def c_struct(self) -> Elastic:
         return Elastic(self.slot_tok.data_ptr(), self.kbuf.data_ptr(), self.vbuf.data_ptr(),
-                       self.n_changed.data_ptr())
+                       self.n_changed.data_ptr(), self.slot_src.data_ptr())
+
+
+def sparse_decode_attn_elastic(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
+                               state: ElasticState, counts: torch.Tensor, scale: float = 0.0,
+                               out: Optional[torch.Tensor] = None,
+                               lse: Optional[torch.Tensor] = None, with_lse: bool = True,
+                               ws: Optional[torch.Tensor] = None):
+    """Attention over the slots of `state` after an update whose rows have
+    not been copied: slots with state.slot_src >= 0 are read from the caches
+    K/V [n_layers, B, L_cap, H_kv, d] at that token and written into the slot
+    on the way; the others are read from the slot.  Returns (out, lse)."""
+    lib = load_library()
+    _need(q, "q", torch.bfloat16, 4)
+    _check_cache(K, V)
+    n_layers, B, L_cap, H_kv, d = K.shape
+    if q.shape[0] != n_layers or q.shape[1] != B or q.shape[3] != d or not q.is_contiguous():
+        raise ValueError("q must be contiguous [n_layers, B, H_q, d]")
+    _i32(counts, "counts", B)
+    k_max = state.slot_tok.shape[1]
+    if tuple(state.kbuf.shape) != (n_layers, B, k_max, H_kv, d):
+        raise ValueError("elastic state shape does not match")
+    dims = _dims_llm(q, K, k_max, scale)
+    ws, nws = _workspace(dims, OP_ATTN, q.device, ws)
+    if out is None:
+        out = torch.empty((n_layers, B, q.shape[2], d), dtype=torch.float32, device=q.device)
+    if lse is None and with_lse:
+        lse = torch.empty((n_layers, B, q.shape[2]), dtype=torch.float32, device=q.device)
+    el = state.c_struct()
+    _check(lib.spec_sparse_decode_attn_elastic(ctypes.byref(dims), _p(q), _p(K), _p(V),
+                                               ctypes.byref(el), _p(counts), _p(out), _p(lse),
+                                               _p(ws), nws, _stream(q)),
+           "spec_sparse_decode_attn_elastic")
+    return out, lse
 
 
 def delta_gather(idx_now: torch.Tensor, counts: torch.Tensor, K: torch.Tensor, V: torch.Tensor,

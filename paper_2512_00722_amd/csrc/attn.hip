@@ -88,18 +88,31 @@ __device__ __forceinline__ uint4 ldkv(const uint16_t* p) {
 //                   them.
 enum AttnMode { kDirect = 0, kGlobalPartials = 1 };
 
+// Where a unit's K/V rows come from:
+//  kKvIndexed: the cache, at the selected token indices (idx);
+//  kKvCompact: the compact slot buffers, slots 0 .. count-1;
+//  kKvElastic: the slot buffers, except the slots an elastic update has just
+//              assigned (src[b][slot] = token >= 0): those rows are read from
+//              the cache and written into their slot as they stream through
+//              (Sec. 5.4's loads fused into the attention's reads).
+enum KvMode { kKvIndexed = 0, kKvCompact = 1, kKvElastic = 2 };
+
 struct AttnArgs {
   const uint16_t* q;      // [n_layers][B][H_q][d]
-  const uint16_t* k;      // indexed: cache; compact: [n_layers][B][k_max][H_kv][d]
+  const uint16_t* k;      // indexed, elastic: cache; compact: [n_layers][B][k_max][H_kv][d]
   const uint16_t* v;
   const int32_t* idx;     // [B][k_max] (indexed mode)
+  uint16_t* kbuf;         // elastic: slot buffers [n_layers][B][k_max][H_kv][d]
+  uint16_t* vbuf;
+  const int32_t* src;     // elastic: [B][k_max] token loaded into the slot, or -1
+  const int32_t* fused;   // elastic: [B] or null; 0: the sequence's rows are all in the slots
   const int32_t* counts;  // [B]
   float* part_acc;        // [n_layers*B][n_split][H_q][d]
   float* part_ml;         // [n_layers*B][n_split][H_q][2]
   float* out;             // [n_layers*B][H_q][d]
   float* lse;             // [n_layers*B][H_q] or null
-  int64_t stride_layer;   // elements between layers (indexed mode)
-  int64_t stride_b;       // elements between sequences (indexed mode)
+  int64_t stride_layer;   // elements between layers of the cache (indexed, elastic)
+  int64_t stride_b;       // elements between sequences of the cache
   int B, H_q, H_kv, G, k_max, L_cap, n_split, split_tokens, n_items;
   int R;                  // column groups per KV head (1; G/16 for more than 16 query heads)
                           // G above: query heads per column group (at most 16)
@@ -191,9 +204,49 @@ __device__ __forceinline__ Unit decode_unit(const AttnArgs& a, int item) {
   return u;
 }
 
+// Elastic mode: the staged value of a row is the cache token to read (and
+// write into the slot), or -1 - slot for a row read from its slot.  Other
+// modes stage the token or slot index clamped into range.
+template <int KV>
+__device__ __forceinline__ int elastic_row(int v, int slot, int L_cap) {
+  if (KV != kKvElastic) return clampi(v, 0, L_cap - 1);
+  return v >= 0 ? min(v, L_cap - 1) : -1 - slot;
+}
+template <int KV>
+__device__ __forceinline__ const uint16_t* row_ptr(const uint16_t* base, const uint16_t* buf,
+                                                   int r, int64_t rs) {
+  if (KV != kKvElastic) return base + (int64_t)r * rs;
+  return r >= 0 ? base + (int64_t)r * rs : buf + (int64_t)(-1 - r) * rs;
+}
+
+// The rows of one chunk that came from the cache, written into their slots
+// (dst: the chunk's first slot, this KV head): the data registers as loaded,
+// so each slot receives the cache row bit for bit.  n: tokens of the unit
+// from this chunk on.
+__device__ __forceinline__ void store_k_rows(const int* rc, const uint4 (&kr)[kTiles][4],
+                                             uint16_t* dst, int64_t rs, int n, int kg, int r16) {
+#pragma unroll
+  for (int t = 0; t < kTiles; ++t) {
+    const int j = 16 * t + r16;
+    if (rc[j] >= 0 && j < n) {
+      uint16_t* p = dst + (int64_t)j * rs + 8 * kg;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) *reinterpret_cast<uint4*>(p + 32 * s) = kr[t][s];
+    }
+  }
+}
+__device__ __forceinline__ void store_v_rows(const int* rc, const uint4 (&vr)[kVRows],
+                                             uint16_t* dst, int64_t rs, int n, int kg, int r16) {
+#pragma unroll
+  for (int r = 0; r < kVRows; ++r) {
+    const int j = 4 * r + kg;
+    if (rc[j] >= 0 && j < n) *reinterpret_cast<uint4*>(dst + (int64_t)j * rs + 8 * r16) = vr[r];
+  }
+}
+
 // One unit from a cold start (a wavefront with a single unit): count, then
 // indices staged in LDS, then the first chunk.
-template <bool INDEXED>
+template <int KV>
 __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, const int lane,
                                              uint16_t* V, int* rows) {
   // A group of more than 16 query heads is covered by R column groups of
@@ -224,17 +277,16 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
   const int n_tok = min(a.split_tokens, count - j0);  // tokens of this work item
 
   const int64_t rs = (int64_t)a.H_kv * kD;  // elements per token row
-  const uint16_t* kb;
-  const uint16_t* vb;
-  if (INDEXED) {
-    const int64_t off = (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b + g * kD;
-    kb = a.k + off;
-    vb = a.v + off;
-  } else {
-    const int64_t off = (int64_t)lb * a.k_max * rs + g * kD;
-    kb = a.k + off;
-    vb = a.v + off;
-  }
+  // kb/vb: the rows a staged row value r >= 0 addresses (the cache, or the
+  // slot buffers in compact mode); kbf/vbf: elastic mode's slot buffers, for
+  // r < 0 (slot -1 - r).
+  const int64_t coff = (int64_t)layer * a.stride_layer + (int64_t)b * a.stride_b + g * kD;
+  const int64_t boff = (int64_t)lb * a.k_max * rs + g * kD;
+  const uint16_t* kb = a.k + (KV == kKvCompact ? boff : coff);
+  const uint16_t* vb = a.v + (KV == kKvCompact ? boff : coff);
+  uint16_t* kbf = a.kbuf + boff;
+  uint16_t* vbf = a.vbuf + boff;
+  const bool writer = KV == kKvElastic && gv % a.R == 0;  // one column group writes the slots
 
   const int r16 = lane & 15;  // head of this lane (MFMA column); token of a K tile row
   const int kg = lane >> 4;   // MFMA k-group; also the token phase of V loads
@@ -258,21 +310,24 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
     // one chunk of padding follows the end: the software pipeline always
     // prefetches the next chunk, and padding rows all read row 0 (cache hits).
     const int32_t* idx_b =
-        INDEXED ? a.idx + ((size_t)b * a.n_sets + (a.n_sets > 1 ? g : 0)) * a.k_max + j0
-                : nullptr;
+        KV == kKvIndexed ? a.idx + ((size_t)b * a.n_sets + (a.n_sets > 1 ? g : 0)) * a.k_max + j0
+        : KV == kKvElastic ? a.src + (size_t)b * a.k_max + j0
+                           : nullptr;
+    const bool fz = KV == kKvElastic && (a.fused == nullptr || a.fused[b] != 0);
     const int n_pad = (n_tok + kChunk - 1) / kChunk * kChunk + kChunk;
     constexpr int kColdRowLoads = (kMaxSplit + kChunk + 63) / 64;
     int rv[kColdRowLoads];
 #pragma unroll
     for (int m = 0; m < kColdRowLoads; ++m) {
       const int j = lane + 64 * m;
-      rv[m] = 0;
-      if (j < n_tok) rv[m] = INDEXED ? idx_b[j] : j0 + j;
+      rv[m] = KV == kKvElastic ? -1 : 0;  // padding: the unit's first slot, or row 0
+      if (j < n_tok && (KV != kKvElastic || fz)) rv[m] = KV == kKvCompact ? j0 + j : idx_b[j];
     }
 #pragma unroll
     for (int m = 0; m < kColdRowLoads; ++m) {
       const int j = lane + 64 * m;
-      if (j < n_pad) rows[j] = clampi(rv[m], 0, a.L_cap - 1);
+      if (j < n_pad)
+        rows[j] = elastic_row<KV>(rv[m], j < n_tok ? j0 + j : j0, a.L_cap);
     }
   }
 
@@ -285,7 +340,7 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
     const int* rc = rows + c;
 #pragma unroll
     for (int t = 0; t < kTiles; ++t) {
-      const uint16_t* p = kb + (int64_t)rc[16 * t + r16] * rs + 8 * kg;
+      const uint16_t* p = row_ptr<KV>(kb, kbf, rc[16 * t + r16], rs) + 8 * kg;
 #pragma unroll
       for (int s = 0; s < 4; ++s) kr[t][s] = ldkv(p + 32 * s);
     }
@@ -293,7 +348,8 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
   auto load_v = [&](int c, uint4 (&vr)[kVRows]) {
     const int* rc = rows + c;
 #pragma unroll
-    for (int r = 0; r < kVRows; ++r) vr[r] = ldkv(vb + (int64_t)rc[4 * r + kg] * rs + 8 * r16);
+    for (int r = 0; r < kVRows; ++r)
+      vr[r] = ldkv(row_ptr<KV>(vb, vbf, rc[4 * r + kg], rs) + 8 * r16);
   };
 
   float m_run = -INFINITY, l_run = 0.f;  // head r16
@@ -316,6 +372,7 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
 #pragma unroll
     for (int r = 0; r < kVRows; ++r)
       *reinterpret_cast<uint4*>(V + (4 * r + kg) * kVPitch + 8 * r16) = vraw[r];
+    if (writer) store_v_rows(rows + c, vraw, vbf + (int64_t)(j0 + c) * rs, rs, n_tok - c, kg, r16);
     load_v(c + kChunk, vraw);
     __builtin_amdgcn_sched_barrier(0);  // keep the refill here: issue order = retire order
 
@@ -329,6 +386,7 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
         sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kraw[t][s]),
                                                           qf[s], sacc[t], 0, 0, 0);
     }
+    if (writer) store_k_rows(rows + c, kraw, kbf + (int64_t)(j0 + c) * rs, rs, n_tok - c, kg, r16);
     load_k(c + kChunk, kraw);
     __builtin_amdgcn_sched_barrier(0);
 
@@ -426,7 +484,7 @@ constexpr size_t lds_reserve(bool pipe) {
 // PIPE: some wavefront has more than one unit, and units are pipelined
 // across their boundaries; otherwise each unit starts cold (the pipeline's
 // bookkeeping made one-unit launches ~1.5 us slower).
-template <bool INDEXED, bool PIPE>
+template <int KV, bool PIPE>
 __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(SPEC_ATTN_WPE)))
 void attn_split_kernel(AttnArgs a) {
   __shared__ __align__(16) uint16_t vlds[kWaves][kChunk * kVPitch];
@@ -460,7 +518,7 @@ void attn_split_kernel(AttnArgs a) {
     for (;;) {
       const int item = take();
       if (item < 0) return;  // uniform per wave: every wave ends here
-      process_item<INDEXED>(a, item, lane, vlds[wave], rows_lds[wave][0]);
+      process_item<KV>(a, item, lane, vlds[wave], rows_lds[wave][0]);
     }
   } else {
   uint16_t* V = vlds[wave];
@@ -468,29 +526,37 @@ void attn_split_kernel(AttnArgs a) {
   const int kg = lane >> 4;   // MFMA k-group; also the token phase of V loads
   const int64_t rs = (int64_t)a.H_kv * kD;  // elements per token row
 
+  // The rows a staged value r >= 0 addresses (the cache; the slot buffers in
+  // compact mode), and elastic mode's slot buffers (r < 0: slot -1 - r).
   auto kv_base = [&](const Unit& u, const uint16_t* p) -> const uint16_t* {
-    if (INDEXED)
+    if (KV != kKvCompact)
       return p + (int64_t)(u.lb / a.B) * a.stride_layer + (int64_t)u.b * a.stride_b + u.g * kD;
     return p + (int64_t)u.lb * a.k_max * rs + u.g * kD;
+  };
+  auto buf_base = [&](const Unit& u, uint16_t* p) -> uint16_t* {
+    return KV == kKvElastic ? p + (int64_t)u.lb * a.k_max * rs + u.g * kD : nullptr;
   };
 
   // The loads that start a unit, all independent of each other: its count,
   // its row indices (all of a split's, clamped into the index row: the count
   // only masks them later) and its queries.  B operand of S^T = K Q^T: Q^T
   // column r16 = query head gv G + r16 (zero if >= G), dims 32s + 8kg .. +8.
-  int cnt_raw;
+  int cnt_raw, fz_raw = 1;
   int rv[kRowLoads];
   uint4 qraw[4];
   auto fetch = [&](const Unit& u) {
     cnt_raw = a.counts[u.b];
+    if (KV == kKvElastic && a.fused) fz_raw = a.fused[u.b];
     const int32_t* idx_b =
-        INDEXED ? a.idx + ((size_t)u.b * a.n_sets + (a.n_sets > 1 ? u.g : 0)) * a.k_max : nullptr;
+        KV == kKvIndexed ? a.idx + ((size_t)u.b * a.n_sets + (a.n_sets > 1 ? u.g : 0)) * a.k_max
+        : KV == kKvElastic ? a.src + (size_t)u.b * a.k_max
+                           : nullptr;
     // loads past the split re-read its last index (one cache line)
     const int jmax = min(u.j0 + a.split_tokens, a.k_max) - 1;
 #pragma unroll
     for (int m = 0; m < kRowLoads; ++m) {
       const int j = u.j0 + lane + 64 * m;
-      rv[m] = INDEXED ? idx_b[min(j, jmax)] : j;
+      rv[m] = KV == kKvCompact ? j : idx_b[min(j, jmax)];
     }
     const uint16_t* qp =
         a.q + ((size_t)u.lb * a.H_q + u.gv * a.G + (r16 < a.G ? r16 : 0)) * kD + 8 * kg;
@@ -498,32 +564,37 @@ void attn_split_kernel(AttnArgs a) {
     for (int s = 0; s < 4; ++s) qraw[s] = ldg16(qp + 32 * s);
   };
   // Rows of a unit's tokens into LDS: tokens past the unit, and the padding
-  // chunk, read row 0 (cache hits).  Sets u.n_tok.
+  // chunk, read row 0 (elastic mode: the unit's first slot; cache hits).
+  // Sets u.n_tok.
   auto stage = [&](Unit& u, int* rows) {
     const int count = __builtin_amdgcn_readfirstlane(clampi(cnt_raw, 0, a.k_max));
     u.n_tok = min(a.split_tokens, count - u.j0);
+    const int pad = KV == kKvElastic ? -1 - u.j0 : 0;
+    const bool fz = __builtin_amdgcn_readfirstlane(fz_raw) != 0;  // elastic: rows may come from the caches
 #pragma unroll
     for (int m = 0; m < kRowLoads; ++m) {
       const int j = lane + 64 * m;
-      rows[j] = j < u.n_tok ? clampi(rv[m], 0, a.L_cap - 1) : 0;
+      rows[j] = j < u.n_tok ? elastic_row<KV>(fz ? rv[m] : -1, u.j0 + j, a.L_cap) : pad;
     }
-    if (lane < kChunk) rows[kMaxSplit + lane] = 0;
+    if (lane < kChunk) rows[kMaxSplit + lane] = pad;
   };
 
   // K rows in the MFMA A-operand layout: tile t, token 16t + r16, dims
   // 32s + 8kg .. +8.  V rows: load r brings token 4r + kg, dims 8 r16 .. +8,
   // i.e. four whole 256-byte rows per instruction.
-  auto load_k = [&](const int* rc, const uint16_t* kb, uint4 (&kr)[kTiles][4]) {
+  auto load_k = [&](const int* rc, const uint16_t* kb, const uint16_t* kbf,
+                    uint4 (&kr)[kTiles][4]) {
 #pragma unroll
     for (int t = 0; t < kTiles; ++t) {
-      const uint16_t* p = kb + (int64_t)rc[16 * t + r16] * rs + 8 * kg;
+      const uint16_t* p = row_ptr<KV>(kb, kbf, rc[16 * t + r16], rs) + 8 * kg;
 #pragma unroll
       for (int s = 0; s < 4; ++s) kr[t][s] = ldkv(p + 32 * s);
     }
   };
-  auto load_v = [&](const int* rc, const uint16_t* vb, uint4 (&vr)[kVRows]) {
+  auto load_v = [&](const int* rc, const uint16_t* vb, const uint16_t* vbf, uint4 (&vr)[kVRows]) {
 #pragma unroll
-    for (int r = 0; r < kVRows; ++r) vr[r] = ldkv(vb + (int64_t)rc[4 * r + kg] * rs + 8 * r16);
+    for (int r = 0; r < kVRows; ++r)
+      vr[r] = ldkv(row_ptr<KV>(vb, vbf, rc[4 * r + kg], rs) + 8 * r16);
   };
 
   int buf = 0;
@@ -537,14 +608,16 @@ void attn_split_kernel(AttnArgs a) {
   uint4 kraw[kTiles][4], vraw[kVRows];
   const uint16_t* kb = kv_base(cur, a.k);
   const uint16_t* vb = kv_base(cur, a.v);
+  uint16_t* kbf = buf_base(cur, a.kbuf);
+  uint16_t* vbf = buf_base(cur, a.vbuf);
   bf16x8 qf[4];
 #pragma unroll
   for (int s = 0; s < 4; ++s)
     qf[s] = __builtin_bit_cast(bf16x8, r16 < a.G ? qraw[s] : make_uint4(0, 0, 0, 0));
   if (cur.n_tok > 0) {  // uniform per wavefront
-    load_v(rows_lds[wave][buf], vb, vraw);
+    load_v(rows_lds[wave][buf], vb, vbf, vraw);
     __builtin_amdgcn_sched_barrier(0);
-    load_k(rows_lds[wave][buf], kb, kraw);
+    load_k(rows_lds[wave][buf], kb, kbf, kraw);
     __builtin_amdgcn_sched_barrier(0);
   }
 
@@ -567,6 +640,9 @@ void attn_split_kernel(AttnArgs a) {
     const bool chain = cur.n_tok > 0 && nitem >= 0 && nxt.n_tok > 0;
     const uint16_t* kbn = kv_base(nxt, a.k);
     const uint16_t* vbn = kv_base(nxt, a.v);
+    uint16_t* kbfn = buf_base(nxt, a.kbuf);
+    uint16_t* vbfn = buf_base(nxt, a.vbuf);
+    const bool writer = KV == kKvElastic && cur.gv % a.R == 0;  // one column group writes
     const int* rows = rows_lds[wave][buf];
     const int* rows_n = rows_lds[wave][buf ^ 1];
     wave_sync_lds();
@@ -588,10 +664,14 @@ void attn_split_kernel(AttnArgs a) {
       const int* rsrc = last && chain ? rows_n : rows + c + kChunk;
       const uint16_t* ksrc = last && chain ? kbn : kb;
       const uint16_t* vsrc = last && chain ? vbn : vb;
+      const uint16_t* kfsrc = last && chain ? kbfn : kbf;
+      const uint16_t* vfsrc = last && chain ? vbfn : vbf;
 #pragma unroll
       for (int r = 0; r < kVRows; ++r)
         *reinterpret_cast<uint4*>(V + (4 * r + kg) * kVPitch + 8 * r16) = vraw[r];
-      load_v(rsrc, vsrc, vraw);
+      if (writer)
+        store_v_rows(rows + c, vraw, vbf + (int64_t)(cur.j0 + c) * rs, rs, n_tok - c, kg, r16);
+      load_v(rsrc, vsrc, vfsrc, vraw);
       __builtin_amdgcn_sched_barrier(0);  // keep the refill here: issue order = retire order
 
       // S^T tiles: lane holds S[head r16][token 16t + 4kg + i].
@@ -604,7 +684,9 @@ void attn_split_kernel(AttnArgs a) {
           sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kraw[t][s]),
                                                             qf[s], sacc[t], 0, 0, 0);
       }
-      load_k(rsrc, ksrc, kraw);
+      if (writer)
+        store_k_rows(rows + c, kraw, kbf + (int64_t)(cur.j0 + c) * rs, rs, n_tok - c, kg, r16);
+      load_k(rsrc, ksrc, kfsrc, kraw);
       __builtin_amdgcn_sched_barrier(0);
 
       float sv[kTiles][4];
@@ -695,12 +777,14 @@ void attn_split_kernel(AttnArgs a) {
     cur = nxt;
     kb = kbn;
     vb = vbn;
+    kbf = kbfn;
+    vbf = vbfn;
 #pragma unroll
     for (int s = 0; s < 4; ++s) qf[s] = qn[s];
     if (!chain && cur.n_tok > 0) {  // not chained (this unit had no tokens): start it cold
-      load_v(rows_n, vb, vraw);
+      load_v(rows_n, vb, vbf, vraw);
       __builtin_amdgcn_sched_barrier(0);
-      load_k(rows_n, kb, kraw);
+      load_k(rows_n, kb, kbf, kraw);
       __builtin_amdgcn_sched_barrier(0);
     }
     buf ^= 1;
@@ -842,9 +926,21 @@ size_t attn_ws_bytes(const Dims& d) {
   return align_up(sizeof(float) * rows * d.d) + align_up(sizeof(float) * rows * 2);
 }
 
-hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
-                       const uint16_t* v, const int32_t* idx, const int32_t* counts,
-                       float* out, float* lse, void* ws, hipStream_t s) {
+namespace {
+
+template <int KV>
+void launch_split(dim3 grid, bool pipe, const AttnArgs& a, hipStream_t s) {
+  if (pipe)
+    attn_split_kernel<KV, true><<<grid, kWaves * 64, lds_reserve(true), s>>>(a);
+  else
+    attn_split_kernel<KV, false><<<grid, kWaves * 64, lds_reserve(false), s>>>(a);
+}
+
+hipError_t launch_attn_mode(const Dims& d, int kv, const uint16_t* q, const uint16_t* k,
+                            const uint16_t* v, const int32_t* idx, uint16_t* kbuf,
+                            uint16_t* vbuf, const int32_t* src, const int32_t* fused,
+                            const int32_t* counts, float* out, float* lse, void* ws,
+                            hipStream_t s) {
   const AttnPlan pl = attn_plan(d);
   // the row staging area holds one split plus a chunk of padding
   if (pl.split > kMaxSplit || pl.split % kChunk != 0) return hipErrorInvalidValue;
@@ -868,9 +964,10 @@ hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
     auto gcd = [](int x, int y) { while (y) { const int t = x % y; x = y; y = t; } return x; };
     while (gcd(perm, n_order) != 1) ++perm;
   }
-  AttnArgs a{q, k, v, idx, counts, part_acc, part_ml, out, lse, d.kv_stride_layer, d.kv_stride_b,
-             d.B, d.H_q, d.H_kv, d.G / R, d.k_max, d.L_cap, pl.n_split, pl.split, (int)n_items,
-             R, pl.mode, n_order, perm, d.n_sets, d.scale * kLog2e};
+  AttnArgs a{q, k, v, idx, kbuf, vbuf, src, fused, counts, part_acc, part_ml, out, lse,
+             d.kv_stride_layer, d.kv_stride_b, d.B, d.H_q, d.H_kv, d.G / R, d.k_max, d.L_cap,
+             pl.n_split, pl.split, (int)n_items, R, pl.mode, n_order, perm, d.n_sets,
+             d.scale * kLog2e};
   // One workgroup per CU, fewer only when there are fewer units than CUs:
   // with few units they are spread over all CUs (each CU's share of the
   // bandwidth is limited) rather than packed four to a CU.
@@ -882,19 +979,34 @@ hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
   const bool force_cold = sched && strcmp(sched, "cold") == 0;
   // some wavefront takes several units: pipeline them
   const bool pipe = !force_cold && n_items > (int64_t)grid.x * kWaves;
-  if (idx && pipe)
-    attn_split_kernel<true, true><<<grid, kWaves * 64, lds_reserve(true), s>>>(a);
-  else if (idx)
-    attn_split_kernel<true, false><<<grid, kWaves * 64, lds_reserve(false), s>>>(a);
-  else if (pipe)
-    attn_split_kernel<false, true><<<grid, kWaves * 64, lds_reserve(true), s>>>(a);
+  if (kv == kKvIndexed)
+    launch_split<kKvIndexed>(grid, pipe, a, s);
+  else if (kv == kKvCompact)
+    launch_split<kKvCompact>(grid, pipe, a, s);
   else
-    attn_split_kernel<false, false><<<grid, kWaves * 64, lds_reserve(false), s>>>(a);
+    launch_split<kKvElastic>(grid, pipe, a, s);
   if (pl.mode != kGlobalPartials) return hipGetLastError();
   CombineArgs c{part_acc, part_ml, counts, out, lse, d.B, d.H_q, d.k_max, pl.n_split, pl.split};
   const dim3 g2(d.n_layers * d.B, (d.H_q + 7) / 8);
   attn_combine_kernel<<<g2, 256, 0, s>>>(c);
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
+                       const uint16_t* v, const int32_t* idx, const int32_t* counts,
+                       float* out, float* lse, void* ws, hipStream_t s) {
+  return launch_attn_mode(d, idx ? kKvIndexed : kKvCompact, q, k, v, idx, nullptr, nullptr,
+                          nullptr, nullptr, counts, out, lse, ws, s);
+}
+
+hipError_t launch_attn_elastic(const Dims& d, const uint16_t* q, const uint16_t* k_cache,
+                               const uint16_t* v_cache, uint16_t* kbuf, uint16_t* vbuf,
+                               const int32_t* slot_src, const int32_t* counts, float* out,
+                               float* lse, void* ws, hipStream_t s, const int32_t* fused) {
+  return launch_attn_mode(d, kKvElastic, q, k_cache, v_cache, nullptr, kbuf, vbuf, slot_src,
+                          fused, counts, out, lse, ws, s);
 }
 
 }  // namespace spec

@@ -112,9 +112,12 @@ struct PlanArgs {
   const int32_t* idx_now;  // [B][k_max], S_now = idx_now[b][0..counts[b]) ascending
   const int32_t* counts;
   int32_t* slot_tok;       // [B][k_max]
+  int32_t* slot_src;       // [B][k_max]: token loaded into the slot by this update, or -1
   int32_t* n_changed;      // [B]
   int32_t* loads;          // ws: [B][k_max][2] (slot, token)
+  int32_t* fused;          // ws: [B] 1: the attention loads this sequence's rows (or null)
   int k_max, L_cap;
+  int fuse_pct;            // fused when more than fuse_pct % of the selection is new
 };
 
 // Exclusive workgroup scan of one int; returns the total.
@@ -159,6 +162,7 @@ __global__ __launch_bounds__(kPlanThreads) void elastic_plan_kernel(PlanArgs a) 
   const int c = clampi(a.counts[b], 0, a.k_max);
   const int32_t* s_now = a.idx_now + (size_t)b * a.k_max;
   int32_t* slot = a.slot_tok + (size_t)b * a.k_max;
+  int32_t* src = a.slot_src + (size_t)b * a.k_max;
   int32_t* loads = a.loads + (size_t)b * a.k_max * 2;
 
   for (int w = tid; w < 2 * words; w += kPlanThreads) bits[w] = 0u;
@@ -215,6 +219,7 @@ __global__ __launch_bounds__(kPlanThreads) void elastic_plan_kernel(PlanArgs a) 
       const int t = slot[s];
       const bool keep = !full && t >= 0 && t < a.L_cap && ((now_bits[t >> 5] >> (t & 31)) & 1u);
       is_free = !keep;
+      src[s] = -1;  // loaded slots are set below, after the barrier
     }
     int tot;
     const int pos = plan_scan(is_free, tot, sh) + base_free;
@@ -230,8 +235,14 @@ __global__ __launch_bounds__(kPlanThreads) void elastic_plan_kernel(PlanArgs a) 
   // a corrupted one must still never index outside the slot row.
   const int n_apply = min(n_in_total, base_free);
   __syncthreads();  // loads[] complete before it is applied
-  for (int i = tid; i < n_apply; i += kPlanThreads) slot[loads[2 * i]] = loads[2 * i + 1];
-  if (tid == 0) a.n_changed[b] = n_apply;
+  for (int i = tid; i < n_apply; i += kPlanThreads) {
+    slot[loads[2 * i]] = loads[2 * i + 1];
+    src[loads[2 * i]] = loads[2 * i + 1];
+  }
+  if (tid == 0) {
+    a.n_changed[b] = n_apply;
+    if (a.fused) a.fused[b] = (int64_t)100 * n_apply > (int64_t)a.fuse_pct * c ? 1 : 0;
+  }
 }
 
 struct CopyArgs {
@@ -239,6 +250,7 @@ struct CopyArgs {
   const uint16_t* v;
   const int32_t* loads;
   const int32_t* n_changed;
+  const int32_t* skip;      // [B] or null: sequences whose rows the attention loads
   uint16_t* kbuf;
   uint16_t* vbuf;
   int64_t stride_layer, stride_b, row_elems;
@@ -249,7 +261,7 @@ struct CopyArgs {
 // slots, every layer.
 __global__ __launch_bounds__(256) void elastic_copy_kernel(CopyArgs a) {
   const int b = blockIdx.y;
-  const int n = clampi(a.n_changed[b], 0, a.k_max);
+  const int n = a.skip && a.skip[b] ? 0 : clampi(a.n_changed[b], 0, a.k_max);
   const int i0 = blockIdx.x * kRowsPerBlock;
   if (i0 >= n) return;
   const int nrows = min(kRowsPerBlock, n - i0);
@@ -287,8 +299,10 @@ size_t elastic_plan_lds_bytes(const Dims& d) {
 }
 
 hipError_t launch_delta_plan(const Dims& d, const int32_t* idx_now, const int32_t* counts,
-                             int32_t* slot_tok, int32_t* n_changed, void* ws, hipStream_t s) {
-  PlanArgs p{idx_now, counts, slot_tok, n_changed, static_cast<int32_t*>(ws), d.k_max, d.L_cap};
+                             int32_t* slot_tok, int32_t* slot_src, int32_t* n_changed, void* ws,
+                             hipStream_t s, int fuse_pct) {
+  PlanArgs p{idx_now, counts, slot_tok, slot_src, n_changed, static_cast<int32_t*>(ws),
+             fuse_pct >= 0 ? delta_ws_fused(d, ws) : nullptr, d.k_max, d.L_cap, fuse_pct};
   elastic_plan_kernel<<<d.B, kPlanThreads, elastic_plan_lds_bytes(d), s>>>(p);
   return hipGetLastError();
 }
@@ -296,8 +310,8 @@ hipError_t launch_delta_plan(const Dims& d, const int32_t* idx_now, const int32_
 hipError_t launch_delta_copy(const Dims& d, const uint16_t* k_src, const uint16_t* v_src,
                              int64_t src_stride_layer, int64_t src_stride_b, int n_layers,
                              const int32_t* n_changed, uint16_t* kbuf, uint16_t* vbuf,
-                             const void* ws, hipStream_t s) {
-  CopyArgs c{k_src, v_src, static_cast<const int32_t*>(ws), n_changed, kbuf, vbuf,
+                             const void* ws, hipStream_t s, const int32_t* skip) {
+  CopyArgs c{k_src, v_src, static_cast<const int32_t*>(ws), n_changed, skip, kbuf, vbuf,
              src_stride_layer, src_stride_b, (int64_t)d.H_kv * d.d, d.B, d.k_max, d.L_cap,
              n_layers};
   const dim3 grid((d.k_max + kRowsPerBlock - 1) / kRowsPerBlock, d.B);
@@ -307,9 +321,9 @@ hipError_t launch_delta_copy(const Dims& d, const uint16_t* k_src, const uint16_
 
 hipError_t launch_delta(const Dims& d, const int32_t* idx_now, const int32_t* counts,
                         const uint16_t* k_cache, const uint16_t* v_cache,
-                        int32_t* slot_tok, uint16_t* kbuf, uint16_t* vbuf,
+                        int32_t* slot_tok, int32_t* slot_src, uint16_t* kbuf, uint16_t* vbuf,
                         int32_t* n_changed, void* ws, hipStream_t s) {
-  hipError_t e = launch_delta_plan(d, idx_now, counts, slot_tok, n_changed, ws, s);
+  hipError_t e = launch_delta_plan(d, idx_now, counts, slot_tok, slot_src, n_changed, ws, s);
   if (e != hipSuccess) return e;
   return launch_delta_copy(d, k_cache, v_cache, d.kv_stride_layer, d.kv_stride_b, d.n_layers,
                            n_changed, kbuf, vbuf, ws, s);

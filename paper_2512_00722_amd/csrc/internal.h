@@ -102,10 +102,22 @@ inline size_t topk_ws_bytes(const Dims& d) { return topk_hist_bytes(d) + topk_li
 int attn_split_tokens(const Dims& d);
 size_t attn_ws_bytes(const Dims& d);
 
-// Elastic loading: per sequence the list of (slot, token) copies.
+// Elastic loading: per sequence the list of (slot, token) copies, then per
+// sequence whether the attention loads its rows itself (the fused step).
 inline size_t delta_ws_bytes(const Dims& d) {
-  return align_up(sizeof(int32_t) * 2 * (size_t)d.B * d.k_max);
+  return align_up(sizeof(int32_t) * 2 * (size_t)d.B * d.k_max) +
+         align_up(sizeof(int32_t) * (size_t)d.B);
 }
+inline int32_t* delta_ws_fused(const Dims& d, void* ws) {
+  return reinterpret_cast<int32_t*>(static_cast<char*>(ws) +
+                                    align_up(sizeof(int32_t) * 2 * (size_t)d.B * d.k_max));
+}
+// The fused step's elastic attention loads a sequence's new rows itself
+// when more than this share (percent) of its selection is new, as in a full
+// reload; otherwise the rows are copied first and the attention only reads.
+// A kernel that writes while it streams runs at ~4.8 TB/s, one that only
+// reads at ~6.3, so the copy wins for small updates.
+constexpr int kElasticFusePct = 50;
 
 // Retrieval-head front end: embedding width, vocabulary and the rotary /
 // YaRN parameters, validated (alpha < beta; orig_ctx > 0 when scale > 1).
@@ -175,20 +187,34 @@ hipError_t launch_gather(const Dims& d, const uint16_t* k_cache, const uint16_t*
 hipError_t launch_attn(const Dims& d, const uint16_t* q, const uint16_t* k,
                        const uint16_t* v, const int32_t* idx, const int32_t* counts,
                        float* out, float* lse, void* ws, hipStream_t s);
+// Attention over the slot buffers after an elastic update: slots with
+// slot_src[b][slot] >= 0 are read from the caches at that token and written
+// into the slot on the way; the others are read from the slot.
+// fused (nullable, [B]): only sequences with fused[b] != 0 load rows from
+// the caches; the others are read from their slots throughout.
+hipError_t launch_attn_elastic(const Dims& d, const uint16_t* q, const uint16_t* k_cache,
+                               const uint16_t* v_cache, uint16_t* kbuf, uint16_t* vbuf,
+                               const int32_t* slot_src, const int32_t* counts, float* out,
+                               float* lse, void* ws, hipStream_t s,
+                               const int32_t* fused = nullptr);
 hipError_t launch_delta(const Dims& d, const int32_t* idx_now, const int32_t* counts,
                         const uint16_t* k_cache, const uint16_t* v_cache,
-                        int32_t* slot_tok, uint16_t* kbuf, uint16_t* vbuf,
+                        int32_t* slot_tok, int32_t* slot_src, uint16_t* kbuf, uint16_t* vbuf,
                         int32_t* n_changed, void* ws, hipStream_t s);
 // Elastic loading in two parts: the slot plan (the (slot, token) list in
-// ws), then the copy of the listed rows of n_layers layers from a source
-// cache (device memory, or pinned host memory through its device address)
-// into the slot buffers.
+// ws; slot_src: per slot the token loaded into it, or -1), then the copy of
+// the listed rows of n_layers layers from a source cache (device memory, or
+// pinned host memory through its device address) into the slot buffers.
+// fuse_pct >= 0: also mark, in ws, the sequences more than fuse_pct % of
+// whose selection is new (the attention loads their rows; the copy skips
+// them).
 hipError_t launch_delta_plan(const Dims& d, const int32_t* idx_now, const int32_t* counts,
-                             int32_t* slot_tok, int32_t* n_changed, void* ws, hipStream_t s);
+                             int32_t* slot_tok, int32_t* slot_src, int32_t* n_changed, void* ws,
+                             hipStream_t s, int fuse_pct = -1);
 hipError_t launch_delta_copy(const Dims& d, const uint16_t* k_src, const uint16_t* v_src,
                              int64_t src_stride_layer, int64_t src_stride_b, int n_layers,
                              const int32_t* n_changed, uint16_t* kbuf, uint16_t* vbuf,
-                             const void* ws, hipStream_t s);
+                             const void* ws, hipStream_t s, const int32_t* skip = nullptr);
 hipError_t launch_mla(const MlaDims& d, const uint16_t* q, const uint16_t* ckv,
                       const uint16_t* w_uk, const uint16_t* w_uv, const int32_t* idx,
                       const int32_t* counts, float* out, float* lse, void* ws, hipStream_t s);

@@ -183,6 +183,28 @@ spec_status debug_selection(int B, int k_max, int n_sets, const int32_t* idx,
   return SPEC_OK;
 }
 
+// Elastic slot sources: -1 (read the slot) or a token index of the caches.
+spec_status debug_slot_src(const spec::Dims& d, const int32_t* slot_src, hipStream_t s) {
+  std::vector<int32_t> h;
+  if (!d2h(h, slot_src, (size_t)d.B * d.k_max, s)) return SPEC_ERR_HIP;
+  for (int32_t v : h)
+    if (v < -1 || v >= d.L_cap) return SPEC_ERR_INVALID;
+  return SPEC_OK;
+}
+
+// How the fused step applies an elastic update.  By default the attention
+// loads the rows of mostly-new sequences itself and the others are copied
+// first; SPEC_ELASTIC_PATH=copy copies every update before a compact
+// attention (spec_delta_gather's path), SPEC_ELASTIC_PATH=fused lets the
+// attention load every update (tests compare the three).
+enum { kElasticAuto = 0, kElasticCopy = 1, kElasticFused = 2 };
+int elastic_path() {
+  const char* e = getenv("SPEC_ELASTIC_PATH");
+  if (e && strcmp(e, "copy") == 0) return kElasticCopy;
+  if (e && strcmp(e, "fused") == 0) return kElasticFused;
+  return kElasticAuto;
+}
+
 // After a launch: in debug mode wait for the stream and report its status.
 spec_status finish(spec_status st, hipStream_t s) {
   if (st != SPEC_OK || !debug_on()) return st;
@@ -192,11 +214,12 @@ spec_status finish(spec_status st, hipStream_t s) {
 }
 
 spec_status check_elastic(const spec::Dims& d, const spec_elastic* el) {
-  if (!el || !el->slot_tok || !el->kbuf || !el->vbuf || !el->n_changed) return SPEC_ERR_INVALID;
+  if (!el || !el->slot_tok || !el->kbuf || !el->vbuf || !el->n_changed || !el->slot_src)
+    return SPEC_ERR_INVALID;
   // the compact slot buffers hold one token per slot for every KV head
   if (d.n_sets != 1) return SPEC_ERR_UNSUPPORTED;
-  if (!aligned4(el->slot_tok) || !aligned4(el->n_changed) || !aligned16(el->kbuf) ||
-      !aligned16(el->vbuf))
+  if (!aligned4(el->slot_tok) || !aligned4(el->n_changed) || !aligned4(el->slot_src) ||
+      !aligned16(el->kbuf) || !aligned16(el->vbuf))
     return SPEC_ERR_INVALID;
   if (d.L_cap > kMaxElasticLcap) return SPEC_ERR_UNSUPPORTED;
   return SPEC_OK;
@@ -359,11 +382,28 @@ spec_status run_step(const spec::Dims& d, const uint16_t* q_r, const uint16_t* k
   hipError_t e = spec::launch_score_select(d, q_r, k_r, seq_lens, ks, scores_out, scores,
                                            idx_out, counts_out, ws_score, ws_topk, s);
   if (e != hipSuccess) return hip_status(e);
-  if (el) {
-    e = spec::launch_delta(d, idx_out, counts_out, k_cache, v_cache, el->slot_tok, el->kbuf,
-                           el->vbuf, el->n_changed, ws_delta, s);
+  const int path = el ? elastic_path() : 0;
+  if (el && path == kElasticCopy) {  // the update's copy, then compact attention
+    e = spec::launch_delta(d, idx_out, counts_out, k_cache, v_cache, el->slot_tok, el->slot_src,
+                           el->kbuf, el->vbuf, el->n_changed, ws_delta, s);
     if (e != hipSuccess) return hip_status(e);
     e = spec::launch_attn(d, q, el->kbuf, el->vbuf, nullptr, counts_out, out, lse, ws_attn, s);
+  } else if (el) {
+    // The plan marks the sequences whose update is mostly new (a full
+    // reload): the attention loads their rows from the caches into the
+    // slots as it streams them.  The other sequences' rows are copied first
+    // and the attention only reads the slots.
+    const int pct = path == kElasticFused ? 0 : spec::kElasticFusePct;
+    e = spec::launch_delta_plan(d, idx_out, counts_out, el->slot_tok, el->slot_src,
+                                el->n_changed, ws_delta, s, pct);
+    if (e != hipSuccess) return hip_status(e);
+    const int32_t* fused = spec::delta_ws_fused(d, ws_delta);
+    e = spec::launch_delta_copy(d, k_cache, v_cache, d.kv_stride_layer, d.kv_stride_b,
+                                d.n_layers, el->n_changed, el->kbuf, el->vbuf, ws_delta, s,
+                                fused);
+    if (e != hipSuccess) return hip_status(e);
+    e = spec::launch_attn_elastic(d, q, k_cache, v_cache, el->kbuf, el->vbuf, el->slot_src,
+                                  counts_out, out, lse, ws_attn, s, fused);
   } else {
     e = spec::launch_attn(d, q, k_cache, v_cache, idx_out, counts_out, out, lse, ws_attn, s);
   }
@@ -504,8 +544,33 @@ spec_status spec_delta_gather(const spec_dims* dm, const int32_t* idx_now,
                                           as_stream(stream))) != SPEC_OK)
     return st;
   return finish(hip_status(spec::launch_delta(d, idx_now, counts, k_cache, v_cache,
-                                              el->slot_tok, el->kbuf, el->vbuf, el->n_changed,
-                                              ws, as_stream(stream))),
+                                              el->slot_tok, el->slot_src, el->kbuf, el->vbuf,
+                                              el->n_changed, ws, as_stream(stream))),
+                as_stream(stream));
+}
+
+spec_status spec_sparse_decode_attn_elastic(const spec_dims* dm, const uint16_t* q,
+                                            const uint16_t* k_cache, const uint16_t* v_cache,
+                                            const spec_elastic* el, const int32_t* counts,
+                                            float* out, float* lse, void* ws, size_t ws_bytes,
+                                            spec_stream stream) {
+  spec::Dims d;
+  spec_status st = resolve(dm, &d);
+  if (st != SPEC_OK) return st;
+  if (!q || !k_cache || !v_cache || !counts || !out) return SPEC_ERR_INVALID;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned4(counts) ||
+      !aligned16(out) || (lse && !aligned4(lse)))
+    return SPEC_ERR_INVALID;
+  if ((st = check_elastic(d, el)) != SPEC_OK) return st;
+  if ((st = check_ws(d, SPEC_OP_ATTN, ws, ws_bytes)) != SPEC_OK) return st;
+  if (debug_on() &&
+      ((st = debug_selection(d.B, d.k_max, 1, nullptr, counts, d.L_cap, as_stream(stream))) !=
+           SPEC_OK ||
+       (st = debug_slot_src(d, el->slot_src, as_stream(stream))) != SPEC_OK))
+    return st;
+  return finish(hip_status(spec::launch_attn_elastic(d, q, k_cache, v_cache, el->kbuf, el->vbuf,
+                                                     el->slot_src, counts, out, lse, ws,
+                                                     as_stream(stream))),
                 as_stream(stream));
 }
 
@@ -562,7 +627,8 @@ spec_status spec_offload_load(const spec_dims* dm, const int32_t* idx_now, const
   const hipStream_t s = as_stream(stream);
   if (debug_on() && (st = debug_selection(d.B, d.k_max, 1, idx_now, counts, d.L_cap, s)) != SPEC_OK)
     return st;
-  hipError_t e = spec::launch_delta_plan(d, idx_now, counts, el->slot_tok, el->n_changed, ws, s);
+  hipError_t e = spec::launch_delta_plan(d, idx_now, counts, el->slot_tok, el->slot_src,
+                                         el->n_changed, ws, s);
   if (e != hipSuccess) return hip_status(e);
   st = enqueue_host_loads(d, hk, el, ws, d.n_layers, s, as_stream(copy_stream), layer_ready);
   if (st == SPEC_OK && debug_on() && copy_stream) st = finish(st, as_stream(copy_stream));
@@ -614,7 +680,8 @@ spec_status spec_step_offload(const spec_dims* dm, const uint16_t* q_r, const ui
   hipError_t e = spec::launch_score_select(d, q_r, k_r, seq_lens, ks, scores_out, scores,
                                            idx_out, counts_out, ws_score, ws_topk, s);
   if (e != hipSuccess) return hip_status(e);
-  e = spec::launch_delta_plan(d_off, idx_out, counts_out, el->slot_tok, el->n_changed, ws_delta,
+  e = spec::launch_delta_plan(d_off, idx_out, counts_out, el->slot_tok, el->slot_src,
+                              el->n_changed, ws_delta,
                               s);
   if (e != hipSuccess) return hip_status(e);
   if ((st = enqueue_host_loads(d_off, hk, el, ws_delta, n_off, s, cs, layer_ready)) != SPEC_OK)

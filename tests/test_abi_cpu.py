@@ -112,12 +112,15 @@ def test_head_level_sets(lib):
     assert ws_size(lib, good_dims(n_sets=8, H_r=12), spec.OP_SCORE)[0] == 2
     assert ws_size(lib, good_dims(n_sets=8, B=9000), spec.OP_TOPK)[0] == 2   # B*n_sets rows
     # elastic loading keeps one token per slot for every head: not with sets
-    el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value)
+    el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value, FAKE.value)
     _, nws = ws_size(lib, d, spec.OP_STEP)
     assert lib.spec_delta_gather(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, ctypes.byref(el), FAKE,
                                  nws, None) == 2
     assert lib.spec_step(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                          FAKE, None, None, ctypes.byref(el), FAKE, nws, None) == 2
+    assert lib.spec_sparse_decode_attn_elastic(ctypes.byref(d), FAKE, FAKE, FAKE,
+                                               ctypes.byref(el), FAKE, FAKE, None, FAKE, nws,
+                                               None) == 2
     assert lib.spec_last_hip_error() == 0
 
 
@@ -164,12 +167,30 @@ def test_entry_points_reject_before_hip(lib):
     assert lib.spec_step(byref(bad), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                          None, None, None, FAKE, nws, None) == 2
     # elastic state with a null member
-    el = spec.Elastic(FAKE.value, FAKE.value, None, FAKE.value)
+    el = spec.Elastic(FAKE.value, FAKE.value, None, FAKE.value, FAKE.value)
     assert lib.spec_delta_gather(byref(d), FAKE, FAKE, FAKE, FAKE, byref(el), FAKE, nws,
                                  None) == 1
+    assert lib.spec_sparse_decode_attn_elastic(byref(d), FAKE, FAKE, FAKE, byref(el), FAKE,
+                                               FAKE, None, FAKE, nws, None) == 1
+    assert lib.spec_sparse_decode_attn_elastic(byref(d), FAKE, FAKE, FAKE, None, FAKE, FAKE,
+                                               None, FAKE, nws, None) == 1
+    # the elastic attention needs the slot sources and its workspace
+    el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value, None)
+    assert lib.spec_sparse_decode_attn_elastic(byref(d), FAKE, FAKE, FAKE, byref(el), FAKE,
+                                               FAKE, None, FAKE, nws, None) == 1
+    assert lib.spec_step(byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                         None, None, byref(el), FAKE, nws, None) == 1
+    el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value, FAKE.value + 2)
+    assert lib.spec_sparse_decode_attn_elastic(byref(d), FAKE, FAKE, FAKE, byref(el), FAKE,
+                                               FAKE, None, FAKE, nws, None) == 1
+    el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value, FAKE.value)
+    assert lib.spec_sparse_decode_attn_elastic(byref(d), FAKE, FAKE, FAKE, byref(el), FAKE,
+                                               FAKE, None, FAKE, 16, None) == 3
+    assert lib.spec_sparse_decode_attn_elastic(byref(d), FAKE_ODD, FAKE, FAKE, byref(el), FAKE,
+                                               FAKE, None, FAKE, nws, None) == 1
     # elastic loading caps L_cap
     big = good_dims(L_cap=300000, L_max=300000)
-    el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value)
+    el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value, FAKE.value)
     assert lib.spec_delta_gather(byref(big), FAKE, FAKE, FAKE, FAKE, byref(el), FAKE, 1 << 40,
                                  None) == 2
     assert lib.spec_last_hip_error() == 0
@@ -353,7 +374,7 @@ def test_offload_rejects_before_launch(lib):
     st_step, n_step = ws_size(lib, d, spec.OP_STEP)
     assert st_off == 0 and n_off >= n_step - ws_size(lib, d, spec.OP_ATTN)[1]
     host = spec.HostKv(FAKE.value, FAKE.value, 0, 0)
-    el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value)
+    el = spec.Elastic(FAKE.value, FAKE.value, FAKE.value, FAKE.value, FAKE.value)
     _, nd = ws_size(lib, d, spec.OP_DELTA)
     ev = (ctypes.c_void_p * 5)()
     # spec_offload_load

@@ -8,7 +8,7 @@ import torch
 import oracle
 import paper_2512_00722_amd as spec
 from tests.gpu_helpers import SCORE_ABS, SCORE_REL, TOL_ATTN, announce, f64, need_gpu
-from workloads import generate, small_workload
+from workloads import elastic_sequence, generate, small_workload
 
 pytestmark = pytest.mark.gpu
 
@@ -471,6 +471,65 @@ def test_step_elastic_equals_indexed(dev):
             c = int(r_ix["counts"][b])
             assert sorted(slots[b, :c].tolist()) == r_ix["idx"][b, :c].cpu().tolist()
             assert np.all(slots[b, c:] == -1)
+
+
+ELASTIC_FUSED_CASES = [
+    # split selections (few groups), ragged lengths
+    dict(B=3, L=3000, H_r=8, d_r=64, n_layers=2, H_q=32, H_kv=8, k=400, heavy_frac=0.02,
+         ragged_min=900, extra_cap=8, steps=6),
+    # one unit per group, several per wavefront (the pipelined schedule)
+    dict(B=40, L=1500, H_r=8, d_r=64, n_layers=2, H_q=32, H_kv=8, k=256, heavy_frac=0.02,
+         ragged_min=300, extra_cap=8, steps=4),
+    # 32 query heads per KV head: two column groups read each row, one writes it
+    dict(B=2, L=2500, H_r=8, d_r=64, n_layers=2, H_q=64, H_kv=2, k=300, heavy_frac=0.02,
+         ragged_min=1000, extra_cap=8, steps=4),
+]
+
+
+@pytest.mark.parametrize("kw", ELASTIC_FUSED_CASES, ids=[str(i) for i in range(3)])
+def test_elastic_attention_loads_equal_copy(dev, kw, monkeypatch):
+    """Sec. 5.4's loads done by the attention (the rows of the slots an
+    update assigned are read from the caches and written into their slots
+    as they stream) against the update's copy followed by compact
+    attention: the same outputs, lse, slot maps, slot sources, changed
+    counts and slot buffers, bit for bit, step after step, with every
+    update loaded by the attention ("fused"), with none ("copy") and with
+    the step's own choice per sequence (mostly-new updates fused: the first
+    step; the last step halves the budgets, which reloads sequences in
+    full)."""
+    announce(f"elastic fused vs copy {kw}")
+    w = small_workload(**kw)
+    x = generate(w, seed=kw["B"] + 17, device=dev)
+    e = elastic_sequence(w, x, seed=kw["B"] + 17, device=dev)
+    paths = ("auto", "fused", "copy")
+    states = {p: spec.ElasticState(w.n_layers, w.B, w.k, w.H_kv, w.d, dev) for p in paths}
+    for s in range(w.steps):
+        ks = x["ks"] if s < w.steps - 1 else torch.clamp(x["ks"] // 2, min=1)
+        r = {}
+        for p in paths:
+            if p == "auto":
+                monkeypatch.delenv("SPEC_ELASTIC_PATH", raising=False)
+            else:
+                monkeypatch.setenv("SPEC_ELASTIC_PATH", p)
+            r[p] = spec.step(e["q_r"][s], x["K_r"], e["seq_lens"][s], ks, e["q"][s], x["K"], x["V"],
+                             k_max=w.k, elastic=states[p], with_lse=True)
+        monkeypatch.delenv("SPEC_ELASTIC_PATH", raising=False)
+        torch.cuda.synchronize()
+        for p in ("auto", "fused"):
+            for key in ("idx", "counts", "out", "lse"):
+                assert torch.equal(r[p][key], r["copy"][key]), (s, p, key)
+            for attr in ("slot_tok", "slot_src", "n_changed", "kbuf", "vbuf"):
+                assert torch.equal(getattr(states[p], attr), getattr(states["copy"], attr)), (s, p, attr)
+        assert int(states["fused"].n_changed.sum()) > 0 or s > 0
+    # the standalone entry point with the last update's slot sources rewrites
+    # the same rows and gives the step's output again
+    st = states["fused"]
+    kb, vb = st.kbuf.clone(), st.vbuf.clone()
+    out, lse = spec.sparse_decode_attn_elastic(e["q"][w.steps - 1], x["K"], x["V"], st,
+                                               r["fused"]["counts"])
+    torch.cuda.synchronize()
+    assert torch.equal(out, r["fused"]["out"]) and torch.equal(lse, r["fused"]["lse"])
+    assert torch.equal(st.kbuf, kb) and torch.equal(st.vbuf, vb)
 
 
 # ------------------------------------------------------- head-level selection

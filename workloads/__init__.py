@@ -348,10 +348,11 @@ def algorithmic_bytes(w: Workload, seq_lens, ks, delta_rows: int = 0) -> int:
     """Bytes the method must move for one decode step.
 
     K_r rows of every cached token, q_r, and per layer the selected K and V
-    rows, the query and the fp32 output; plus, for elastic loading, a read
-    and a write of every changed K/V row in every layer (delta_rows = total
-    changed indices over the batch).  Scratch (logits, scores, indices,
-    partials) is implementation traffic and is not counted.
+    rows, the query and the fp32 output; plus, for elastic loading, a write
+    of every changed K/V row in every layer into its slot (delta_rows =
+    total changed indices over the batch; the changed rows are among the
+    selected rows, read once).  Scratch (logits, scores, indices, partials)
+    is implementation traffic and is not counted.
     """
     seq_lens = [int(x) for x in seq_lens]
     ks = [int(x) for x in ks]
@@ -359,5 +360,5 @@ def algorithmic_bytes(w: Workload, seq_lens, ks, delta_rows: int = 0) -> int:
     kr = sum(seq_lens) * w.H_r * w.d_r * 2 + w.B * w.H_r * w.d_r * 2
     per_layer = (sum(kb) * w.H_kv * w.d * 2 * 2 + w.B * w.H_q * w.d * 2
                  + w.B * w.H_q * w.d * 4)
-    delta = 2 * delta_rows * w.H_kv * w.d * 2 * 2 * w.n_layers
+    delta = delta_rows * w.H_kv * w.d * 2 * 2 * w.n_layers
     return kr + w.n_layers * per_layer + delta
