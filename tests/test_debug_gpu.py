@@ -84,3 +84,37 @@ def test_debug_mode_offload(dev, monkeypatch):
     torch.cuda.synchronize()
     assert torch.equal(st.slot_tok, before)          # nothing was enqueued
     monkeypatch.delenv("SPEC_DEBUG")
+
+
+def test_debug_mode_elastic_attention(dev, monkeypatch):
+    """SPEC_DEBUG=1 on the elastic attention: a count above k_max or a slot
+    source outside [-1, L_cap) is rejected with nothing enqueued (the output
+    keeps its sentinel); valid state gives the same bits as without the
+    checks."""
+    announce("SPEC_DEBUG elastic attention")
+    w = small_workload(B=2, L=500, H_r=4, d_r=64, n_layers=2, H_q=8, H_kv=2, k=64)
+    x = generate(w, seed=2, device=dev)
+    st = spec.ElasticState(w.n_layers, w.B, w.k, w.H_kv, w.d, dev)
+    r = spec.step(x["q_r"], x["K_r"], x["seq_lens"], x["ks"], x["q"], x["K"], x["V"], k_max=w.k,
+                  elastic=st)
+    ref, _ = spec.sparse_decode_attn_elastic(x["q"], x["K"], x["V"], st, r["counts"])
+    torch.cuda.synchronize()
+    monkeypatch.setenv("SPEC_DEBUG", "1")
+    got, _ = spec.sparse_decode_attn_elastic(x["q"], x["K"], x["V"], st, r["counts"])
+    assert torch.equal(got, ref)
+    out = torch.full_like(ref, 7.0)
+    with pytest.raises(spec.SpecError) as e:
+        spec.sparse_decode_attn_elastic(x["q"], x["K"], x["V"], st,
+                                        torch.tensor([64, 65], dtype=torch.int32, device=dev),
+                                        out=out)
+    assert e.value.status == 1
+    for bad in (500, -2):
+        saved = st.slot_src.clone()
+        st.slot_src[1, 3] = bad
+        with pytest.raises(spec.SpecError) as e:
+            spec.sparse_decode_attn_elastic(x["q"], x["K"], x["V"], st, r["counts"], out=out)
+        assert e.value.status == 1
+        st.slot_src.copy_(saved)
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0)
+    monkeypatch.delenv("SPEC_DEBUG")

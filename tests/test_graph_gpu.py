@@ -110,3 +110,70 @@ def test_step_offload_graph_replays_match_eager():
         for k, v in ref.items():
             assert torch.equal(outputs[k], v), (rep, k)
         assert torch.equal(st.slot_tok, ref_slots) and torch.equal(st.n_changed, ref_nch), rep
+
+
+@pytest.mark.parametrize("path", ["auto", "fused"])
+def test_step_elastic_graph_replays_match_eager(path, monkeypatch):
+    """The elastic step captured in a graph (plan, copy of the sequences with
+    small updates, attention that loads the rows of mostly-new ones): each
+    replay from the same slot state matches the eager step bit for bit,
+    outputs, slot maps and slot buffers."""
+    dev = need_gpu()
+    if path == "fused":
+        monkeypatch.setenv("SPEC_ELASTIC_PATH", "fused")
+    announce(f"graph replay of the elastic step, path {path}")
+    w = small_workload(B=3, L=2500, H_r=8, d_r=64, n_layers=2, H_q=32, H_kv=8, k=300,
+                       heavy_frac=0.02, ragged_min=1000)
+    x = generate(w, seed=13, device=dev)
+    args = dict(q_r=x["q_r"], K_r=x["K_r"], seq_lens=x["seq_lens"], ks=x["ks"], q=x["q"],
+                K=x["K"], V=x["V"], k_max=w.k)
+    dims = spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, H_r=w.H_r, d_r=w.d_r,
+                          n_layers=w.n_layers, H_q=w.H_q, H_kv=w.H_kv, d=w.d,
+                          kr_stride_b=x["K_r"].stride(0), kv_stride_layer=x["K"].stride(0),
+                          kv_stride_b=x["K"].stride(1))
+    ws = torch.zeros(spec.workspace_size(dims, spec.OP_STEP), dtype=torch.uint8, device=dev)
+    st = spec.ElasticState(w.n_layers, w.B, w.k, w.H_kv, w.d, dev)
+    # a state from smaller budgets (the same scores: a subset of the step's
+    # selection): sequence 0 gets two thirds of its rows new (loaded by the
+    # attention), sequence 1 ten rows and sequence 2 half (copied first)
+    ks = x["ks"].cpu()
+    ks_pre = torch.tensor([max(1, int(ks[0]) // 3), int(ks[1]) - 10, max(1, int(ks[2]) // 2)],
+                          dtype=torch.int32, device=dev)
+    spec.step(**{**args, "ks": ks_pre}, elastic=st, ws=ws)
+    torch.cuda.synchronize()
+    st0 = {k: getattr(st, k).clone() for k in ("slot_tok", "kbuf", "vbuf")}
+    eager = spec.step(**args, elastic=st, with_lse=True, ws=ws)
+    torch.cuda.synchronize()
+    nch, cnt = st.n_changed.cpu(), eager["counts"].cpu()
+    assert 2 * nch[0] > cnt[0] and 2 * nch[1] < cnt[1] and 2 * nch[2] <= cnt[2]  # a mix
+    ref = {k: v.clone() for k, v in eager.items() if v is not None}
+    ref_state = {k: getattr(st, k).clone() for k in ("slot_tok", "slot_src", "n_changed", "kbuf", "vbuf")}
+
+    def restore():
+        for k, v in st0.items():
+            getattr(st, k).copy_(v)
+
+    outputs = {}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        restore()
+        spec.step(**args, elastic=st, with_lse=True, outputs=outputs, ws=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        spec.step(**args, elastic=st, with_lse=True, outputs=outputs, ws=ws)
+    for rep in range(3):
+        for v in outputs.values():
+            if v is not None:
+                v.fill_(7)
+        restore()
+        spec.score(x["q_r"], x["K_r"], x["seq_lens"])   # eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k, v in ref.items():
+            assert torch.equal(outputs[k], v), (rep, k)
+        for k, v in ref_state.items():
+            assert torch.equal(getattr(st, k), v), (rep, k)
