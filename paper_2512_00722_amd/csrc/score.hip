@@ -95,15 +95,19 @@ __global__ __launch_bounds__(256) void logits_kernel(LogitsArgs a) {
   }
   __syncthreads();
 
-  // The block's logits leave in one coalesced burst after the stream: stores
-  // issued between the K_r loads would hold up every later load wait (the
-  // vector memory counter retires loads and stores in order).
+  // The block's logits leave in one coalesced burst after the stream (stores
+  // spread through the stream cost far more: writes mixed into the reads).
+  // They are device-scope stores, which pass through this XCD's L2 as they
+  // are issued: the blocks are all resident at once and end together, and
+  // dirty lines left in the L2s would all be written back at the kernel's
+  // end, with nothing to overlap them.
   {
     // head-major: each head's logits of the block are one contiguous run
     for (int e = threadIdx.x; e < n_tok * a.H_r; e += 256) {
       const int h = e / n_tok;
       const int i = e - h * n_tok;
-      a.logits[((size_t)b * a.H_r + h) * a.L_max + t_begin + i] = lg[i * 17 + h];
+      __hip_atomic_store(&a.logits[((size_t)b * a.H_r + h) * a.L_max + t_begin + i],
+                         lg[i * 17 + h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 
