@@ -203,3 +203,56 @@ def test_elastic_random_shapes(dev, seed):
                 assert torch.equal(vb[:, b, ss].view(torch.int16), V[:, b, tt].view(torch.int16))
         prev = now
     print(f"[elastic] seed={seed}: {n_reload} full reloads", flush=True)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_elastic_attention_random_shapes(dev, seed):
+    """Sec. 5.4's loads done by the attention, on random shapes (query-group
+    sizes up to 64, so that some KV heads are read by several column groups,
+    one of which writes) and random update sequences: after each update
+    (spec_delta_gather, which records the slot sources) the slots it loaded
+    are overwritten with garbage; the elastic attention must read those rows
+    from the caches, give the compact attention's output over the clean
+    slots bit for bit, and leave the slots exactly as the copy had."""
+    rng = np.random.default_rng(500 + seed)
+    n_layers = int(rng.integers(1, 4))
+    B = int(rng.integers(1, 5))
+    H_kv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([g for g in (1, 2, 4, 8, 16, 32, 64) if g * H_kv <= 128]))
+    H_q = H_kv * G
+    L_cap = int(rng.integers(64, 3001))
+    k_max = int(rng.integers(1, min(L_cap, 1500) + 1))
+    announce(f"elastic attention random seed={seed} layers={n_layers} B={B} H_q={H_q} "
+             f"H_kv={H_kv} L_cap={L_cap} k_max={k_max}")
+    g = torch.Generator().manual_seed(50_000 + seed)
+    Kd = torch.randn((n_layers, B, L_cap, H_kv, 128), generator=g).to(torch.bfloat16).to(dev)
+    Vd = torch.randn((n_layers, B, L_cap, H_kv, 128), generator=g).to(torch.bfloat16).to(dev)
+    st = spec.ElasticState(n_layers, B, k_max, H_kv, 128, dev)
+    prev = [np.zeros(0, dtype=np.int64) for _ in range(B)]
+    for it in range(6):
+        keep_p = float(rng.choice([0.0, 0.5, 0.8, 1.0]))
+        now = []
+        for b in range(B):
+            budget = int(rng.integers(0, k_max + 1))
+            keep = prev[b][rng.random(len(prev[b])) < keep_p][:budget]
+            pool = np.setdiff1d(np.arange(L_cap), keep)
+            add = rng.choice(pool, budget - len(keep), replace=False)
+            now.append(np.sort(np.concatenate([keep, add]).astype(np.int64)))
+        idx = torch.full((B, k_max), -1, dtype=torch.int32)
+        for b in range(B):
+            idx[b, :len(now[b])] = torch.tensor(now[b], dtype=torch.int32)
+        cnt = torch.tensor([len(x) for x in now], dtype=torch.int32).to(dev)
+        spec.delta_gather(idx.to(dev), cnt, Kd, Vd, st)
+        q = torch.randn((n_layers, B, H_q, 128), generator=g).to(torch.bfloat16).to(dev)
+        ref_out, ref_lse = spec.sparse_decode_attn(q, st.kbuf, st.vbuf, cnt)
+        torch.cuda.synchronize()
+        clean_k, clean_v = st.kbuf.clone(), st.vbuf.clone()
+        loaded = st.slot_src >= 0                       # [B, k_max]
+        assert int(loaded.sum()) == int(st.n_changed.sum()), it
+        st.kbuf[:, loaded] = 7.0                        # garbage in every loaded slot
+        st.vbuf[:, loaded] = -3.0
+        out, lse = spec.sparse_decode_attn_elastic(q, Kd, Vd, st, cnt)
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref_out) and torch.equal(lse, ref_lse), it
+        assert torch.equal(st.kbuf, clean_k) and torch.equal(st.vbuf, clean_v), it
+        prev = now
