@@ -29,7 +29,9 @@
 //    boundary costs no round trip.
 // The workgroups own contiguous ranges of a permuted unit order (groups of a
 // (layer, sequence, split) spread over the whole range), so that ragged
-// selections even out across workgroups.
+// selections even out across workgroups.  Pipelined launches over batches
+// of unequal selections deal the groups to the workgroups by selection size
+// instead (longest first, in a snake), which evens them out further.
 // A unit that covers a whole selection normalises and writes out/lse itself;
 // split selections leave (max, sum, acc) partials that a second kernel merges
 // with a log-sum-exp combine.
@@ -121,6 +123,7 @@ struct AttnArgs {
                           // (g perm) mod n_groups, perm coprime to n_groups
   int n_sets;             // 1: idx [B][k_max]; H_kv: idx [B][H_kv][k_max], one set per KV head
   float scale_log2;       // scale * log2(e)
+  int sorted;             // pipelined launches: groups by selection size (see attn_split_kernel)
 };
 
 __device__ __forceinline__ void wave_sync_lds() {
@@ -181,6 +184,8 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const uint16_t* p) {
 // no unit follows).
 constexpr int kRowsCap = kMaxSplit + kChunk;
 constexpr int kRowLoads = kMaxSplit / 64;  // index loads per lane for one unit
+// Sequences a launch may rank by selection size (one per thread of the workgroup).
+constexpr int kSortMaxB = kWaves * 64;
 
 // One work unit: (layer, sequence, KV-head column group, split).  A group of
 // more than 16 query heads is covered by R column groups of 16 (gv = g R ..
@@ -475,7 +480,8 @@ __device__ __forceinline__ void process_item(const AttnArgs& a, const int item, 
 // takes more than half of a CU's 160 KiB: exactly one per CU.
 constexpr size_t kLdsPerCU = 160 * 1024;
 constexpr size_t static_lds(bool pipe) {
-  return sizeof(uint16_t) * kWaves * kChunk * kVPitch + sizeof(int) * kWaves * (pipe ? 2 : 1) * kRowsCap + 16;
+  return sizeof(uint16_t) * kWaves * kChunk * kVPitch + sizeof(int) * kWaves * (pipe ? 2 : 1) * kRowsCap +
+         sizeof(int) * (pipe ? kSortMaxB : 1) + 16;
 }
 constexpr size_t lds_reserve(bool pipe) {
   return kLdsPerCU / 2 + 1024 > static_lds(pipe) ? kLdsPerCU / 2 + 1024 - static_lds(pipe) : 0;
@@ -490,6 +496,7 @@ void attn_split_kernel(AttnArgs a) {
   __shared__ __align__(16) uint16_t vlds[kWaves][kChunk * kVPitch];
   __shared__ int rows_lds[kWaves][PIPE ? 2 : 1][kRowsCap];
   __shared__ int next_unit;
+  __shared__ int seq_order[PIPE ? kSortMaxB : 1];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   // One workgroup per CU, one wavefront per SIMD.  Two wavefronts on a SIMD
@@ -499,8 +506,33 @@ void attn_split_kernel(AttnArgs a) {
   // permuted unit order; its wavefronts take them on demand from an LDS
   // counter, which evens out units of unequal length within the workgroup
   // (the permutation evens them out across workgroups).
+  //
+  // Sorted order (pipelined launches over ragged batches): the sequences are
+  // ranked by selection size, longest first, and the (layer, sequence,
+  // split) groups in that order are dealt to the workgroups in a snake
+  // (row r of gridDim.x groups left to right for even r, right to left for
+  // odd r), so that every workgroup receives about the same number of
+  // tokens.  The units of one group (its KV heads) stay consecutive.
+  // Selections of one size need no sorting: the permuted order is kept.
+  bool sorted = false;
+  if (PIPE && a.sorted) {
+    int* cnt = &rows_lds[0][0][0];  // scratch until the first unit is staged
+    const int t = threadIdx.x;      // kWaves * 64 = kSortMaxB >= B threads
+    const int c = t < a.B ? clampi(a.counts[t], 0, a.k_max) : -1;
+    cnt[t] = c;
+    __syncthreads();
+    sorted = !__syncthreads_and(t >= a.B || c == cnt[0]);  // uniform for the workgroup
+    if (sorted && t < a.B) {
+      int r = 0;
+      for (int u = 0; u < a.B; ++u) {
+        const int cu = cnt[u];
+        r += cu > c || (cu == c && u < t);
+      }
+      seq_order[r] = t;
+    }
+  }
   const int per_block = (a.n_items + gridDim.x - 1) / gridDim.x;
-  const int u0 = blockIdx.x * per_block;
+  const int u0 = sorted ? 0 : blockIdx.x * per_block;
   const int u1 = min(u0 + per_block, a.n_items);
   if (threadIdx.x == 0) next_unit = u0;
   __syncthreads();
@@ -508,8 +540,21 @@ void attn_split_kernel(AttnArgs a) {
     int t = 0;
     if (lane == 0) t = atomicAdd(&next_unit, 1);
     const int unit = __builtin_amdgcn_readfirstlane(t);
-    if (unit >= u1) return -1;  // uniform per wave
     const int gu = a.H_kv * a.R;  // units per group (all column groups of one (layer, sequence, split))
+    if (sorted) {
+      const int row = unit / gu;
+      const int col = (row & 1) ? (int)gridDim.x - 1 - (int)blockIdx.x : (int)blockIdx.x;
+      const int64_t j = (int64_t)row * gridDim.x + col;  // group in size order
+      if (j >= a.n_groups) return -1;  // uniform per wave; later rows are past the end too
+      const int per_seq = a.n_groups / a.B;  // layers x splits
+      const int rank = (int)(j / per_seq);
+      const int rem = (int)(j - (int64_t)rank * per_seq);
+      const int layer = rem / a.n_split;
+      const int split = rem - layer * a.n_split;
+      const int lb = layer * a.B + seq_order[rank];
+      return (lb * a.n_split + split) * gu + (unit - row * gu);
+    }
+    if (unit >= u1) return -1;  // uniform per wave
     const int grp = unit / gu;
     return (int)(((int64_t)grp * a.perm) % a.n_groups) * gu + (unit - grp * gu);
   };
@@ -967,7 +1012,7 @@ hipError_t launch_attn_mode(const Dims& d, int kv, const uint16_t* q, const uint
   AttnArgs a{q, k, v, idx, kbuf, vbuf, src, fused, counts, part_acc, part_ml, out, lse,
              d.kv_stride_layer, d.kv_stride_b, d.B, d.H_q, d.H_kv, d.G / R, d.k_max, d.L_cap,
              pl.n_split, pl.split, (int)n_items, R, pl.mode, n_order, perm, d.n_sets,
-             d.scale * kLog2e};
+             d.scale * kLog2e, 0};
   // One workgroup per CU, fewer only when there are fewer units than CUs:
   // with few units they are spread over all CUs (each CU's share of the
   // bandwidth is limited) rather than packed four to a CU.
@@ -979,6 +1024,12 @@ hipError_t launch_attn_mode(const Dims& d, int kv, const uint16_t* q, const uint
   const bool force_cold = sched && strcmp(sched, "cold") == 0;
   // some wavefront takes several units: pipeline them
   const bool pipe = !force_cold && n_items > (int64_t)grid.x * kWaves;
+  // Sorted order: pipelined, at most one sequence per thread of a workgroup
+  // to rank, and at least two groups per workgroup.  SPEC_ATTN_ORDER=perm
+  // keeps the permuted order (the tests compare both orders bit for bit).
+  const char* order = getenv("SPEC_ATTN_ORDER");
+  const bool want_sorted = !(order && strcmp(order, "perm") == 0);
+  a.sorted = pipe && want_sorted && d.B <= kSortMaxB && n_order >= 2 * (int64_t)grid.x;
   if (kv == kKvIndexed)
     launch_split<kKvIndexed>(grid, pipe, a, s);
   else if (kv == kKvCompact)

@@ -257,6 +257,45 @@ def test_pipelined_units_equal_cold_units(dev, case, monkeypatch):
             assert torch.equal(l_l[0], runs["auto"][0][1][layer]), layer
 
 
+# Pipelined launches over ragged batches with at least two (layer, sequence,
+# split) groups per workgroup on a 256-CU device (and at most 256
+# sequences): the groups are dealt to the workgroups by selection size.
+# Sizes repeat (ties keep the lower sequence first) and include empty ones.
+SORTED_CASES = [
+    # one unit per group: 4 x 130 groups
+    (4, 130, 160, 32, 8, [(53 * b) % 129 if b % 7 else 64 for b in range(130)], 128),
+    # split selections (3 splits of 864): 200 x 3 groups, partials merged
+    (1, 200, 3000, 8, 2, [(911 * b) % 2501 if b % 5 else 1200 for b in range(200)], 2500),
+]
+
+
+@pytest.mark.parametrize("case", SORTED_CASES, ids=[str(c[:5]) for c in SORTED_CASES])
+def test_sorted_order_equals_permuted(dev, case, monkeypatch):
+    """Groups dealt by selection size give the same bits as the permuted
+    order (every unit computes the same thing wherever it runs), in indexed
+    and compact mode, and match the oracle on every (layer, sequence)."""
+    announce(f"attn sorted vs permuted order {case[:5]}")
+    g = torch.Generator().manual_seed(11 + sum(case[:5]))
+    q, K, V, idx, counts = _attn_inputs(case, g)
+    qd, Kd, Vd, idxd, cd = q.to(dev), K.to(dev), V.to(dev), idx.to(dev), counts.to(dev)
+    ks, vs = spec.gather(Kd, Vd, idxd, cd)
+    runs = {}
+    for order in ("auto", "perm"):
+        if order == "perm":
+            monkeypatch.setenv("SPEC_ATTN_ORDER", "perm")
+        else:
+            monkeypatch.delenv("SPEC_ATTN_ORDER", raising=False)
+        runs[order] = (spec.sparse_decode_attn(qd, Kd, Vd, cd, idx=idxd),
+                       spec.sparse_decode_attn(qd, ks, vs, cd))
+    monkeypatch.delenv("SPEC_ATTN_ORDER", raising=False)
+    for mode in (0, 1):
+        (o_a, l_a), (o_p, l_p) = runs["auto"][mode], runs["perm"][mode]
+        assert torch.equal(o_a, o_p) and torch.equal(l_a, l_p), mode
+    assert torch.equal(runs["auto"][0][0], runs["auto"][1][0])
+    _check_attn(runs["auto"][0][0].cpu().numpy(), runs["auto"][0][1].cpu().numpy(), q, K, V, idx,
+                counts, case)
+
+
 @pytest.mark.parametrize("case", ATTN_CASES[:4], ids=[str(c) for c in ATTN_CASES[:4]])
 def test_gather_then_compact_attention(dev, case):
     """spec_gather is a bit-exact row copy; compact-mode attention over its
