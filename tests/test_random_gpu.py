@@ -15,7 +15,9 @@
   supported query-group size up to 64, one to three layers, one token set per
   sequence or one per KV head, ragged and empty selections, budgets up to the
   whole cache; max-abs error within the
-  attention tolerance, lse included.
+  attention tolerance, lse included.  Batches of 64-256 ragged sequences
+  (the attention's order by selection size) give the same bits as the
+  permuted order.
 """
 import numpy as np
 import pytest
@@ -116,6 +118,57 @@ def test_attention_random_shapes(dev, seed):
                 err = np.abs(out[layer, b] - want).max()
                 assert err <= TOL_ATTN, (it, layer, b, err)
                 assert np.abs(lse[layer, b] - want_lse).max() <= TOL_ATTN, (it, layer, b)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_attention_random_ragged_batches(dev, seed, monkeypatch):
+    """Batches of 64-256 sequences with unequal selections, enough
+    (layer, sequence) groups for the attention to deal them to its
+    workgroups by selection size: the same bits as the permuted order, and
+    sampled (layer, sequence) outputs against the oracle."""
+    rng = np.random.default_rng(500 + seed)
+    for it in range(4):
+        B = int(rng.integers(64, 257))
+        n_layers = int(rng.integers(-(-520 // B), -(-520 // B) + 3))
+        H_kv = int(rng.choice([1, 2, 4, 8]))
+        G = int(rng.choice([g for g in (1, 2, 4, 8, 16, 32) if g * H_kv <= 128]))
+        H_q = H_kv * G
+        L_cap = int(rng.integers(32, 257))
+        k_max = int(rng.integers(1, L_cap + 1))
+        counts = _ragged(rng, B, k_max, p_other=0.7)
+        announce(f"attn ragged batch seed={seed} it={it} layers={n_layers} B={B} H_q={H_q} "
+                 f"H_kv={H_kv} L_cap={L_cap} k_max={k_max}")
+        g = torch.Generator(device=dev).manual_seed(30_000 * seed + it)
+        q = torch.randn((n_layers, B, H_q, 128), generator=g, device=dev).to(torch.bfloat16)
+        K = torch.randn((n_layers, B, L_cap, H_kv, 128), generator=g, device=dev).to(torch.bfloat16)
+        V = torch.randn((n_layers, B, L_cap, H_kv, 128), generator=g, device=dev).to(torch.bfloat16)
+        gc = torch.Generator().manual_seed(40_000 * seed + it)
+        idx = torch.full((B, k_max), -1, dtype=torch.int32)
+        for b in range(B):
+            idx[b, :counts[b]] = torch.randperm(L_cap, generator=gc)[:counts[b]].sort().values.int()
+        cnt = torch.tensor(counts, dtype=torch.int32)
+        runs = {}
+        for order in ("auto", "perm"):
+            if order == "perm":
+                monkeypatch.setenv("SPEC_ATTN_ORDER", "perm")
+            else:
+                monkeypatch.delenv("SPEC_ATTN_ORDER", raising=False)
+            runs[order] = spec.sparse_decode_attn(q, K, V, cnt.to(dev), idx=idx.to(dev))
+        monkeypatch.delenv("SPEC_ATTN_ORDER", raising=False)
+        assert torch.equal(runs["auto"][0], runs["perm"][0]), it
+        assert torch.equal(runs["auto"][1], runs["perm"][1]), it
+        out, lse = runs["auto"][0].cpu().numpy(), runs["auto"][1].cpu().numpy()
+        assert np.all(np.isfinite(out)), it
+        for _ in range(12):
+            layer, b = int(rng.integers(0, n_layers)), int(rng.integers(0, B))
+            want, want_lse = oracle.sparse_gqa_attention(
+                f64(q[layer, b].cpu()), f64(K[layer, b].cpu()), f64(V[layer, b].cpu()),
+                idx[b, :counts[b]].numpy())
+            if counts[b] == 0:
+                assert np.all(out[layer, b] == 0.0) and np.all(np.isneginf(lse[layer, b]))
+                continue
+            assert np.abs(out[layer, b] - want).max() <= TOL_ATTN, (it, layer, b)
+            assert np.abs(lse[layer, b] - want_lse).max() <= TOL_ATTN, (it, layer, b)
 
 
 @pytest.mark.parametrize("seed", range(3))
