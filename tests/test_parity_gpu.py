@@ -107,6 +107,12 @@ TOPK_CASES = [
     ("narrow", 2, 9000, 1000, [9000, 8191], [1000, 999]),
     ("random", 4, 1024, 1024, [1024, 0, 5, 1024], [1024, 3, 9, 0]),
     ("random", 1, 32768, 2048, [32768], [2048]),
+    # rows of 8193-32768 tokens (tiled): crowded bins, row lengths not a
+    # multiple of 4, every token or none selected, a one-token budget
+    ("equal", 2, 16384, 4000, [16384, 9000], [4000, 8999]),
+    ("ties", 3, 32767, 3000, [32767, 20000, 0], [3000, 20000, 5]),
+    ("signed", 2, 24000, 5000, [24000, 12345], [5000, 1]),
+    ("narrow", 1, 32768, 4096, [32768], [4096]),
     ("ties", 1, 40000, 4096, [40000], [4096]),
     # rows whose start is not 16-byte aligned (row length not a multiple of 4)
     ("random", 3, 5001, 600, [5001, 4999, 17], [600, 600, 5]),
