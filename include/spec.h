@@ -66,6 +66,13 @@
  *    vocabulary; after the launch it synchronises the stream and reports an
  *    asynchronous failure as SPEC_ERR_HIP.  The calls then synchronise and
  *    cannot be captured in a graph.
+ *  - Schedule switches (environment, read at every call; results are the
+ *    same bit for bit, only the kernels' schedule changes):
+ *    SPEC_TOPK_PATH=tiles takes the tiled selection kernels for short rows
+ *    too; SPEC_ATTN_SCHEDULE=cold starts every attention work unit cold (no
+ *    pipelining across units); SPEC_ATTN_ORDER=perm keeps the permuted work
+ *    order on ragged batches; SPEC_ELASTIC_PATH=copy or =fused takes one
+ *    elastic-loading path for every sequence of spec_step.
  */
 #ifndef SPEC_H_
 #define SPEC_H_
