@@ -221,10 +221,21 @@ __global__ __launch_bounds__(256) void softmax_headsum_kernel(SoftArgs a) {
     if (sh_hist[i]) atomicAdd(&gh[i], sh_hist[i]);
 }
 
+// Large grids run at most kLogitsPerCU workgroups per CU (dynamic LDS is
+// reserved for the purpose): with eight per CU (what registers and LDS
+// allow), 2048 workgroups of 256 tokens scored 32 sequences of 16K tokens
+// ~8 us slower than with four, the grid then running in two rounds.
+constexpr int kLogitsPerCU = 4;
+constexpr size_t kLogitsLdsPerCU = 160 * 1024;
+constexpr size_t logits_lds_reserve(int tpb) {
+  // a workgroup then holds just under a quarter of the CU's LDS: four fit, five do not
+  return kLogitsLdsPerCU / kLogitsPerCU - 2048 - sizeof(float) * tpb * 17;
+}
+
 template <int LPH>
 void logits_dispatch(dim3 g, int tpb, bool wide, const LogitsArgs& a, hipStream_t s) {
   if (tpb == 256) {
-    if (wide) logits_kernel<LPH, kUnrollWide, 256><<<g, 256, 0, s>>>(a);
+    if (wide) logits_kernel<LPH, kUnrollWide, 256><<<g, 256, logits_lds_reserve(256), s>>>(a);
     else logits_kernel<LPH, kUnrollNarrow, 256><<<g, 256, 0, s>>>(a);
   } else if (tpb == 128) {
     logits_kernel<LPH, kUnrollNarrow, 128><<<g, 256, 0, s>>>(a);
