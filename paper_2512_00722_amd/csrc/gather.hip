@@ -307,15 +307,25 @@ hipError_t launch_delta_plan(const Dims& d, const int32_t* idx_now, const int32_
   return hipGetLastError();
 }
 
+// Device-to-device copies run at most kCopyPerCU workgroups per CU (dynamic
+// LDS is reserved for the purpose; registers would allow five): on the
+// ragged workload's steady updates (2.75 GB read and written per step) the
+// step went from 3618 to 3522 us with two per CU (one and three: within
+// 1%).  Copies from host memory keep every workgroup the CU holds: the host
+// link's latency needs their requests in flight.
+constexpr int kCopyPerCU = 2;
+constexpr size_t kCopyLdsPerCU = 160 * 1024;
+
 hipError_t launch_delta_copy(const Dims& d, const uint16_t* k_src, const uint16_t* v_src,
                              int64_t src_stride_layer, int64_t src_stride_b, int n_layers,
                              const int32_t* n_changed, uint16_t* kbuf, uint16_t* vbuf,
-                             const void* ws, hipStream_t s, const int32_t* skip) {
+                             const void* ws, hipStream_t s, const int32_t* skip, bool from_host) {
   CopyArgs c{k_src, v_src, static_cast<const int32_t*>(ws), n_changed, skip, kbuf, vbuf,
              src_stride_layer, src_stride_b, (int64_t)d.H_kv * d.d, d.B, d.k_max, d.L_cap,
              n_layers};
   const dim3 grid((d.k_max + kRowsPerBlock - 1) / kRowsPerBlock, d.B);
-  elastic_copy_kernel<<<grid, 256, 0, s>>>(c);
+  const size_t lds = from_host ? 0 : kCopyLdsPerCU / kCopyPerCU - 4096;  // two fit, three do not
+  elastic_copy_kernel<<<grid, 256, lds, s>>>(c);
   return hipGetLastError();
 }
 

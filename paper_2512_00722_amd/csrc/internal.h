@@ -211,10 +211,13 @@ hipError_t launch_delta(const Dims& d, const int32_t* idx_now, const int32_t* co
 hipError_t launch_delta_plan(const Dims& d, const int32_t* idx_now, const int32_t* counts,
                              int32_t* slot_tok, int32_t* slot_src, int32_t* n_changed, void* ws,
                              hipStream_t s, int fuse_pct = -1);
+// from_host: the source rows are in pinned host memory (the host-offloaded
+// layers); device-to-device copies run fewer workgroups per CU.
 hipError_t launch_delta_copy(const Dims& d, const uint16_t* k_src, const uint16_t* v_src,
                              int64_t src_stride_layer, int64_t src_stride_b, int n_layers,
                              const int32_t* n_changed, uint16_t* kbuf, uint16_t* vbuf,
-                             const void* ws, hipStream_t s, const int32_t* skip = nullptr);
+                             const void* ws, hipStream_t s, const int32_t* skip = nullptr,
+                             bool from_host = false);
 hipError_t launch_mla(const MlaDims& d, const uint16_t* q, const uint16_t* ckv,
                       const uint16_t* w_uk, const uint16_t* w_uv, const int32_t* idx,
                       const int32_t* counts, float* out, float* lse, void* ws, hipStream_t s);

@@ -277,7 +277,8 @@ spec_status enqueue_host_loads(const spec::Dims& d_off, const HostKv& hk, const 
     e = spec::launch_delta_copy(d_off, hk.k + (int64_t)l * hk.stride_layer,
                                 hk.v + (int64_t)l * hk.stride_layer, hk.stride_layer, hk.stride_b,
                                 1, el->n_changed, el->kbuf + l * slot_layer,
-                                el->vbuf + l * slot_layer, ws_delta, q);
+                                el->vbuf + l * slot_layer, ws_delta, q, nullptr,
+                                /*from_host=*/true);
     if (e != hipSuccess) return hip_status(e);
     if (ready && (e = hipEventRecord(static_cast<hipEvent_t>(ready[l]), q)) != hipSuccess)
       return hip_status(e);
