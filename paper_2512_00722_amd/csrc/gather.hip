@@ -284,6 +284,15 @@ __global__ __launch_bounds__(256) void elastic_copy_kernel(CopyArgs a) {
 
 }  // namespace
 
+// Device-to-device copies run at most kCopyPerCU workgroups per CU (dynamic
+// LDS is reserved for the purpose; registers would allow five): on the
+// ragged workload's steady updates (2.75 GB read and written per step) the
+// step went from 3618 to 3522 us with two per CU (one and three: within
+// 1%).  Copies from host memory keep every workgroup the CU holds: the host
+// link's latency needs their requests in flight.
+constexpr int kCopyPerCU = 2;
+constexpr size_t kCopyLdsPerCU = 160 * 1024;
+
 hipError_t launch_gather(const Dims& d, const uint16_t* k_cache, const uint16_t* v_cache,
                          const int32_t* idx, const int32_t* counts, uint16_t* k_sel,
                          uint16_t* v_sel, hipStream_t s) {
@@ -306,15 +315,6 @@ hipError_t launch_delta_plan(const Dims& d, const int32_t* idx_now, const int32_
   elastic_plan_kernel<<<d.B, kPlanThreads, elastic_plan_lds_bytes(d), s>>>(p);
   return hipGetLastError();
 }
-
-// Device-to-device copies run at most kCopyPerCU workgroups per CU (dynamic
-// LDS is reserved for the purpose; registers would allow five): on the
-// ragged workload's steady updates (2.75 GB read and written per step) the
-// step went from 3618 to 3522 us with two per CU (one and three: within
-// 1%).  Copies from host memory keep every workgroup the CU holds: the host
-// link's latency needs their requests in flight.
-constexpr int kCopyPerCU = 2;
-constexpr size_t kCopyLdsPerCU = 160 * 1024;
 
 hipError_t launch_delta_copy(const Dims& d, const uint16_t* k_src, const uint16_t* v_src,
                              int64_t src_stride_layer, int64_t src_stride_b, int n_layers,
