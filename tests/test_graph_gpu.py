@@ -51,6 +51,48 @@ def test_step_graph_replays_match_eager():
             assert torch.equal(outputs[k], v), (rep, k)
 
 
+def test_step_graph_ragged_batch_replays_match_eager():
+    """A ragged batch large enough for the attention to deal its work by
+    selection size (96 sequences x 6 layers, several units per wavefront):
+    graph replays match the eager step bit for bit."""
+    dev = need_gpu()
+    announce("graph replay of a ragged 96-sequence step")
+    w = small_workload(B=96, L=2048, H_r=8, d_r=64, n_layers=6, H_q=32, H_kv=8, k=256,
+                       heavy_frac=0.02, ragged_min=300, k_frac_den=4)
+    x = generate(w, seed=17, device=dev)
+    assert len(set(x["ks"].clamp(max=w.k).tolist())) > 1   # unequal selections
+    args = dict(q_r=x["q_r"], K_r=x["K_r"], seq_lens=x["seq_lens"], ks=x["ks"], q=x["q"],
+                K=x["K"], V=x["V"], k_max=w.k)
+    dims = spec.Dims.make(B=w.B, L_cap=w.L_cap, L_max=w.L_cap, k_max=w.k, H_r=w.H_r, d_r=w.d_r,
+                          n_layers=w.n_layers, H_q=w.H_q, H_kv=w.H_kv, d=w.d,
+                          kr_stride_b=x["K_r"].stride(0), kv_stride_layer=x["K"].stride(0),
+                          kv_stride_b=x["K"].stride(1))
+    ws = torch.zeros(spec.workspace_size(dims, spec.OP_STEP), dtype=torch.uint8, device=dev)
+    eager = spec.step(**args, with_lse=True)
+    torch.cuda.synchronize()
+    ref = {k: v.clone() for k, v in eager.items() if v is not None}
+    outputs = {}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        spec.step(**args, with_lse=True, outputs=outputs, ws=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        spec.step(**args, with_lse=True, outputs=outputs, ws=ws)
+    for rep in range(3):
+        for v in outputs.values():
+            if v is not None:
+                v.fill_(7)
+        spec.score(x["q_r"], x["K_r"], x["seq_lens"])   # eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for k, v in ref.items():
+            assert torch.equal(outputs[k], v), (rep, k)
+
+
 def test_step_offload_graph_replays_match_eager():
     """The step with host-offloaded layers captured in a graph: the copy
     stream joins the capture through the caller's events (fork after the
