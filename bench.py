@@ -354,7 +354,8 @@ def run_fixed(args, spec, w, x, name):
     a_bytes = attn_bytes(w, counts)
     attn_s = op_us["attn"] * 1e-6
     achieved = a_bytes / attn_s / 1e9
-    traffic = stored_traffic(name)
+    # the stored counters were taken with one token set per sequence
+    traffic = None if args.head_level else stored_traffic(name)
     value = args.steps / wall
     line = {
         "metric": METRIC,
