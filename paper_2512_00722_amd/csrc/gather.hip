@@ -284,12 +284,13 @@ __global__ __launch_bounds__(256) void elastic_copy_kernel(CopyArgs a) {
 
 }  // namespace
 
-// Device-to-device copies run at most kCopyPerCU workgroups per CU (dynamic
-// LDS is reserved for the purpose; registers would allow five): on the
-// ragged workload's steady updates (2.75 GB read and written per step) the
-// step went from 3618 to 3522 us with two per CU (one and three: within
-// 1%).  Copies from host memory keep every workgroup the CU holds: the host
-// link's latency needs their requests in flight.
+// The elastic copy, device to device, runs at most kCopyPerCU workgroups per
+// CU (dynamic LDS is reserved for the purpose; registers would allow five):
+// on 64 ragged sequences whose steady updates read and write 2.75 GB, whole
+// steps went from 3622 to 3439 us with two per CU (one and three: within 1%
+// of two).  Copies from host memory keep every workgroup the CU holds: the
+// host link's latency needs their requests in flight.  The materialised
+// gather keeps full occupancy too (the cap made it slower).
 constexpr int kCopyPerCU = 2;
 constexpr size_t kCopyLdsPerCU = 160 * 1024;
 
